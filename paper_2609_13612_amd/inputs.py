@@ -1,0 +1,38 @@
+"""Seeded synthetic inputs shared by the HIP path's tests, the bench and the oracle checks.
+
+This module holds none of the method's arithmetic.  It draws i.i.d. N(0, 1)
+tensors from a CPU ``torch.Generator`` in a fixed order -- Q, K, V, then dO --
+as fp32, and rounds them to the storage dtype (bf16 rounds to nearest even).
+Both sides of a parity check consume exactly these values: the HIP path after
+a copy to the GPU, the oracle after an exact upcast to fp64.
+"""
+import torch
+
+DTYPES = {"bf16": torch.bfloat16, "fp32": torch.float32}
+
+
+def make_qkv(B, H, Hkv, S, D, *, dtype="bf16", seed=0, with_do=False):
+    """Dict with q [B,H,S,D], k and v [B,Hkv,S,D] (and do [B,H,S,D]) on the CPU."""
+    if dtype not in DTYPES:
+        raise ValueError(f"dtype must be one of {sorted(DTYPES)}")
+    g = torch.Generator("cpu").manual_seed(seed)
+    out = {
+        "q": torch.randn(B, H, S, D, generator=g, dtype=torch.float32),
+        "k": torch.randn(B, Hkv, S, D, generator=g, dtype=torch.float32),
+        "v": torch.randn(B, Hkv, S, D, generator=g, dtype=torch.float32),
+    }
+    if with_do:
+        out["do"] = torch.randn(B, H, S, D, generator=g, dtype=torch.float32)
+    t = DTYPES[dtype]
+    return {name: x.to(t).contiguous() for name, x in out.items()}
+
+
+def alibi_slopes(H):
+    """The ALiBi workload's per-head slopes 2^(-8h/H) for h = 1..H, as fp32 [H]."""
+    h = torch.arange(1, H + 1, dtype=torch.float64)
+    return torch.pow(2.0, -8.0 * h / H).to(torch.float32)
+
+
+def to_f64(t):
+    """Exact upcast of a (CPU or GPU) tensor to an fp64 numpy array."""
+    return t.detach().to("cpu", torch.float64).numpy()

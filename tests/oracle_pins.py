@@ -1,0 +1,343 @@
+"""Checks that pin the fp64 oracle to things other than itself.
+
+Each ``check_*`` raises AssertionError on failure.  They are run as tests in
+``test_oracle_pins.py`` and, with a mistake planted in the oracle, in
+``test_oracle_mutations.py`` (which asserts that some check then fails).
+
+Sources of truth used here, none of them the oracle:
+* closed forms (D = 2 rotations, frequencies of a tiny head, the first rows of
+  a causal softmax, a width-1 window);
+* invariants of the definitions (rotation norms, relative-position dot
+  products, softmax rows summing to one, rows of dS summing to zero);
+* an independent brute force (tests/bruteforce.py: explicit Givens matrices and
+  scalar loops) and its finite-difference gradients;
+* library routines: torch's fp64 scaled_dot_product_attention on the CPU, and
+  torch autograd through a separately written torch forward that applies RoPE
+  as complex multiplication.
+"""
+import math
+
+import numpy as np
+import torch
+
+import oracle
+import bruteforce
+
+TOL = 1e-12
+
+
+def _rng(seed):
+    return np.random.default_rng(seed)
+
+
+def _tiny(seed, B=1, H=2, Hkv=1, S=6, D=4):
+    r = _rng(seed)
+    q = r.standard_normal((B, H, S, D))
+    k = r.standard_normal((B, Hkv, S, D))
+    v = r.standard_normal((B, Hkv, S, D))
+    do = r.standard_normal((B, H, S, D))
+    return q, k, v, do
+
+
+# ----------------------------------------------------------------------------- RoPE
+
+def check_frequencies():
+    w = oracle.rope_frequencies(8, 10000.0)
+    assert np.allclose(w, [1.0, 0.1, 0.01, 0.001], rtol=1e-14, atol=0)
+    w = oracle.rope_frequencies(128, 500000.0)
+    assert w[0] == 1.0
+    assert abs(w[1] - 500000.0 ** (-1.0 / 64.0)) < 1e-16
+
+
+def check_rope_d2_closed_form(kind):
+    p = 3.0   # D = 2 has one pair with omega_0 = 1, so the angle is p radians
+    x = np.array([[1.0, 0.0], [0.0, 1.0]])   # two "positions" sharing p
+    out = oracle.rope_rotate(x, np.array([p, p]), 10000.0, kind)
+    assert np.allclose(out[0], [math.cos(p), math.sin(p)], atol=1e-15)
+    assert np.allclose(out[1], [-math.sin(p), math.cos(p)], atol=1e-15)
+
+
+def check_rope_pairing(kind):
+    D, p = 8, 5.0
+    partner = {"neox": lambda a: (a + D // 2) % D, "interleaved": lambda a: a ^ 1}[kind]
+    for a in range(D):
+        x = np.zeros((1, D))
+        x[0, a] = 1.0
+        out = oracle.rope_rotate(x, np.array([p]), 7.0, kind)[0]
+        nz = set(np.flatnonzero(np.abs(out) > 1e-14).tolist())
+        assert nz == {a, partner(a)}, (kind, a, nz)
+
+
+def check_rope_norm(kind, seed=1):
+    x = _rng(seed).standard_normal((2, 3, 50, 16))
+    pos = np.arange(50) * 37.0
+    out = oracle.rope_rotate(x, pos, 10000.0, kind)
+    a, b = {"neox": (np.arange(8), np.arange(8) + 8),
+            "interleaved": (np.arange(0, 16, 2), np.arange(1, 16, 2))}[kind]
+    assert np.allclose(out[..., a] ** 2 + out[..., b] ** 2, x[..., a] ** 2 + x[..., b] ** 2, atol=1e-12)
+    assert np.allclose(np.linalg.norm(out, axis=-1), np.linalg.norm(x, axis=-1), atol=1e-12)
+
+
+def check_rope_relative(kind, seed=2):
+    r = _rng(seed)
+    q = r.standard_normal(16)
+    k = r.standard_normal(16)
+    for (m, n, t) in [(5, 2, 11), (0, 9, 100), (300, 1, 7)]:
+        def rot(x, p):
+            return oracle.rope_rotate(x[None], np.array([float(p)]), 10000.0, kind)[0]
+        base = rot(q, m) @ rot(k, n)
+        shifted = rot(q, m + t) @ rot(k, n + t)
+        assert abs(base - shifted) < 1e-12
+    # and it is not position-blind: a different offset changes the product
+    assert abs(rot(q, 5) @ rot(k, 2) - rot(q, 5) @ rot(k, 3)) > 1e-6
+
+
+def check_rope_inverse(kind, seed=3):
+    x = _rng(seed).standard_normal((4, 32))
+    pos = np.arange(4) * 1000.0
+    y = oracle.rope_rotate(x, pos, 500000.0, kind)
+    assert np.allclose(oracle.rope_rotate(y, pos, 500000.0, kind, inverse=True), x, atol=1e-12)
+    assert np.allclose(oracle.rope_rotate(x, np.zeros(4), 500000.0, kind), x, atol=0)
+
+
+def check_rope_vs_givens(kind, seed=4):
+    D, S = 8, 5
+    x = _rng(seed).standard_normal((S, D))
+    pos = np.arange(S) + 3.0
+    out = oracle.rope_rotate(x, pos, 10000.0, kind)
+    for s in range(S):
+        R = bruteforce.givens_matrix(D, pos[s], 10000.0, kind)
+        assert np.allclose(out[s], bruteforce.matvec(R, list(x[s])), atol=1e-13)
+
+
+# ----------------------------------------------------------------------------- forward
+
+VARIANTS = [
+    # (rope, mask, window, alibi)
+    ("none", "none", None, False),
+    ("none", "causal", None, False),
+    ("neox", "causal", None, False),
+    ("interleaved", "causal", None, False),
+    ("neox", "none", None, False),
+    ("neox", "sliding_window", 3, False),
+    ("interleaved", "sliding_window", 1, False),
+    ("none", "causal", None, True),
+    ("neox", "causal", None, True),
+    ("neox", "sliding_window", 2, True),
+]
+
+
+def _kw(rope, mask, window, alibi, H):
+    slopes = [0.3 * (h + 1) for h in range(H)] if alibi else None
+    return dict(rope=rope, theta=10000.0, mask=mask, window=window, alibi_slopes=slopes, scale=0.41)
+
+
+def check_forward_vs_bruteforce(variant, seed=5):
+    rope, mask, window, alibi = variant
+    q, k, v, _ = _tiny(seed, B=2, H=4, Hkv=2, S=7, D=4)
+    kw = _kw(rope, mask, window, alibi, 4)
+    O, L = oracle.attention_forward(q, k, v, **kw)
+    Ob, Lb = bruteforce.forward(q.tolist(), k.tolist(), v.tolist(), **kw)
+    assert np.allclose(O, np.array(Ob), atol=TOL, rtol=0)
+    assert np.allclose(L, np.array(Lb), atol=TOL, rtol=0)
+
+
+def check_softmax_rows(variant, seed=6):
+    rope, mask, window, alibi = variant
+    q, k, v, _ = _tiny(seed, H=2, Hkv=2, S=9, D=8)
+    kw = _kw(rope, mask, window, alibi, 2)
+    for h in range(2):
+        P = oracle.attention_probs(q, k, 0, h, **kw)
+        assert np.allclose(P.sum(axis=1), 1.0, atol=1e-14)
+        assert (P >= 0).all()
+        i = np.arange(9)[:, None]
+        j = np.arange(9)[None, :]
+        if mask == "causal":
+            assert (P[j > i] == 0).all()
+        if mask == "sliding_window":
+            assert (P[(j > i) | (j <= i - window)] == 0).all()
+
+
+def check_causal_first_rows(kind, seed=7):
+    # Row 0 sees only key 0 and RoPE is the identity at position 0, so
+    # O_0 = v_0 and LSE_0 = scale * q_0 . k_0.
+    q, k, v, _ = _tiny(seed, H=1, Hkv=1, S=5, D=2)
+    scale = 0.8
+    O, L = oracle.attention_forward(q, k, v, rope=kind, mask="causal", scale=scale)
+    assert np.allclose(O[0, 0, 0], v[0, 0, 0], atol=1e-15)
+    assert abs(L[0, 0, 0] - scale * q[0, 0, 0] @ k[0, 0, 0]) < 1e-14
+    # Row 1 (D = 2, omega = 1): q_1 rotated by 1 rad against k_0 (unrotated) and
+    # k_1 (rotated by the same 1 rad, so that product is rotation-free).
+    if kind != "none":
+        c, s = math.cos(1.0), math.sin(1.0)
+        q1 = q[0, 0, 1]
+        q1r = np.array([q1[0] * c - q1[1] * s, q1[0] * s + q1[1] * c])
+        s10 = scale * q1r @ k[0, 0, 0]
+        s11 = scale * q1 @ k[0, 0, 1]
+        e0, e1 = math.exp(s10), math.exp(s11)
+        assert np.allclose(O[0, 0, 1], (e0 * v[0, 0, 0] + e1 * v[0, 0, 1]) / (e0 + e1), atol=1e-14)
+        assert abs(L[0, 0, 1] - math.log(e0 + e1)) < 1e-14
+
+
+def check_window_one(kind, seed=8):
+    # Width-1 window: each row sees only itself, so O = V and, because both
+    # sides rotate by the same angle, LSE_i = scale * q_i . k_i.
+    q, k, v, _ = _tiny(seed, H=2, Hkv=2, S=10, D=8)
+    O, L = oracle.attention_forward(q, k, v, rope=kind, mask="sliding_window", window=1, scale=0.5)
+    assert np.allclose(O, v, atol=1e-15)
+    assert np.allclose(L, 0.5 * np.einsum("bhsd,bhsd->bhs", q, k), atol=1e-13)
+
+
+def check_window_reductions(seed=9):
+    q, k, v, _ = _tiny(seed, H=2, Hkv=1, S=12, D=8)
+    causal = oracle.attention_forward(q, k, v, rope="neox", mask="causal")
+    for W in (12, 13, 100):
+        sw = oracle.attention_forward(q, k, v, rope="neox", mask="sliding_window", window=W)
+        assert np.allclose(sw[0], causal[0], atol=1e-14) and np.allclose(sw[1], causal[1], atol=1e-14)
+    # a window of 11 differs from causal only in rows that can see 12 keys
+    sw = oracle.attention_forward(q, k, v, rope="neox", mask="sliding_window", window=11)
+    assert np.allclose(sw[0][:, :, :11], causal[0][:, :, :11], atol=1e-14)
+    assert not np.allclose(sw[0][:, :, 11], causal[0][:, :, 11], atol=1e-6)
+
+
+def check_alibi_special_cases(seed=10):
+    q, k, v, _ = _tiny(seed, H=3, Hkv=3, S=8, D=4)
+    plain = oracle.attention_forward(q, k, v, rope="neox", mask="causal")
+    zero = oracle.attention_forward(q, k, v, rope="neox", mask="causal", alibi_slopes=[0.0] * 3)
+    assert np.allclose(plain[0], zero[0], atol=1e-15) and np.allclose(plain[1], zero[1], atol=1e-15)
+    # A huge slope makes every earlier key vanish: O -> V and LSE -> the diagonal score.
+    big = oracle.attention_forward(q, k, v, rope="neox", mask="causal", alibi_slopes=[1e3] * 3)
+    assert np.allclose(big[0], v, atol=1e-12)
+    assert np.allclose(big[1], 0.5 * np.einsum("bhsd,bhsd->bhs", q, k), atol=1e-12)
+    # Row 1 with two visible keys: the earlier key is penalised by exactly one slope.
+    s = 0.7
+    one = oracle.attention_forward(q, k, v, mask="causal", alibi_slopes=[s] * 3, scale=0.5)
+    s10 = 0.5 * q[0, 0, 1] @ k[0, 0, 0] - s
+    s11 = 0.5 * q[0, 0, 1] @ k[0, 0, 1]
+    assert abs(one[1][0, 0, 1] - math.log(math.exp(s10) + math.exp(s11))) < 1e-13
+
+
+def check_vs_torch_sdpa(mask, seed=11):
+    q, k, v, _ = _tiny(seed, B=2, H=3, Hkv=3, S=33, D=16)
+    O, _ = oracle.attention_forward(q, k, v, rope="none", mask=mask, scale=0.3)
+    t = [torch.from_numpy(x) for x in (q, k, v)]
+    ref = torch.nn.functional.scaled_dot_product_attention(*t, is_causal=(mask == "causal"), scale=0.3)
+    assert np.allclose(O, ref.numpy(), atol=1e-12)
+
+
+def check_position_shift(kind, mask, seed=12):
+    q, k, v, _ = _tiny(seed, H=2, Hkv=1, S=10, D=8)
+    kw = dict(rope=kind, mask=mask, window=4 if mask == "sliding_window" else None, alibi_slopes=[0.2, 0.1])
+    a = oracle.attention_forward(q, k, v, **kw)
+    b = oracle.attention_forward(q, k, v, pos_offset=1234, **kw)
+    assert np.allclose(a[0], b[0], atol=1e-10) and np.allclose(a[1], b[1], atol=1e-10)
+
+
+def check_gqa_repeat_kv(seed=13):
+    q, k, v, do = _tiny(seed, B=2, H=6, Hkv=2, S=7, D=8)
+    kw = dict(rope="neox", mask="causal", alibi_slopes=[0.1 * h for h in range(6)])
+    O, L = oracle.attention_forward(q, k, v, **kw)
+    kr = np.repeat(k, 3, axis=1)   # HF repeat_kv: query head h reads K/V head h // 3
+    vr = np.repeat(v, 3, axis=1)
+    O2, L2 = oracle.attention_forward(q, kr, vr, **kw)
+    assert np.allclose(O, O2, atol=1e-15) and np.allclose(L, L2, atol=1e-15)
+    dq, dk, dv = oracle.attention_backward(q, k, v, do, **kw)
+    dq2, dk2, dv2 = oracle.attention_backward(q, kr, vr, do, **kw)
+    assert np.allclose(dq, dq2, atol=1e-13)
+    assert np.allclose(dk, dk2.reshape(2, 2, 3, 7, 8).sum(axis=2), atol=1e-13)
+    assert np.allclose(dv, dv2.reshape(2, 2, 3, 7, 8).sum(axis=2), atol=1e-13)
+
+
+def check_rows_match_full(seed=14):
+    q, k, v, _ = _tiny(seed, B=1, H=4, Hkv=2, S=40, D=8)
+    slopes = [0.05, 0.1, 0.2, 0.4]
+    for rope, mask, W in [("neox", "causal", None), ("interleaved", "sliding_window", 5), ("none", "none", None)]:
+        O, L = oracle.attention_forward(q, k, v, rope=rope, mask=mask, window=W, alibi_slopes=slopes)
+        rows = np.array([0, 3, 17, 39])
+        for h in range(4):
+            o, l = oracle.attention_forward_rows(q[0, h], k[0, h // 2], v[0, h // 2], rows, h=h, H=4,
+                                                 rope=rope, mask=mask, window=W, alibi_slopes=slopes)
+            assert np.allclose(o, O[0, h, rows], atol=1e-14) and np.allclose(l, L[0, h, rows], atol=1e-14)
+
+
+# ----------------------------------------------------------------------------- backward
+
+def check_backward_fd(variant, seed=15):
+    rope, mask, window, alibi = variant
+    q, k, v, do = _tiny(seed, B=1, H=2, Hkv=1, S=5, D=4)
+    kw = _kw(rope, mask, window, alibi, 2)
+    dq, dk, dv = oracle.attention_backward(q, k, v, do, **kw)
+    ql, kl, vl, dol = q.tolist(), k.tolist(), v.tolist(), do.tolist()
+
+    def f():
+        return bruteforce.loss(ql, kl, vl, dol, **kw)
+
+    assert np.allclose(dq, np.array(bruteforce.finite_difference_grad(ql, f)), atol=1e-7)
+    assert np.allclose(dk, np.array(bruteforce.finite_difference_grad(kl, f)), atol=1e-7)
+    assert np.allclose(dv, np.array(bruteforce.finite_difference_grad(vl, f)), atol=1e-7)
+
+
+def _torch_forward(q, k, v, rope, mask, window, slopes, scale, theta):
+    """A separately written torch fp64 forward: RoPE as complex multiplication."""
+    B, H, S, D = q.shape
+    Hkv = k.shape[1]
+    pos = torch.arange(S, dtype=torch.float64)
+    inv = theta ** (-torch.arange(0, D, 2, dtype=torch.float64) / D)
+    phase = torch.polar(torch.ones(S, D // 2, dtype=torch.float64), pos[:, None] * inv[None, :])
+
+    def rot(x):
+        if rope == "none":
+            return x
+        if rope == "interleaved":
+            z = torch.view_as_complex(x.reshape(*x.shape[:-1], D // 2, 2))
+            return torch.view_as_real(z * phase).reshape(x.shape)
+        z = torch.complex(x[..., : D // 2], x[..., D // 2:])
+        z = z * phase
+        return torch.cat([z.real, z.imag], dim=-1)
+
+    qr, kr = rot(q), rot(k)
+    kr = kr.repeat_interleave(H // Hkv, dim=1)
+    vv = v.repeat_interleave(H // Hkv, dim=1)
+    s = scale * qr @ kr.transpose(-1, -2)
+    i = torch.arange(S)[:, None]
+    j = torch.arange(S)[None, :]
+    if slopes is not None:
+        s = s + torch.tensor(slopes, dtype=torch.float64)[None, :, None, None] * (j - i).to(torch.float64)
+    keep = torch.ones(S, S, dtype=torch.bool)
+    if mask in ("causal", "sliding_window"):
+        keep &= j <= i
+    if mask == "sliding_window":
+        keep &= (i - j) < window
+    s = s.masked_fill(~keep, float("-inf"))
+    return torch.softmax(s, dim=-1) @ vv
+
+
+def check_backward_vs_torch_autograd(variant, seed=16):
+    rope, mask, window, alibi = variant
+    q, k, v, do = _tiny(seed, B=2, H=4, Hkv=2, S=11, D=8)
+    kw = _kw(rope, mask, window, alibi, 4)
+    dq, dk, dv = oracle.attention_backward(q, k, v, do, **kw)
+    O, _ = oracle.attention_forward(q, k, v, **kw)
+    t = [torch.tensor(x, requires_grad=True) for x in (q, k, v)]
+    out = _torch_forward(*t, rope, mask, window, kw["alibi_slopes"], kw["scale"], kw["theta"])
+    assert np.allclose(out.detach().numpy(), O, atol=1e-12)
+    out.backward(torch.from_numpy(do))
+    assert np.allclose(t[0].grad.numpy(), dq, atol=1e-12)
+    assert np.allclose(t[1].grad.numpy(), dk, atol=1e-12)
+    assert np.allclose(t[2].grad.numpy(), dv, atol=1e-12)
+
+
+def check_backward_identities(seed=17):
+    q, k, v, do = _tiny(seed, B=1, H=2, Hkv=2, S=9, D=8)
+    kw = dict(rope="neox", mask="causal", alibi_slopes=[0.3, 0.6])
+    dq, dk, dv, inter = oracle.attention_backward(q, k, v, do, return_intermediates=True, **kw)
+    O, _ = oracle.attention_forward(q, k, v, **kw)
+    for h in range(2):
+        dS = inter["dS"][(0, h)]
+        assert np.allclose(dS.sum(axis=1), 0.0, atol=1e-13)          # softmax Jacobian rows
+        assert np.allclose(inter["delta"][(0, h)], (do[0, h] * O[0, h]).sum(axis=1), atol=1e-13)
+    # Causal row 0 only sees key 0 with weight 1: its query gradient is zero.
+    assert np.allclose(dq[:, :, 0], 0.0, atol=1e-14)
+    # The last key is seen only by the last query: dV_{S-1} = sum over heads of P * dO.
+    P_last = [inter["P"][(0, h)][-1, -1] for h in range(2)]
+    assert np.allclose(dv[0, :, -1], np.array([P_last[h] * do[0, h, -1] for h in range(2)]), atol=1e-13)

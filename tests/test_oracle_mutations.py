@@ -1,0 +1,114 @@
+"""Plant plausible mistakes in the oracle (on the CPU) and check that some pin catches each.
+
+This shows the pins in oracle_pins.py are discriminating: a dropped term, a
+wrong sign or index, or a transposed operand anywhere in the oracle fails at
+least one of them.
+"""
+import numpy as np
+import pytest
+
+import oracle
+import oracle.attention as oatt
+import oracle.rope as orope
+import oracle_pins as P
+
+FWD = ("neox", "causal", None, False)
+ALIBI = ("neox", "causal", None, True)
+SW = ("neox", "sliding_window", 3, False)
+
+
+def _fails(checks):
+    for check in checks:
+        try:
+            check()
+        except AssertionError:
+            return True
+    return False
+
+
+def _wrong_sign_rotate(x, positions, theta, kind, inverse=False):
+    return _REAL_ROTATE(x, positions, theta, kind, inverse=not inverse)
+
+
+def _no_inverse_rotate(x, positions, theta, kind, inverse=False):
+    return _REAL_ROTATE(x, positions, theta, kind, inverse=False)
+
+
+_REAL_ROTATE = orope.rope_rotate
+
+
+def _bad_pairs(D, kind):
+    half = D // 2
+    i = np.arange(half)
+    if kind == "neox":                       # reversed partner: (i, D-1-i)
+        return i, D - 1 - i
+    return 2 * i, 2 * i + 1
+
+
+def _bad_freq(D, theta):
+    i = np.arange(D // 2, dtype=np.float64)
+    return np.power(np.float64(theta), -1.0 * i / D)   # dropped factor 2
+
+
+def _bad_kv_head(h, H, Hkv):
+    return h % Hkv                           # interleaved instead of contiguous groups
+
+
+def _bad_alibi(slope, rows, cols):
+    return slope * (np.asarray(rows)[:, None] - np.asarray(cols)[None, :]).astype(np.float64)
+
+
+def _bad_visibility(i, j, mask, window=None):
+    i2 = np.asarray(i)[:, None]
+    j2 = np.asarray(j)[None, :]
+    if mask == "sliding_window":
+        return (j2 <= i2) & (j2 >= i2 - window)   # W + 1 keys
+    return _REAL_VIS(i, j, mask, window)
+
+
+_REAL_VIS = oatt.visibility
+
+
+def _no_scale_defaults(D, scale, alibi_slopes, H):
+    sc, slopes = _REAL_DEFAULTS(D, scale, alibi_slopes, H)
+    return 1.0, slopes
+
+
+_REAL_DEFAULTS = oatt._defaults
+
+
+MUTATIONS = {
+    "rotation_sign": [(oatt, "rope_rotate", _wrong_sign_rotate), (orope, "rope_rotate", _wrong_sign_rotate),
+                      (oracle, "rope_rotate", _wrong_sign_rotate)],
+    "neox_partner": [(orope, "rope_pair_indices", _bad_pairs)],
+    "frequency_exponent": [(orope, "rope_frequencies", _bad_freq), (oracle, "rope_frequencies", _bad_freq)],
+    "gqa_mapping": [(oatt, "kv_head", _bad_kv_head)],
+    "alibi_sign": [(oatt, "alibi_bias", _bad_alibi)],
+    "window_boundary": [(oatt, "visibility", _bad_visibility)],
+    "dropped_scale": [(oatt, "_defaults", _no_scale_defaults)],
+    "gradient_not_unrotated": [(oatt, "rope_rotate", _no_inverse_rotate)],
+}
+
+CHECKS = [
+    P.check_frequencies,
+    lambda: P.check_rope_vs_givens("neox"),
+    lambda: P.check_rope_d2_closed_form("neox"),
+    lambda: P.check_forward_vs_bruteforce(FWD),
+    lambda: P.check_forward_vs_bruteforce(ALIBI),
+    lambda: P.check_forward_vs_bruteforce(SW),
+    lambda: P.check_window_one("neox"),
+    P.check_gqa_repeat_kv,
+    P.check_alibi_special_cases,
+    lambda: P.check_backward_fd(FWD),
+]
+
+
+def test_pins_pass_unmutated():
+    assert not _fails(CHECKS)
+
+
+@pytest.mark.parametrize("name", sorted(MUTATIONS))
+def test_planted_mistake_is_caught(name, monkeypatch):
+    for module, attr, fake in MUTATIONS[name]:
+        monkeypatch.setattr(module, attr, fake)
+    assert _fails(CHECKS), f"no pin caught the planted mistake {name!r}"

@@ -1,0 +1,264 @@
+"""Benchmark of the fused RoPE + causal attention hot path on one MI355X.
+
+Default workload: the Llama-3-8B attention layer (B=1, H=32, H_kv=8, S=8192,
+D=128, bf16, NeoX RoPE theta=500000, causal).  One step = the fused forward
+plus the three-kernel backward on one batch of synthetic N(0,1) inputs that
+are already resident in HBM.  `value` is the algorithmic (causal-effective)
+TFLOP/s of that step: 4*D flops per visible (query, key) pair forward and
+10*D backward.
+
+Alongside, on the same inputs and outside the timed steps:
+* per-call durations from HIP events (fused forward, backward, rotation,
+  separate forward) and the roofline of the fused forward kernel;
+* the separate-RoPE path (rotation kernel, then the forward without RoPE) and
+  the rotation kernel's HBM bandwidth, measured over a buffer pool larger than
+  twice the 256 MB Infinity Cache;
+* with --sweep, the fuse-vs-separate crossover over S = 1024..16384;
+* the fp64 CPU oracle timed on a bounded sample (cpu_baseline).
+
+Prints ONE JSON line.  Only --gpus 1 is supported.
+"""
+import argparse
+import json
+import math
+import os
+import statistics
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2516.6     # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="llama3_8b_b1h32kv8s8192d128")
+    ap.add_argument("--sweep", action="store_true", help="fuse-vs-separate sweep over S")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--seed", type=int, default=0)
+    return ap.parse_args()
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path (--gpus must be 1)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2609_13612_amd import api, inputs
+    from paper_2609_13612_amd.workloads import LLAMA_SWEEP_S, WORKLOADS
+
+    w = WORKLOADS[args.workload]
+    torch.cuda.set_device(0)
+    dev = torch.device("cuda:0")
+    log(f"workload {w.name}: B={w.B} H={w.H} Hkv={w.Hkv} S={w.S} D={w.D} rope={w.rope} mask={w.mask}")
+    cpu = inputs.make_qkv(w.B, w.H, w.Hkv, w.S, w.D, seed=args.seed, with_do=True)
+    q, k, v, do = (cpu[n].to(dev) for n in ("q", "k", "v", "do"))
+    slopes = inputs.alibi_slopes(w.H).to(dev) if w.alibi else None
+    kw = dict(rope=w.rope, theta=w.theta, mask=w.mask, window=w.window or None, alibi_slopes=slopes)
+    o = torch.empty_like(q)
+    lse = torch.empty(w.B, w.H, w.S, device=dev, dtype=torch.float32)
+    dq, dk, dv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
+    ws = torch.empty(api.attnfuse_bwd_workspace_bytes(w.B, w.H, w.S), device=dev, dtype=torch.uint8)
+    do_bwd = w.backward
+
+    def step(ev=None):
+        if ev is not None:
+            ev[0].record()
+        api.attnfuse_fwd(q, k, v, out=o, lse=lse, **kw)
+        if ev is not None:
+            ev[1].record()
+        if do_bwd:
+            api.attnfuse_bwd(q, k, v, o, do, lse, dq=dq, dk=dk, dv=dv, workspace=ws, **kw)
+            if ev is not None:
+                ev[2].record()
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    log(f"warmup done ({args.warmup} steps)")
+
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0.record()
+    for i in range(args.steps):
+        step(evs[i])
+    t1.record()
+    torch.cuda.synchronize()
+    total_ms = t0.elapsed_time(t1)
+    ms_step = total_ms / args.steps
+    fwd_ms = [e[0].elapsed_time(e[1]) for e in evs]
+    bwd_ms = [e[1].elapsed_time(e[2]) for e in evs] if do_bwd else []
+    log(f"timed {args.steps} steps: {ms_step:.3f} ms/step")
+
+    fwd_flops = w.fwd_flops()
+    bwd_flops = w.bwd_flops() if do_bwd else 0
+    step_flops = fwd_flops + bwd_flops
+    value = step_flops / (ms_step * 1e-3) / 1e12
+    fwd_avg = statistics.mean(fwd_ms)
+    fwd_tf = fwd_flops / (fwd_avg * 1e-3) / 1e12
+    result_extra = {
+        "fwd": {"ms_avg": round(fwd_avg, 4), "ms_median": round(statistics.median(fwd_ms), 4),
+                "tflops": round(fwd_tf, 1), "frac_peak": round(fwd_tf / PEAK_BF16_TFLOPS, 4),
+                "flops": fwd_flops},
+    }
+    if do_bwd:
+        bwd_avg = statistics.mean(bwd_ms)
+        bwd_tf = bwd_flops / (bwd_avg * 1e-3) / 1e12
+        result_extra["bwd"] = {"ms_avg": round(bwd_avg, 4), "ms_median": round(statistics.median(bwd_ms), 4),
+                               "tflops": round(bwd_tf, 1), "frac_peak": round(bwd_tf / PEAK_BF16_TFLOPS, 4),
+                               "flops": bwd_flops, "kernels": 3}
+
+    # ---------------------------------------------------------------- separate-RoPE path
+    def time_calls(fn, reps):
+        es = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+        for a, b in es:
+            a.record()
+            fn()
+            b.record()
+        torch.cuda.synchronize()
+        return [a.elapsed_time(b) for a, b in es]
+
+    separate = None
+    rope_bw = None
+    if w.rope != "none":
+        nbytes = w.rope_bytes()
+        npool = max(2, math.ceil(600e6 / nbytes))
+        pool = [(q.clone(), k.clone()) for _ in range(npool)]
+        outs = [(torch.empty_like(q), torch.empty_like(k)) for _ in range(npool)]
+        it = [0]
+
+        def rot():
+            i = it[0] % npool
+            it[0] += 1
+            api.attnfuse_rope(pool[i][0], pool[i][1], rope=w.rope, theta=w.theta, out_q=outs[i][0], out_k=outs[i][1])
+
+        for _ in range(3):
+            rot()
+        rot_ms = time_calls(rot, 4 * npool)
+        rot_avg = statistics.mean(rot_ms)
+        rope_bw = nbytes / (rot_avg * 1e-3) / 1e9
+        qr, kr = outs[0]
+        kw_none = dict(kw, rope="none")
+
+        def sep_fwd():
+            api.attnfuse_fwd(qr, kr, v, out=o, lse=lse, **kw_none)
+
+        sep_ms = time_calls(sep_fwd, max(10, args.steps))
+        sep_avg = statistics.mean(sep_ms)
+        separate = {"rope_ms_avg": round(rot_avg, 4), "fwd_norope_ms_avg": round(sep_avg, 4),
+                    "total_ms": round(rot_avg + sep_avg, 4),
+                    "fused_speedup": round((rot_avg + sep_avg) / fwd_avg, 4),
+                    "rope_bytes": nbytes, "rope_gbs": round(rope_bw, 1),
+                    "rope_frac_hbm_peak": round(rope_bw / PEAK_HBM_GBS, 4), "rope_buffer_pool": npool}
+        del pool, outs
+        log(f"separate path: rope {rot_avg:.4f} ms ({rope_bw:.0f} GB/s) + fwd {sep_avg:.4f} ms")
+
+    sweep = None
+    if args.sweep and w.rope != "none":
+        sweep = []
+        for S in LLAMA_SWEEP_S:
+            c = inputs.make_qkv(w.B, w.H, w.Hkv, S, w.D, seed=args.seed)
+            qs, ks, vs = (c[n].to(dev) for n in ("q", "k", "v"))
+            os_ = torch.empty_like(qs)
+            ls = torch.empty(w.B, w.H, S, device=dev, dtype=torch.float32)
+            nb = w.rope_bytes(S)
+            npool = max(2, math.ceil(600e6 / nb))
+            pq = [(qs.clone(), ks.clone()) for _ in range(npool)]
+            po = [(torch.empty_like(qs), torch.empty_like(ks)) for _ in range(npool)]
+            cnt = [0]
+
+            def rot_s():
+                i = cnt[0] % npool
+                cnt[0] += 1
+                api.attnfuse_rope(pq[i][0], pq[i][1], rope=w.rope, theta=w.theta, out_q=po[i][0], out_k=po[i][1])
+
+            def fused_s():
+                api.attnfuse_fwd(qs, ks, vs, out=os_, lse=ls, **kw)
+
+            def none_s():
+                api.attnfuse_fwd(po[0][0], po[0][1], vs, out=os_, lse=ls, **dict(kw, rope="none"))
+
+            for fn in (rot_s, fused_s, none_s):
+                fn()
+            reps = 20
+            r_ms = statistics.mean(time_calls(rot_s, max(reps, 2 * npool)))
+            f_ms = statistics.mean(time_calls(fused_s, reps))
+            n_ms = statistics.mean(time_calls(none_s, reps))
+            sweep.append({"S": S, "fused_ms": round(f_ms, 4), "rope_ms": round(r_ms, 4), "norope_ms": round(n_ms, 4),
+                          "fused_speedup": round((r_ms + n_ms) / f_ms, 4),
+                          "fused_tflops": round(w.fwd_flops(S) / (f_ms * 1e-3) / 1e12, 1)})
+            log(f"sweep S={S}: fused {f_ms:.4f} ms, rope {r_ms:.4f} + norope {n_ms:.4f} ms")
+            del pq, po, qs, ks, vs, os_, ls
+        torch.cuda.empty_cache()
+
+    # ---------------------------------------------------------------- CPU oracle baseline
+    cpu_baseline = None
+    if not args.no_cpu_baseline:
+        import numpy as np
+        import oracle
+        G = w.H // w.Hkv
+        f = inputs.to_f64
+        sl = slice(0, G)
+        okw = dict(rope=w.rope, theta=w.theta, mask=w.mask, window=w.window or None,
+                   alibi_slopes=None if slopes is None else f(slopes.cpu())[sl])
+        qs, ks, vs, dos = f(cpu["q"][:1, sl]), f(cpu["k"][:1, :1]), f(cpu["v"][:1, :1]), f(cpu["do"][:1, sl])
+        ta = time.perf_counter()
+        oracle.attention_forward(qs, ks, vs, **okw)
+        if do_bwd:
+            oracle.attention_backward(qs, ks, vs, dos, **okw)
+        tb = time.perf_counter()
+        frac = G / (w.B * w.H)
+        sample_flops = (fwd_flops + bwd_flops) * frac
+        cores = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+        cpu_baseline = {"value": round(sample_flops / (tb - ta) / 1e12, 6), "unit": "TFLOP/s", "cores": cores,
+                        "kind": "oracle", "seconds": round(tb - ta, 2),
+                        "sample": f"batch 0, query heads 0..{G - 1} with K/V head 0 ({G} of {w.B * w.H} heads), "
+                                  f"{'forward + backward' if do_bwd else 'forward'}, fp64 numpy, full S={w.S}"}
+        log(f"cpu oracle sample: {tb - ta:.1f} s")
+
+    roofline = {"bound": "mfma", "kernel": "fwd_bf16_kernel (fused RoPE + mask, one launch per forward)",
+                "achieved": round(fwd_tf, 1), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(fwd_tf / PEAK_BF16_TFLOPS, 4), "traffic": None}
+
+    line = {
+        "metric": "fused RoPE+causal attention TFLOP/s (fwd, bwd) and % of bf16 MFMA peak",
+        "value": round(value, 1),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": w.name, "B": w.B, "H": w.H, "H_kv": w.Hkv, "S": w.S, "D": w.D, "rope": w.rope,
+                   "rope_theta": w.theta, "mask": w.mask, "window": w.window, "alibi": w.alibi,
+                   "step": "fused fwd + bwd" if do_bwd else "fused fwd", "seed": args.seed},
+        "frac_peak": round(value / PEAK_BF16_TFLOPS, 4),
+        "roofline": roofline,
+        "cpu_baseline": cpu_baseline,
+        **result_extra,
+        "separate_rope": separate,
+    }
+    if sweep is not None:
+        line["crossover_sweep"] = sweep
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

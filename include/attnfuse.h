@@ -1,0 +1,143 @@
+/*
+ * attnfuse.h -- C ABI of the MI355X (gfx950) fused RoPE + masked attention library.
+ *
+ * The method is AttnFuse (arXiv 2609.13612): attention whose query/key rotation
+ * (RoPE, a pre-matmul transform) and score modifications (causal mask, sliding
+ * window, ALiBi bias; post-matmul) run inside one online-softmax pass.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * Layout.   Q, O, dO, dQ are [B, H, S, D]; K, V, dK, dV are [B, H_kv, S, D];
+ *           LSE is [B, H, S]; all row-major and contiguous.  bf16 tensors hold
+ *           IEEE bfloat16 bit patterns (2 bytes), fp32 tensors IEEE binary32.
+ * Pointers. Every tensor pointer is a DEVICE pointer on the current HIP device,
+ *           16-byte aligned.  ALiBi slopes are a device fp32 array [H].
+ * Heads.    Query head h reads K/V head h / (H / H_kv) (grouped-query
+ *           attention with contiguous groups); H must be a multiple of H_kv.
+ * Positions 0..S-1 for queries and keys alike (self-attention, S_q = S_k = S).
+ * Ownership The caller owns every buffer; nothing is retained after a call.
+ *           The library itself keeps one read-only device table per
+ *           (device, D, rope_theta): cos/sin of position * omega_i, fp32,
+ *           built with one hipMalloc and one stream synchronisation the first
+ *           time a RoPE call needs more rows than the table holds (so make that
+ *           first call outside HIP graph capture).
+ * Streams.  All work is enqueued on `stream` (a hipStream_t; NULL = default
+ *           stream) and runs asynchronously; no call synchronises otherwise.
+ * Errors.   Arguments are validated before any HIP call; no C++ exception
+ *           crosses the ABI.  Return codes:
+ *             AF_OK               success (work enqueued)
+ *             AF_ERR_INVALID_ARG  bad pointer, size, enum or scalar
+ *             AF_ERR_UNSUPPORTED  valid request with no compiled kernel
+ *                                 (e.g. D not in {64, 128}, fp32 backward)
+ *             AF_ERR_HIP          a HIP runtime call or kernel launch failed
+ *           attnfuse_strerror() maps a code to text.
+ */
+#ifndef ATTNFUSE_H
+#define ATTNFUSE_H
+
+#include <stddef.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Element type of Q, K, V, O, dO, dQ, dK, dV.  fp32 is the debug path: same
+ * method, fp32 arithmetic throughout, no MFMA (forward and rotation only). */
+enum { AF_DTYPE_BF16 = 0, AF_DTYPE_FP32 = 1 };
+
+/* RoPE pairing (Section 4.1 "Fused RoPE": the paper's NeoX convention pairs
+ * dimension i with i + D/2; interleaved pairs 2i with 2i+1).  Pair i rotates by
+ * position * omega_i, omega_i = rope_theta^(-2i/D); the second element of a
+ * pair gets +sin:  x_a' = x_a cos - x_b sin,  x_b' = x_a sin + x_b cos. */
+enum { AF_ROPE_NONE = 0, AF_ROPE_NEOX = 1, AF_ROPE_INTERLEAVED = 2 };
+
+/* Mask (Section 3.1 combinators full / causal / sliding_window).  Query i sees
+ * key j when: NONE always; CAUSAL j <= i; SLIDING_WINDOW i - window < j <= i
+ * (window keys, the diagonal included). */
+enum { AF_MASK_NONE = 0, AF_MASK_CAUSAL = 1, AF_MASK_SLIDING_WINDOW = 2 };
+
+enum { AF_OK = 0, AF_ERR_INVALID_ARG = -1, AF_ERR_UNSUPPORTED = -2, AF_ERR_HIP = -3 };
+
+/*
+ * Fused forward (Section 2 online softmax; Section 4.1 fused RoPE; Section 3.1
+ * score modifications; Section 4.4 saved row statistic).  Computes
+ *     s_ij  = softmax_scale * <R_i q_i, R_j k_j> - slope_h * (i - j)
+ *     O_i   = sum_j softmax_j(s_ij over visible j) v_j
+ *     LSE_i = ln sum_{visible j} exp(s_ij)
+ * where R_p is the RoPE rotation at position p (identity for AF_ROPE_NONE)
+ * and the slope term is present only when alibi_slopes != NULL.
+ *
+ *   Q [B,H,S,D], K/V [B,H_kv,S,D]   inputs (dtype)
+ *   O [B,H,S,D]                     output (dtype); must not alias an input
+ *   LSE [B,H,S] fp32                output, natural log; a row with no visible
+ *                                   key gets O = 0, LSE = -inf
+ *   B, H, H_kv, S >= 1; H % H_kv == 0; D in {64, 128} (others: UNSUPPORTED)
+ *   dtype       AF_DTYPE_*
+ *   rope        AF_ROPE_*; rope_theta > 0 and finite when rope != NONE
+ *   mask        AF_MASK_*; window >= 1 when SLIDING_WINDOW (ignored otherwise)
+ *   alibi_slopes  device fp32 [H] or NULL
+ *   softmax_scale finite, > 0 (typically 1/sqrt(D))
+ */
+int attnfuse_fwd(const void* Q, const void* K, const void* V, void* O, float* LSE,
+                 int B, int H, int H_kv, int S, int D, int dtype,
+                 int rope, float rope_theta, int mask, int window,
+                 const float* alibi_slopes, float softmax_scale, void* stream);
+
+/* Bytes of device workspace attnfuse_bwd needs: two fp32 values per query row
+ * (delta_i = rowsum(dO_i * O_i) and LSE_i in log2 units), i.e. 8*B*H*S. */
+size_t attnfuse_bwd_workspace_bytes(int B, int H, int S);
+
+/*
+ * Backward of attnfuse_fwd (Section 4.4: three kernels, no atomics -- a
+ * row-statistic pass, a dK/dV pass over query tiles and a dQ pass over key
+ * tiles; probabilities are re-derived from the saved LSE).  With RoPE the
+ * rotated operands are recomputed in both passes and the gradients leave
+ * through the inverse rotation: dQ = R^T dQ', dK = R^T dK'.  For grouped-query
+ * attention dK and dV sum over the H/H_kv query heads of their group.
+ *
+ *   Q, K, V, O, dO, LSE  as produced/consumed by attnfuse_fwd with the same
+ *                        variant arguments (LSE must be the forward's)
+ *   dQ [B,H,S,D], dK/dV [B,H_kv,S,D]  outputs (dtype), fully overwritten; must
+ *                        not alias inputs
+ *   workspace            device memory of >= attnfuse_bwd_workspace_bytes()
+ *                        bytes (16-byte aligned), caller-owned scratch
+ *   other arguments      as attnfuse_fwd.  Only AF_DTYPE_BF16 is compiled.
+ */
+int attnfuse_bwd(const void* Q, const void* K, const void* V, const void* O, const void* dO,
+                 const float* LSE, void* dQ, void* dK, void* dV,
+                 void* workspace, size_t workspace_bytes,
+                 int B, int H, int H_kv, int S, int D, int dtype,
+                 int rope, float rope_theta, int mask, int window,
+                 const float* alibi_slopes, float softmax_scale, void* stream);
+
+/*
+ * Standalone rotation, the separate-RoPE path (Section 5.3 "The Rotation
+ * Calculus": pre-rotation reads Q and K and writes Q' and K' once, an HBM round
+ * trip, before an attention that has no RoPE).  One bandwidth-bound launch
+ * rotates both tensors:  Qr = R Q,  Kr = R K  (positions 0..S-1).
+ *
+ *   Q [B,H,S,D] -> Qr;  K [B,H_kv,S,D] -> Kr  (dtype).  In-place is allowed
+ *   (Qr == Q, Kr == K).  K and Kr may both be NULL to rotate Q alone (H_kv is
+ *   then ignored).  rope must be NEOX or INTERLEAVED.  D in {64, 128}.
+ */
+int attnfuse_rope(const void* Q, const void* K, void* Qr, void* Kr,
+                  int B, int H, int H_kv, int S, int D, int dtype,
+                  int rope, float rope_theta, void* stream);
+
+/* Inverse rotation (the separate path's backward): dQ = R^T dQr, dK = R^T dKr.
+ * Same arguments and rules as attnfuse_rope. */
+int attnfuse_rope_bwd(const void* dQr, const void* dKr, void* dQ, void* dK,
+                      int B, int H, int H_kv, int S, int D, int dtype,
+                      int rope, float rope_theta, void* stream);
+
+/* Static text for a return code (never NULL). */
+const char* attnfuse_strerror(int code);
+
+/* ABI version; bumped on any incompatible change. */
+int attnfuse_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ATTNFUSE_H */

@@ -1,0 +1,135 @@
+"""Python binding of the C ABI in include/attnfuse.h -- argument marshalling only.
+
+Each function takes torch tensors that already live on the GPU, checks their
+shape/dtype/contiguity against the call, passes raw device pointers and the
+current torch stream to the library, and raises AttnFuseError on a non-zero
+return code.  Every step of the computation runs in the HIP kernels.
+"""
+import math
+
+import torch
+
+from . import _lib
+
+DTYPE = {torch.bfloat16: 0, torch.float32: 1}
+ROPE = {"none": 0, "neox": 1, "interleaved": 2}
+MASK = {"none": 0, "causal": 1, "sliding_window": 2}
+
+
+class AttnFuseError(RuntimeError):
+    def __init__(self, code, where):
+        msg = _lib.load().attnfuse_strerror(code).decode()
+        super().__init__(f"{where}: {msg} (code {code})")
+        self.code = code
+
+
+def _check(code, where):
+    if code != 0:
+        raise AttnFuseError(code, where)
+
+
+def _ptr(t):
+    return None if t is None else t.data_ptr()
+
+
+def _stream():
+    return torch.cuda.current_stream().cuda_stream
+
+
+def _shape(q, k):
+    if q.dim() != 4 or k.dim() != 4:
+        raise ValueError("q must be [B, H, S, D] and k/v [B, H_kv, S, D]")
+    B, H, S, D = q.shape
+    if k.shape[0] != B or k.shape[2] != S or k.shape[3] != D:
+        raise ValueError("k/v must be [B, H_kv, S, D] matching q")
+    return B, H, k.shape[1], S, D
+
+
+def _same(ref, *ts):
+    for t in ts:
+        if t is None:
+            continue
+        if not t.is_cuda or t.dtype != ref.dtype or not t.is_contiguous():
+            raise ValueError("tensors must be contiguous, on the GPU, and share one dtype")
+
+
+def _variant(rope, theta, mask, window, alibi_slopes, scale, D):
+    if scale is None:
+        scale = 1.0 / math.sqrt(D)
+    if alibi_slopes is not None and (alibi_slopes.dtype != torch.float32 or not alibi_slopes.is_cuda):
+        raise ValueError("alibi_slopes must be an fp32 GPU tensor [H]")
+    return ROPE[rope], float(theta), MASK[mask], int(window or 0), scale
+
+
+def attnfuse_fwd(q, k, v, *, rope="none", theta=10000.0, mask="causal", window=None,
+                 alibi_slopes=None, scale=None, out=None, lse=None):
+    """O, LSE = attention(q, k, v); see attnfuse_fwd in include/attnfuse.h."""
+    B, H, Hkv, S, D = _shape(q, k)
+    _same(q, k, v, out)
+    if v.shape != k.shape:
+        raise ValueError("v must have k's shape")
+    out = torch.empty_like(q) if out is None else out
+    lse = torch.empty(B, H, S, device=q.device, dtype=torch.float32) if lse is None else lse
+    r, th, m, w, sc = _variant(rope, theta, mask, window, alibi_slopes, scale, D)
+    code = _lib.load().attnfuse_fwd(_ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(lse), B, H, Hkv, S, D,
+                                    DTYPE[q.dtype], r, th, m, w, _ptr(alibi_slopes), sc, _stream())
+    _check(code, "attnfuse_fwd")
+    return out, lse
+
+
+def attnfuse_bwd_workspace_bytes(B, H, S):
+    return _lib.load().attnfuse_bwd_workspace_bytes(B, H, S)
+
+
+def attnfuse_bwd(q, k, v, o, do, lse, *, rope="none", theta=10000.0, mask="causal", window=None,
+                 alibi_slopes=None, scale=None, dq=None, dk=None, dv=None, workspace=None):
+    """dQ, dK, dV of attnfuse_fwd; see attnfuse_bwd in include/attnfuse.h."""
+    B, H, Hkv, S, D = _shape(q, k)
+    _same(q, k, v, o, do, dq, dk, dv)
+    dq = torch.empty_like(q) if dq is None else dq
+    dk = torch.empty_like(k) if dk is None else dk
+    dv = torch.empty_like(v) if dv is None else dv
+    nbytes = attnfuse_bwd_workspace_bytes(B, H, S)
+    if workspace is None:
+        workspace = torch.empty(nbytes, device=q.device, dtype=torch.uint8)
+    r, th, m, w, sc = _variant(rope, theta, mask, window, alibi_slopes, scale, D)
+    code = _lib.load().attnfuse_bwd(_ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(do), _ptr(lse),
+                                    _ptr(dq), _ptr(dk), _ptr(dv), _ptr(workspace), workspace.numel(),
+                                    B, H, Hkv, S, D, DTYPE[q.dtype], r, th, m, w,
+                                    _ptr(alibi_slopes), sc, _stream())
+    _check(code, "attnfuse_bwd")
+    return dq, dk, dv
+
+
+def _rope_call(name, x0, x1, y0, y1, rope, theta):
+    if x1 is not None:
+        B, H, Hkv, S, D = _shape(x0, x1)
+    else:
+        B, H, S, D = x0.shape
+        Hkv = 1
+    _same(x0, x1, y0, y1)
+    y0 = torch.empty_like(x0) if y0 is None else y0
+    if x1 is not None and y1 is None:
+        y1 = torch.empty_like(x1)
+    code = getattr(_lib.load(), name)(_ptr(x0), _ptr(x1), _ptr(y0), _ptr(y1), B, H, Hkv, S, D,
+                                      DTYPE[x0.dtype], ROPE[rope], float(theta), _stream())
+    _check(code, name)
+    return y0, y1
+
+
+def attnfuse_rope(q, k=None, *, rope="neox", theta=10000.0, out_q=None, out_k=None):
+    """Qr, Kr = R q, R k (separate pre-rotation); see attnfuse_rope."""
+    return _rope_call("attnfuse_rope", q, k, out_q, out_k, rope, theta)
+
+
+def attnfuse_rope_bwd(dqr, dkr=None, *, rope="neox", theta=10000.0, out_q=None, out_k=None):
+    """dQ, dK = R^T dQr, R^T dKr; see attnfuse_rope_bwd."""
+    return _rope_call("attnfuse_rope_bwd", dqr, dkr, out_q, out_k, rope, theta)
+
+
+def attnfuse_strerror(code):
+    return _lib.load().attnfuse_strerror(code).decode()
+
+
+def attnfuse_version():
+    return _lib.load().attnfuse_version()

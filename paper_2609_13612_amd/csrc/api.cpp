@@ -1,0 +1,200 @@
+// C-ABI entry points (declared in include/attnfuse.h): argument validation,
+// the per-device cos/sin table cache, and dispatch to the kernel launchers.
+// Every argument is checked before the first HIP call; no exception leaves
+// this file.
+#include "attnfuse.h"
+
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdint>
+#include <cstring>
+#include <mutex>
+#include <vector>
+
+#include "launch.hpp"
+
+namespace {
+
+constexpr int kMaxS = 1 << 20;
+constexpr int kAbiVersion = 1;
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+int map_launch(int rc) {
+  if (rc == 0) return AF_OK;
+  if (rc == -2) return AF_ERR_UNSUPPORTED;
+  return AF_ERR_HIP;
+}
+
+// ---------------------------------------------------------------- cos/sin table cache
+struct RopeTable {
+  int device;
+  int D;
+  uint32_t theta_bits;
+  int rows;
+  float2* ptr;
+};
+std::mutex g_table_mu;
+std::vector<RopeTable> g_tables;   // never freed: kernels on any stream may still read them
+
+int rope_table(int D, float theta, int S, hipStream_t stream, const float2** out) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return AF_ERR_HIP;
+  uint32_t bits;
+  std::memcpy(&bits, &theta, sizeof bits);
+  std::lock_guard<std::mutex> lock(g_table_mu);
+  for (const RopeTable& t : g_tables) {
+    if (t.device == dev && t.D == D && t.theta_bits == bits && t.rows >= S) {
+      *out = t.ptr;
+      return AF_OK;
+    }
+  }
+  int rows = 4096;
+  while (rows < S) rows *= 2;
+  float2* ptr = nullptr;
+  if (hipMalloc(&ptr, (size_t)rows * (D / 2) * sizeof(float2)) != hipSuccess) return AF_ERR_HIP;
+  if (af::launch_rope_table(ptr, rows, D, (double)theta, stream) != 0 || hipStreamSynchronize(stream) != hipSuccess) {
+    (void)hipFree(ptr);
+    return AF_ERR_HIP;
+  }
+  g_tables.push_back({dev, D, bits, rows, ptr});
+  *out = ptr;
+  return AF_OK;
+}
+
+// ---------------------------------------------------------------- validation
+int check_common(int B, int H, int H_kv, int S, int D, int dtype, int rope, float rope_theta) {
+  if (B < 1 || H < 1 || H_kv < 1 || S < 1 || S > kMaxS || D < 2 || (D & 1)) return AF_ERR_INVALID_ARG;
+  if (H % H_kv != 0) return AF_ERR_INVALID_ARG;
+  if (dtype != AF_DTYPE_BF16 && dtype != AF_DTYPE_FP32) return AF_ERR_INVALID_ARG;
+  if (rope != AF_ROPE_NONE && rope != AF_ROPE_NEOX && rope != AF_ROPE_INTERLEAVED) return AF_ERR_INVALID_ARG;
+  if (rope != AF_ROPE_NONE && !(std::isfinite(rope_theta) && rope_theta > 0.f)) return AF_ERR_INVALID_ARG;
+  // grid sizes and element offsets must stay inside their integer types
+  if ((long long)B * H * ((S + 63) / 64) >= (1LL << 31)) return AF_ERR_INVALID_ARG;
+  return AF_OK;
+}
+
+int check_attn(int mask, int window, float scale) {
+  if (mask != AF_MASK_NONE && mask != AF_MASK_CAUSAL && mask != AF_MASK_SLIDING_WINDOW) return AF_ERR_INVALID_ARG;
+  if (mask == AF_MASK_SLIDING_WINDOW && window < 1) return AF_ERR_INVALID_ARG;
+  if (!(std::isfinite(scale) && scale > 0.f)) return AF_ERR_INVALID_ARG;
+  return AF_OK;
+}
+
+bool supported_d(int D) { return D == 64 || D == 128; }
+
+}  // namespace
+
+extern "C" {
+
+int attnfuse_version(void) { return kAbiVersion; }
+
+const char* attnfuse_strerror(int code) {
+  switch (code) {
+    case AF_OK: return "success";
+    case AF_ERR_INVALID_ARG: return "invalid argument";
+    case AF_ERR_UNSUPPORTED: return "unsupported variant (no compiled kernel)";
+    case AF_ERR_HIP: return "HIP runtime error";
+  }
+  return "unknown error code";
+}
+
+int attnfuse_fwd(const void* Q, const void* K, const void* V, void* O, float* LSE,
+                 int B, int H, int H_kv, int S, int D, int dtype,
+                 int rope, float rope_theta, int mask, int window,
+                 const float* alibi_slopes, float softmax_scale, void* stream) {
+  if (!Q || !K || !V || !O || !LSE) return AF_ERR_INVALID_ARG;
+  if (!aligned16(Q) || !aligned16(K) || !aligned16(V) || !aligned16(O) || !aligned16(LSE)) return AF_ERR_INVALID_ARG;
+  if (O == Q || O == K || O == V || (const void*)LSE == Q || (const void*)LSE == K || (const void*)LSE == V)
+    return AF_ERR_INVALID_ARG;
+  int rc = check_common(B, H, H_kv, S, D, dtype, rope, rope_theta);
+  if (rc != AF_OK) return rc;
+  if ((rc = check_attn(mask, window, softmax_scale)) != AF_OK) return rc;
+  if (!supported_d(D)) return AF_ERR_UNSUPPORTED;
+
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  af::FwdParams p{};
+  p.q = Q; p.k = K; p.v = V; p.o = O; p.lse = LSE;
+  p.B = B; p.H = H; p.Hkv = H_kv; p.S = S;
+  // a window of S or more keys is the causal mask; clamping keeps n + window in int range
+  p.window = (mask == AF_MASK_SLIDING_WINDOW) ? (window < S ? window : S) : 0;
+  p.slopes = alibi_slopes;
+  p.scale = softmax_scale;
+  p.table = nullptr;
+  if (rope != AF_ROPE_NONE && (rc = rope_table(D, rope_theta, S, st, &p.table)) != AF_OK) return rc;
+  const bool alibi = alibi_slopes != nullptr;
+  if (dtype == AF_DTYPE_BF16) return map_launch(af::launch_fwd_bf16(D, rope, mask, alibi, p, st));
+  return map_launch(af::launch_fwd_fp32(D, rope, mask, alibi, p, st));
+}
+
+size_t attnfuse_bwd_workspace_bytes(int B, int H, int S) {
+  if (B < 1 || H < 1 || S < 1) return 0;
+  return (size_t)2 * sizeof(float) * (size_t)B * (size_t)H * (size_t)S;
+}
+
+int attnfuse_bwd(const void* Q, const void* K, const void* V, const void* O, const void* dO,
+                 const float* LSE, void* dQ, void* dK, void* dV,
+                 void* workspace, size_t workspace_bytes,
+                 int B, int H, int H_kv, int S, int D, int dtype,
+                 int rope, float rope_theta, int mask, int window,
+                 const float* alibi_slopes, float softmax_scale, void* stream) {
+  const void* ins[] = {Q, K, V, O, dO, LSE};
+  void* outs[] = {dQ, dK, dV, workspace};
+  for (const void* x : ins) if (!x || !aligned16(x)) return AF_ERR_INVALID_ARG;
+  for (const void* x : outs) if (!x || !aligned16(x)) return AF_ERR_INVALID_ARG;
+  for (const void* x : outs)
+    for (const void* y : ins) if (x == y) return AF_ERR_INVALID_ARG;
+  int rc = check_common(B, H, H_kv, S, D, dtype, rope, rope_theta);
+  if (rc != AF_OK) return rc;
+  if ((rc = check_attn(mask, window, softmax_scale)) != AF_OK) return rc;
+  if (workspace_bytes < attnfuse_bwd_workspace_bytes(B, H, S)) return AF_ERR_INVALID_ARG;
+  if (!supported_d(D) || dtype != AF_DTYPE_BF16) return AF_ERR_UNSUPPORTED;
+
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  af::BwdParams p{};
+  p.q = Q; p.k = K; p.v = V; p.o = O; p.dout = dO; p.lse = LSE;
+  p.dq = dQ; p.dk = dK; p.dv = dV;
+  const size_t rows = (size_t)B * H * S;
+  p.delta = static_cast<float*>(workspace);
+  p.lse2 = static_cast<float*>(workspace) + rows;
+  p.B = B; p.H = H; p.Hkv = H_kv; p.S = S;
+  // a window of S or more keys is the causal mask; clamping keeps n + window in int range
+  p.window = (mask == AF_MASK_SLIDING_WINDOW) ? (window < S ? window : S) : 0;
+  p.slopes = alibi_slopes;
+  p.scale = softmax_scale;
+  p.table = nullptr;
+  if (rope != AF_ROPE_NONE && (rc = rope_table(D, rope_theta, S, st, &p.table)) != AF_OK) return rc;
+  return map_launch(af::launch_bwd_bf16(D, rope, mask, alibi_slopes != nullptr, p, st));
+}
+
+static int rope_common(const void* X0, const void* X1, void* Y0, void* Y1, int B, int H, int H_kv, int S, int D,
+                       int dtype, int rope, float rope_theta, void* stream, bool inverse) {
+  if (!X0 || !Y0 || !aligned16(X0) || !aligned16(Y0)) return AF_ERR_INVALID_ARG;
+  if ((X1 == nullptr) != (Y1 == nullptr)) return AF_ERR_INVALID_ARG;
+  if (X1 && (!aligned16(X1) || !aligned16(Y1))) return AF_ERR_INVALID_ARG;
+  if (!X1) H_kv = 1;
+  int rc = check_common(B, H, H_kv, S, D, dtype, rope, rope_theta);
+  if (rc != AF_OK) return rc;
+  if (rope == AF_ROPE_NONE) return AF_ERR_INVALID_ARG;
+  if (!supported_d(D)) return AF_ERR_UNSUPPORTED;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  af::RopeParams p{};
+  p.x0 = X0; p.y0 = Y0; p.heads0 = H;
+  p.x1 = X1; p.y1 = Y1; p.heads1 = X1 ? H_kv : 0;
+  p.B = B; p.S = S;
+  if ((rc = rope_table(D, rope_theta, S, st, &p.table)) != AF_OK) return rc;
+  return map_launch(af::launch_rope(dtype == AF_DTYPE_FP32, D, rope, inverse, p, st));
+}
+
+int attnfuse_rope(const void* Q, const void* K, void* Qr, void* Kr, int B, int H, int H_kv, int S, int D,
+                  int dtype, int rope, float rope_theta, void* stream) {
+  return rope_common(Q, K, Qr, Kr, B, H, H_kv, S, D, dtype, rope, rope_theta, stream, false);
+}
+
+int attnfuse_rope_bwd(const void* dQr, const void* dKr, void* dQ, void* dK, int B, int H, int H_kv, int S, int D,
+                      int dtype, int rope, float rope_theta, void* stream) {
+  return rope_common(dQr, dKr, dQ, dK, B, H, H_kv, S, D, dtype, rope, rope_theta, stream, true);
+}
+
+}  // extern "C"

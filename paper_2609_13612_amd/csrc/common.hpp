@@ -1,0 +1,152 @@
+// Device helpers shared by the gfx950 kernels: vector types, bf16 packing,
+// the 32x32x16 bf16 MFMA, wave-level lane swaps, and the RoPE pair rotation.
+//
+// MFMA register layout used throughout (v_mfma_f32_32x32x16_bf16, wave64):
+//   * A operand (32 x 16): lane l supplies row (l % 32) and 8 k-values;
+//   * B operand (16 x 32): lane l supplies column (l % 32) and 8 k-values;
+//     the lane group g = l / 32 selects which 8 of the 16 k-values, and A and B
+//     use the same (g, element) -> k assignment, so a contraction only needs
+//     both operands to list their k-values in the same order;
+//   * C/D (32 x 32, 16 floats per lane): element r of lane l is
+//     row 8*(r/4) + 4*(l/32) + (r%4), column l % 32.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace af {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+
+enum RopeKind { ROPE_NONE = 0, ROPE_NEOX = 1, ROPE_INTERLEAVED = 2 };
+enum MaskKind { MASK_NONE = 0, MASK_CAUSAL = 1, MASK_SLIDING_WINDOW = 2 };
+
+// ---------------------------------------------------------------- bf16 <-> fp32
+__device__ __forceinline__ float bf_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+
+// Round two floats to bf16 (nearest even) and pack: a in the low half.
+__device__ __forceinline__ uint32_t pack_bf16(float a, float b) {
+  f32x2 v = {a, b};
+  bf16x2 r = __builtin_convertvector(v, bf16x2);
+  return __builtin_bit_cast(uint32_t, r);
+}
+
+// Round two floats to fp16 (nearest even) and pack: a in the low half.
+__device__ __forceinline__ uint32_t pack_f16(float a, float b) {
+  f32x2 v = {a, b};
+  f16x2 r = __builtin_convertvector(v, f16x2);
+  return __builtin_bit_cast(uint32_t, r);
+}
+
+// Pack in the MFMA operand type: fp16 when F16, else bf16.
+template <bool F16>
+__device__ __forceinline__ uint32_t pack_op(float a, float b) {
+  if constexpr (F16) return pack_f16(a, b);
+  else return pack_bf16(a, b);
+}
+
+// ---------------------------------------------------------------- MFMA
+// 32x32x16 MFMA with fp32 accumulation on bf16 (F16 = false) or fp16 operands.
+template <bool F16 = false>
+__device__ __forceinline__ f32x16 mfma32(u32x4 a, u32x4 b, f32x16 c) {
+  if constexpr (F16)
+    return __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8, a), __builtin_bit_cast(f16x8, b), c, 0, 0, 0);
+  else
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
+}
+
+// Reductions over the lane pair (l, l ^ 32).  v_permlane32_swap exchanges the
+// upper half of its first operand with the lower half of its second; with the
+// same value in both, each lane ends up holding its own value in one result
+// and its partner's in the other, so combining the two results reduces the pair.
+__device__ __forceinline__ float pair_max(float x) {
+  auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float pair_sum(float x) {
+  auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// ---------------------------------------------------------------- RoPE
+// One pair (x_a, x_b) rotated by the angle whose cosine and sine are (c, s):
+//   forward:  x_a' = x_a c - x_b s,   x_b' = x_a s + x_b c
+//   inverse:  x_a' = x_a c + x_b s,   x_b' = -x_a s + x_b c   (rotation by -angle)
+// Every kernel rotates through this one function (fp32 arithmetic from an
+// fp32 cos/sin table); only the final rounding differs by destination.
+template <bool INVERSE>
+__device__ __forceinline__ void rotate_pair(float& xa, float& xb, float c, float s) {
+  const float a = xa, b = xb;
+  if (!INVERSE) {
+    xa = __builtin_fmaf(a, c, -(b * s));
+    xb = __builtin_fmaf(a, s, b * c);
+  } else {
+    xa = __builtin_fmaf(a, c, b * s);
+    xb = __builtin_fmaf(-a, s, b * c);
+  }
+}
+
+// NeoX: 8 consecutive pair indices i0..i0+7 whose first elements are the 8 bf16
+// of `a` and whose partners (half a head away) are the 8 bf16 of `b`.
+// cs points at the table entries (cos, sin) of those 8 pairs for one position.
+// The rotated values are rounded to fp16 when F16OUT (the attention kernels'
+// rotated MFMA operands), else back to bf16 (the rotation kernel's tensors).
+template <bool INVERSE, bool F16OUT = false>
+__device__ __forceinline__ void rotate_neox8(u32x4& a, u32x4& b, const float2* __restrict__ cs) {
+  const float4* t = reinterpret_cast<const float4*>(cs);
+  float4 t0 = t[0], t1 = t[1], t2 = t[2], t3 = t[3];
+  float c[8] = {t0.x, t0.z, t1.x, t1.z, t2.x, t2.z, t3.x, t3.z};
+  float s[8] = {t0.y, t0.w, t1.y, t1.w, t2.y, t2.w, t3.y, t3.w};
+#pragma unroll
+  for (int w = 0; w < 4; ++w) {
+    float a0 = bf_lo(a[w]), a1 = bf_hi(a[w]);
+    float b0 = bf_lo(b[w]), b1 = bf_hi(b[w]);
+    rotate_pair<INVERSE>(a0, b0, c[2 * w], s[2 * w]);
+    rotate_pair<INVERSE>(a1, b1, c[2 * w + 1], s[2 * w + 1]);
+    a[w] = pack_op<F16OUT>(a0, a1);
+    b[w] = pack_op<F16OUT>(b0, b1);
+  }
+}
+
+// Interleaved: the 8 bf16 of `x` are 4 pairs (2i, 2i+1), i = i0..i0+3.
+template <bool INVERSE, bool F16OUT = false>
+__device__ __forceinline__ void rotate_interleaved8(u32x4& x, const float2* __restrict__ cs) {
+  const float4* t = reinterpret_cast<const float4*>(cs);
+  float4 t0 = t[0], t1 = t[1];
+  float c[4] = {t0.x, t0.z, t1.x, t1.z};
+  float s[4] = {t0.y, t0.w, t1.y, t1.w};
+#pragma unroll
+  for (int w = 0; w < 4; ++w) {
+    float a = bf_lo(x[w]), b = bf_hi(x[w]);
+    rotate_pair<INVERSE>(a, b, c[w], s[w]);
+    x[w] = pack_op<F16OUT>(a, b);
+  }
+}
+
+// ---------------------------------------------------------------- global memory
+__device__ __forceinline__ u32x4 ld16(const void* p) {
+  return *reinterpret_cast<const u32x4*>(p);
+}
+__device__ __forceinline__ void st16(void* p, u32x4 v) { *reinterpret_cast<u32x4*>(p) = v; }
+
+// Swap bits 2 and 3 of a key (or query) index inside a block of 16.  P^T leaves
+// the S^T MFMA with lane group g holding rows {8a + 4g + b}; storing the
+// transposed operand with this permutation makes those 8 rows contiguous, so
+// the PV-style MFMA reads them with one 16-byte LDS load.
+__device__ __forceinline__ int perm16(int x) {
+  return (x & ~0xC) | ((x & 0x8) >> 1) | ((x & 0x4) << 1);
+}
+
+}  // namespace af

@@ -1,0 +1,53 @@
+// Internal host-side interface between the C-ABI layer (api.cpp) and the
+// kernel translation units.  Each launcher maps runtime enums onto one
+// compile-time template instantiation and enqueues it on the given stream.
+#pragma once
+#include <hip/hip_runtime.h>
+
+namespace af {
+
+struct FwdParams {
+  const void* q;
+  const void* k;
+  const void* v;
+  void* o;
+  float* lse;
+  int B, H, Hkv, S, window;
+  const float* slopes;    // [H] or nullptr
+  float scale;
+  const float2* table;    // [rows >= S][D/2] (cos, sin); nullptr without RoPE
+};
+
+struct BwdParams {
+  const void* q;
+  const void* k;
+  const void* v;
+  const void* o;
+  const void* dout;
+  const float* lse;
+  void* dq;
+  void* dk;
+  void* dv;
+  float* delta;           // workspace [B*H*S]: rowsum(dO * O)
+  float* lse2;            // workspace [B*H*S]: LSE in log2 units (+inf for empty rows)
+  int B, H, Hkv, S, window;
+  const float* slopes;
+  float scale;
+  const float2* table;
+};
+
+struct RopeParams {
+  const void* x0;  void* y0;  int heads0;   // first tensor [B, heads0, S, D]
+  const void* x1;  void* y1;  int heads1;   // optional second tensor (heads1 may be 0)
+  int B, S;
+  const float2* table;
+};
+
+// Return 0 on success, -2 when the variant is not compiled, -3 on a HIP error.
+int launch_fwd_bf16(int D, int rope, int mask, bool alibi, const FwdParams& p, hipStream_t st);
+int launch_fwd_fp32(int D, int rope, int mask, bool alibi, const FwdParams& p, hipStream_t st);
+int launch_bwd_bf16(int D, int rope, int mask, bool alibi, const BwdParams& p, hipStream_t st);
+int launch_rope(bool fp32, int D, int rope, bool inverse, const RopeParams& p, hipStream_t st);
+int launch_rope_table(float2* table, int rows, int D, double theta, hipStream_t st);
+
+}  // namespace af

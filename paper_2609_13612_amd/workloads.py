@@ -1,0 +1,65 @@
+"""Named workload shapes and their algorithmic FLOP / byte counts.
+
+The five workloads are the parity and benchmark shapes of the build; inputs
+are seeded N(0, 1) tensors (see ``inputs``).  FLOPs count only visible
+(query, key) pairs: 4*D per pair for the forward (Q K^T and P V) and 10*D for
+the backward (five matmuls: S, dV, dP, dQ, dK), the FlashAttention convention.
+The separate rotation moves 4 bytes per bf16 element of Q and K (read + write).
+"""
+from dataclasses import dataclass, field
+
+
+@dataclass(frozen=True)
+class Workload:
+    name: str
+    B: int
+    H: int
+    Hkv: int
+    S: int
+    D: int
+    rope: str = "neox"
+    theta: float = 10000.0
+    mask: str = "causal"
+    window: int = 0
+    alibi: bool = False
+    dtype: str = "bf16"
+    backward: bool = False
+    notes: str = field(default="", compare=False)
+
+    def visible_pairs(self, S=None):
+        """Visible (query, key) pairs per (batch, head)."""
+        S = self.S if S is None else S
+        if self.mask == "none":
+            return S * S
+        if self.mask == "causal":
+            return S * (S + 1) // 2
+        W = self.window
+        # rows i < W see i+1 keys, the rest see W keys
+        w = min(W, S)
+        return w * (w + 1) // 2 + (S - w) * W
+
+    def fwd_flops(self, S=None):
+        return 4 * self.D * self.B * self.H * self.visible_pairs(S)
+
+    def bwd_flops(self, S=None):
+        return 10 * self.D * self.B * self.H * self.visible_pairs(S)
+
+    def rope_bytes(self, S=None):
+        S = self.S if S is None else S
+        return 4 * self.B * (self.H + self.Hkv) * S * self.D
+
+
+WORKLOADS = {
+    "rope_causal_tiny": Workload("rope_causal_tiny", 1, 2, 2, 128, 64, rope="interleaved",
+                                 notes="fp32 and bf16 parity case; interleaved pairs"),
+    "rope_causal_b8h16s2048d64": Workload("rope_causal_b8h16s2048d64", 8, 16, 16, 2048, 64,
+                                          notes="fused and separate-RoPE forward"),
+    "rope_swa1024_b4h32kv8s8192d128": Workload("rope_swa1024_b4h32kv8s8192d128", 4, 32, 8, 8192, 128,
+                                               mask="sliding_window", window=1024, notes="GQA, forward only"),
+    "alibi_causal_b4h16s4096d128": Workload("alibi_causal_b4h16s4096d128", 4, 16, 16, 4096, 128, rope="none",
+                                            alibi=True, notes="post-matmul modification only"),
+    "llama3_8b_b1h32kv8s8192d128": Workload("llama3_8b_b1h32kv8s8192d128", 1, 32, 8, 8192, 128, theta=500000.0,
+                                            backward=True, notes="Llama-3-8B attention layer, fwd + bwd"),
+}
+
+LLAMA_SWEEP_S = (1024, 2048, 4096, 8192, 16384)

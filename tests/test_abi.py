@@ -1,0 +1,127 @@
+"""The C-ABI library loads without a GPU, exports every declared symbol, and
+rejects bad arguments before any HIP call (CPU tests; no compute calls)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2609_13612_amd import _lib
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "attnfuse.h")
+FAKE = 0x10000   # aligned, never dereferenced: validation fails first
+ODD = 0x10008    # not 16-byte aligned
+
+
+def declared_symbols():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(attnfuse_\w+)\s*\(", text)))
+
+
+def test_header_declares_the_boundary():
+    assert declared_symbols() == sorted(["attnfuse_bwd", "attnfuse_bwd_workspace_bytes", "attnfuse_fwd",
+                                         "attnfuse_rope", "attnfuse_rope_bwd", "attnfuse_strerror",
+                                         "attnfuse_version"])
+
+
+def test_library_loads_and_exports_every_declared_symbol():
+    lib = _lib.load()
+    for name in declared_symbols():
+        assert hasattr(lib, name), name
+    assert set(declared_symbols()) == set(_lib.SIGNATURES)
+    assert lib.attnfuse_version() == 1
+
+
+def test_strerror():
+    lib = _lib.load()
+    assert lib.attnfuse_strerror(0) == b"success"
+    assert b"invalid" in lib.attnfuse_strerror(-1)
+    assert b"unsupported" in lib.attnfuse_strerror(-2)
+    assert b"HIP" in lib.attnfuse_strerror(-3)
+    assert lib.attnfuse_strerror(7) == b"unknown error code"
+
+
+def test_workspace_bytes():
+    lib = _lib.load()
+    assert lib.attnfuse_bwd_workspace_bytes(1, 32, 8192) == 8 * 32 * 8192
+    assert lib.attnfuse_bwd_workspace_bytes(0, 32, 8192) == 0
+
+
+def _fwd(**over):
+    a = dict(Q=FAKE, K=FAKE + 0x100, V=FAKE + 0x200, O=FAKE + 0x300, LSE=FAKE + 0x400, B=1, H=4, H_kv=2, S=16,
+             D=64, dtype=0, rope=1, theta=10000.0, mask=1, window=0, slopes=None, scale=0.125, stream=None)
+    a.update(over)
+    return _lib.load().attnfuse_fwd(a["Q"], a["K"], a["V"], a["O"], a["LSE"], a["B"], a["H"], a["H_kv"], a["S"],
+                                    a["D"], a["dtype"], a["rope"], a["theta"], a["mask"], a["window"], a["slopes"],
+                                    a["scale"], a["stream"])
+
+
+INVALID_FWD = [
+    dict(Q=None), dict(K=None), dict(V=None), dict(O=None), dict(LSE=None), dict(Q=ODD), dict(LSE=ODD + 0x400),
+    dict(O=FAKE), dict(B=0), dict(H=0), dict(H_kv=0), dict(S=0), dict(S=-5), dict(S=(1 << 20) + 1),
+    dict(H=3, H_kv=2), dict(D=0), dict(D=63), dict(dtype=2), dict(rope=3), dict(rope=-1),
+    dict(theta=0.0), dict(theta=-1.0), dict(theta=float("inf")), dict(theta=float("nan")), dict(mask=3),
+    dict(mask=2, window=0), dict(mask=2, window=-4), dict(scale=0.0), dict(scale=-1.0), dict(scale=float("nan")),
+]
+
+
+@pytest.mark.parametrize("over", INVALID_FWD, ids=lambda o: ",".join(f"{k}={v}" for k, v in o.items()))
+def test_fwd_rejects_invalid_arguments(over):
+    assert _fwd(**over) == -1
+
+
+@pytest.mark.parametrize("over", [dict(D=96), dict(D=256), dict(D=32), dict(D=96, rope=0)])
+def test_fwd_unsupported_head_dim(over):
+    assert _fwd(**over) == -2
+
+
+def test_rope_none_ignores_theta_validation_only_in_attention():
+    # theta is irrelevant without RoPE, but D is still checked first for support
+    assert _fwd(rope=0, theta=0.0, D=96) == -2
+
+
+def _bwd(**over):
+    base = FAKE
+    a = dict(Q=base, K=base + 0x100, V=base + 0x200, O=base + 0x300, dO=base + 0x400, LSE=base + 0x500,
+             dQ=base + 0x600, dK=base + 0x700, dV=base + 0x800, ws=base + 0x900, ws_bytes=8 * 4 * 16,
+             B=1, H=4, H_kv=2, S=16, D=64, dtype=0, rope=1, theta=1e4, mask=1, window=0, slopes=None,
+             scale=0.125, stream=None)
+    a.update(over)
+    return _lib.load().attnfuse_bwd(a["Q"], a["K"], a["V"], a["O"], a["dO"], a["LSE"], a["dQ"], a["dK"], a["dV"],
+                                    a["ws"], a["ws_bytes"], a["B"], a["H"], a["H_kv"], a["S"], a["D"], a["dtype"],
+                                    a["rope"], a["theta"], a["mask"], a["window"], a["slopes"], a["scale"],
+                                    a["stream"])
+
+
+@pytest.mark.parametrize("over", [dict(Q=None), dict(dO=None), dict(ws=None), dict(dQ=FAKE), dict(ws_bytes=8 * 4 * 16 - 1),
+                                  dict(H=4, H_kv=3), dict(mask=2, window=0), dict(dK=ODD), dict(S=0)],
+                         ids=lambda o: ",".join(f"{k}={v}" for k, v in o.items()))
+def test_bwd_rejects_invalid_arguments(over):
+    assert _bwd(**over) == -1
+
+
+def test_bwd_unsupported():
+    assert _bwd(D=96) == -2
+    assert _bwd(dtype=1) == -2   # fp32 backward is not compiled
+
+
+def _rope(fn="attnfuse_rope", **over):
+    a = dict(Q=FAKE, K=FAKE + 0x100, Qr=FAKE + 0x200, Kr=FAKE + 0x300, B=1, H=4, H_kv=2, S=16, D=64, dtype=0,
+             rope=1, theta=1e4, stream=None)
+    a.update(over)
+    return getattr(_lib.load(), fn)(a["Q"], a["K"], a["Qr"], a["Kr"], a["B"], a["H"], a["H_kv"], a["S"], a["D"],
+                                    a["dtype"], a["rope"], a["theta"], a["stream"])
+
+
+@pytest.mark.parametrize("fn", ["attnfuse_rope", "attnfuse_rope_bwd"])
+@pytest.mark.parametrize("over", [dict(Q=None), dict(Qr=None), dict(K=None), dict(Kr=None), dict(rope=0),
+                                  dict(theta=0.0), dict(H=3), dict(Q=ODD), dict(S=0), dict(dtype=5)],
+                         ids=lambda o: ",".join(f"{k}={v}" for k, v in o.items()))
+def test_rope_rejects_invalid_arguments(fn, over):
+    assert _rope(fn, **over) == -1
+
+
+def test_rope_unsupported():
+    assert _rope(D=96) == -2

@@ -100,39 +100,57 @@ __device__ __forceinline__ void rotate_pair(float& xa, float& xb, float c, float
 
 // NeoX: 8 consecutive pair indices i0..i0+7 whose first elements are the 8 bf16
 // of `a` and whose partners (half a head away) are the 8 bf16 of `b`.
-// cs points at the table entries (cos, sin) of those 8 pairs for one position.
-// The rotated values are rounded to fp16 when F16OUT (the attention kernels'
-// rotated MFMA operands), else back to bf16 (the rotation kernel's tensors).
+// t holds the (cos, sin) table entries of those 8 pairs for one position
+// (t[j] = entries 2j and 2j+1).  The rotated values are rounded to fp16 when
+// F16OUT (the attention kernels' rotated MFMA operands), else back to bf16
+// (the rotation kernel's tensors).
 template <bool INVERSE, bool F16OUT = false>
-__device__ __forceinline__ void rotate_neox8(u32x4& a, u32x4& b, const float2* __restrict__ cs) {
-  const float4* t = reinterpret_cast<const float4*>(cs);
-  float4 t0 = t[0], t1 = t[1], t2 = t[2], t3 = t[3];
-  float c[8] = {t0.x, t0.z, t1.x, t1.z, t2.x, t2.z, t3.x, t3.z};
-  float s[8] = {t0.y, t0.w, t1.y, t1.w, t2.y, t2.w, t3.y, t3.w};
+__device__ __forceinline__ void rotate_neox8(u32x4& a, u32x4& b, const float4 (&t)[4]) {
 #pragma unroll
   for (int w = 0; w < 4; ++w) {
     float a0 = bf_lo(a[w]), a1 = bf_hi(a[w]);
     float b0 = bf_lo(b[w]), b1 = bf_hi(b[w]);
-    rotate_pair<INVERSE>(a0, b0, c[2 * w], s[2 * w]);
-    rotate_pair<INVERSE>(a1, b1, c[2 * w + 1], s[2 * w + 1]);
+    rotate_pair<INVERSE>(a0, b0, t[w].x, t[w].y);
+    rotate_pair<INVERSE>(a1, b1, t[w].z, t[w].w);
     a[w] = pack_op<F16OUT>(a0, a1);
     b[w] = pack_op<F16OUT>(b0, b1);
   }
 }
 
-// Interleaved: the 8 bf16 of `x` are 4 pairs (2i, 2i+1), i = i0..i0+3.
+// Interleaved: the 8 bf16 of `x` are 4 pairs (2i, 2i+1), i = i0..i0+3, with
+// table entries t[0] = (i0, i0+1), t[1] = (i0+2, i0+3).
 template <bool INVERSE, bool F16OUT = false>
-__device__ __forceinline__ void rotate_interleaved8(u32x4& x, const float2* __restrict__ cs) {
-  const float4* t = reinterpret_cast<const float4*>(cs);
-  float4 t0 = t[0], t1 = t[1];
-  float c[4] = {t0.x, t0.z, t1.x, t1.z};
-  float s[4] = {t0.y, t0.w, t1.y, t1.w};
+__device__ __forceinline__ void rotate_interleaved8(u32x4& x, const float4 (&t)[2]) {
 #pragma unroll
   for (int w = 0; w < 4; ++w) {
     float a = bf_lo(x[w]), b = bf_hi(x[w]);
-    rotate_pair<INVERSE>(a, b, c[w], s[w]);
+    const float c = (w & 1) ? t[w >> 1].z : t[w >> 1].x;
+    const float sn = (w & 1) ? t[w >> 1].w : t[w >> 1].y;
+    rotate_pair<INVERSE>(a, b, c, sn);
     x[w] = pack_op<F16OUT>(a, b);
   }
+}
+
+// Load N float4 = 2N consecutive (cos, sin) table entries.
+template <int N>
+__device__ __forceinline__ void load_cs(float4 (&t)[N], const float2* __restrict__ cs) {
+  const float4* q = reinterpret_cast<const float4*>(cs);
+#pragma unroll
+  for (int j = 0; j < N; ++j) t[j] = q[j];
+}
+
+template <bool INVERSE, bool F16OUT = false>
+__device__ __forceinline__ void rotate_neox8(u32x4& a, u32x4& b, const float2* __restrict__ cs) {
+  float4 t[4];
+  load_cs(t, cs);
+  rotate_neox8<INVERSE, F16OUT>(a, b, t);
+}
+
+template <bool INVERSE, bool F16OUT = false>
+__device__ __forceinline__ void rotate_interleaved8(u32x4& x, const float2* __restrict__ cs) {
+  float4 t[2];
+  load_cs(t, cs);
+  rotate_interleaved8<INVERSE, F16OUT>(x, t);
 }
 
 // ---------------------------------------------------------------- global memory
@@ -140,6 +158,16 @@ __device__ __forceinline__ u32x4 ld16(const void* p) {
   return *reinterpret_cast<const u32x4*>(p);
 }
 __device__ __forceinline__ void st16(void* p, u32x4 v) { *reinterpret_cast<u32x4*>(p) = v; }
+
+// gfx950 LDS transpose read (ds_read_b64_tr_b16).  Within each group of 16
+// lanes the sixteen 8-byte chunks the lanes address form a 4 x 16 matrix of
+// 16-bit values (row r = the chunks of lanes 4r..4r+3, in lane order); lane i
+// of the group receives column i, i.e. one value from each of the 4 rows.
+__device__ __forceinline__ u32x2 lds_read_tr16(const uint16_t* p) {
+  typedef short v4i16 __attribute__((ext_vector_type(4)));
+  v4i16 r = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) v4i16*)(p));
+  return __builtin_bit_cast(u32x2, r);
+}
 
 // Swap bits 2 and 3 of a key (or query) index inside a block of 16.  P^T leaves
 // the S^T MFMA with lane group g holding rows {8a + 4g + b}; storing the

@@ -1,136 +1,171 @@
-// Fused RoPE + masked attention forward, bf16 inputs, bf16 MFMA with fp32
+// Fused RoPE + masked attention forward, bf16 inputs, MFMA with fp32
 // accumulation, for gfx950.
 //
 // Method (AttnFuse, Section 2 online softmax, Section 4.1 fused RoPE): the
-// query block is rotated once before the key loop; every key tile is rotated
+// query rows are rotated once before the key loop; every key tile is rotated
 // on the fly as it is staged into LDS; the post-matmul modifications (ALiBi,
 // causal, sliding window) are applied to the scores in registers; fully
 // masked key tiles are never visited.
 //
 // Work decomposition
-//   workgroup = 4 waves = 128 query rows of one (batch, head); wave = 32 rows.
-//   Key tiles of BN = 64 rows are staged in LDS and shared by the 4 waves.
+//   workgroup = 8 waves (two per SIMD, so one wave's softmax VALU work runs
+//   under the other's MFMA work) = 256 query rows.  The rows are HP query
+//   heads of one GQA group x 256/HP positions, so one rotated K tile serves
+//   every head that reads it.  Key tiles of BN = 64 rows are double-buffered
+//   in LDS: the next tile's K, V and cos/sin are loaded into registers before
+//   the current tile is computed and committed (rotated) after it, with one
+//   barrier per tile.
 //   Scores are formed transposed, S^T = K' Q'^T (keys x queries), so every
 //   lane owns ONE query column and 16 keys per 32x32 MFMA tile: the row max
-//   is an in-lane reduction plus a single swap with lane l^32, and the row
-//   sum stays per lane until the epilogue.  P^T then feeds O^T += V^T P^T
-//   straight from registers as the B operand; V is stored transposed in LDS
-//   with the bit-2/3 key permutation that lines the keys up with P^T's
-//   register order.
+//   is an in-lane reduction plus one v_permlane32_swap, and the row sum stays
+//   per lane until the epilogue.  P^T feeds O^T += V^T P^T straight from
+//   registers as the B operand; V stays row-major in LDS and its transposed
+//   A operand comes from ds_read_b64_tr_b16.
+//   The running max is only raised when a row's max grows by more than 2^8,
+//   so the O accumulator is rarely rescaled (exact: O and l share the scale).
 //
 // Precision: without RoPE the bf16 inputs feed Q K^T exactly.  With RoPE the
-// rotated Q' and K' must be rounded to some 16-bit MFMA operand type; they are
-// rounded to fp16 (11-bit significand) rather than bf16 (8-bit), which keeps
-// the row statistic LSE within 1e-3 of the exact value.  The fp16 range then
-// bounds the rotated inputs: |q|, |k| well below 65504.  P and V stay bf16.
+// rotated Q' and K' are rounded to fp16 (11-bit significand) rather than bf16
+// (8-bit), which keeps the row statistic LSE within 1e-3 of the exact value;
+// the fp16 range then bounds the rotated inputs (|q|, |k| well below 65504).
+// P and V stay bf16.
 #include "common.hpp"
 #include "launch.hpp"
 
 namespace af {
 
-template <int D>
+template <int D, int ROPE>
 struct FwdCfg {
-  static constexpr int NW = 4;          // waves per workgroup
-  static constexpr int BM = 32 * NW;    // query rows per workgroup
-  static constexpr int BN = 64;         // keys per tile
-  static constexpr int KS = D / 16;     // MFMA k-steps over the head dimension
-  static constexpr int MT = D / 32;     // 32-row output tiles over the head dimension
-  static constexpr int KROW = D + 8;    // LDS pitch (bf16) of the K tile   [BN][KROW]
-  static constexpr int VROW = BN + 8;   // LDS pitch (bf16) of the V^T tile [D][VROW]
+  static constexpr int NW = 8;                 // waves per workgroup
+  static constexpr int THREADS = 64 * NW;
+  static constexpr int ROWS = 32 * NW;         // query rows per workgroup
+  static constexpr int BN = 64;                // keys per tile
+  static constexpr int KS = D / 16;            // MFMA k-steps over the head dimension
+  static constexpr int MT = D / 32;            // 32-row output tiles over the head dimension
+  static constexpr int KP = D + 8;             // K tile pitch (elements): conflict-free 16-byte reads
+  static constexpr int VP = D + 16;            // V tile pitch: conflict-free transpose reads
+  static constexpr int K_ELEMS = BN * KP;
+  static constexpr int V_ELEMS = BN * VP;
+  static constexpr int STAGE = K_ELEMS + V_ELEMS;
+  // staging work items: NeoX rotates chunk pairs (c, c + D/2); otherwise single chunks
+  static constexpr int K_UNITS = (ROPE == ROPE_NEOX) ? D / 16 : D / 8;
+  static constexpr int K_ITEMS = BN * K_UNITS;
+  static constexpr int KPT = (K_ITEMS + THREADS - 1) / THREADS;
+  static constexpr int V_ITEMS = BN * (D / 8);
+  static constexpr int VPT = (V_ITEMS + THREADS - 1) / THREADS;
+  static constexpr int CS = (ROPE == ROPE_NEOX) ? 4 : (ROPE == ROPE_INTERLEAVED ? 2 : 1);   // float4 per item
 };
 
-// Stage key tile n0..n0+BN-1 into LDS: K rotated (RoPE) as [key][d], V as
-// V^T [d][perm16(key)].  Rows at or beyond S are zero.
+// Registers holding one key tile between its global load and its LDS commit.
 template <int D, int ROPE>
-__device__ __forceinline__ void stage_kv_tile(uint16_t* __restrict__ Ks, uint16_t* __restrict__ Vt,
-                                              const uint16_t* __restrict__ K,
-                                              const uint16_t* __restrict__ V,
-                                              const float2* __restrict__ table, int n0, int S,
-                                              int tid) {
-  using C = FwdCfg<D>;
-  if constexpr (ROPE == ROPE_NEOX) {
-    constexpr int CP = D / 16;   // chunk pairs per row: chunk c and chunk c + D/16
-    constexpr int N = C::BN * CP;
+struct TileRegs {
+  using C = FwdCfg<D, ROPE>;
+  u32x4 ka[C::KPT];
+  u32x4 kb[(ROPE == ROPE_NEOX) ? C::KPT : 1];
+  float4 cs[C::KPT][C::CS];
+  u32x4 v[C::VPT];
+};
+
+template <int D, int ROPE>
+__device__ __forceinline__ void tile_load(TileRegs<D, ROPE>& R, const uint16_t* __restrict__ K,
+                                          const uint16_t* __restrict__ V, const float2* __restrict__ table,
+                                          int n0, int S, int tid) {
+  using C = FwdCfg<D, ROPE>;
 #pragma unroll
-    for (int i = 0; i < (N + 255) / 256; ++i) {
-      const int it = tid + 256 * i;
-      if (N % 256 != 0 && it >= N) break;
-      const int r = it / CP, c = it % CP, n = n0 + r;
-      u32x4 a = {0, 0, 0, 0}, b = {0, 0, 0, 0};
-      if (n < S) {
-        a = ld16(K + (size_t)n * D + 8 * c);
-        b = ld16(K + (size_t)n * D + D / 2 + 8 * c);
-        rotate_neox8<false, true>(a, b, table + (size_t)n * (D / 2) + 8 * c);
-      }
-      *reinterpret_cast<u32x4*>(Ks + r * C::KROW + 8 * c) = a;
-      *reinterpret_cast<u32x4*>(Ks + r * C::KROW + D / 2 + 8 * c) = b;
-    }
-  } else {
-    constexpr int CH = D / 8;    // 16-byte chunks per row
-    constexpr int N = C::BN * CH;
+  for (int i = 0; i < C::KPT; ++i) {
+    const int it = tid + C::THREADS * i;
+    const int r = it / C::K_UNITS, c = it % C::K_UNITS, n = n0 + r;
+    const bool ok = (C::K_ITEMS % C::THREADS == 0 || it < C::K_ITEMS) && n < S;
+    R.ka[i] = ok ? ld16(K + (size_t)n * D + 8 * c) : u32x4{0, 0, 0, 0};
+    if constexpr (ROPE == ROPE_NEOX) {
+      R.kb[i] = ok ? ld16(K + (size_t)n * D + D / 2 + 8 * c) : u32x4{0, 0, 0, 0};
+      if (ok) {
+        load_cs(R.cs[i], table + (size_t)n * (D / 2) + 8 * c);
+      } else {
 #pragma unroll
-    for (int i = 0; i < (N + 255) / 256; ++i) {
-      const int it = tid + 256 * i;
-      if (N % 256 != 0 && it >= N) break;
-      const int r = it / CH, c = it % CH, n = n0 + r;
-      u32x4 a = {0, 0, 0, 0};
-      if (n < S) {
-        a = ld16(K + (size_t)n * D + 8 * c);
-        if constexpr (ROPE == ROPE_INTERLEAVED)
-          rotate_interleaved8<false, true>(a, table + (size_t)n * (D / 2) + 4 * c);
+        for (int j = 0; j < 4; ++j) R.cs[i][j] = float4{1.f, 0.f, 1.f, 0.f};
       }
-      *reinterpret_cast<u32x4*>(Ks + r * C::KROW + 8 * c) = a;
+    } else if constexpr (ROPE == ROPE_INTERLEAVED) {
+      if (ok) {
+        load_cs(R.cs[i], table + (size_t)n * (D / 2) + 4 * c);
+      } else {
+#pragma unroll
+        for (int j = 0; j < 2; ++j) R.cs[i][j] = float4{1.f, 0.f, 1.f, 0.f};
+      }
     }
   }
-  // V^T: each thread transposes a 4-key x 8-dim block.
-  constexpr int OCT = D / 8;
-  constexpr int NV = (C::BN / 4) * OCT;
 #pragma unroll
-  for (int i = 0; i < (NV + 255) / 256; ++i) {
-    const int it = tid + 256 * i;
-    if (NV % 256 != 0 && it >= NV) break;
-    const int j = it / OCT, o = it % OCT;
-    u32x4 r[4];
+  for (int i = 0; i < C::VPT; ++i) {
+    const int it = tid + C::THREADS * i;
+    const int r = it / (D / 8), c = it % (D / 8), n = n0 + r;
+    const bool ok = (C::V_ITEMS % C::THREADS == 0 || it < C::V_ITEMS) && n < S;
+    R.v[i] = ok ? ld16(V + (size_t)n * D + 8 * c) : u32x4{0, 0, 0, 0};
+  }
+}
+
+// Rotate the staged K rows and write K' and V into one LDS stage.
+template <int D, int ROPE>
+__device__ __forceinline__ void tile_commit(TileRegs<D, ROPE>& R, uint16_t* __restrict__ Ks,
+                                            uint16_t* __restrict__ Vs, int tid) {
+  using C = FwdCfg<D, ROPE>;
 #pragma unroll
-    for (int b = 0; b < 4; ++b) {
-      const int n = n0 + 4 * j + b;
-      r[b] = (n < S) ? ld16(V + (size_t)n * D + 8 * o) : u32x4{0, 0, 0, 0};
+  for (int i = 0; i < C::KPT; ++i) {
+    const int it = tid + C::THREADS * i;
+    if (C::K_ITEMS % C::THREADS != 0 && it >= C::K_ITEMS) break;
+    const int r = it / C::K_UNITS, c = it % C::K_UNITS;
+    if constexpr (ROPE == ROPE_NEOX) {
+      rotate_neox8<false, true>(R.ka[i], R.kb[i], R.cs[i]);
+      *reinterpret_cast<u32x4*>(Ks + r * C::KP + 8 * c) = R.ka[i];
+      *reinterpret_cast<u32x4*>(Ks + r * C::KP + D / 2 + 8 * c) = R.kb[i];
+    } else {
+      if constexpr (ROPE == ROPE_INTERLEAVED) rotate_interleaved8<false, true>(R.ka[i], R.cs[i]);
+      *reinterpret_cast<u32x4*>(Ks + r * C::KP + 8 * c) = R.ka[i];
     }
-    const int col = perm16(4 * j);
+  }
 #pragma unroll
-    for (int w = 0; w < 4; ++w) {
-      u32x2 lo = {(r[0][w] & 0xffffu) | (r[1][w] << 16), (r[2][w] & 0xffffu) | (r[3][w] << 16)};
-      u32x2 hi = {(r[0][w] >> 16) | (r[1][w] & 0xffff0000u), (r[2][w] >> 16) | (r[3][w] & 0xffff0000u)};
-      *reinterpret_cast<u32x2*>(Vt + (8 * o + 2 * w) * C::VROW + col) = lo;
-      *reinterpret_cast<u32x2*>(Vt + (8 * o + 2 * w + 1) * C::VROW + col) = hi;
-    }
+  for (int i = 0; i < C::VPT; ++i) {
+    const int it = tid + C::THREADS * i;
+    if (C::V_ITEMS % C::THREADS != 0 && it >= C::V_ITEMS) break;
+    const int r = it / (D / 8), c = it % (D / 8);
+    *reinterpret_cast<u32x4*>(Vs + r * C::VP + 8 * c) = R.v[i];
   }
 }
 
 template <int D, int ROPE, int MASK, bool ALIBI>
-__global__ __launch_bounds__(256) void fwd_bf16_kernel(FwdParams p) {
-  using C = FwdCfg<D>;
-  __shared__ __attribute__((aligned(16))) uint16_t Ks[C::BN * C::KROW];
-  __shared__ __attribute__((aligned(16))) uint16_t Vt[D * C::VROW];
+__global__ __launch_bounds__(512) void fwd_bf16_kernel(FwdParams p) {
+  using C = FwdCfg<D, ROPE>;
+  constexpr bool QF16 = ROPE != ROPE_NONE;
+  __shared__ __attribute__((aligned(16))) uint16_t smem[2 * C::STAGE];
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int lq = lane & 31, lg = lane >> 5;
   const int S = p.S;
-  const int BH = p.B * p.H;
-  const int nqb = (S + C::BM - 1) / C::BM;
-  // Longest (last) query blocks first; all blocks of one head share
-  // blockIdx % (B*H), so with B*H a multiple of 8 they land on one XCD.
-  const int bh = blockIdx.x % BH;
-  const int qb = nqb - 1 - (int)(blockIdx.x / BH);
-  const int b = bh / p.H, h = bh % p.H;
-  const int g = h / (p.H / p.Hkv);
-  const int m0 = qb * C::BM;
-  const int mw = m0 + wave * 32;
-  const int m = mw + lq;
+  // Workgroup -> (batch, K/V head, head group, position block).  The position
+  // block is the slow index and runs backwards, so the longest causal blocks
+  // start first; consecutive workgroups walk (batch, K/V head, head group), and
+  // with that count a multiple of 8 every block of one K/V head lands on the
+  // same XCD and shares its L2.
+  const int HP = p.heads_per_wg;                 // query heads per workgroup
+  const int WPH = C::NW / HP;                    // waves per head
+  const int P = 32 * WPH;                        // positions per workgroup
+  const int G = p.H / p.Hkv;
+  const int groups = G / HP;
+  const int units = p.B * p.Hkv * groups;
+  const int npb = (S + P - 1) / P;
+  const int unit = blockIdx.x % units;
+  const int pb = npb - 1 - (int)(blockIdx.x / units);
+  const int hg = unit % groups, bg = unit / groups;
+  const int b = bg / p.Hkv, g = bg % p.Hkv;
+  const int h = g * G + hg * HP + wave / WPH;
+  const int p0 = pb * P;
+  const int mw = p0 + 32 * (wave % WPH);         // first query row of this wave
+  const int m = mw + lq;                         // this lane's query row
+  const int p_end = min(p0 + P, S);
 
-  const uint16_t* __restrict__ Q = static_cast<const uint16_t*>(p.q) + (size_t)bh * S * D;
-  const uint16_t* __restrict__ K = static_cast<const uint16_t*>(p.k) + (size_t)(b * p.Hkv + g) * S * D;
-  const uint16_t* __restrict__ V = static_cast<const uint16_t*>(p.v) + (size_t)(b * p.Hkv + g) * S * D;
+  const size_t bh = (size_t)b * p.H + h;
+  const uint16_t* __restrict__ Q = static_cast<const uint16_t*>(p.q) + bh * S * D;
+  const uint16_t* __restrict__ K = static_cast<const uint16_t*>(p.k) + (size_t)bg * S * D;
+  const uint16_t* __restrict__ V = static_cast<const uint16_t*>(p.v) + (size_t)bg * S * D;
 
   // Query operand (B of S^T = K Q^T): lane holds row m, dims 16s + 8lg .. +7.
   u32x4 qreg[C::KS];
@@ -155,113 +190,137 @@ __global__ __launch_bounds__(256) void fwd_bf16_kernel(FwdParams p) {
 
   const int ntiles = (S + C::BN - 1) / C::BN;
   int t_begin = 0, t_end = ntiles;
-  if constexpr (MASK != MASK_NONE) t_end = min(ntiles, (min(m0 + C::BM, S) - 1) / C::BN + 1);
-  if constexpr (MASK == MASK_SLIDING_WINDOW) t_begin = max(0, m0 - W + 1) / C::BN;
+  if constexpr (MASK != MASK_NONE) t_end = min(ntiles, (p_end - 1) / C::BN + 1);
+  if constexpr (MASK == MASK_SLIDING_WINDOW) t_begin = max(0, p0 - W + 1) / C::BN;
 
   f32x16 acc[C::MT];
 #pragma unroll
   for (int i = 0; i < C::MT; ++i) acc[i] = f32x16{};
-  float m_run = -INFINITY;   // running max, log2 units
-  float l_run = 0.f;         // this lane's partial row sum
+  float m_run = -INFINITY;   // reference max of the row, log2 units
+  float l_run = 0.f;         // this lane's partial row sum (relative to m_run)
+
+  // Transpose-read addressing for the V^T operand (see lds_read_tr16): lane i
+  // of each 16-lane group reads 4 dims of key (4 lg + i/4) [+8 for the second
+  // read]; the group's 16 lanes cover 16 dims starting at 16 * ((lane/16) & 1).
+  const int tr_key = 4 * lg + ((lane & 15) >> 2);
+  const int tr_col = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+
+  TileRegs<D, ROPE> R;
+  if (t_begin < t_end) {
+    tile_load<D, ROPE>(R, K, V, p.table, t_begin * C::BN, S, tid);
+    tile_commit<D, ROPE>(R, smem, smem + C::K_ELEMS, tid);
+  }
+  __syncthreads();
 
   for (int t = t_begin; t < t_end; ++t) {
     const int n0 = t * C::BN;
-    __syncthreads();
-    stage_kv_tile<D, ROPE>(Ks, Vt, K, V, p.table, n0, S, tid);
-    __syncthreads();
+    const uint16_t* Ks = smem + ((t - t_begin) & 1) * C::STAGE;
+    const uint16_t* Vs = Ks + C::K_ELEMS;
+    const bool more = t + 1 < t_end;
+    if (more) tile_load<D, ROPE>(R, K, V, p.table, n0 + C::BN, S, tid);
 
     bool visible = mw < S;
     if constexpr (MASK != MASK_NONE) visible = visible && (n0 <= mw + 31);
     if constexpr (MASK == MASK_SLIDING_WINDOW) visible = visible && (n0 + C::BN - 1 > mw - W);
-    if (!visible) continue;   // wave-uniform
-
-    // S^T = K' Q'^T: two 32-key subtiles.
-    f32x16 st[2];
+    if (visible) {   // wave-uniform
+      // S^T = K' Q'^T: two 32-key subtiles.
+      f32x16 st[2];
 #pragma unroll
-    for (int kt = 0; kt < 2; ++kt) {
-      st[kt] = f32x16{};
+      for (int kt = 0; kt < 2; ++kt) {
+        st[kt] = f32x16{};
 #pragma unroll
-      for (int s = 0; s < C::KS; ++s) {
-        u32x4 a = *reinterpret_cast<const u32x4*>(Ks + (32 * kt + lq) * C::KROW + 16 * s + 8 * lg);
-        st[kt] = mfma32<(ROPE != ROPE_NONE)>(a, qreg[s], st[kt]);
-      }
-    }
-
-    bool need_mask = n0 + C::BN > S;
-    if constexpr (MASK != MASK_NONE) need_mask = need_mask || (n0 + C::BN - 1 > mw);
-    if constexpr (MASK == MASK_SLIDING_WINDOW) need_mask = need_mask || (n0 <= mw + 31 - W);
-
-    // Scores in log2 units (ALiBi folded in), masked entries at -inf.
-#pragma unroll
-    for (int kt = 0; kt < 2; ++kt) {
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int n = n0 + 32 * kt + 8 * (r >> 2) + 4 * lg + (r & 3);
-        float x = st[kt][r];
-        if constexpr (ALIBI) x = __builtin_fmaf(x, c2, slope2 * (float)(n - m));
-        if (need_mask) {
-          bool ok = n < S;
-          if constexpr (MASK != MASK_NONE) ok = ok && (n <= m);
-          if constexpr (MASK == MASK_SLIDING_WINDOW) ok = ok && (n > m - W);
-          if (!ok) x = -INFINITY;
+        for (int s = 0; s < C::KS; ++s) {
+          u32x4 a = *reinterpret_cast<const u32x4*>(Ks + (32 * kt + lq) * C::KP + 16 * s + 8 * lg);
+          st[kt] = mfma32<QF16>(a, qreg[s], st[kt]);
         }
-        st[kt][r] = x;
       }
-    }
 
-    float mx = -INFINITY;
-#pragma unroll
-    for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, st[kt][r]);
-    mx = pair_max(mx);
-    if constexpr (!ALIBI) mx *= c2;
-    const float m_new = fmaxf(m_run, mx);
-    const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
-    const float alpha = fast_exp2(m_run - m_use);
+      bool need_mask = n0 + C::BN > S;
+      if constexpr (MASK != MASK_NONE) need_mask = need_mask || (n0 + C::BN - 1 > mw);
+      if constexpr (MASK == MASK_SLIDING_WINDOW) need_mask = need_mask || (n0 <= mw + 31 - W);
 
-    u32x4 pb[2][2];
-    float rs = 0.f;
-#pragma unroll
-    for (int kt = 0; kt < 2; ++kt) {
-      float pv[16];
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const float arg = ALIBI ? (st[kt][r] - m_use) : __builtin_fmaf(st[kt][r], c2, -m_use);
-        pv[r] = fast_exp2(arg);
-        rs += pv[r];
-      }
-#pragma unroll
-      for (int hf = 0; hf < 2; ++hf)
-#pragma unroll
-        for (int w = 0; w < 4; ++w) pb[kt][hf][w] = pack_bf16(pv[8 * hf + 2 * w], pv[8 * hf + 2 * w + 1]);
-    }
-    l_run = l_run * alpha + rs;
-    m_run = m_new;
-    if (__any(alpha != 1.f)) {
-#pragma unroll
-      for (int i = 0; i < C::MT; ++i) acc[i] *= alpha;
-    }
-
-    // O^T += V^T P^T.
-#pragma unroll
-    for (int mt = 0; mt < C::MT; ++mt) {
+      // Scores in log2 units (ALiBi folded in), masked entries at -inf.
 #pragma unroll
       for (int kt = 0; kt < 2; ++kt) {
 #pragma unroll
-        for (int hf = 0; hf < 2; ++hf) {
-          u32x4 a = *reinterpret_cast<const u32x4*>(Vt + (32 * mt + lq) * C::VROW + 32 * kt + 16 * hf + 8 * lg);
-          acc[mt] = mfma32(a, pb[kt][hf], acc[mt]);
+        for (int r = 0; r < 16; ++r) {
+          const int n = n0 + 32 * kt + 8 * (r >> 2) + 4 * lg + (r & 3);
+          float x = st[kt][r];
+          if constexpr (ALIBI) x = __builtin_fmaf(x, c2, slope2 * (float)(n - m));
+          if (need_mask) {
+            bool ok = n < S;
+            if constexpr (MASK != MASK_NONE) ok = ok && (n <= m);
+            if constexpr (MASK == MASK_SLIDING_WINDOW) ok = ok && (n > m - W);
+            if (!ok) x = -INFINITY;
+          }
+          st[kt][r] = x;
+        }
+      }
+
+      float mx = -INFINITY;
+#pragma unroll
+      for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, st[kt][r]);
+      mx = pair_max(mx);
+      if constexpr (!ALIBI) mx *= c2;
+      const float m_new = fmaxf(m_run, mx);
+      if (__any(m_new > m_run + 8.f)) {   // raise the reference max (wave-uniform)
+        const float alpha = (m_run == -INFINITY) ? 0.f : fast_exp2(m_run - m_new);
+        l_run *= alpha;
+#pragma unroll
+        for (int i = 0; i < C::MT; ++i) acc[i] *= alpha;
+        m_run = m_new;
+      }
+      const float m_use = (m_run == -INFINITY) ? 0.f : m_run;
+
+      u32x4 pb[2][2];
+      float rs = 0.f;
+#pragma unroll
+      for (int kt = 0; kt < 2; ++kt) {
+        float pv[16];
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const float arg = ALIBI ? (st[kt][r] - m_use) : __builtin_fmaf(st[kt][r], c2, -m_use);
+          pv[r] = fast_exp2(arg);
+          rs += pv[r];
+        }
+#pragma unroll
+        for (int hf = 0; hf < 2; ++hf)
+#pragma unroll
+          for (int w = 0; w < 4; ++w) pb[kt][hf][w] = pack_bf16(pv[8 * hf + 2 * w], pv[8 * hf + 2 * w + 1]);
+      }
+      l_run += rs;
+
+      // O^T += V^T P^T; the V^T operand is two transpose reads of row-major V.
+#pragma unroll
+      for (int mt = 0; mt < C::MT; ++mt) {
+#pragma unroll
+        for (int kt = 0; kt < 2; ++kt) {
+#pragma unroll
+          for (int hf = 0; hf < 2; ++hf) {
+            const uint16_t* base = Vs + (32 * kt + 16 * hf + tr_key) * C::VP + 32 * mt + tr_col;
+            const u32x2 lo = lds_read_tr16(base);
+            const u32x2 hi = lds_read_tr16(base + 8 * C::VP);
+            const u32x4 a = {lo[0], lo[1], hi[0], hi[1]};
+            acc[mt] = mfma32(a, pb[kt][hf], acc[mt]);
+          }
         }
       }
     }
+
+    if (more) {
+      uint16_t* Kn = smem + ((t + 1 - t_begin) & 1) * C::STAGE;
+      tile_commit<D, ROPE>(R, Kn, Kn + C::K_ELEMS, tid);
+    }
+    __syncthreads();
   }
 
   // Epilogue: O = acc / l, LSE = (m + log2 l) ln 2.
   const float l_tot = pair_sum(l_run);
   if (m < S) {
     const float inv = (l_tot > 0.f) ? 1.f / l_tot : 0.f;
-    uint16_t* O = static_cast<uint16_t*>(p.o) + ((size_t)bh * S + m) * D;
+    uint16_t* O = static_cast<uint16_t*>(p.o) + (bh * S + m) * D;
 #pragma unroll
     for (int mt = 0; mt < C::MT; ++mt) {
 #pragma unroll
@@ -271,17 +330,26 @@ __global__ __launch_bounds__(256) void fwd_bf16_kernel(FwdParams p) {
         *reinterpret_cast<u32x2*>(O + 32 * mt + 8 * a + 4 * lg) = w;
       }
     }
-    if (lg == 0)
-      p.lse[(size_t)bh * S + m] = (l_tot > 0.f) ? (m_run + __log2f(l_tot)) * kLn2 : -INFINITY;
+    if (lg == 0) p.lse[bh * S + m] = (l_tot > 0.f) ? (m_run + __log2f(l_tot)) * kLn2 : -INFINITY;
   }
 }
 
+// Query heads packed per workgroup: the largest power of two <= 8 dividing the
+// GQA group size.
+static int heads_per_wg(int G) {
+  int hp = 1;
+  while (hp < 8 && G % (2 * hp) == 0) hp *= 2;
+  return hp;
+}
+
 template <int D, int ROPE, int MASK, bool ALIBI>
-static int launch_one(const FwdParams& p, hipStream_t st) {
-  using C = FwdCfg<D>;
-  const int nqb = (p.S + C::BM - 1) / C::BM;
-  dim3 grid((unsigned)(nqb * p.B * p.H));
-  hipLaunchKernelGGL((fwd_bf16_kernel<D, ROPE, MASK, ALIBI>), grid, dim3(256), 0, st, p);
+static int launch_one(const FwdParams& p0, hipStream_t st) {
+  using C = FwdCfg<D, ROPE>;
+  FwdParams p = p0;
+  p.heads_per_wg = heads_per_wg(p.H / p.Hkv);
+  const int P = C::ROWS / p.heads_per_wg;
+  const long long blocks = (long long)((p.S + P - 1) / P) * p.B * p.Hkv * ((p.H / p.Hkv) / p.heads_per_wg);
+  hipLaunchKernelGGL((fwd_bf16_kernel<D, ROPE, MASK, ALIBI>), dim3((unsigned)blocks), dim3(C::THREADS), 0, st, p);
   return hipGetLastError() == hipSuccess ? 0 : -3;
 }
 

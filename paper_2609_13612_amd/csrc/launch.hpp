@@ -16,6 +16,7 @@ struct FwdParams {
   const float* slopes;    // [H] or nullptr
   float scale;
   const float2* table;    // [rows >= S][D/2] (cos, sin); nullptr without RoPE
+  int heads_per_wg;       // set by the bf16 launcher: query heads packed per workgroup
 };
 
 struct BwdParams {

@@ -26,7 +26,7 @@
 // exactly from bf16 when its transposed copy is staged); this bounds the
 // accumulated rounding of P at 2^-12 per term and needs |dO| < 65504.
 // dP = dO V^T uses the bf16 inputs as they are.
-#include "common.hpp"
+#include "attn_tiles.hpp"
 #include "launch.hpp"
 
 namespace af {
@@ -55,72 +55,11 @@ __global__ __launch_bounds__(256) void bwd_rowstat_kernel(BwdParams p) {
   }
 }
 
-// ---------------------------------------------------------------- staging
-// Stage rows r0..r0+ROWS-1 of a [S][D] bf16 matrix into LDS as rows [ROWS][RP]
-// and, if T_PITCH > 0, transposed as [D][T_PITCH] with row order perm16.
-// Rows are optionally RoPE-rotated (position = row index; rotated values in
-// fp16 when F16OUT); rows >= S are 0.  T_F16 converts an unrotated bf16
-// matrix to fp16 in the transposed copy only.
-// Each thread handles 4 consecutive rows x one chunk unit (NeoX: the chunk
-// pair c, c + D/2; otherwise one 8-element chunk).
-template <int D, int ROPE, int ROWS, int RP, int T_PITCH, bool F16OUT = (ROPE != ROPE_NONE), bool T_F16 = false>
-__device__ __forceinline__ void stage_rows(uint16_t* __restrict__ dst, uint16_t* __restrict__ dst_t,
-                                           const uint16_t* __restrict__ src,
-                                           const float2* __restrict__ table, int r0, int S, int tid) {
-  constexpr int UNITS = (ROPE == ROPE_NEOX) ? D / 16 : D / 8;
-  constexpr int N = (ROWS / 4) * UNITS;
-#pragma unroll
-  for (int i = 0; i < (N + 255) / 256; ++i) {
-    const int it = tid + 256 * i;
-    if (N % 256 != 0 && it >= N) break;
-    const int j = it / UNITS, u = it % UNITS;
-    constexpr int NCH = (ROPE == ROPE_NEOX) ? 2 : 1;
-    const int d0[2] = {8 * u, 8 * u + D / 2};
-    u32x4 v[4][NCH];
-#pragma unroll
-    for (int b = 0; b < 4; ++b) {
-      const int n = r0 + 4 * j + b;
-#pragma unroll
-      for (int k = 0; k < NCH; ++k) v[b][k] = u32x4{0, 0, 0, 0};
-      if (n < S) {
-#pragma unroll
-        for (int k = 0; k < NCH; ++k) v[b][k] = ld16(src + (size_t)n * D + d0[k]);
-        if constexpr (ROPE == ROPE_NEOX)
-          rotate_neox8<false, F16OUT>(v[b][0], v[b][1], table + (size_t)n * (D / 2) + 8 * u);
-        if constexpr (ROPE == ROPE_INTERLEAVED)
-          rotate_interleaved8<false, F16OUT>(v[b][0], table + (size_t)n * (D / 2) + 4 * u);
-      }
-#pragma unroll
-      for (int k = 0; k < NCH; ++k) *reinterpret_cast<u32x4*>(dst + (4 * j + b) * RP + d0[k]) = v[b][k];
-    }
-    if constexpr (T_PITCH > 0) {
-      static_assert(!(T_F16 && ROPE != ROPE_NONE), "T_F16 converts unrotated bf16 rows only");
-      if constexpr (T_F16) {
-#pragma unroll
-        for (int b = 0; b < 4; ++b)
-#pragma unroll
-          for (int k = 0; k < NCH; ++k)
-#pragma unroll
-            for (int w = 0; w < 4; ++w) v[b][k][w] = pack_f16(bf_lo(v[b][k][w]), bf_hi(v[b][k][w]));
-      }
-      const int col = perm16(4 * j);
-#pragma unroll
-      for (int k = 0; k < NCH; ++k) {
-#pragma unroll
-        for (int w = 0; w < 4; ++w) {
-          u32x2 lo = {(v[0][k][w] & 0xffffu) | (v[1][k][w] << 16), (v[2][k][w] & 0xffffu) | (v[3][k][w] << 16)};
-          u32x2 hi = {(v[0][k][w] >> 16) | (v[1][k][w] & 0xffff0000u), (v[2][k][w] >> 16) | (v[3][k][w] & 0xffff0000u)};
-          *reinterpret_cast<u32x2*>(dst_t + (d0[k] + 2 * w) * T_PITCH + col) = lo;
-          *reinterpret_cast<u32x2*>(dst_t + (d0[k] + 2 * w + 1) * T_PITCH + col) = hi;
-        }
-      }
-    }
-  }
-}
-
+// ---------------------------------------------------------------- helpers
 // Load one lane's row of a bf16 matrix as the MFMA B operand (dims 16s + 8lg..+7),
-// RoPE-rotated in-lane (rotated values rounded to fp16).  Rows >= S give zeros.
-template <int D, int ROPE>
+// RoPE-rotated in-lane (rotated values rounded to fp16) or, with TO_F16,
+// converted to fp16 unrotated.  Rows >= S give zeros.
+template <int D, int ROPE, bool TO_F16 = false>
 __device__ __forceinline__ void load_row_operand(u32x4 (&reg)[D / 16], const uint16_t* __restrict__ src,
                                                  const float2* __restrict__ table, int n, int S, int lg) {
   constexpr int KS = D / 16;
@@ -135,6 +74,12 @@ __device__ __forceinline__ void load_row_operand(u32x4 (&reg)[D / 16], const uin
 #pragma unroll
       for (int s = 0; s < KS; ++s) rotate_interleaved8<false, true>(reg[s], table + (size_t)n * (D / 2) + 8 * s + 4 * lg);
     }
+  }
+  if constexpr (TO_F16 && ROPE == ROPE_NONE) {
+#pragma unroll
+    for (int s = 0; s < KS; ++s)
+#pragma unroll
+      for (int w = 0; w < 4; ++w) reg[s][w] = pack_f16(bf_lo(reg[s][w]), bf_hi(reg[s][w]));
   }
 }
 
@@ -190,45 +135,149 @@ __device__ __forceinline__ void store_grad_rows(f32x16 (&acc)[D / 32], float sca
   }
 }
 
-template <int D>
-struct BwdCfg {
-  static constexpr int BQ = 64;         // query rows per staged tile (dK/dV kernel)
-  static constexpr int BK = 64;         // key rows per staged tile (dQ kernel)
-  static constexpr int KS = D / 16;
-  static constexpr int MT = D / 32;
-  static constexpr int RP = D + 8;      // LDS pitch of [rows][D] tiles
-  static constexpr int TP = 64 + 8;     // LDS pitch of [D][64] transposed tiles
-};
+// Transposed MFMA A operand from a row-major LDS tile: rows (keys or queries)
+// base_row + {4 lg + i/4, +8} and 16 dims per 16-lane group (lds_read_tr16).
+__device__ __forceinline__ u32x4 tr_operand(const uint16_t* tile, int pitch, int row0, int col0, int lane) {
+  const int lg = lane >> 5;
+  const uint16_t* p = tile + (row0 + 4 * lg + ((lane & 15) >> 2)) * pitch + col0 + 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+  const u32x2 lo = lds_read_tr16(p);
+  const u32x2 hi = lds_read_tr16(p + 8 * pitch);
+  return u32x4{lo[0], lo[1], hi[0], hi[1]};
+}
 
 // ---------------------------------------------------------------- dK / dV
+// Query-side tile of the dK/dV kernel: 64 query rows of Q' (rotated, fp16 under
+// RoPE) and dO (converted to fp16), plus their LSE (log2 units) and delta.
+template <int D, int ROPE>
+struct QTileCfg {
+  static constexpr int NW = 4;
+  static constexpr int THREADS = 64 * NW;
+  static constexpr int KEYS = 32 * NW;        // keys per workgroup
+  static constexpr int BQ = 64;               // query rows per tile
+  static constexpr int KS = D / 16;
+  static constexpr int MT = D / 32;
+  static constexpr int QP = D + 16;           // pitch of Q' and dO rows (transpose reads)
+  static constexpr int Q_ELEMS = BQ * QP;
+  static constexpr int STAGE = 2 * Q_ELEMS;   // Q' then dO
+  static constexpr int Q_UNITS = (ROPE == ROPE_NEOX) ? D / 16 : D / 8;
+  static constexpr int Q_ITEMS = BQ * Q_UNITS;
+  static constexpr int QPT = (Q_ITEMS + THREADS - 1) / THREADS;
+  static constexpr int O_ITEMS = BQ * (D / 8);
+  static constexpr int OPT = (O_ITEMS + THREADS - 1) / THREADS;
+  static constexpr int CS = (ROPE == ROPE_NEOX) ? 4 : (ROPE == ROPE_INTERLEAVED ? 2 : 1);
+};
+
+template <int D, int ROPE>
+struct QTileRegs {
+  using C = QTileCfg<D, ROPE>;
+  u32x4 qa[C::QPT];
+  u32x4 qb[(ROPE == ROPE_NEOX) ? C::QPT : 1];
+  float4 cs[C::QPT][C::CS];
+  u32x4 o[C::OPT];
+  float lse2, del;
+};
+
+template <int D, int ROPE>
+__device__ __forceinline__ void qtile_load(QTileRegs<D, ROPE>& R, const uint16_t* __restrict__ Q,
+                                           const uint16_t* __restrict__ dO, const float* __restrict__ lse2,
+                                           const float* __restrict__ delta, const float2* __restrict__ table,
+                                           int m0, int S, int tid) {
+  using C = QTileCfg<D, ROPE>;
+#pragma unroll
+  for (int i = 0; i < C::QPT; ++i) {
+    const int it = tid + C::THREADS * i;
+    const int r = it / C::Q_UNITS, c = it % C::Q_UNITS, m = m0 + r;
+    const bool ok = (C::Q_ITEMS % C::THREADS == 0 || it < C::Q_ITEMS) && m < S;
+    R.qa[i] = ok ? ld16(Q + (size_t)m * D + 8 * c) : u32x4{0, 0, 0, 0};
+    if constexpr (ROPE == ROPE_NEOX) {
+      R.qb[i] = ok ? ld16(Q + (size_t)m * D + D / 2 + 8 * c) : u32x4{0, 0, 0, 0};
+      if (ok) {
+        load_cs(R.cs[i], table + (size_t)m * (D / 2) + 8 * c);
+      } else {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) R.cs[i][j] = float4{1.f, 0.f, 1.f, 0.f};
+      }
+    } else if constexpr (ROPE == ROPE_INTERLEAVED) {
+      if (ok) {
+        load_cs(R.cs[i], table + (size_t)m * (D / 2) + 4 * c);
+      } else {
+#pragma unroll
+        for (int j = 0; j < 2; ++j) R.cs[i][j] = float4{1.f, 0.f, 1.f, 0.f};
+      }
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < C::OPT; ++i) {
+    const int it = tid + C::THREADS * i;
+    const int r = it / (D / 8), c = it % (D / 8), m = m0 + r;
+    const bool ok = (C::O_ITEMS % C::THREADS == 0 || it < C::O_ITEMS) && m < S;
+    R.o[i] = ok ? ld16(dO + (size_t)m * D + 8 * c) : u32x4{0, 0, 0, 0};
+  }
+  // rows past S: P = exp2(x - inf) = 0 and delta = 0, so they contribute nothing
+  R.lse2 = (tid < C::BQ && m0 + tid < S) ? lse2[m0 + tid] : INFINITY;
+  R.del = (tid < C::BQ && m0 + tid < S) ? delta[m0 + tid] : 0.f;
+}
+
+template <int D, int ROPE>
+__device__ __forceinline__ void qtile_commit(QTileRegs<D, ROPE>& R, uint16_t* __restrict__ Qs,
+                                             uint16_t* __restrict__ Os, float* __restrict__ lse2s,
+                                             float* __restrict__ dels, int tid) {
+  using C = QTileCfg<D, ROPE>;
+#pragma unroll
+  for (int i = 0; i < C::QPT; ++i) {
+    const int it = tid + C::THREADS * i;
+    if (C::Q_ITEMS % C::THREADS != 0 && it >= C::Q_ITEMS) break;
+    const int r = it / C::Q_UNITS, c = it % C::Q_UNITS;
+    if constexpr (ROPE == ROPE_NEOX) {
+      rotate_neox8<false, true>(R.qa[i], R.qb[i], R.cs[i]);
+      *reinterpret_cast<u32x4*>(Qs + r * C::QP + 8 * c) = R.qa[i];
+      *reinterpret_cast<u32x4*>(Qs + r * C::QP + D / 2 + 8 * c) = R.qb[i];
+    } else {
+      if constexpr (ROPE == ROPE_INTERLEAVED) rotate_interleaved8<false, true>(R.qa[i], R.cs[i]);
+      *reinterpret_cast<u32x4*>(Qs + r * C::QP + 8 * c) = R.qa[i];
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < C::OPT; ++i) {
+    const int it = tid + C::THREADS * i;
+    if (C::O_ITEMS % C::THREADS != 0 && it >= C::O_ITEMS) break;
+    const int r = it / (D / 8), c = it % (D / 8);
+    u32x4 v = R.o[i];
+#pragma unroll
+    for (int w = 0; w < 4; ++w) v[w] = pack_f16(bf_lo(v[w]), bf_hi(v[w]));
+    *reinterpret_cast<u32x4*>(Os + r * C::QP + 8 * c) = v;
+  }
+  if (tid < C::BQ) {
+    lse2s[tid] = R.lse2;
+    dels[tid] = R.del;
+  }
+}
+
 template <int D, int ROPE, int MASK, bool ALIBI>
 __global__ __launch_bounds__(256) void bwd_dkdv_kernel(BwdParams p) {
-  using C = BwdCfg<D>;
+  using C = QTileCfg<D, ROPE>;
   constexpr bool QF16 = ROPE != ROPE_NONE;   // rotated operands (and dS with them) in fp16
-  __shared__ __attribute__((aligned(16))) uint16_t Qs[C::BQ * C::RP];
-  __shared__ __attribute__((aligned(16))) uint16_t Qt[D * C::TP];
-  __shared__ __attribute__((aligned(16))) uint16_t Os[C::BQ * C::RP];   // dO rows
-  __shared__ __attribute__((aligned(16))) uint16_t Ot[D * C::TP];       // dO^T, fp16
-  __shared__ __attribute__((aligned(16))) float lse2s[C::BQ];
-  __shared__ __attribute__((aligned(16))) float dels[C::BQ];
+  __shared__ __attribute__((aligned(16))) uint16_t smem[2 * C::STAGE];
+  __shared__ __attribute__((aligned(16))) float stat[2][2][C::BQ];   // [stage][lse2, delta][query]
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, lq = lane & 31, lg = lane >> 5;
   const int S = p.S;
-  const int nkb = (S + 127) / 128;
+  const int nkb = (S + C::KEYS - 1) / C::KEYS;
   const int BG = p.B * p.Hkv;
   const int bg = blockIdx.x % BG;
-  const int kb = nkb - 1 - (int)(blockIdx.x / BG);
+  const int kb = (int)(blockIdx.x / BG);   // ascending: under a causal mask the first key blocks see the most queries
   const int b = bg / p.Hkv, g = bg % p.Hkv;
   const int G = p.H / p.Hkv;
-  const int nb = kb * 128;            // first key of the block
+  const int nb = kb * C::KEYS;        // first key of the block
   const int nw = nb + 32 * wave;      // first key of this wave
   const int n = nw + lq;              // this lane's key
+  (void)nkb;
 
   const uint16_t* Kg = static_cast<const uint16_t*>(p.k) + (size_t)bg * S * D;
   const uint16_t* Vg = static_cast<const uint16_t*>(p.v) + (size_t)bg * S * D;
   u32x4 kreg[C::KS], vreg[C::KS];
   load_row_operand<D, ROPE>(kreg, Kg, p.table, n, S, lg);
-  load_row_operand<D, ROPE_NONE>(vreg, Vg, nullptr, n, S, lg);
+  load_row_operand<D, ROPE_NONE, true>(vreg, Vg, nullptr, n, S, lg);   // V as fp16 for dP = dO V^T
 
   f32x16 dk[C::MT], dv[C::MT];
 #pragma unroll
@@ -239,49 +288,68 @@ __global__ __launch_bounds__(256) void bwd_dkdv_kernel(BwdParams p) {
   const int ntq = (S + C::BQ - 1) / C::BQ;
   int tq_begin = 0, tq_end = ntq;
   if constexpr (MASK != MASK_NONE) tq_begin = nb / C::BQ;
-  if constexpr (MASK == MASK_SLIDING_WINDOW) tq_end = min(ntq, (min(nb + 127, S - 1) + W - 1) / C::BQ + 1);
+  if constexpr (MASK == MASK_SLIDING_WINDOW) tq_end = min(ntq, (min(nb + C::KEYS - 1, S - 1) + W - 1) / C::BQ + 1);
+  const int nq = max(0, tq_end - tq_begin);
+  const int steps = G * nq;           // (query head of the group, query tile) pairs
 
-  for (int hq = 0; hq < G; ++hq) {
-    const int h = g * G + hq;
-    const size_t bh = (size_t)b * p.H + h;
-    const uint16_t* Qh = static_cast<const uint16_t*>(p.q) + bh * S * D;
-    const uint16_t* dOh = static_cast<const uint16_t*>(p.dout) + bh * S * D;
-    const float* lse2h = p.lse2 + bh * S;
-    const float* delh = p.delta + bh * S;
+  auto head_of = [&](int s) { return g * G + s / nq; };
+  auto tile_of = [&](int s) { return tq_begin + s % nq; };
+  auto src = [&](int s, const uint16_t*& Qh, const uint16_t*& dOh, const float*& l2, const float*& dl) {
+    const size_t bh = (size_t)b * p.H + head_of(s);
+    Qh = static_cast<const uint16_t*>(p.q) + bh * S * D;
+    dOh = static_cast<const uint16_t*>(p.dout) + bh * S * D;
+    l2 = p.lse2 + bh * S;
+    dl = p.delta + bh * S;
+  };
+
+  QTileRegs<D, ROPE> R;
+  if (steps > 0) {
+    const uint16_t *Qh, *dOh;
+    const float *l2, *dl;
+    src(0, Qh, dOh, l2, dl);
+    qtile_load<D, ROPE>(R, Qh, dOh, l2, dl, p.table, tile_of(0) * C::BQ, S, tid);
+    qtile_commit<D, ROPE>(R, smem, smem + C::Q_ELEMS, stat[0][0], stat[0][1], tid);
+  }
+  __syncthreads();
+
+  for (int s = 0; s < steps; ++s) {
+    const int st = s & 1;
+    const uint16_t* Qs = smem + st * C::STAGE;
+    const uint16_t* Os = Qs + C::Q_ELEMS;
+    const float* lse2s = stat[st][0];
+    const float* dels = stat[st][1];
+    const bool more = s + 1 < steps;
+    if (more) {
+      const uint16_t *Qh, *dOh;
+      const float *l2, *dl;
+      src(s + 1, Qh, dOh, l2, dl);
+      qtile_load<D, ROPE>(R, Qh, dOh, l2, dl, p.table, tile_of(s + 1) * C::BQ, S, tid);
+    }
+    const int h = head_of(s);
+    const int mq0 = tile_of(s) * C::BQ;
     const float slope2 = ALIBI ? p.slopes[h] * kLog2e : 0.f;
 
-    for (int tq = tq_begin; tq < tq_end; ++tq) {
-      const int mq0 = tq * C::BQ;
-      __syncthreads();
-      stage_rows<D, ROPE, C::BQ, C::RP, C::TP>(Qs, Qt, Qh, p.table, mq0, S, tid);
-      stage_rows<D, ROPE_NONE, C::BQ, C::RP, C::TP, false, true>(Os, Ot, dOh, nullptr, mq0, S, tid);
-      if (tid < C::BQ) {
-        const int m = mq0 + tid;
-        lse2s[tid] = (m < S) ? lse2h[m] : INFINITY;
-        dels[tid] = (m < S) ? delh[m] : 0.f;
-      }
-      __syncthreads();
-
-      bool visible = nw < S;
-      if constexpr (MASK != MASK_NONE) visible = visible && (mq0 + C::BQ - 1 >= nw);
-      if constexpr (MASK == MASK_SLIDING_WINDOW) visible = visible && (mq0 <= nw + 31 + W - 1);
-      if (!visible) continue;
+    bool visible = nw < S;
+    if constexpr (MASK != MASK_NONE) visible = visible && (mq0 + C::BQ - 1 >= nw);
+    if constexpr (MASK == MASK_SLIDING_WINDOW) visible = visible && (mq0 <= nw + 31 + W - 1);
+    if (visible) {
       bool need_mask = nw + 32 > S;
       if constexpr (MASK != MASK_NONE) need_mask = need_mask || (mq0 < nw + 31);
       if constexpr (MASK == MASK_SLIDING_WINDOW) need_mask = need_mask || (mq0 + C::BQ - 1 - W >= nw);
-
-#pragma unroll
+      // one 32-query half at a time keeps the live register set small
+#pragma unroll 1
       for (int qt = 0; qt < 2; ++qt) {
-        f32x16 s = f32x16{}, dp = f32x16{};
+        // S = Q' K'^T and dP = dO V^T for 32 queries (rows) x this wave's 32 keys (columns)
+        f32x16 sc = f32x16{}, dp = f32x16{};
 #pragma unroll
         for (int k = 0; k < C::KS; ++k) {
-          u32x4 aq = *reinterpret_cast<const u32x4*>(Qs + (32 * qt + lq) * C::RP + 16 * k + 8 * lg);
-          s = mfma32<QF16>(aq, kreg[k], s);
+          const u32x4 aq = *reinterpret_cast<const u32x4*>(Qs + (32 * qt + lq) * C::QP + 16 * k + 8 * lg);
+          sc = mfma32<QF16>(aq, kreg[k], sc);
         }
 #pragma unroll
         for (int k = 0; k < C::KS; ++k) {
-          u32x4 ao = *reinterpret_cast<const u32x4*>(Os + (32 * qt + lq) * C::RP + 16 * k + 8 * lg);
-          dp = mfma32(ao, vreg[k], dp);
+          const u32x4 ao = *reinterpret_cast<const u32x4*>(Os + (32 * qt + lq) * C::QP + 16 * k + 8 * lg);
+          dp = mfma32<true>(ao, vreg[k], dp);
         }
         // element r: query ql = 32 qt + 8 (r/4) + 4 lg + r%4, key n
         float pr[16], ds[16];
@@ -296,7 +364,7 @@ __global__ __launch_bounds__(256) void bwd_dkdv_kernel(BwdParams p) {
           for (int e = 0; e < 4; ++e) {
             const int r = 4 * a + e;
             const int m = mq0 + qlb + e;
-            float x = ALIBI ? __builtin_fmaf(s[r], c2, slope2 * (float)(n - m)) : s[r] * c2;
+            const float x = ALIBI ? __builtin_fmaf(sc[r], c2, slope2 * (float)(n - m)) : sc[r] * c2;
             float pv = fast_exp2(x - lv[e]);
             if (need_mask) {
               bool ok = n < S;
@@ -316,19 +384,23 @@ __global__ __launch_bounds__(256) void bwd_dkdv_kernel(BwdParams p) {
             pb[hf][w] = pack_f16(pr[8 * hf + 2 * w], pr[8 * hf + 2 * w + 1]);
             db[hf][w] = pack_op<QF16>(ds[8 * hf + 2 * w], ds[8 * hf + 2 * w + 1]);
           }
+        // dV^T += dO^T P and dK'^T += Q'^T dS (transposed operands from row-major tiles)
 #pragma unroll
         for (int mt = 0; mt < C::MT; ++mt) {
 #pragma unroll
           for (int hf = 0; hf < 2; ++hf) {
-            const int col = 32 * qt + 16 * hf + 8 * lg;
-            u32x4 ao = *reinterpret_cast<const u32x4*>(Ot + (32 * mt + lq) * C::TP + col);
-            dv[mt] = mfma32<true>(ao, pb[hf], dv[mt]);
-            u32x4 aq = *reinterpret_cast<const u32x4*>(Qt + (32 * mt + lq) * C::TP + col);
-            dk[mt] = mfma32<QF16>(aq, db[hf], dk[mt]);
+            dv[mt] = mfma32<true>(tr_operand(Os, C::QP, 32 * qt + 16 * hf, 32 * mt, lane), pb[hf], dv[mt]);
+            dk[mt] = mfma32<QF16>(tr_operand(Qs, C::QP, 32 * qt + 16 * hf, 32 * mt, lane), db[hf], dk[mt]);
           }
         }
       }
     }
+
+    if (more) {
+      const int sn = (s + 1) & 1;
+      qtile_commit<D, ROPE>(R, smem + sn * C::STAGE, smem + sn * C::STAGE + C::Q_ELEMS, stat[sn][0], stat[sn][1], tid);
+    }
+    __syncthreads();
   }
 
   if (n < S) {
@@ -338,36 +410,44 @@ __global__ __launch_bounds__(256) void bwd_dkdv_kernel(BwdParams p) {
 }
 
 // ---------------------------------------------------------------- dQ
+// Same decomposition as the forward: 8 waves, GQA heads packed, double-buffered
+// K'/V tiles (attn_tiles.hpp); dQ'^T += K'^T dS^T with K'^T from transpose reads.
 template <int D, int ROPE, int MASK, bool ALIBI>
-__global__ __launch_bounds__(256) void bwd_dq_kernel(BwdParams p) {
-  using C = BwdCfg<D>;
+__global__ __launch_bounds__(512) void bwd_dq_kernel(BwdParams p) {
+  using C = TileCfg<D, ROPE>;
   constexpr bool QF16 = ROPE != ROPE_NONE;
-  __shared__ __attribute__((aligned(16))) uint16_t Ks[C::BK * C::RP];
-  __shared__ __attribute__((aligned(16))) uint16_t Kt[D * C::TP];
-  __shared__ __attribute__((aligned(16))) uint16_t Vs[C::BK * C::RP];
+  __shared__ __attribute__((aligned(16))) uint16_t smem[2 * C::STAGE];
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, lq = lane & 31, lg = lane >> 5;
   const int S = p.S;
-  const int BH = p.B * p.H;
-  const int nqb = (S + 127) / 128;
-  const int bh = blockIdx.x % BH;
-  const int qb = nqb - 1 - (int)(blockIdx.x / BH);
-  const int b = bh / p.H, h = bh % p.H;
-  const int g = h / (p.H / p.Hkv);
-  const int m0 = qb * 128;
-  const int mw = m0 + 32 * wave;
+  const int HP = p.heads_per_wg;
+  const int WPH = C::NW / HP;
+  const int P = 32 * WPH;
+  const int G = p.H / p.Hkv;
+  const int groups = G / HP;
+  const int units = p.B * p.Hkv * groups;
+  const int npb = (S + P - 1) / P;
+  const int unit = blockIdx.x % units;
+  const int pb = npb - 1 - (int)(blockIdx.x / units);
+  const int hg = unit % groups, bg = unit / groups;
+  const int b = bg / p.Hkv, g = bg % p.Hkv;
+  const int h = g * G + hg * HP + wave / WPH;
+  const int p0 = pb * P;
+  const int mw = p0 + 32 * (wave % WPH);
   const int m = mw + lq;
+  const int p_end = min(p0 + P, S);
+  const size_t bh = (size_t)b * p.H + h;
 
-  const uint16_t* Qh = static_cast<const uint16_t*>(p.q) + (size_t)bh * S * D;
-  const uint16_t* dOh = static_cast<const uint16_t*>(p.dout) + (size_t)bh * S * D;
-  const uint16_t* Kg = static_cast<const uint16_t*>(p.k) + (size_t)(b * p.Hkv + g) * S * D;
-  const uint16_t* Vg = static_cast<const uint16_t*>(p.v) + (size_t)(b * p.Hkv + g) * S * D;
+  const uint16_t* Qh = static_cast<const uint16_t*>(p.q) + bh * S * D;
+  const uint16_t* dOh = static_cast<const uint16_t*>(p.dout) + bh * S * D;
+  const uint16_t* Kg = static_cast<const uint16_t*>(p.k) + (size_t)bg * S * D;
+  const uint16_t* Vg = static_cast<const uint16_t*>(p.v) + (size_t)bg * S * D;
 
   u32x4 qreg[C::KS], oreg[C::KS];
   load_row_operand<D, ROPE>(qreg, Qh, p.table, m, S, lg);
   load_row_operand<D, ROPE_NONE>(oreg, dOh, nullptr, m, S, lg);
-  const float lse2 = (m < S) ? p.lse2[(size_t)bh * S + m] : INFINITY;
-  const float del = (m < S) ? p.delta[(size_t)bh * S + m] : 0.f;
+  const float lse2 = (m < S) ? p.lse2[bh * S + m] : INFINITY;
+  const float del = (m < S) ? p.delta[bh * S + m] : 0.f;
 
   f32x16 dq[C::MT];
 #pragma unroll
@@ -376,70 +456,79 @@ __global__ __launch_bounds__(256) void bwd_dq_kernel(BwdParams p) {
   const float c2 = p.scale * kLog2e;
   const float slope2 = ALIBI ? p.slopes[h] * kLog2e : 0.f;
   const int W = p.window;
-  const int ntiles = (S + C::BK - 1) / C::BK;
+  const int ntiles = (S + C::BN - 1) / C::BN;
   int t_begin = 0, t_end = ntiles;
-  if constexpr (MASK != MASK_NONE) t_end = min(ntiles, (min(m0 + 128, S) - 1) / C::BK + 1);
-  if constexpr (MASK == MASK_SLIDING_WINDOW) t_begin = max(0, m0 - W + 1) / C::BK;
+  if constexpr (MASK != MASK_NONE) t_end = min(ntiles, (p_end - 1) / C::BN + 1);
+  if constexpr (MASK == MASK_SLIDING_WINDOW) t_begin = max(0, p0 - W + 1) / C::BN;
+
+  TileRegs<D, ROPE> R;
+  if (t_begin < t_end) {
+    tile_load<D, ROPE>(R, Kg, Vg, p.table, t_begin * C::BN, S, tid);
+    tile_commit<D, ROPE>(R, smem, smem + C::K_ELEMS, tid);
+  }
+  __syncthreads();
 
   for (int t = t_begin; t < t_end; ++t) {
-    const int n0 = t * C::BK;
-    __syncthreads();
-    stage_rows<D, ROPE, C::BK, C::RP, C::TP>(Ks, Kt, Kg, p.table, n0, S, tid);
-    stage_rows<D, ROPE_NONE, C::BK, C::RP, 0>(Vs, nullptr, Vg, nullptr, n0, S, tid);
-    __syncthreads();
+    const int n0 = t * C::BN;
+    const uint16_t* Ks = smem + ((t - t_begin) & 1) * C::STAGE;
+    const uint16_t* Vs = Ks + C::K_ELEMS;
+    const bool more = t + 1 < t_end;
+    if (more) tile_load<D, ROPE>(R, Kg, Vg, p.table, n0 + C::BN, S, tid);
 
     bool visible = mw < S;
     if constexpr (MASK != MASK_NONE) visible = visible && (n0 <= mw + 31);
-    if constexpr (MASK == MASK_SLIDING_WINDOW) visible = visible && (n0 + C::BK - 1 > mw - W);
-    if (!visible) continue;
-    bool need_mask = n0 + C::BK > S;
-    if constexpr (MASK != MASK_NONE) need_mask = need_mask || (n0 + C::BK - 1 > mw);
-    if constexpr (MASK == MASK_SLIDING_WINDOW) need_mask = need_mask || (n0 <= mw + 31 - W);
-
+    if constexpr (MASK == MASK_SLIDING_WINDOW) visible = visible && (n0 + C::BN - 1 > mw - W);
+    if (visible) {
+      bool need_mask = n0 + C::BN > S;
+      if constexpr (MASK != MASK_NONE) need_mask = need_mask || (n0 + C::BN - 1 > mw);
+      if constexpr (MASK == MASK_SLIDING_WINDOW) need_mask = need_mask || (n0 <= mw + 31 - W);
 #pragma unroll
-    for (int kt = 0; kt < 2; ++kt) {
-      f32x16 s = f32x16{}, dp = f32x16{};
+      for (int kt = 0; kt < 2; ++kt) {
+        f32x16 sc = f32x16{}, dp = f32x16{};
 #pragma unroll
-      for (int k = 0; k < C::KS; ++k) {
-        u32x4 ak = *reinterpret_cast<const u32x4*>(Ks + (32 * kt + lq) * C::RP + 16 * k + 8 * lg);
-        s = mfma32<QF16>(ak, qreg[k], s);
-      }
-#pragma unroll
-      for (int k = 0; k < C::KS; ++k) {
-        u32x4 av = *reinterpret_cast<const u32x4*>(Vs + (32 * kt + lq) * C::RP + 16 * k + 8 * lg);
-        dp = mfma32(av, oreg[k], dp);
-      }
-      // element r: key nn = n0 + 32 kt + 8 (r/4) + 4 lg + r%4, query m
-      float ds[16];
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int nn = n0 + 32 * kt + 8 * (r >> 2) + 4 * lg + (r & 3);
-        float x = ALIBI ? __builtin_fmaf(s[r], c2, slope2 * (float)(nn - m)) : s[r] * c2;
-        float pv = fast_exp2(x - lse2);
-        if (need_mask) {
-          bool ok = nn < S;
-          if constexpr (MASK != MASK_NONE) ok = ok && (nn <= m);
-          if constexpr (MASK == MASK_SLIDING_WINDOW) ok = ok && (nn > m - W);
-          if (!ok) pv = 0.f;
+        for (int k = 0; k < C::KS; ++k) {
+          const u32x4 ak = *reinterpret_cast<const u32x4*>(Ks + (32 * kt + lq) * C::KP + 16 * k + 8 * lg);
+          sc = mfma32<QF16>(ak, qreg[k], sc);
         }
-        ds[r] = pv * (dp[r] - del);
-      }
-      u32x4 db[2];
 #pragma unroll
-      for (int hf = 0; hf < 2; ++hf)
-#pragma unroll
-        for (int w = 0; w < 4; ++w) db[hf][w] = pack_op<QF16>(ds[8 * hf + 2 * w], ds[8 * hf + 2 * w + 1]);
-#pragma unroll
-      for (int mt = 0; mt < C::MT; ++mt) {
-#pragma unroll
-        for (int hf = 0; hf < 2; ++hf) {
-          u32x4 ak = *reinterpret_cast<const u32x4*>(Kt + (32 * mt + lq) * C::TP + 32 * kt + 16 * hf + 8 * lg);
-          dq[mt] = mfma32<QF16>(ak, db[hf], dq[mt]);
+        for (int k = 0; k < C::KS; ++k) {
+          const u32x4 av = *reinterpret_cast<const u32x4*>(Vs + (32 * kt + lq) * C::VP + 16 * k + 8 * lg);
+          dp = mfma32(av, oreg[k], dp);
         }
+        // element r: key nn = n0 + 32 kt + 8 (r/4) + 4 lg + r%4, query m
+        float ds[16];
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int nn = n0 + 32 * kt + 8 * (r >> 2) + 4 * lg + (r & 3);
+          const float x = ALIBI ? __builtin_fmaf(sc[r], c2, slope2 * (float)(nn - m)) : sc[r] * c2;
+          float pv = fast_exp2(x - lse2);
+          if (need_mask) {
+            bool ok = nn < S;
+            if constexpr (MASK != MASK_NONE) ok = ok && (nn <= m);
+            if constexpr (MASK == MASK_SLIDING_WINDOW) ok = ok && (nn > m - W);
+            if (!ok) pv = 0.f;
+          }
+          ds[r] = pv * (dp[r] - del);
+        }
+        u32x4 db[2];
+#pragma unroll
+        for (int hf = 0; hf < 2; ++hf)
+#pragma unroll
+          for (int w = 0; w < 4; ++w) db[hf][w] = pack_op<QF16>(ds[8 * hf + 2 * w], ds[8 * hf + 2 * w + 1]);
+#pragma unroll
+        for (int mt = 0; mt < C::MT; ++mt)
+#pragma unroll
+          for (int hf = 0; hf < 2; ++hf)
+            dq[mt] = mfma32<QF16>(tr_operand(Ks, C::KP, 32 * kt + 16 * hf, 32 * mt, lane), db[hf], dq[mt]);
       }
     }
+    if (more) {
+      uint16_t* Kn = smem + ((t + 1 - t_begin) & 1) * C::STAGE;
+      tile_commit<D, ROPE>(R, Kn, Kn + C::K_ELEMS, tid);
+    }
+    __syncthreads();
   }
-  if (m < S) store_grad_rows<D, ROPE>(dq, p.scale, static_cast<uint16_t*>(p.dq) + (size_t)bh * S * D, p.table, m, lg);
+  if (m < S) store_grad_rows<D, ROPE>(dq, p.scale, static_cast<uint16_t*>(p.dq) + bh * S * D, p.table, m, lg);
 }
 
 // ---------------------------------------------------------------- launch
@@ -448,9 +537,15 @@ static int launch_one(const BwdParams& p, hipStream_t st) {
   constexpr int RPB = 256 / (D / 8);
   const long long rows = (long long)p.B * p.H * p.S;
   hipLaunchKernelGGL(bwd_rowstat_kernel<D>, dim3((unsigned)((rows + RPB - 1) / RPB)), dim3(256), 0, st, p);
-  const int nkb = (p.S + 127) / 128;
-  hipLaunchKernelGGL((bwd_dkdv_kernel<D, ROPE, MASK, ALIBI>), dim3((unsigned)(nkb * p.B * p.Hkv)), dim3(256), 0, st, p);
-  hipLaunchKernelGGL((bwd_dq_kernel<D, ROPE, MASK, ALIBI>), dim3((unsigned)(nkb * p.B * p.H)), dim3(256), 0, st, p);
+  using QC = QTileCfg<D, ROPE>;
+  const int nkb = (p.S + QC::KEYS - 1) / QC::KEYS;
+  hipLaunchKernelGGL((bwd_dkdv_kernel<D, ROPE, MASK, ALIBI>), dim3((unsigned)(nkb * p.B * p.Hkv)), dim3(QC::THREADS), 0, st, p);
+  using TC = TileCfg<D, ROPE>;
+  BwdParams pq = p;
+  pq.heads_per_wg = heads_per_wg(p.H / p.Hkv);
+  const int P = TC::ROWS / pq.heads_per_wg;
+  const long long qblocks = (long long)((p.S + P - 1) / P) * p.B * p.Hkv * ((p.H / p.Hkv) / pq.heads_per_wg);
+  hipLaunchKernelGGL((bwd_dq_kernel<D, ROPE, MASK, ALIBI>), dim3((unsigned)qblocks), dim3(TC::THREADS), 0, st, pq);
   return hipGetLastError() == hipSuccess ? 0 : -3;
 }
 

@@ -35,6 +35,7 @@ struct BwdParams {
   const float* slopes;
   float scale;
   const float2* table;
+  int heads_per_wg;       // set by the launcher for the dQ kernel
 };
 
 struct RopeParams {

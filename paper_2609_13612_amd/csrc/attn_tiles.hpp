@@ -41,6 +41,9 @@ struct TileRegs {
   u32x4 v[C::VPT];
 };
 
+// Rows past S are clamped to row S-1 so every load is unconditional: those
+// keys are masked out of the scores and their V rows (finite data) receive
+// zero probability.
 template <int D, int ROPE>
 __device__ __forceinline__ void tile_load(TileRegs<D, ROPE>& R, const uint16_t* __restrict__ K,
                                           const uint16_t* __restrict__ V, const float2* __restrict__ table,
@@ -49,32 +52,22 @@ __device__ __forceinline__ void tile_load(TileRegs<D, ROPE>& R, const uint16_t* 
 #pragma unroll
   for (int i = 0; i < C::KPT; ++i) {
     const int it = tid + C::THREADS * i;
-    const int r = it / C::K_UNITS, c = it % C::K_UNITS, n = n0 + r;
-    const bool ok = (C::K_ITEMS % C::THREADS == 0 || it < C::K_ITEMS) && n < S;
-    R.ka[i] = ok ? ld16(K + (size_t)n * D + 8 * c) : u32x4{0, 0, 0, 0};
+    if (C::K_ITEMS % C::THREADS != 0 && it >= C::K_ITEMS) break;
+    const int r = it / C::K_UNITS, c = it % C::K_UNITS, n = min(n0 + r, S - 1);
+    R.ka[i] = ld16(K + (size_t)n * D + 8 * c);
     if constexpr (ROPE == ROPE_NEOX) {
-      R.kb[i] = ok ? ld16(K + (size_t)n * D + D / 2 + 8 * c) : u32x4{0, 0, 0, 0};
-      if (ok) {
-        load_cs(R.cs[i], table + (size_t)n * (D / 2) + 8 * c);
-      } else {
-#pragma unroll
-        for (int j = 0; j < 4; ++j) R.cs[i][j] = float4{1.f, 0.f, 1.f, 0.f};
-      }
+      R.kb[i] = ld16(K + (size_t)n * D + D / 2 + 8 * c);
+      load_cs(R.cs[i], table + (size_t)n * (D / 2) + 8 * c);
     } else if constexpr (ROPE == ROPE_INTERLEAVED) {
-      if (ok) {
-        load_cs(R.cs[i], table + (size_t)n * (D / 2) + 4 * c);
-      } else {
-#pragma unroll
-        for (int j = 0; j < 2; ++j) R.cs[i][j] = float4{1.f, 0.f, 1.f, 0.f};
-      }
+      load_cs(R.cs[i], table + (size_t)n * (D / 2) + 4 * c);
     }
   }
 #pragma unroll
   for (int i = 0; i < C::VPT; ++i) {
     const int it = tid + C::THREADS * i;
-    const int r = it / (D / 8), c = it % (D / 8), n = n0 + r;
-    const bool ok = (C::V_ITEMS % C::THREADS == 0 || it < C::V_ITEMS) && n < S;
-    R.v[i] = ok ? ld16(V + (size_t)n * D + 8 * c) : u32x4{0, 0, 0, 0};
+    if (C::V_ITEMS % C::THREADS != 0 && it >= C::V_ITEMS) break;
+    const int r = it / (D / 8), c = it % (D / 8), n = min(n0 + r, S - 1);
+    R.v[i] = ld16(V + (size_t)n * D + 8 * c);
   }
 }
 

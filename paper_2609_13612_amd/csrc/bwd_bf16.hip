@@ -177,6 +177,8 @@ struct QTileRegs {
   float lse2, del;
 };
 
+// Rows past S are clamped to row S-1 so every load is unconditional; they get
+// LSE = +inf (so P = 0) and delta = 0, so they contribute nothing.
 template <int D, int ROPE>
 __device__ __forceinline__ void qtile_load(QTileRegs<D, ROPE>& R, const uint16_t* __restrict__ Q,
                                            const uint16_t* __restrict__ dO, const float* __restrict__ lse2,
@@ -186,36 +188,28 @@ __device__ __forceinline__ void qtile_load(QTileRegs<D, ROPE>& R, const uint16_t
 #pragma unroll
   for (int i = 0; i < C::QPT; ++i) {
     const int it = tid + C::THREADS * i;
-    const int r = it / C::Q_UNITS, c = it % C::Q_UNITS, m = m0 + r;
-    const bool ok = (C::Q_ITEMS % C::THREADS == 0 || it < C::Q_ITEMS) && m < S;
-    R.qa[i] = ok ? ld16(Q + (size_t)m * D + 8 * c) : u32x4{0, 0, 0, 0};
+    if (C::Q_ITEMS % C::THREADS != 0 && it >= C::Q_ITEMS) break;
+    const int r = it / C::Q_UNITS, c = it % C::Q_UNITS, m = min(m0 + r, S - 1);
+    R.qa[i] = ld16(Q + (size_t)m * D + 8 * c);
     if constexpr (ROPE == ROPE_NEOX) {
-      R.qb[i] = ok ? ld16(Q + (size_t)m * D + D / 2 + 8 * c) : u32x4{0, 0, 0, 0};
-      if (ok) {
-        load_cs(R.cs[i], table + (size_t)m * (D / 2) + 8 * c);
-      } else {
-#pragma unroll
-        for (int j = 0; j < 4; ++j) R.cs[i][j] = float4{1.f, 0.f, 1.f, 0.f};
-      }
+      R.qb[i] = ld16(Q + (size_t)m * D + D / 2 + 8 * c);
+      load_cs(R.cs[i], table + (size_t)m * (D / 2) + 8 * c);
     } else if constexpr (ROPE == ROPE_INTERLEAVED) {
-      if (ok) {
-        load_cs(R.cs[i], table + (size_t)m * (D / 2) + 4 * c);
-      } else {
-#pragma unroll
-        for (int j = 0; j < 2; ++j) R.cs[i][j] = float4{1.f, 0.f, 1.f, 0.f};
-      }
+      load_cs(R.cs[i], table + (size_t)m * (D / 2) + 4 * c);
     }
   }
 #pragma unroll
   for (int i = 0; i < C::OPT; ++i) {
     const int it = tid + C::THREADS * i;
-    const int r = it / (D / 8), c = it % (D / 8), m = m0 + r;
-    const bool ok = (C::O_ITEMS % C::THREADS == 0 || it < C::O_ITEMS) && m < S;
-    R.o[i] = ok ? ld16(dO + (size_t)m * D + 8 * c) : u32x4{0, 0, 0, 0};
+    if (C::O_ITEMS % C::THREADS != 0 && it >= C::O_ITEMS) break;
+    const int r = it / (D / 8), c = it % (D / 8), m = min(m0 + r, S - 1);
+    R.o[i] = ld16(dO + (size_t)m * D + 8 * c);
   }
-  // rows past S: P = exp2(x - inf) = 0 and delta = 0, so they contribute nothing
-  R.lse2 = (tid < C::BQ && m0 + tid < S) ? lse2[m0 + tid] : INFINITY;
-  R.del = (tid < C::BQ && m0 + tid < S) ? delta[m0 + tid] : 0.f;
+  const int ms = min(m0 + (tid & (C::BQ - 1)), S - 1);
+  const bool in = m0 + (tid & (C::BQ - 1)) < S;
+  const float l = lse2[ms], dl = delta[ms];
+  R.lse2 = in ? l : INFINITY;
+  R.del = in ? dl : 0.f;
 }
 
 template <int D, int ROPE>
@@ -339,16 +333,14 @@ __global__ __launch_bounds__(256) void bwd_dkdv_kernel(BwdParams p) {
       // one 32-query half at a time keeps the live register set small
 #pragma unroll 1
       for (int qt = 0; qt < 2; ++qt) {
-        // S = Q' K'^T and dP = dO V^T for 32 queries (rows) x this wave's 32 keys (columns)
+        // S = Q' K'^T and dP = dO V^T for 32 queries (rows) x this wave's 32 keys
+        // (columns); the two MFMA chains are interleaved.
         f32x16 sc = f32x16{}, dp = f32x16{};
 #pragma unroll
         for (int k = 0; k < C::KS; ++k) {
           const u32x4 aq = *reinterpret_cast<const u32x4*>(Qs + (32 * qt + lq) * C::QP + 16 * k + 8 * lg);
-          sc = mfma32<QF16>(aq, kreg[k], sc);
-        }
-#pragma unroll
-        for (int k = 0; k < C::KS; ++k) {
           const u32x4 ao = *reinterpret_cast<const u32x4*>(Os + (32 * qt + lq) * C::QP + 16 * k + 8 * lg);
+          sc = mfma32<QF16>(aq, kreg[k], sc);
           dp = mfma32<true>(ao, vreg[k], dp);
         }
         // element r: query ql = 32 qt + 8 (r/4) + 4 lg + r%4, key n
@@ -363,19 +355,23 @@ __global__ __launch_bounds__(256) void bwd_dkdv_kernel(BwdParams p) {
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
             const int r = 4 * a + e;
-            const int m = mq0 + qlb + e;
-            const float x = ALIBI ? __builtin_fmaf(sc[r], c2, slope2 * (float)(n - m)) : sc[r] * c2;
-            float pv = fast_exp2(x - lv[e]);
-            if (need_mask) {
-              bool ok = n < S;
-              if constexpr (MASK != MASK_NONE) ok = ok && (n <= m);
-              if constexpr (MASK == MASK_SLIDING_WINDOW) ok = ok && (n > m - W);
-              if (!ok) pv = 0.f;
-            }
-            pr[r] = pv;
-            ds[r] = pv * (dp[r] - dv4[e]);
+            const float x = ALIBI ? __builtin_fmaf(sc[r], c2, slope2 * (float)(n - (mq0 + qlb + e))) : sc[r] * c2;
+            pr[r] = fast_exp2(x - lv[e]);
+            ds[r] = dp[r] - dv4[e];
           }
         }
+        if (need_mask) {   // wave-uniform: diagonal, window-edge and sequence-end tiles only
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int m = mq0 + 32 * qt + 8 * (r >> 2) + 4 * lg + (r & 3);
+            bool ok = n < S;
+            if constexpr (MASK != MASK_NONE) ok = ok && (n <= m);
+            if constexpr (MASK == MASK_SLIDING_WINDOW) ok = ok && (n > m - W);
+            pr[r] = ok ? pr[r] : 0.f;
+          }
+        }
+#pragma unroll
+        for (int r = 0; r < 16; ++r) ds[r] *= pr[r];
         u32x4 pb[2], db[2];
 #pragma unroll
         for (int hf = 0; hf < 2; ++hf)
@@ -386,9 +382,9 @@ __global__ __launch_bounds__(256) void bwd_dkdv_kernel(BwdParams p) {
           }
         // dV^T += dO^T P and dK'^T += Q'^T dS (transposed operands from row-major tiles)
 #pragma unroll
-        for (int mt = 0; mt < C::MT; ++mt) {
+        for (int hf = 0; hf < 2; ++hf) {
 #pragma unroll
-          for (int hf = 0; hf < 2; ++hf) {
+          for (int mt = 0; mt < C::MT; ++mt) {
             dv[mt] = mfma32<true>(tr_operand(Os, C::QP, 32 * qt + 16 * hf, 32 * mt, lane), pb[hf], dv[mt]);
             dk[mt] = mfma32<QF16>(tr_operand(Qs, C::QP, 32 * qt + 16 * hf, 32 * mt, lane), db[hf], dk[mt]);
           }
@@ -444,10 +440,11 @@ __global__ __launch_bounds__(512) void bwd_dq_kernel(BwdParams p) {
   const uint16_t* Vg = static_cast<const uint16_t*>(p.v) + (size_t)bg * S * D;
 
   u32x4 qreg[C::KS], oreg[C::KS];
-  load_row_operand<D, ROPE>(qreg, Qh, p.table, m, S, lg);
-  load_row_operand<D, ROPE_NONE>(oreg, dOh, nullptr, m, S, lg);
-  const float lse2 = (m < S) ? p.lse2[bh * S + m] : INFINITY;
-  const float del = (m < S) ? p.delta[bh * S + m] : 0.f;
+  const int mc = min(m, S - 1);   // rows past S compute on row S-1 and are never stored
+  load_row_operand<D, ROPE>(qreg, Qh, p.table, mc, S, lg);
+  load_row_operand<D, ROPE_NONE>(oreg, dOh, nullptr, mc, S, lg);
+  const float lse2 = (m < S) ? p.lse2[bh * S + mc] : INFINITY;
+  const float del = (m < S) ? p.delta[bh * S + mc] : 0.f;
 
   f32x16 dq[C::MT];
 #pragma unroll
@@ -488,11 +485,8 @@ __global__ __launch_bounds__(512) void bwd_dq_kernel(BwdParams p) {
 #pragma unroll
         for (int k = 0; k < C::KS; ++k) {
           const u32x4 ak = *reinterpret_cast<const u32x4*>(Ks + (32 * kt + lq) * C::KP + 16 * k + 8 * lg);
-          sc = mfma32<QF16>(ak, qreg[k], sc);
-        }
-#pragma unroll
-        for (int k = 0; k < C::KS; ++k) {
           const u32x4 av = *reinterpret_cast<const u32x4*>(Vs + (32 * kt + lq) * C::VP + 16 * k + 8 * lg);
+          sc = mfma32<QF16>(ak, qreg[k], sc);
           dp = mfma32(av, oreg[k], dp);
         }
         // element r: key nn = n0 + 32 kt + 8 (r/4) + 4 lg + r%4, query m
@@ -501,15 +495,20 @@ __global__ __launch_bounds__(512) void bwd_dq_kernel(BwdParams p) {
         for (int r = 0; r < 16; ++r) {
           const int nn = n0 + 32 * kt + 8 * (r >> 2) + 4 * lg + (r & 3);
           const float x = ALIBI ? __builtin_fmaf(sc[r], c2, slope2 * (float)(nn - m)) : sc[r] * c2;
-          float pv = fast_exp2(x - lse2);
-          if (need_mask) {
+          ds[r] = fast_exp2(x - lse2);
+        }
+        if (need_mask) {   // wave-uniform
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int nn = n0 + 32 * kt + 8 * (r >> 2) + 4 * lg + (r & 3);
             bool ok = nn < S;
             if constexpr (MASK != MASK_NONE) ok = ok && (nn <= m);
             if constexpr (MASK == MASK_SLIDING_WINDOW) ok = ok && (nn > m - W);
-            if (!ok) pv = 0.f;
+            ds[r] = ok ? ds[r] : 0.f;
           }
-          ds[r] = pv * (dp[r] - del);
         }
+#pragma unroll
+        for (int r = 0; r < 16; ++r) ds[r] *= dp[r] - del;
         u32x4 db[2];
 #pragma unroll
         for (int hf = 0; hf < 2; ++hf)

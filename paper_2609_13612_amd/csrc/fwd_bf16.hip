@@ -71,20 +71,19 @@ __global__ __launch_bounds__(512) void fwd_bf16_kernel(FwdParams p) {
   const uint16_t* __restrict__ V = static_cast<const uint16_t*>(p.v) + (size_t)bg * S * D;
 
   // Query operand (B of S^T = K Q^T): lane holds row m, dims 16s + 8lg .. +7.
+  // Rows past S load row S-1 (finite data; never stored).
+  const int mc = min(m, S - 1);
   u32x4 qreg[C::KS];
 #pragma unroll
-  for (int s = 0; s < C::KS; ++s)
-    qreg[s] = (m < S) ? ld16(Q + (size_t)m * D + 16 * s + 8 * lg) : u32x4{0, 0, 0, 0};
-  if (m < S) {
-    if constexpr (ROPE == ROPE_NEOX) {
+  for (int s = 0; s < C::KS; ++s) qreg[s] = ld16(Q + (size_t)mc * D + 16 * s + 8 * lg);
+  if constexpr (ROPE == ROPE_NEOX) {
 #pragma unroll
-      for (int s = 0; s < C::KS / 2; ++s)
-        rotate_neox8<false, true>(qreg[s], qreg[s + C::KS / 2], p.table + (size_t)m * (D / 2) + 16 * s + 8 * lg);
-    } else if constexpr (ROPE == ROPE_INTERLEAVED) {
+    for (int s = 0; s < C::KS / 2; ++s)
+      rotate_neox8<false, true>(qreg[s], qreg[s + C::KS / 2], p.table + (size_t)mc * (D / 2) + 16 * s + 8 * lg);
+  } else if constexpr (ROPE == ROPE_INTERLEAVED) {
 #pragma unroll
-      for (int s = 0; s < C::KS; ++s)
-        rotate_interleaved8<false, true>(qreg[s], p.table + (size_t)m * (D / 2) + 8 * s + 4 * lg);
-    }
+    for (int s = 0; s < C::KS; ++s)
+      rotate_interleaved8<false, true>(qreg[s], p.table + (size_t)mc * (D / 2) + 8 * s + 4 * lg);
   }
 
   const float c2 = p.scale * kLog2e;                          // score -> log2 units
@@ -126,38 +125,44 @@ __global__ __launch_bounds__(512) void fwd_bf16_kernel(FwdParams p) {
     if constexpr (MASK != MASK_NONE) visible = visible && (n0 <= mw + 31);
     if constexpr (MASK == MASK_SLIDING_WINDOW) visible = visible && (n0 + C::BN - 1 > mw - W);
     if (visible) {   // wave-uniform
-      // S^T = K' Q'^T: two 32-key subtiles.
-      f32x16 st[2];
+      // S^T = K' Q'^T: two 32-key subtiles, their MFMA chains interleaved.
+      f32x16 st[2] = {f32x16{}, f32x16{}};
 #pragma unroll
-      for (int kt = 0; kt < 2; ++kt) {
-        st[kt] = f32x16{};
+      for (int s = 0; s < C::KS; ++s) {
 #pragma unroll
-        for (int s = 0; s < C::KS; ++s) {
+        for (int kt = 0; kt < 2; ++kt) {
           u32x4 a = *reinterpret_cast<const u32x4*>(Ks + (32 * kt + lq) * C::KP + 16 * s + 8 * lg);
           st[kt] = mfma32<QF16>(a, qreg[s], st[kt]);
         }
       }
 
+      // Scores in log2 units (ALiBi folded in); element r of subtile kt is key
+      // n0 + 32 kt + 8 (r/4) + 4 lg + r%4.
+      if constexpr (ALIBI) {
+#pragma unroll
+        for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int n = n0 + 32 * kt + 8 * (r >> 2) + 4 * lg + (r & 3);
+            st[kt][r] = __builtin_fmaf(st[kt][r], c2, slope2 * (float)(n - m));
+          }
+      }
+      // Masked entries at -inf; only tiles that cross the diagonal, the window
+      // edge or the sequence end pay for it (one wave-uniform branch).
       bool need_mask = n0 + C::BN > S;
       if constexpr (MASK != MASK_NONE) need_mask = need_mask || (n0 + C::BN - 1 > mw);
       if constexpr (MASK == MASK_SLIDING_WINDOW) need_mask = need_mask || (n0 <= mw + 31 - W);
-
-      // Scores in log2 units (ALiBi folded in), masked entries at -inf.
+      if (need_mask) {
 #pragma unroll
-      for (int kt = 0; kt < 2; ++kt) {
+        for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int n = n0 + 32 * kt + 8 * (r >> 2) + 4 * lg + (r & 3);
-          float x = st[kt][r];
-          if constexpr (ALIBI) x = __builtin_fmaf(x, c2, slope2 * (float)(n - m));
-          if (need_mask) {
+          for (int r = 0; r < 16; ++r) {
+            const int n = n0 + 32 * kt + 8 * (r >> 2) + 4 * lg + (r & 3);
             bool ok = n < S;
             if constexpr (MASK != MASK_NONE) ok = ok && (n <= m);
             if constexpr (MASK == MASK_SLIDING_WINDOW) ok = ok && (n > m - W);
-            if (!ok) x = -INFINITY;
+            st[kt][r] = ok ? st[kt][r] : -INFINITY;
           }
-          st[kt][r] = x;
-        }
       }
 
       float mx = -INFINITY;
@@ -196,12 +201,13 @@ __global__ __launch_bounds__(512) void fwd_bf16_kernel(FwdParams p) {
       l_run += rs;
 
       // O^T += V^T P^T; the V^T operand is two transpose reads of row-major V.
+      // The head-dimension tiles are independent accumulators, interleaved.
 #pragma unroll
-      for (int mt = 0; mt < C::MT; ++mt) {
+      for (int kt = 0; kt < 2; ++kt) {
 #pragma unroll
-        for (int kt = 0; kt < 2; ++kt) {
+        for (int hf = 0; hf < 2; ++hf) {
 #pragma unroll
-          for (int hf = 0; hf < 2; ++hf) {
+          for (int mt = 0; mt < C::MT; ++mt) {
             const uint16_t* base = Vs + (32 * kt + 16 * hf + tr_key) * C::VP + 32 * mt + tr_col;
             const u32x2 lo = lds_read_tr16(base);
             const u32x2 hi = lds_read_tr16(base + 8 * C::VP);

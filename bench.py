@@ -70,7 +70,7 @@ def main():
     o = torch.empty_like(q)
     lse = torch.empty(w.B, w.H, w.S, device=dev, dtype=torch.float32)
     dq, dk, dv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
-    ws = torch.empty(api.attnfuse_bwd_workspace_bytes(w.B, w.H, w.S), device=dev, dtype=torch.uint8)
+    ws = torch.empty(api.attnfuse_bwd_workspace_bytes(w.B, w.H, w.Hkv, w.S, w.D, w.rope), device=dev, dtype=torch.uint8)
     do_bwd = w.backward
 
     def step(ev=None):

@@ -83,24 +83,32 @@ int attnfuse_fwd(const void* Q, const void* K, const void* V, void* O, float* LS
                  int rope, float rope_theta, int mask, int window,
                  const float* alibi_slopes, float softmax_scale, void* stream);
 
-/* Bytes of device workspace attnfuse_bwd needs: two fp32 values per query row
- * (delta_i = rowsum(dO_i * O_i) and LSE_i in log2 units), i.e. 8*B*H*S. */
-size_t attnfuse_bwd_workspace_bytes(int B, int H, int S);
+/* Bytes of device workspace attnfuse_bwd needs for these sizes and RoPE kind:
+ *   8*B*H*S                  per query row: delta_i = rowsum(dO_i * O_i) and
+ *                            LSE_i in log2 units (fp32 each)
+ * + 2*B*H*S*D                dO converted once to fp16
+ * + 2*(B*H + B*H_kv)*S*D     with RoPE only: Q' = R Q and K' = R K, rotated
+ *                            once and rounded to fp16
+ * Returns 0 for invalid sizes. */
+size_t attnfuse_bwd_workspace_bytes(int B, int H, int H_kv, int S, int D, int rope);
 
 /*
  * Backward of attnfuse_fwd (Section 4.4: three kernels, no atomics -- a
- * row-statistic pass, a dK/dV pass over query tiles and a dQ pass over key
- * tiles; probabilities are re-derived from the saved LSE).  With RoPE the
- * rotated operands are recomputed in both passes and the gradients leave
- * through the inverse rotation: dQ = R^T dQ', dK = R^T dK'.  For grouped-query
- * attention dK and dV sum over the H/H_kv query heads of their group.
+ * preprocessing pass, a dK/dV pass over query tiles and a dQ pass over key
+ * tiles; probabilities are re-derived from the saved LSE).  The preprocessing
+ * pass computes the row statistics and, with RoPE, rotates Q and K once into
+ * the workspace (both later passes read every tile many times, so rotating
+ * once is cheaper than re-rotating per visit); the gradients leave through the
+ * inverse rotation: dQ = R^T dQ', dK = R^T dK'.  For grouped-query attention
+ * dK and dV sum over the H/H_kv query heads of their group.
  *
  *   Q, K, V, O, dO, LSE  as produced/consumed by attnfuse_fwd with the same
  *                        variant arguments (LSE must be the forward's)
  *   dQ [B,H,S,D], dK/dV [B,H_kv,S,D]  outputs (dtype), fully overwritten; must
  *                        not alias inputs
- *   workspace            device memory of >= attnfuse_bwd_workspace_bytes()
- *                        bytes (16-byte aligned), caller-owned scratch
+ *   workspace            device memory of >= attnfuse_bwd_workspace_bytes(B,
+ *                        H, H_kv, S, D, rope) bytes (16-byte aligned),
+ *                        caller-owned scratch, overwritten
  *   other arguments      as attnfuse_fwd.  Only AF_DTYPE_BF16 is compiled.
  */
 int attnfuse_bwd(const void* Q, const void* K, const void* V, const void* O, const void* dO,

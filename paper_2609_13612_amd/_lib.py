@@ -14,7 +14,7 @@ _I = ctypes.c_int
 _F = ctypes.c_float
 SIGNATURES = {
     "attnfuse_fwd": (_I, [_P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _F, _I, _I, _P, _F, _P]),
-    "attnfuse_bwd_workspace_bytes": (ctypes.c_size_t, [_I, _I, _I]),
+    "attnfuse_bwd_workspace_bytes": (ctypes.c_size_t, [_I, _I, _I, _I, _I, _I]),
     "attnfuse_bwd": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t,
                           _I, _I, _I, _I, _I, _I, _I, _F, _I, _I, _P, _F, _P]),
     "attnfuse_rope": (_I, [_P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _F, _P]),

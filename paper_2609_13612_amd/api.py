@@ -77,8 +77,8 @@ def attnfuse_fwd(q, k, v, *, rope="none", theta=10000.0, mask="causal", window=N
     return out, lse
 
 
-def attnfuse_bwd_workspace_bytes(B, H, S):
-    return _lib.load().attnfuse_bwd_workspace_bytes(B, H, S)
+def attnfuse_bwd_workspace_bytes(B, H, H_kv, S, D, rope="none"):
+    return _lib.load().attnfuse_bwd_workspace_bytes(B, H, H_kv, S, D, ROPE[rope])
 
 
 def attnfuse_bwd(q, k, v, o, do, lse, *, rope="none", theta=10000.0, mask="causal", window=None,
@@ -89,7 +89,7 @@ def attnfuse_bwd(q, k, v, o, do, lse, *, rope="none", theta=10000.0, mask="causa
     dq = torch.empty_like(q) if dq is None else dq
     dk = torch.empty_like(k) if dk is None else dk
     dv = torch.empty_like(v) if dv is None else dv
-    nbytes = attnfuse_bwd_workspace_bytes(B, H, S)
+    nbytes = attnfuse_bwd_workspace_bytes(B, H, Hkv, S, D, rope)
     if workspace is None:
         workspace = torch.empty(nbytes, device=q.device, dtype=torch.uint8)
     r, th, m, w, sc = _variant(rope, theta, mask, window, alibi_slopes, scale, D)

@@ -17,7 +17,7 @@
 namespace {
 
 constexpr int kMaxS = 1 << 20;
-constexpr int kAbiVersion = 1;
+constexpr int kAbiVersion = 2;
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
@@ -84,6 +84,29 @@ int check_attn(int mask, int window, float scale) {
 
 bool supported_d(int D) { return D == 64 || D == 128; }
 
+// Backward workspace: [delta f32 | lse2 f32 | dO fp16 | Q' fp16 | K' fp16], each
+// section starting on a 256-byte boundary; the last two only with RoPE.
+struct BwdWorkspace {
+  size_t delta, lse2, do16, qr16, kr16, total;
+};
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+BwdWorkspace bwd_workspace(int B, int H, int H_kv, int S, int D, int rope) {
+  const size_t rows = (size_t)B * H * S, krows = (size_t)B * H_kv * S;
+  BwdWorkspace w{};
+  size_t off = 0;
+  w.delta = off; off += align256(rows * sizeof(float));
+  w.lse2 = off;  off += align256(rows * sizeof(float));
+  w.do16 = off;  off += align256(rows * D * 2);
+  if (rope != AF_ROPE_NONE) {
+    w.qr16 = off; off += align256(rows * D * 2);
+    w.kr16 = off; off += align256(krows * D * 2);
+  }
+  w.total = off;
+  return w;
+}
+
 }  // namespace
 
 extern "C" {
@@ -128,9 +151,10 @@ int attnfuse_fwd(const void* Q, const void* K, const void* V, void* O, float* LS
   return map_launch(af::launch_fwd_fp32(D, rope, mask, alibi, p, st));
 }
 
-size_t attnfuse_bwd_workspace_bytes(int B, int H, int S) {
-  if (B < 1 || H < 1 || S < 1) return 0;
-  return (size_t)2 * sizeof(float) * (size_t)B * (size_t)H * (size_t)S;
+size_t attnfuse_bwd_workspace_bytes(int B, int H, int H_kv, int S, int D, int rope) {
+  if (B < 1 || H < 1 || H_kv < 1 || S < 1 || D < 2 || (D & 1)) return 0;
+  if (rope != AF_ROPE_NONE && rope != AF_ROPE_NEOX && rope != AF_ROPE_INTERLEAVED) return 0;
+  return bwd_workspace(B, H, H_kv, S, D, rope).total;
 }
 
 int attnfuse_bwd(const void* Q, const void* K, const void* V, const void* O, const void* dO,
@@ -148,16 +172,20 @@ int attnfuse_bwd(const void* Q, const void* K, const void* V, const void* O, con
   int rc = check_common(B, H, H_kv, S, D, dtype, rope, rope_theta);
   if (rc != AF_OK) return rc;
   if ((rc = check_attn(mask, window, softmax_scale)) != AF_OK) return rc;
-  if (workspace_bytes < attnfuse_bwd_workspace_bytes(B, H, S)) return AF_ERR_INVALID_ARG;
+  if (workspace_bytes < attnfuse_bwd_workspace_bytes(B, H, H_kv, S, D, rope)) return AF_ERR_INVALID_ARG;
   if (!supported_d(D) || dtype != AF_DTYPE_BF16) return AF_ERR_UNSUPPORTED;
 
   hipStream_t st = static_cast<hipStream_t>(stream);
   af::BwdParams p{};
   p.q = Q; p.k = K; p.v = V; p.o = O; p.dout = dO; p.lse = LSE;
   p.dq = dQ; p.dk = dK; p.dv = dV;
-  const size_t rows = (size_t)B * H * S;
-  p.delta = static_cast<float*>(workspace);
-  p.lse2 = static_cast<float*>(workspace) + rows;
+  const BwdWorkspace ws = bwd_workspace(B, H, H_kv, S, D, rope);
+  char* wb = static_cast<char*>(workspace);
+  p.delta = reinterpret_cast<float*>(wb + ws.delta);
+  p.lse2 = reinterpret_cast<float*>(wb + ws.lse2);
+  p.do16 = wb + ws.do16;
+  p.qr16 = (rope != AF_ROPE_NONE) ? wb + ws.qr16 : nullptr;
+  p.kr16 = (rope != AF_ROPE_NONE) ? wb + ws.kr16 : nullptr;
   p.B = B; p.H = H; p.Hkv = H_kv; p.S = S;
   // a window of S or more keys is the causal mask; clamping keeps n + window in int range
   p.window = (mask == AF_MASK_SLIDING_WINDOW) ? (window < S ? window : S) : 0;

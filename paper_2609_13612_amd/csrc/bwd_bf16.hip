@@ -3,16 +3,19 @@
 //
 // Three kernels, no atomics (Section 4.4): every output tile has exactly one
 // writer.
-//   1. bwd_rowstat:  delta_i = rowsum(dO_i * O_i) and LSE_i in log2 units.
-//   2. bwd_dkdv:     one workgroup per 128 keys of one (batch, K/V head); it
-//                    loops over the query heads of the GQA group and their
-//                    visible query tiles, re-deriving P = exp(S - LSE) tile by
-//                    tile:  dV += P^T dO,  dS = P o (dO V^T - delta),
-//                    dK' += scale dS^T Q'.  K' = R K is rotated once; each Q'
-//                    tile is rotated as it is staged.  dK = R^T dK'.
-//   3. bwd_dq:       one workgroup per 128 queries of one (batch, head); it
-//                    loops over visible key tiles:  dQ' += scale dS K',
-//                    dQ = R^T dQ'.
+//   1. bwd_prep:  delta_i = rowsum(dO_i * O_i), LSE_i in log2 units, dO in
+//                 fp16, and with RoPE Q' = R Q and K' = R K rotated once into
+//                 the workspace (fp16).  The two later kernels read each Q'
+//                 and K' tile many times (dK/dV reads every Q' tile once per
+//                 key block), so one rotation pass replaces all of those.
+//   2. bwd_dkdv:  one workgroup per 128 keys of one (batch, K/V head); it
+//                 loops over the query heads of the GQA group and their
+//                 visible query tiles, re-deriving P = exp(S - LSE) tile by
+//                 tile:  dV += P^T dO,  dS = P o (dO V^T - delta),
+//                 dK' += scale dS^T Q';  dK = R^T dK'.
+//   3. bwd_dq:    one workgroup per 256 query rows (GQA heads packed, as in
+//                 the forward); it loops over visible key tiles:
+//                 dQ' += scale dS K',  dQ = R^T dQ'.
 // Register layouts follow the forward: the operand held in registers is the
 // MFMA B operand (lane = its row), tiles staged in LDS are the A operand, and
 // contractions over queries/keys read a transposed LDS copy stored with the
@@ -31,27 +34,78 @@
 
 namespace af {
 
-// ---------------------------------------------------------------- row statistics
-template <int D>
-__global__ __launch_bounds__(256) void bwd_rowstat_kernel(BwdParams p) {
-  constexpr int TPR = D / 8;             // threads per row (16 bytes each)
+// ---------------------------------------------------------------- preprocessing
+// One thread per (row, chunk pair c): chunks c and c + D/16 (dims 8c.. and
+// D/2 + 8c..), which are NeoX partners; interleaved pairs stay in-chunk.
+// Blocks [0, q_blocks) cover the B*H query rows, the rest the B*H_kv key rows.
+template <int D, int ROPE>
+__global__ __launch_bounds__(256) void bwd_prep_kernel(BwdParams p, int q_blocks) {
+  constexpr int TPR = D / 16;            // threads per row
   constexpr int RPB = 256 / TPR;         // rows per block
-  const long long rows = (long long)p.B * p.H * p.S;
-  const long long row = (long long)blockIdx.x * RPB + threadIdx.x / TPR;
   const int c = threadIdx.x % TPR;
-  float acc = 0.f;
-  if (row < rows) {
-    u32x4 a = ld16(static_cast<const uint16_t*>(p.dout) + row * D + 8 * c);
-    u32x4 o = ld16(static_cast<const uint16_t*>(p.o) + row * D + 8 * c);
+  const int d0 = 8 * c, d1 = D / 2 + 8 * c;
+  if ((int)blockIdx.x < q_blocks) {
+    const long long rows = (long long)p.B * p.H * p.S;
+    const long long row = (long long)blockIdx.x * RPB + threadIdx.x / TPR;
+    const long long rc = row < rows ? row : rows - 1;   // clamp: every lane joins the reduction
+    const uint16_t* dOr = static_cast<const uint16_t*>(p.dout) + rc * D;
+    const uint16_t* Or = static_cast<const uint16_t*>(p.o) + rc * D;
+    const u32x4 a0 = ld16(dOr + d0), a1 = ld16(dOr + d1);
+    const u32x4 o0 = ld16(Or + d0), o1 = ld16(Or + d1);
+    float acc = 0.f;
 #pragma unroll
-    for (int w = 0; w < 4; ++w) acc += bf_lo(a[w]) * bf_lo(o[w]) + bf_hi(a[w]) * bf_hi(o[w]);
-  }
+    for (int w = 0; w < 4; ++w)
+      acc += bf_lo(a0[w]) * bf_lo(o0[w]) + bf_hi(a0[w]) * bf_hi(o0[w]) + bf_lo(a1[w]) * bf_lo(o1[w]) +
+             bf_hi(a1[w]) * bf_hi(o1[w]);
 #pragma unroll
-  for (int off = TPR / 2; off > 0; off >>= 1) acc += __shfl_xor(acc, off, TPR);
-  if (row < rows && c == 0) {
-    p.delta[row] = acc;
-    const float l = p.lse[row];
-    p.lse2[row] = (l == -INFINITY) ? INFINITY : l * kLog2e;
+    for (int off = TPR / 2; off > 0; off >>= 1) acc += __shfl_xor(acc, off, TPR);
+    if (row < rows) {
+      u32x4 h0, h1;
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        h0[w] = pack_f16(bf_lo(a0[w]), bf_hi(a0[w]));
+        h1[w] = pack_f16(bf_lo(a1[w]), bf_hi(a1[w]));
+      }
+      uint16_t* dst = static_cast<uint16_t*>(p.do16) + row * D;
+      st16(dst + d0, h0);
+      st16(dst + d1, h1);
+      if (c == 0) {
+        p.delta[row] = acc;
+        const float l = p.lse[row];
+        p.lse2[row] = (l == -INFINITY) ? INFINITY : l * kLog2e;
+      }
+      if constexpr (ROPE != ROPE_NONE) {
+        const int pos = (int)(row % p.S);
+        const uint16_t* Qr = static_cast<const uint16_t*>(p.q) + row * D;
+        u32x4 q0 = ld16(Qr + d0), q1 = ld16(Qr + d1);
+        if constexpr (ROPE == ROPE_NEOX) {
+          rotate_neox8<false, true>(q0, q1, p.table + (size_t)pos * (D / 2) + 8 * c);
+        } else {
+          rotate_interleaved8<false, true>(q0, p.table + (size_t)pos * (D / 2) + 4 * c);
+          rotate_interleaved8<false, true>(q1, p.table + (size_t)pos * (D / 2) + D / 4 + 4 * c);
+        }
+        uint16_t* qd = static_cast<uint16_t*>(p.qr16) + row * D;
+        st16(qd + d0, q0);
+        st16(qd + d1, q1);
+      }
+    }
+  } else if constexpr (ROPE != ROPE_NONE) {
+    const long long rows = (long long)p.B * p.Hkv * p.S;
+    const long long row = (long long)(blockIdx.x - q_blocks) * RPB + threadIdx.x / TPR;
+    if (row < rows) {
+      const int pos = (int)(row % p.S);
+      const uint16_t* Kr = static_cast<const uint16_t*>(p.k) + row * D;
+      u32x4 k0 = ld16(Kr + d0), k1 = ld16(Kr + d1);
+      if constexpr (ROPE == ROPE_NEOX) {
+        rotate_neox8<false, true>(k0, k1, p.table + (size_t)pos * (D / 2) + 8 * c);
+      } else {
+        rotate_interleaved8<false, true>(k0, p.table + (size_t)pos * (D / 2) + 4 * c);
+        rotate_interleaved8<false, true>(k1, p.table + (size_t)pos * (D / 2) + D / 4 + 4 * c);
+      }
+      uint16_t* kd = static_cast<uint16_t*>(p.kr16) + row * D;
+      st16(kd + d0, k0);
+      st16(kd + d1, k1);
+    }
   }
 }
 
@@ -146,9 +200,10 @@ __device__ __forceinline__ u32x4 tr_operand(const uint16_t* tile, int pitch, int
 }
 
 // ---------------------------------------------------------------- dK / dV
-// Query-side tile of the dK/dV kernel: 64 query rows of Q' (rotated, fp16 under
-// RoPE) and dO (converted to fp16), plus their LSE (log2 units) and delta.
-template <int D, int ROPE>
+// Query-side tile of the dK/dV kernel: 64 query rows of Q' (fp16, rotated by
+// the preprocessing kernel) or Q (bf16, without RoPE) and of dO (fp16), plus
+// their LSE (log2 units) and delta.  Staging is a plain copy.
+template <int D>
 struct QTileCfg {
   static constexpr int NW = 4;
   static constexpr int THREADS = 64 * NW;
@@ -159,50 +214,31 @@ struct QTileCfg {
   static constexpr int QP = D + 16;           // pitch of Q' and dO rows (transpose reads)
   static constexpr int Q_ELEMS = BQ * QP;
   static constexpr int STAGE = 2 * Q_ELEMS;   // Q' then dO
-  static constexpr int Q_UNITS = (ROPE == ROPE_NEOX) ? D / 16 : D / 8;
-  static constexpr int Q_ITEMS = BQ * Q_UNITS;
-  static constexpr int QPT = (Q_ITEMS + THREADS - 1) / THREADS;
-  static constexpr int O_ITEMS = BQ * (D / 8);
-  static constexpr int OPT = (O_ITEMS + THREADS - 1) / THREADS;
-  static constexpr int CS = (ROPE == ROPE_NEOX) ? 4 : (ROPE == ROPE_INTERLEAVED ? 2 : 1);
+  static constexpr int ITEMS = BQ * (D / 8);  // 16-byte chunks per matrix
+  static constexpr int IPT = (ITEMS + THREADS - 1) / THREADS;
 };
 
-template <int D, int ROPE>
+template <int D>
 struct QTileRegs {
-  using C = QTileCfg<D, ROPE>;
-  u32x4 qa[C::QPT];
-  u32x4 qb[(ROPE == ROPE_NEOX) ? C::QPT : 1];
-  float4 cs[C::QPT][C::CS];
-  u32x4 o[C::OPT];
+  using C = QTileCfg<D>;
+  u32x4 q[C::IPT];
+  u32x4 o[C::IPT];
   float lse2, del;
 };
 
 // Rows past S are clamped to row S-1 so every load is unconditional; they get
 // LSE = +inf (so P = 0) and delta = 0, so they contribute nothing.
-template <int D, int ROPE>
-__device__ __forceinline__ void qtile_load(QTileRegs<D, ROPE>& R, const uint16_t* __restrict__ Q,
+template <int D>
+__device__ __forceinline__ void qtile_load(QTileRegs<D>& R, const uint16_t* __restrict__ Q,
                                            const uint16_t* __restrict__ dO, const float* __restrict__ lse2,
-                                           const float* __restrict__ delta, const float2* __restrict__ table,
-                                           int m0, int S, int tid) {
-  using C = QTileCfg<D, ROPE>;
+                                           const float* __restrict__ delta, int m0, int S, int tid) {
+  using C = QTileCfg<D>;
 #pragma unroll
-  for (int i = 0; i < C::QPT; ++i) {
+  for (int i = 0; i < C::IPT; ++i) {
     const int it = tid + C::THREADS * i;
-    if (C::Q_ITEMS % C::THREADS != 0 && it >= C::Q_ITEMS) break;
-    const int r = it / C::Q_UNITS, c = it % C::Q_UNITS, m = min(m0 + r, S - 1);
-    R.qa[i] = ld16(Q + (size_t)m * D + 8 * c);
-    if constexpr (ROPE == ROPE_NEOX) {
-      R.qb[i] = ld16(Q + (size_t)m * D + D / 2 + 8 * c);
-      load_cs(R.cs[i], table + (size_t)m * (D / 2) + 8 * c);
-    } else if constexpr (ROPE == ROPE_INTERLEAVED) {
-      load_cs(R.cs[i], table + (size_t)m * (D / 2) + 4 * c);
-    }
-  }
-#pragma unroll
-  for (int i = 0; i < C::OPT; ++i) {
-    const int it = tid + C::THREADS * i;
-    if (C::O_ITEMS % C::THREADS != 0 && it >= C::O_ITEMS) break;
+    if (C::ITEMS % C::THREADS != 0 && it >= C::ITEMS) break;
     const int r = it / (D / 8), c = it % (D / 8), m = min(m0 + r, S - 1);
+    R.q[i] = ld16(Q + (size_t)m * D + 8 * c);
     R.o[i] = ld16(dO + (size_t)m * D + 8 * c);
   }
   const int ms = min(m0 + (tid & (C::BQ - 1)), S - 1);
@@ -212,34 +248,18 @@ __device__ __forceinline__ void qtile_load(QTileRegs<D, ROPE>& R, const uint16_t
   R.del = in ? dl : 0.f;
 }
 
-template <int D, int ROPE>
-__device__ __forceinline__ void qtile_commit(QTileRegs<D, ROPE>& R, uint16_t* __restrict__ Qs,
+template <int D>
+__device__ __forceinline__ void qtile_commit(const QTileRegs<D>& R, uint16_t* __restrict__ Qs,
                                              uint16_t* __restrict__ Os, float* __restrict__ lse2s,
                                              float* __restrict__ dels, int tid) {
-  using C = QTileCfg<D, ROPE>;
+  using C = QTileCfg<D>;
 #pragma unroll
-  for (int i = 0; i < C::QPT; ++i) {
+  for (int i = 0; i < C::IPT; ++i) {
     const int it = tid + C::THREADS * i;
-    if (C::Q_ITEMS % C::THREADS != 0 && it >= C::Q_ITEMS) break;
-    const int r = it / C::Q_UNITS, c = it % C::Q_UNITS;
-    if constexpr (ROPE == ROPE_NEOX) {
-      rotate_neox8<false, true>(R.qa[i], R.qb[i], R.cs[i]);
-      *reinterpret_cast<u32x4*>(Qs + r * C::QP + 8 * c) = R.qa[i];
-      *reinterpret_cast<u32x4*>(Qs + r * C::QP + D / 2 + 8 * c) = R.qb[i];
-    } else {
-      if constexpr (ROPE == ROPE_INTERLEAVED) rotate_interleaved8<false, true>(R.qa[i], R.cs[i]);
-      *reinterpret_cast<u32x4*>(Qs + r * C::QP + 8 * c) = R.qa[i];
-    }
-  }
-#pragma unroll
-  for (int i = 0; i < C::OPT; ++i) {
-    const int it = tid + C::THREADS * i;
-    if (C::O_ITEMS % C::THREADS != 0 && it >= C::O_ITEMS) break;
+    if (C::ITEMS % C::THREADS != 0 && it >= C::ITEMS) break;
     const int r = it / (D / 8), c = it % (D / 8);
-    u32x4 v = R.o[i];
-#pragma unroll
-    for (int w = 0; w < 4; ++w) v[w] = pack_f16(bf_lo(v[w]), bf_hi(v[w]));
-    *reinterpret_cast<u32x4*>(Os + r * C::QP + 8 * c) = v;
+    *reinterpret_cast<u32x4*>(Qs + r * C::QP + 8 * c) = R.q[i];
+    *reinterpret_cast<u32x4*>(Os + r * C::QP + 8 * c) = R.o[i];
   }
   if (tid < C::BQ) {
     lse2s[tid] = R.lse2;
@@ -249,7 +269,7 @@ __device__ __forceinline__ void qtile_commit(QTileRegs<D, ROPE>& R, uint16_t* __
 
 template <int D, int ROPE, int MASK, bool ALIBI>
 __global__ __launch_bounds__(256) void bwd_dkdv_kernel(BwdParams p) {
-  using C = QTileCfg<D, ROPE>;
+  using C = QTileCfg<D>;
   constexpr bool QF16 = ROPE != ROPE_NONE;   // rotated operands (and dS with them) in fp16
   __shared__ __attribute__((aligned(16))) uint16_t smem[2 * C::STAGE];
   __shared__ __attribute__((aligned(16))) float stat[2][2][C::BQ];   // [stage][lse2, delta][query]
@@ -267,10 +287,11 @@ __global__ __launch_bounds__(256) void bwd_dkdv_kernel(BwdParams p) {
   const int n = nw + lq;              // this lane's key
   (void)nkb;
 
-  const uint16_t* Kg = static_cast<const uint16_t*>(p.k) + (size_t)bg * S * D;
+  // K' (fp16, rotated by the preprocessing kernel) or K (bf16), and V as fp16
+  const uint16_t* Kg = static_cast<const uint16_t*>(QF16 ? p.kr16 : p.k) + (size_t)bg * S * D;
   const uint16_t* Vg = static_cast<const uint16_t*>(p.v) + (size_t)bg * S * D;
   u32x4 kreg[C::KS], vreg[C::KS];
-  load_row_operand<D, ROPE>(kreg, Kg, p.table, n, S, lg);
+  load_row_operand<D, ROPE_NONE>(kreg, Kg, nullptr, n, S, lg);
   load_row_operand<D, ROPE_NONE, true>(vreg, Vg, nullptr, n, S, lg);   // V as fp16 for dP = dO V^T
 
   f32x16 dk[C::MT], dv[C::MT];
@@ -290,19 +311,19 @@ __global__ __launch_bounds__(256) void bwd_dkdv_kernel(BwdParams p) {
   auto tile_of = [&](int s) { return tq_begin + s % nq; };
   auto src = [&](int s, const uint16_t*& Qh, const uint16_t*& dOh, const float*& l2, const float*& dl) {
     const size_t bh = (size_t)b * p.H + head_of(s);
-    Qh = static_cast<const uint16_t*>(p.q) + bh * S * D;
-    dOh = static_cast<const uint16_t*>(p.dout) + bh * S * D;
+    Qh = static_cast<const uint16_t*>(QF16 ? p.qr16 : p.q) + bh * S * D;
+    dOh = static_cast<const uint16_t*>(p.do16) + bh * S * D;
     l2 = p.lse2 + bh * S;
     dl = p.delta + bh * S;
   };
 
-  QTileRegs<D, ROPE> R;
+  QTileRegs<D> R;
   if (steps > 0) {
     const uint16_t *Qh, *dOh;
     const float *l2, *dl;
     src(0, Qh, dOh, l2, dl);
-    qtile_load<D, ROPE>(R, Qh, dOh, l2, dl, p.table, tile_of(0) * C::BQ, S, tid);
-    qtile_commit<D, ROPE>(R, smem, smem + C::Q_ELEMS, stat[0][0], stat[0][1], tid);
+    qtile_load<D>(R, Qh, dOh, l2, dl, tile_of(0) * C::BQ, S, tid);
+    qtile_commit<D>(R, smem, smem + C::Q_ELEMS, stat[0][0], stat[0][1], tid);
   }
   __syncthreads();
 
@@ -317,7 +338,7 @@ __global__ __launch_bounds__(256) void bwd_dkdv_kernel(BwdParams p) {
       const uint16_t *Qh, *dOh;
       const float *l2, *dl;
       src(s + 1, Qh, dOh, l2, dl);
-      qtile_load<D, ROPE>(R, Qh, dOh, l2, dl, p.table, tile_of(s + 1) * C::BQ, S, tid);
+      qtile_load<D>(R, Qh, dOh, l2, dl, tile_of(s + 1) * C::BQ, S, tid);
     }
     const int h = head_of(s);
     const int mq0 = tile_of(s) * C::BQ;
@@ -394,7 +415,7 @@ __global__ __launch_bounds__(256) void bwd_dkdv_kernel(BwdParams p) {
 
     if (more) {
       const int sn = (s + 1) & 1;
-      qtile_commit<D, ROPE>(R, smem + sn * C::STAGE, smem + sn * C::STAGE + C::Q_ELEMS, stat[sn][0], stat[sn][1], tid);
+      qtile_commit<D>(R, smem + sn * C::STAGE, smem + sn * C::STAGE + C::Q_ELEMS, stat[sn][0], stat[sn][1], tid);
     }
     __syncthreads();
   }
@@ -410,7 +431,7 @@ __global__ __launch_bounds__(256) void bwd_dkdv_kernel(BwdParams p) {
 // K'/V tiles (attn_tiles.hpp); dQ'^T += K'^T dS^T with K'^T from transpose reads.
 template <int D, int ROPE, int MASK, bool ALIBI>
 __global__ __launch_bounds__(512) void bwd_dq_kernel(BwdParams p) {
-  using C = TileCfg<D, ROPE>;
+  using C = TileCfg<D, ROPE_NONE>;            // K' arrives rotated: staging is a plain copy
   constexpr bool QF16 = ROPE != ROPE_NONE;
   __shared__ __attribute__((aligned(16))) uint16_t smem[2 * C::STAGE];
 
@@ -434,14 +455,14 @@ __global__ __launch_bounds__(512) void bwd_dq_kernel(BwdParams p) {
   const int p_end = min(p0 + P, S);
   const size_t bh = (size_t)b * p.H + h;
 
-  const uint16_t* Qh = static_cast<const uint16_t*>(p.q) + bh * S * D;
+  const uint16_t* Qh = static_cast<const uint16_t*>(QF16 ? p.qr16 : p.q) + bh * S * D;
   const uint16_t* dOh = static_cast<const uint16_t*>(p.dout) + bh * S * D;
-  const uint16_t* Kg = static_cast<const uint16_t*>(p.k) + (size_t)bg * S * D;
+  const uint16_t* Kg = static_cast<const uint16_t*>(QF16 ? p.kr16 : p.k) + (size_t)bg * S * D;
   const uint16_t* Vg = static_cast<const uint16_t*>(p.v) + (size_t)bg * S * D;
 
   u32x4 qreg[C::KS], oreg[C::KS];
   const int mc = min(m, S - 1);   // rows past S compute on row S-1 and are never stored
-  load_row_operand<D, ROPE>(qreg, Qh, p.table, mc, S, lg);
+  load_row_operand<D, ROPE_NONE>(qreg, Qh, nullptr, mc, S, lg);
   load_row_operand<D, ROPE_NONE>(oreg, dOh, nullptr, mc, S, lg);
   const float lse2 = (m < S) ? p.lse2[bh * S + mc] : INFINITY;
   const float del = (m < S) ? p.delta[bh * S + mc] : 0.f;
@@ -458,10 +479,10 @@ __global__ __launch_bounds__(512) void bwd_dq_kernel(BwdParams p) {
   if constexpr (MASK != MASK_NONE) t_end = min(ntiles, (p_end - 1) / C::BN + 1);
   if constexpr (MASK == MASK_SLIDING_WINDOW) t_begin = max(0, p0 - W + 1) / C::BN;
 
-  TileRegs<D, ROPE> R;
+  TileRegs<D, ROPE_NONE> R;
   if (t_begin < t_end) {
-    tile_load<D, ROPE>(R, Kg, Vg, p.table, t_begin * C::BN, S, tid);
-    tile_commit<D, ROPE>(R, smem, smem + C::K_ELEMS, tid);
+    tile_load<D, ROPE_NONE>(R, Kg, Vg, nullptr, t_begin * C::BN, S, tid);
+    tile_commit<D, ROPE_NONE>(R, smem, smem + C::K_ELEMS, tid);
   }
   __syncthreads();
 
@@ -470,7 +491,7 @@ __global__ __launch_bounds__(512) void bwd_dq_kernel(BwdParams p) {
     const uint16_t* Ks = smem + ((t - t_begin) & 1) * C::STAGE;
     const uint16_t* Vs = Ks + C::K_ELEMS;
     const bool more = t + 1 < t_end;
-    if (more) tile_load<D, ROPE>(R, Kg, Vg, p.table, n0 + C::BN, S, tid);
+    if (more) tile_load<D, ROPE_NONE>(R, Kg, Vg, nullptr, n0 + C::BN, S, tid);
 
     bool visible = mw < S;
     if constexpr (MASK != MASK_NONE) visible = visible && (n0 <= mw + 31);
@@ -523,7 +544,7 @@ __global__ __launch_bounds__(512) void bwd_dq_kernel(BwdParams p) {
     }
     if (more) {
       uint16_t* Kn = smem + ((t + 1 - t_begin) & 1) * C::STAGE;
-      tile_commit<D, ROPE>(R, Kn, Kn + C::K_ELEMS, tid);
+      tile_commit<D, ROPE_NONE>(R, Kn, Kn + C::K_ELEMS, tid);
     }
     __syncthreads();
   }
@@ -533,13 +554,16 @@ __global__ __launch_bounds__(512) void bwd_dq_kernel(BwdParams p) {
 // ---------------------------------------------------------------- launch
 template <int D, int ROPE, int MASK, bool ALIBI>
 static int launch_one(const BwdParams& p, hipStream_t st) {
-  constexpr int RPB = 256 / (D / 8);
-  const long long rows = (long long)p.B * p.H * p.S;
-  hipLaunchKernelGGL(bwd_rowstat_kernel<D>, dim3((unsigned)((rows + RPB - 1) / RPB)), dim3(256), 0, st, p);
-  using QC = QTileCfg<D, ROPE>;
+  constexpr int RPB = 256 / (D / 16);
+  const long long qrows = (long long)p.B * p.H * p.S;
+  const long long krows = (ROPE != ROPE_NONE) ? (long long)p.B * p.Hkv * p.S : 0;
+  const int q_blocks = (int)((qrows + RPB - 1) / RPB);
+  const int k_blocks = (int)((krows + RPB - 1) / RPB);
+  hipLaunchKernelGGL((bwd_prep_kernel<D, ROPE>), dim3((unsigned)(q_blocks + k_blocks)), dim3(256), 0, st, p, q_blocks);
+  using QC = QTileCfg<D>;
   const int nkb = (p.S + QC::KEYS - 1) / QC::KEYS;
   hipLaunchKernelGGL((bwd_dkdv_kernel<D, ROPE, MASK, ALIBI>), dim3((unsigned)(nkb * p.B * p.Hkv)), dim3(QC::THREADS), 0, st, p);
-  using TC = TileCfg<D, ROPE>;
+  using TC = TileCfg<D, ROPE_NONE>;
   BwdParams pq = p;
   pq.heads_per_wg = heads_per_wg(p.H / p.Hkv);
   const int P = TC::ROWS / pq.heads_per_wg;

@@ -31,6 +31,9 @@ struct BwdParams {
   void* dv;
   float* delta;           // workspace [B*H*S]: rowsum(dO * O)
   float* lse2;            // workspace [B*H*S]: LSE in log2 units (+inf for empty rows)
+  void* do16;             // workspace [B,H,S,D] fp16: dO
+  void* qr16;             // workspace [B,H,S,D] fp16: Q' = R Q (RoPE only, else nullptr)
+  void* kr16;             // workspace [B,H_kv,S,D] fp16: K' = R K (RoPE only, else nullptr)
   int B, H, Hkv, S, window;
   const float* slopes;
   float scale;

@@ -31,7 +31,7 @@ def test_library_loads_and_exports_every_declared_symbol():
     for name in declared_symbols():
         assert hasattr(lib, name), name
     assert set(declared_symbols()) == set(_lib.SIGNATURES)
-    assert lib.attnfuse_version() == 1
+    assert lib.attnfuse_version() == 2
 
 
 def test_strerror():
@@ -45,8 +45,14 @@ def test_strerror():
 
 def test_workspace_bytes():
     lib = _lib.load()
-    assert lib.attnfuse_bwd_workspace_bytes(1, 32, 8192) == 8 * 32 * 8192
-    assert lib.attnfuse_bwd_workspace_bytes(0, 32, 8192) == 0
+    rows, krows = 32 * 8192, 8 * 8192
+    # delta + lse2 (fp32) + dO (fp16); with RoPE also Q' and K' (fp16)
+    assert lib.attnfuse_bwd_workspace_bytes(1, 32, 8, 8192, 128, 0) == 8 * rows + 2 * rows * 128
+    assert lib.attnfuse_bwd_workspace_bytes(1, 32, 8, 8192, 128, 1) == 8 * rows + 2 * rows * 128 * 2 + 2 * krows * 128
+    # sections start on 256-byte boundaries
+    assert lib.attnfuse_bwd_workspace_bytes(1, 1, 1, 3, 64, 2) == 256 * 2 + 512 * 3
+    assert lib.attnfuse_bwd_workspace_bytes(0, 32, 8, 8192, 128, 0) == 0
+    assert lib.attnfuse_bwd_workspace_bytes(1, 32, 8, 8192, 128, 7) == 0
 
 
 def _fwd(**over):
@@ -85,7 +91,7 @@ def test_rope_none_ignores_theta_validation_only_in_attention():
 def _bwd(**over):
     base = FAKE
     a = dict(Q=base, K=base + 0x100, V=base + 0x200, O=base + 0x300, dO=base + 0x400, LSE=base + 0x500,
-             dQ=base + 0x600, dK=base + 0x700, dV=base + 0x800, ws=base + 0x900, ws_bytes=8 * 4 * 16,
+             dQ=base + 0x600, dK=base + 0x700, dV=base + 0x800, ws=base + 0x900, ws_bytes=1 << 20,
              B=1, H=4, H_kv=2, S=16, D=64, dtype=0, rope=1, theta=1e4, mask=1, window=0, slopes=None,
              scale=0.125, stream=None)
     a.update(over)
@@ -95,7 +101,7 @@ def _bwd(**over):
                                     a["stream"])
 
 
-@pytest.mark.parametrize("over", [dict(Q=None), dict(dO=None), dict(ws=None), dict(dQ=FAKE), dict(ws_bytes=8 * 4 * 16 - 1),
+@pytest.mark.parametrize("over", [dict(Q=None), dict(dO=None), dict(ws=None), dict(dQ=FAKE), dict(ws_bytes=20991),
                                   dict(H=4, H_kv=3), dict(mask=2, window=0), dict(dK=ODD), dict(S=0)],
                          ids=lambda o: ",".join(f"{k}={v}" for k, v in o.items()))
 def test_bwd_rejects_invalid_arguments(over):

@@ -13,8 +13,15 @@ Alongside, on the same inputs and outside the timed steps:
 * the separate-RoPE path (rotation kernel, then the forward without RoPE) and
   the rotation kernel's HBM bandwidth, measured over a buffer pool larger than
   twice the 256 MB Infinity Cache;
-* with --sweep, the fuse-vs-separate crossover over S = 1024..16384;
+* the fuse-vs-separate crossover over S = 1024..16384 (skip with --no-sweep);
+* a plain device-to-device copy of 512 MiB: the achievable HBM bandwidth next
+  to the rotation kernel's, and the calibration kernel for the HBM-traffic
+  counters;
 * the fp64 CPU oracle timed on a bounded sample (cpu_baseline).
+
+roofline.traffic is the forward kernel's measured HBM bytes per launch,
+taken from profiles/fwd_llama3_8b_hbm_traffic.json, which records the hash of
+the kernel sources it was measured on; if the sources differ, it is null.
 
 Prints ONE JSON line.  Only --gpus 1 is supported.
 """
@@ -31,6 +38,29 @@ sys.path.insert(0, ROOT)
 
 PEAK_BF16_TFLOPS = 2516.6     # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "fwd_llama3_8b_hbm_traffic.json")
+FWD_SOURCES = ("fwd_bf16.hip", "attn_tiles.hpp", "common.hpp")
+
+
+def fwd_source_hash():
+    import hashlib
+    h = hashlib.sha256()
+    for name in FWD_SOURCES:
+        with open(os.path.join(ROOT, "paper_2609_13612_amd", "csrc", name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def measured_traffic(workload):
+    """HBM bytes per fused-forward launch from the committed counter summary, if current."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            rec = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if rec.get("workload") != workload or rec.get("source_sha256") != fwd_source_hash():
+        return None
+    return rec.get("traffic_bytes_per_launch")
 
 
 def log(msg):
@@ -43,7 +73,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="llama3_8b_b1h32kv8s8192d128")
-    ap.add_argument("--sweep", action="store_true", help="fuse-vs-separate sweep over S")
+    ap.add_argument("--no-sweep", action="store_true", help="skip the fuse-vs-separate sweep over S")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--seed", type=int, default=0)
     return ap.parse_args()
@@ -167,7 +197,7 @@ def main():
         log(f"separate path: rope {rot_avg:.4f} ms ({rope_bw:.0f} GB/s) + fwd {sep_avg:.4f} ms")
 
     sweep = None
-    if args.sweep and w.rope != "none":
+    if not args.no_sweep and w.rope != "none":
         sweep = []
         for S in LLAMA_SWEEP_S:
             c = inputs.make_qkv(w.B, w.H, w.Hkv, S, w.D, seed=args.seed)
@@ -192,17 +222,28 @@ def main():
                 api.attnfuse_fwd(po[0][0], po[0][1], vs, out=os_, lse=ls, **dict(kw, rope="none"))
 
             for fn in (rot_s, fused_s, none_s):
-                fn()
+                for _ in range(3):
+                    fn()
             reps = 20
-            r_ms = statistics.mean(time_calls(rot_s, max(reps, 2 * npool)))
-            f_ms = statistics.mean(time_calls(fused_s, reps))
-            n_ms = statistics.mean(time_calls(none_s, reps))
+            r_ms = statistics.median(time_calls(rot_s, max(reps, 2 * npool)))
+            f_ms = statistics.median(time_calls(fused_s, reps))
+            n_ms = statistics.median(time_calls(none_s, reps))
             sweep.append({"S": S, "fused_ms": round(f_ms, 4), "rope_ms": round(r_ms, 4), "norope_ms": round(n_ms, 4),
                           "fused_speedup": round((r_ms + n_ms) / f_ms, 4),
                           "fused_tflops": round(w.fwd_flops(S) / (f_ms * 1e-3) / 1e12, 1)})
             log(f"sweep S={S}: fused {f_ms:.4f} ms, rope {r_ms:.4f} + norope {n_ms:.4f} ms")
             del pq, po, qs, ks, vs, os_, ls
         torch.cuda.empty_cache()
+
+    # ---------------------------------------------------------------- plain copy reference
+    copy_bytes = 512 << 20
+    src = torch.empty(copy_bytes, device=dev, dtype=torch.uint8)
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    cp_ms = statistics.median(time_calls(lambda: dst.copy_(src), 10))
+    copy_gbs = 2 * copy_bytes / (cp_ms * 1e-3) / 1e9
+    del src, dst
+    log(f"plain copy of 512 MiB: {cp_ms:.4f} ms, {copy_gbs:.0f} GB/s moved")
 
     # ---------------------------------------------------------------- CPU oracle baseline
     cpu_baseline = None
@@ -231,7 +272,7 @@ def main():
 
     roofline = {"bound": "mfma", "kernel": "fwd_bf16_kernel (fused RoPE + mask, one launch per forward)",
                 "achieved": round(fwd_tf, 1), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                "frac": round(fwd_tf / PEAK_BF16_TFLOPS, 4), "traffic": None}
+                "frac": round(fwd_tf / PEAK_BF16_TFLOPS, 4), "traffic": measured_traffic(w.name)}
 
     line = {
         "metric": "fused RoPE+causal attention TFLOP/s (fwd, bwd) and % of bf16 MFMA peak",
@@ -254,6 +295,8 @@ def main():
         "cpu_baseline": cpu_baseline,
         **result_extra,
         "separate_rope": separate,
+        "hbm_copy_reference": {"bytes_moved": 2 * copy_bytes, "ms": round(cp_ms, 4), "gbs": round(copy_gbs, 1),
+                               "frac_hbm_peak": round(copy_gbs / PEAK_HBM_GBS, 4)},
     }
     if sweep is not None:
         line["crossover_sweep"] = sweep

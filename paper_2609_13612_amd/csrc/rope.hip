@@ -53,57 +53,71 @@ __device__ __forceinline__ void rotate_interleaved4_f32(float4& x, const float2*
 constexpr int ROPE_HEADS_PER_THREAD = 8;
 
 // Thread item: (head group, batch, position n, chunk c).  For NeoX an item is
-// the chunk pair (c, c + D/2); for interleaved a single chunk.
+// the chunk pair (c, c + D/2); for interleaved a single chunk.  A thread loads
+// its cos/sin entries once, issues the loads of all its heads before rotating
+// any of them (memory-level parallelism), then stores.
 template <bool FP32, int D, int ROPE, bool INV>
 __global__ __launch_bounds__(256) void rope_kernel(RopeParams p) {
   constexpr int E = FP32 ? 4 : 8;                                  // elements per 16-byte chunk
   constexpr int CPR = (ROPE == ROPE_NEOX) ? D / (2 * E) : D / E;   // items per row
+  constexpr int HPT = ROPE_HEADS_PER_THREAD;
+  constexpr int NCH = (ROPE == ROPE_NEOX) ? 2 : 1;                 // chunks per item
+  constexpr int NT = (ROPE == ROPE_NEOX) ? E / 2 : E / 4;          // float4 of cos/sin per item
+  constexpr int EB = FP32 ? 4 : 2;                                 // bytes per element
   const long long idx = (long long)blockIdx.x * 256 + threadIdx.x;
   const long long per_b = (long long)p.S * CPR;
   const int nh = p.heads0 + p.heads1;
-  const int ngroups = (nh + ROPE_HEADS_PER_THREAD - 1) / ROPE_HEADS_PER_THREAD;
+  const int ngroups = (nh + HPT - 1) / HPT;
   if (idx >= per_b * p.B * ngroups) return;
   const int item = (int)(idx % per_b);
   const long long rest = idx / per_b;
   const int b = (int)(rest % p.B), hg = (int)(rest / p.B);
   const int n = item / CPR, c = item % CPR;
-  const int h_begin = hg * ROPE_HEADS_PER_THREAD;
-  const int h_end = min(nh, h_begin + ROPE_HEADS_PER_THREAD);
-  const float2* __restrict__ cs = p.table + (size_t)n * (D / 2) + ((ROPE == ROPE_NEOX) ? E * c : (E / 2) * c);
+  const int h_begin = hg * HPT;
 
-#pragma unroll 4
-  for (int hh = h_begin; hh < h_end; ++hh) {
+  float4 t[NT];
+  load_cs(t, p.table + (size_t)n * (D / 2) + ((ROPE == ROPE_NEOX) ? E * c : (E / 2) * c));
+  const size_t off0 = (size_t)n * D + (size_t)E * c;             // element offset of chunk 0 in the row
+  const size_t off1 = off0 + D / 2;                               // NeoX partner chunk
+
+  u32x4 x[HPT][NCH];
+#pragma unroll
+  for (int j = 0; j < HPT; ++j) {
+    const int hh = min(h_begin + j, nh - 1);   // clamped: the surplus lanes' results are not stored
     const bool first = hh < p.heads0;
     const int head = first ? hh : hh - p.heads0;
-    const int nheads = first ? p.heads0 : p.heads1;
-    const size_t row = ((size_t)(b * nheads + head) * p.S + n) * D;
+    const size_t base = (size_t)(b * (first ? p.heads0 : p.heads1) + head) * p.S * D;
     const char* X = static_cast<const char*>(first ? p.x0 : p.x1);
-    char* Y = static_cast<char*>(first ? p.y0 : p.y1);
-    constexpr int EB = FP32 ? 4 : 2;   // bytes per element
-    if constexpr (ROPE == ROPE_NEOX) {
-      const size_t oa = (row + (size_t)E * c) * EB, ob = (row + D / 2 + (size_t)E * c) * EB;
-      if constexpr (FP32) {
-        float4 a = *reinterpret_cast<const float4*>(X + oa), bb = *reinterpret_cast<const float4*>(X + ob);
-        rotate_neox4_f32<INV>(a, bb, cs);
-        *reinterpret_cast<float4*>(Y + oa) = a;
-        *reinterpret_cast<float4*>(Y + ob) = bb;
+    x[j][0] = ld16(X + (base + off0) * EB);
+    if constexpr (NCH == 2) x[j][1] = ld16(X + (base + off1) * EB);
+  }
+#pragma unroll
+  for (int j = 0; j < HPT; ++j) {
+    if constexpr (FP32) {
+      float4 a = __builtin_bit_cast(float4, x[j][0]);
+      if constexpr (ROPE == ROPE_NEOX) {
+        float4 bb = __builtin_bit_cast(float4, x[j][1]);
+        rotate_neox4_f32<INV>(a, bb, reinterpret_cast<const float2*>(t));
+        x[j][1] = __builtin_bit_cast(u32x4, bb);
       } else {
-        u32x4 a = ld16(X + oa), bb = ld16(X + ob);
-        rotate_neox8<INV>(a, bb, cs);
-        st16(Y + oa, a);
-        st16(Y + ob, bb);
+        rotate_interleaved4_f32<INV>(a, reinterpret_cast<const float2*>(t));
       }
+      x[j][0] = __builtin_bit_cast(u32x4, a);
     } else {
-      const size_t o = (row + (size_t)E * c) * EB;
-      if constexpr (FP32) {
-        float4 x = *reinterpret_cast<const float4*>(X + o);
-        rotate_interleaved4_f32<INV>(x, cs);
-        *reinterpret_cast<float4*>(Y + o) = x;
-      } else {
-        u32x4 x = ld16(X + o);
-        rotate_interleaved8<INV>(x, cs);
-        st16(Y + o, x);
-      }
+      if constexpr (ROPE == ROPE_NEOX) rotate_neox8<INV>(x[j][0], x[j][1], t);
+      else rotate_interleaved8<INV>(x[j][0], t);
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < HPT; ++j) {
+    const int hh = h_begin + j;
+    if (hh < nh) {
+      const bool first = hh < p.heads0;
+      const int head = first ? hh : hh - p.heads0;
+      const size_t base = (size_t)(b * (first ? p.heads0 : p.heads1) + head) * p.S * D;
+      char* Y = static_cast<char*>(first ? p.y0 : p.y1);
+      st16(Y + (base + off0) * EB, x[j][0]);
+      if constexpr (NCH == 2) st16(Y + (base + off1) * EB, x[j][1]);
     }
   }
 }

@@ -205,10 +205,12 @@ __device__ __forceinline__ u32x4 tr_operand(const uint16_t* tile, int pitch, int
 // their LSE (log2 units) and delta.  Staging is a plain copy.
 template <int D>
 struct QTileCfg {
-  static constexpr int NW = 4;
+  static constexpr int NW = 8;                // two waves per SIMD
   static constexpr int THREADS = 64 * NW;
-  static constexpr int KEYS = 32 * NW;        // keys per workgroup
-  static constexpr int BQ = 64;               // query rows per tile
+  static constexpr int KEYS = 32 * NW / 2;    // keys per workgroup: each 32 keys are shared by a wave pair
+  static constexpr int BQ = 64;               // query rows per tile: the pair splits them 32 + 32
+  static constexpr int VP = D + 8;            // pitch of the resident K' and V rows (16-byte reads)
+  static constexpr int V_ELEMS = KEYS * VP;
   static constexpr int KS = D / 16;
   static constexpr int MT = D / 32;
   static constexpr int QP = D + 16;           // pitch of Q' and dO rows (transpose reads)
@@ -267,32 +269,53 @@ __device__ __forceinline__ void qtile_commit(const QTileRegs<D>& R, uint16_t* __
   }
 }
 
+// One workgroup = 8 waves = 128 keys of one (batch, K/V head).  Waves w and
+// w + 4 share keys 32 (w % 4) .. +31 and split every 64-query tile, w taking
+// its first 32 rows and w + 4 the rest, so two waves per SIMD hide each
+// other's latencies; their partial dK/dV are summed through LDS at the end.
+// The block's K' rows (B operand of S = Q' K'^T) and V rows (fp16, B operand
+// of dP = dO V^T) stay resident in LDS, leaving the registers to the dK/dV
+// accumulators.
 template <int D, int ROPE, int MASK, bool ALIBI>
-__global__ __launch_bounds__(256) void bwd_dkdv_kernel(BwdParams p) {
+__global__ __launch_bounds__(512) void bwd_dkdv_kernel(BwdParams p) {
   using C = QTileCfg<D>;
   constexpr bool QF16 = ROPE != ROPE_NONE;   // rotated operands (and dS with them) in fp16
-  __shared__ __attribute__((aligned(16))) uint16_t smem[2 * C::STAGE];
+  constexpr int SMEM = 2 * C::STAGE + 2 * C::V_ELEMS;
+  static_assert(SMEM * 2 >= 4 * 16 * C::MT * 64 * 4, "the partial-sum exchange reuses the staging memory");
+  __shared__ __attribute__((aligned(16))) uint16_t smem[SMEM];
   __shared__ __attribute__((aligned(16))) float stat[2][2][C::BQ];   // [stage][lse2, delta][query]
+  uint16_t* Ks = smem + 2 * C::STAGE;
+  uint16_t* Vs = Ks + C::V_ELEMS;
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, lq = lane & 31, lg = lane >> 5;
+  const int kw = wave & 3, qh = wave >> 2;    // key block within the workgroup, query half
   const int S = p.S;
-  const int nkb = (S + C::KEYS - 1) / C::KEYS;
   const int BG = p.B * p.Hkv;
   const int bg = blockIdx.x % BG;
   const int kb = (int)(blockIdx.x / BG);   // ascending: under a causal mask the first key blocks see the most queries
   const int b = bg / p.Hkv, g = bg % p.Hkv;
   const int G = p.H / p.Hkv;
   const int nb = kb * C::KEYS;        // first key of the block
-  const int nw = nb + 32 * wave;      // first key of this wave
+  const int nw = nb + 32 * kw;        // first key of this wave
   const int n = nw + lq;              // this lane's key
-  (void)nkb;
 
-  // K' (fp16, rotated by the preprocessing kernel) or K (bf16), and V as fp16
+  // K' (fp16, rotated by the preprocessing kernel) or K (bf16) as is, and V
+  // converted to fp16; rows past S clamped (their results are not stored)
   const uint16_t* Kg = static_cast<const uint16_t*>(QF16 ? p.kr16 : p.k) + (size_t)bg * S * D;
   const uint16_t* Vg = static_cast<const uint16_t*>(p.v) + (size_t)bg * S * D;
-  u32x4 kreg[C::KS], vreg[C::KS];
-  load_row_operand<D, ROPE_NONE>(kreg, Kg, nullptr, n, S, lg);
-  load_row_operand<D, ROPE_NONE, true>(vreg, Vg, nullptr, n, S, lg);   // V as fp16 for dP = dO V^T
+  constexpr int VITEMS = C::KEYS * (D / 8);
+#pragma unroll
+  for (int i = 0; i < VITEMS / C::THREADS; ++i) {
+    const int it = tid + C::THREADS * i;
+    const int r = it / (D / 8), c = it % (D / 8);
+    const size_t off = (size_t)min(nb + r, S - 1) * D + 8 * c;
+    u32x4 v = ld16(Vg + off);
+    const u32x4 k = ld16(Kg + off);
+#pragma unroll
+    for (int w = 0; w < 4; ++w) v[w] = pack_f16(bf_lo(v[w]), bf_hi(v[w]));
+    *reinterpret_cast<u32x4*>(Vs + r * C::VP + 8 * c) = v;
+    *reinterpret_cast<u32x4*>(Ks + r * C::VP + 8 * c) = k;
+  }
 
   f32x16 dk[C::MT], dv[C::MT];
 #pragma unroll
@@ -327,6 +350,7 @@ __global__ __launch_bounds__(256) void bwd_dkdv_kernel(BwdParams p) {
   }
   __syncthreads();
 
+  const int qt = qh;                  // this wave's 32 rows of every query tile
   for (int s = 0; s < steps; ++s) {
     const int st = s & 1;
     const uint16_t* Qs = smem + st * C::STAGE;
@@ -341,74 +365,72 @@ __global__ __launch_bounds__(256) void bwd_dkdv_kernel(BwdParams p) {
       qtile_load<D>(R, Qh, dOh, l2, dl, tile_of(s + 1) * C::BQ, S, tid);
     }
     const int h = head_of(s);
-    const int mq0 = tile_of(s) * C::BQ;
+    const int mq = tile_of(s) * C::BQ + 32 * qt;   // first query row of this wave's half
     const float slope2 = ALIBI ? p.slopes[h] * kLog2e : 0.f;
 
     bool visible = nw < S;
-    if constexpr (MASK != MASK_NONE) visible = visible && (mq0 + C::BQ - 1 >= nw);
-    if constexpr (MASK == MASK_SLIDING_WINDOW) visible = visible && (mq0 <= nw + 31 + W - 1);
+    if constexpr (MASK != MASK_NONE) visible = visible && (mq + 31 >= nw);
+    if constexpr (MASK == MASK_SLIDING_WINDOW) visible = visible && (mq <= nw + 31 + W - 1);
     if (visible) {
       bool need_mask = nw + 32 > S;
-      if constexpr (MASK != MASK_NONE) need_mask = need_mask || (mq0 < nw + 31);
-      if constexpr (MASK == MASK_SLIDING_WINDOW) need_mask = need_mask || (mq0 + C::BQ - 1 - W >= nw);
-      // one 32-query half at a time keeps the live register set small
-#pragma unroll 1
-      for (int qt = 0; qt < 2; ++qt) {
-        // S = Q' K'^T and dP = dO V^T for 32 queries (rows) x this wave's 32 keys
-        // (columns); the two MFMA chains are interleaved.
-        f32x16 sc = f32x16{}, dp = f32x16{};
+      if constexpr (MASK != MASK_NONE) need_mask = need_mask || (mq < nw + 31);
+      if constexpr (MASK == MASK_SLIDING_WINDOW) need_mask = need_mask || (mq + 31 - W >= nw);
+      // S = Q' K'^T and dP = dO V^T for 32 queries (rows) x this wave's 32 keys
+      // (columns); the two MFMA chains are interleaved.
+      f32x16 sc = f32x16{}, dp = f32x16{};
 #pragma unroll
-        for (int k = 0; k < C::KS; ++k) {
-          const u32x4 aq = *reinterpret_cast<const u32x4*>(Qs + (32 * qt + lq) * C::QP + 16 * k + 8 * lg);
-          const u32x4 ao = *reinterpret_cast<const u32x4*>(Os + (32 * qt + lq) * C::QP + 16 * k + 8 * lg);
-          sc = mfma32<QF16>(aq, kreg[k], sc);
-          dp = mfma32<true>(ao, vreg[k], dp);
+      for (int k = 0; k < C::KS; ++k) {
+        const u32x4 aq = *reinterpret_cast<const u32x4*>(Qs + (32 * qt + lq) * C::QP + 16 * k + 8 * lg);
+        const u32x4 ao = *reinterpret_cast<const u32x4*>(Os + (32 * qt + lq) * C::QP + 16 * k + 8 * lg);
+        const u32x4 bk = *reinterpret_cast<const u32x4*>(Ks + (32 * kw + lq) * C::VP + 16 * k + 8 * lg);
+        const u32x4 bv = *reinterpret_cast<const u32x4*>(Vs + (32 * kw + lq) * C::VP + 16 * k + 8 * lg);
+        sc = mfma32<QF16>(aq, bk, sc);
+        dp = mfma32<true>(ao, bv, dp);
+      }
+      // element r: query mq + 8 (r/4) + 4 lg + r%4, key n
+      float pr[16], ds[16];
+#pragma unroll
+      for (int a = 0; a < 4; ++a) {
+        const int qlb = 32 * qt + 8 * a + 4 * lg;
+        const float4 l4 = *reinterpret_cast<const float4*>(lse2s + qlb);
+        const float4 d4 = *reinterpret_cast<const float4*>(dels + qlb);
+        const float lv[4] = {l4.x, l4.y, l4.z, l4.w};
+        const float dv4[4] = {d4.x, d4.y, d4.z, d4.w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int r = 4 * a + e;
+          const float x = ALIBI ? __builtin_fmaf(sc[r], c2, slope2 * (float)(n - (mq + 8 * a + 4 * lg + e))) : sc[r] * c2;
+          pr[r] = fast_exp2(x - lv[e]);
+          ds[r] = dp[r] - dv4[e];
         }
-        // element r: query ql = 32 qt + 8 (r/4) + 4 lg + r%4, key n
-        float pr[16], ds[16];
+      }
+      if (need_mask) {   // wave-uniform: diagonal, window-edge and sequence-end tiles only
 #pragma unroll
-        for (int a = 0; a < 4; ++a) {
-          const int qlb = 32 * qt + 8 * a + 4 * lg;
-          const float4 l4 = *reinterpret_cast<const float4*>(lse2s + qlb);
-          const float4 d4 = *reinterpret_cast<const float4*>(dels + qlb);
-          const float lv[4] = {l4.x, l4.y, l4.z, l4.w};
-          const float dv4[4] = {d4.x, d4.y, d4.z, d4.w};
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const int r = 4 * a + e;
-            const float x = ALIBI ? __builtin_fmaf(sc[r], c2, slope2 * (float)(n - (mq0 + qlb + e))) : sc[r] * c2;
-            pr[r] = fast_exp2(x - lv[e]);
-            ds[r] = dp[r] - dv4[e];
-          }
+        for (int r = 0; r < 16; ++r) {
+          const int m = mq + 8 * (r >> 2) + 4 * lg + (r & 3);
+          bool ok = n < S;
+          if constexpr (MASK != MASK_NONE) ok = ok && (n <= m);
+          if constexpr (MASK == MASK_SLIDING_WINDOW) ok = ok && (n > m - W);
+          pr[r] = ok ? pr[r] : 0.f;
         }
-        if (need_mask) {   // wave-uniform: diagonal, window-edge and sequence-end tiles only
+      }
 #pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const int m = mq0 + 32 * qt + 8 * (r >> 2) + 4 * lg + (r & 3);
-            bool ok = n < S;
-            if constexpr (MASK != MASK_NONE) ok = ok && (n <= m);
-            if constexpr (MASK == MASK_SLIDING_WINDOW) ok = ok && (n > m - W);
-            pr[r] = ok ? pr[r] : 0.f;
-          }
+      for (int r = 0; r < 16; ++r) ds[r] *= pr[r];
+      u32x4 pb[2], db[2];
+#pragma unroll
+      for (int hf = 0; hf < 2; ++hf)
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+          pb[hf][w] = pack_f16(pr[8 * hf + 2 * w], pr[8 * hf + 2 * w + 1]);
+          db[hf][w] = pack_op<QF16>(ds[8 * hf + 2 * w], ds[8 * hf + 2 * w + 1]);
         }
+      // dV^T += dO^T P and dK'^T += Q'^T dS (transposed operands from row-major tiles)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) ds[r] *= pr[r];
-        u32x4 pb[2], db[2];
+      for (int hf = 0; hf < 2; ++hf) {
 #pragma unroll
-        for (int hf = 0; hf < 2; ++hf)
-#pragma unroll
-          for (int w = 0; w < 4; ++w) {
-            pb[hf][w] = pack_f16(pr[8 * hf + 2 * w], pr[8 * hf + 2 * w + 1]);
-            db[hf][w] = pack_op<QF16>(ds[8 * hf + 2 * w], ds[8 * hf + 2 * w + 1]);
-          }
-        // dV^T += dO^T P and dK'^T += Q'^T dS (transposed operands from row-major tiles)
-#pragma unroll
-        for (int hf = 0; hf < 2; ++hf) {
-#pragma unroll
-          for (int mt = 0; mt < C::MT; ++mt) {
-            dv[mt] = mfma32<true>(tr_operand(Os, C::QP, 32 * qt + 16 * hf, 32 * mt, lane), pb[hf], dv[mt]);
-            dk[mt] = mfma32<QF16>(tr_operand(Qs, C::QP, 32 * qt + 16 * hf, 32 * mt, lane), db[hf], dk[mt]);
-          }
+        for (int mt = 0; mt < C::MT; ++mt) {
+          dv[mt] = mfma32<true>(tr_operand(Os, C::QP, 32 * qt + 16 * hf, 32 * mt, lane), pb[hf], dv[mt]);
+          dk[mt] = mfma32<QF16>(tr_operand(Qs, C::QP, 32 * qt + 16 * hf, 32 * mt, lane), db[hf], dk[mt]);
         }
       }
     }
@@ -420,9 +442,32 @@ __global__ __launch_bounds__(256) void bwd_dkdv_kernel(BwdParams p) {
     __syncthreads();
   }
 
+  // Sum the pair's partials: the second wave of a pair hands over its dK, the
+  // first its dV, through [key block][element][lane] in the staging memory.
+  float* xch = reinterpret_cast<float*>(smem);
+  auto put = [&](f32x16 (&x)[C::MT]) {
+#pragma unroll
+    for (int mt = 0; mt < C::MT; ++mt)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) xch[(kw * (16 * C::MT) + 16 * mt + r) * 64 + lane] = x[mt][r];
+  };
+  auto add = [&](f32x16 (&x)[C::MT]) {
+#pragma unroll
+    for (int mt = 0; mt < C::MT; ++mt)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) x[mt][r] += xch[(kw * (16 * C::MT) + 16 * mt + r) * 64 + lane];
+  };
+  if (qh == 1) put(dk);
+  __syncthreads();
+  if (qh == 0) add(dk);
+  __syncthreads();
+  if (qh == 0) put(dv);
+  __syncthreads();
+  if (qh == 1) add(dv);
+
   if (n < S) {
-    store_grad_rows<D, ROPE>(dk, p.scale, static_cast<uint16_t*>(p.dk) + (size_t)bg * S * D, p.table, n, lg);
-    store_grad_rows<D, ROPE_NONE>(dv, 1.f, static_cast<uint16_t*>(p.dv) + (size_t)bg * S * D, nullptr, n, lg);
+    if (qh == 0) store_grad_rows<D, ROPE>(dk, p.scale, static_cast<uint16_t*>(p.dk) + (size_t)bg * S * D, p.table, n, lg);
+    else store_grad_rows<D, ROPE_NONE>(dv, 1.f, static_cast<uint16_t*>(p.dv) + (size_t)bg * S * D, nullptr, n, lg);
   }
 }
 

@@ -43,11 +43,10 @@ struct TileRegs {
 
 // Rows past S are clamped to row S-1 so every load is unconditional: those
 // keys are masked out of the scores and their V rows (finite data) receive
-// zero probability.
+// zero probability.  K and V halves can be loaded and committed separately.
 template <int D, int ROPE>
-__device__ __forceinline__ void tile_load(TileRegs<D, ROPE>& R, const uint16_t* __restrict__ K,
-                                          const uint16_t* __restrict__ V, const float2* __restrict__ table,
-                                          int n0, int S, int tid) {
+__device__ __forceinline__ void tile_load_k(TileRegs<D, ROPE>& R, const uint16_t* __restrict__ K,
+                                            const float2* __restrict__ table, int n0, int S, int tid) {
   using C = TileCfg<D, ROPE>;
 #pragma unroll
   for (int i = 0; i < C::KPT; ++i) {
@@ -62,6 +61,12 @@ __device__ __forceinline__ void tile_load(TileRegs<D, ROPE>& R, const uint16_t* 
       load_cs(R.cs[i], table + (size_t)n * (D / 2) + 4 * c);
     }
   }
+}
+
+template <int D, int ROPE>
+__device__ __forceinline__ void tile_load_v(TileRegs<D, ROPE>& R, const uint16_t* __restrict__ V, int n0, int S,
+                                            int tid) {
+  using C = TileCfg<D, ROPE>;
 #pragma unroll
   for (int i = 0; i < C::VPT; ++i) {
     const int it = tid + C::THREADS * i;
@@ -71,10 +76,17 @@ __device__ __forceinline__ void tile_load(TileRegs<D, ROPE>& R, const uint16_t* 
   }
 }
 
-// Rotate the staged K rows and write K' and V into one LDS stage.
 template <int D, int ROPE>
-__device__ __forceinline__ void tile_commit(TileRegs<D, ROPE>& R, uint16_t* __restrict__ Ks,
-                                            uint16_t* __restrict__ Vs, int tid) {
+__device__ __forceinline__ void tile_load(TileRegs<D, ROPE>& R, const uint16_t* __restrict__ K,
+                                          const uint16_t* __restrict__ V, const float2* __restrict__ table,
+                                          int n0, int S, int tid) {
+  tile_load_k<D, ROPE>(R, K, table, n0, S, tid);
+  tile_load_v<D, ROPE>(R, V, n0, S, tid);
+}
+
+// Rotate the staged K rows and write K' (and, separately, V) into an LDS stage.
+template <int D, int ROPE>
+__device__ __forceinline__ void tile_commit_k(TileRegs<D, ROPE>& R, uint16_t* __restrict__ Ks, int tid) {
   using C = TileCfg<D, ROPE>;
 #pragma unroll
   for (int i = 0; i < C::KPT; ++i) {
@@ -82,14 +94,21 @@ __device__ __forceinline__ void tile_commit(TileRegs<D, ROPE>& R, uint16_t* __re
     if (C::K_ITEMS % C::THREADS != 0 && it >= C::K_ITEMS) break;
     const int r = it / C::K_UNITS, c = it % C::K_UNITS;
     if constexpr (ROPE == ROPE_NEOX) {
-      rotate_neox8<false, true>(R.ka[i], R.kb[i], R.cs[i]);
-      *reinterpret_cast<u32x4*>(Ks + r * C::KP + 8 * c) = R.ka[i];
-      *reinterpret_cast<u32x4*>(Ks + r * C::KP + D / 2 + 8 * c) = R.kb[i];
+      u32x4 a = R.ka[i], bb = R.kb[i];
+      rotate_neox8<false, true>(a, bb, R.cs[i]);
+      *reinterpret_cast<u32x4*>(Ks + r * C::KP + 8 * c) = a;
+      *reinterpret_cast<u32x4*>(Ks + r * C::KP + D / 2 + 8 * c) = bb;
     } else {
-      if constexpr (ROPE == ROPE_INTERLEAVED) rotate_interleaved8<false, true>(R.ka[i], R.cs[i]);
-      *reinterpret_cast<u32x4*>(Ks + r * C::KP + 8 * c) = R.ka[i];
+      u32x4 a = R.ka[i];
+      if constexpr (ROPE == ROPE_INTERLEAVED) rotate_interleaved8<false, true>(a, R.cs[i]);
+      *reinterpret_cast<u32x4*>(Ks + r * C::KP + 8 * c) = a;
     }
   }
+}
+
+template <int D, int ROPE>
+__device__ __forceinline__ void tile_commit_v(const TileRegs<D, ROPE>& R, uint16_t* __restrict__ Vs, int tid) {
+  using C = TileCfg<D, ROPE>;
 #pragma unroll
   for (int i = 0; i < C::VPT; ++i) {
     const int it = tid + C::THREADS * i;
@@ -97,6 +116,13 @@ __device__ __forceinline__ void tile_commit(TileRegs<D, ROPE>& R, uint16_t* __re
     const int r = it / (D / 8), c = it % (D / 8);
     *reinterpret_cast<u32x4*>(Vs + r * C::VP + 8 * c) = R.v[i];
   }
+}
+
+template <int D, int ROPE>
+__device__ __forceinline__ void tile_commit(TileRegs<D, ROPE>& R, uint16_t* __restrict__ Ks,
+                                            uint16_t* __restrict__ Vs, int tid) {
+  tile_commit_k<D, ROPE>(R, Ks, tid);
+  tile_commit_v<D, ROPE>(R, Vs, tid);
 }
 
 // Query heads packed per workgroup by the forward and the dQ kernel: the

@@ -8,13 +8,19 @@
 // masked key tiles are never visited.
 //
 // Work decomposition
-//   workgroup = 8 waves (two per SIMD, so one wave's softmax VALU work runs
-//   under the other's MFMA work) = 256 query rows.  The rows are HP query
-//   heads of one GQA group x 256/HP positions, so one rotated K tile serves
-//   every head that reads it.  Key tiles of BN = 64 rows are double-buffered
-//   in LDS: the next tile's K, V and cos/sin are loaded into registers before
-//   the current tile is computed and committed (rotated) after it, with one
-//   barrier per tile.
+//   workgroup = 8 waves (two per SIMD) = 256 query rows.  The rows are HP
+//   query heads of one GQA group x 256/HP positions, so one rotated K tile
+//   serves every head that reads it.  Each wave owns 32 query rows and walks
+//   the key tiles (BN = 64 keys) as a two-stage software pipeline with one
+//   barrier per tile: part A issues tile t+1's score MFMAs while the VALU
+//   turns tile t's scores into probabilities (exp2, row sum, bf16 packing);
+//   part B issues tile t's PV MFMAs while the VALU rotates and stages later
+//   tiles and masks / reduces tile t+1's scores.  gfx950 issues MFMA and VALU
+//   instructions of one wave concurrently when they are independent, so each
+//   part keeps both units busy; a wave that stalls on LDS leaves its SIMD to
+//   the other wave.  K' and V tiles are double-buffered in LDS (K'_{t+2} and
+//   V_{t+1} are staged during iteration t, from registers loaded one
+//   iteration earlier).
 //   Scores are formed transposed, S^T = K' Q'^T (keys x queries), so every
 //   lane owns ONE query column and 16 keys per 32x32 MFMA tile: the row max
 //   is an in-lane reduction plus one v_permlane32_swap, and the row sum stays
@@ -29,6 +35,8 @@
 // (8-bit), which keeps the row statistic LSE within 1e-3 of the exact value;
 // the fp16 range then bounds the rotated inputs (|q|, |k| well below 65504).
 // P and V stay bf16.
+#include <type_traits>
+
 #include "attn_tiles.hpp"
 #include "launch.hpp"
 
@@ -40,7 +48,8 @@ __global__ __launch_bounds__(512) void fwd_bf16_kernel(FwdParams p) {
   constexpr bool QF16 = ROPE != ROPE_NONE;
   __shared__ __attribute__((aligned(16))) uint16_t smem[2 * C::STAGE];
 
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int lq = lane & 31, lg = lane >> 5;
   const int S = p.S;
   // Workgroup -> (batch, K/V head, head group, position block).  The position
@@ -70,6 +79,19 @@ __global__ __launch_bounds__(512) void fwd_bf16_kernel(FwdParams p) {
   const uint16_t* __restrict__ K = static_cast<const uint16_t*>(p.k) + (size_t)bg * S * D;
   const uint16_t* __restrict__ V = static_cast<const uint16_t*>(p.v) + (size_t)bg * S * D;
 
+  const float c2 = p.scale * kLog2e;                          // score -> log2 units
+  const float slope2 = ALIBI ? p.slopes[h] * kLog2e : 0.f;   // ALiBi slope, log2 units
+  const int W = p.window;
+
+  const int ntiles = (S + C::BN - 1) / C::BN;
+  int t_begin = 0, t_end = ntiles;
+  if constexpr (MASK != MASK_NONE) t_end = min(ntiles, (p_end - 1) / C::BN + 1);
+  if constexpr (MASK == MASK_SLIDING_WINDOW) t_begin = max(0, p0 - W + 1) / C::BN;
+  // LDS stage of key tile X (K' and V); the index is wave-uniform and kept
+  // opaque so per-read offsets fold into the LDS instructions.
+  auto kst = [&](int X) { return smem + __builtin_amdgcn_readfirstlane((X - t_begin) & 1) * C::STAGE; };
+  auto vst = [&](int X) { return kst(X) + C::K_ELEMS; };
+
   // Query operand (B of S^T = K Q^T): lane holds row m, dims 16s + 8lg .. +7.
   // Rows past S load row S-1 (finite data; never stored).
   const int mc = min(m, S - 1);
@@ -86,144 +108,203 @@ __global__ __launch_bounds__(512) void fwd_bf16_kernel(FwdParams p) {
       rotate_interleaved8<false, true>(qreg[s], p.table + (size_t)mc * (D / 2) + 8 * s + 4 * lg);
   }
 
-  const float c2 = p.scale * kLog2e;                          // score -> log2 units
-  const float slope2 = ALIBI ? p.slopes[h] * kLog2e : 0.f;   // ALiBi slope, log2 units
-  const int W = p.window;
-
-  const int ntiles = (S + C::BN - 1) / C::BN;
-  int t_begin = 0, t_end = ntiles;
-  if constexpr (MASK != MASK_NONE) t_end = min(ntiles, (p_end - 1) / C::BN + 1);
-  if constexpr (MASK == MASK_SLIDING_WINDOW) t_begin = max(0, p0 - W + 1) / C::BN;
+  // Prologue: stage K'_{t_begin}, K'_{t_begin+1}, V_{t_begin}; load the
+  // registers of the first in-loop commit (K'_{t_begin+2}, V_{t_begin+1}).
+  TileRegs<D, ROPE> R;
+  for (int X = t_begin; X < min(t_begin + 2, t_end); ++X) {
+    tile_load<D, ROPE>(R, K, V, p.table, X * C::BN, S, tid);
+    tile_commit_k<D, ROPE>(R, kst(X), tid);
+    if (X == t_begin) tile_commit_v<D, ROPE>(R, vst(X), tid);
+  }
+  // Every global load so far has landed (the commits waited for theirs);
+  // saying so explicitly keeps the compiler from guarding the loop's
+  // query-operand MFMAs with waits on the staging loads issued in the loop.
+  __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0), expcnt and lgkmcnt unconstrained
+  if (t_begin + 2 < t_end) tile_load_k<D, ROPE>(R, K, p.table, (t_begin + 2) * C::BN, S, tid);
+  if (t_begin + 1 < t_end) tile_load_v<D, ROPE>(R, V, (t_begin + 1) * C::BN, S, tid);
 
   f32x16 acc[C::MT];
 #pragma unroll
   for (int i = 0; i < C::MT; ++i) acc[i] = f32x16{};
   float m_run = -INFINITY;   // reference max of the row, log2 units
   float l_run = 0.f;         // this lane's partial row sum (relative to m_run)
+  float m_new = -INFINITY;   // max of the scores in flight (with m_run)
 
   // Transpose-read addressing for the V^T operand (see lds_read_tr16): lane i
   // of each 16-lane group reads 4 dims of key (4 lg + i/4) [+8 for the second
   // read]; the group's 16 lanes cover 16 dims starting at 16 * ((lane/16) & 1).
   const int tr_key = 4 * lg + ((lane & 15) >> 2);
   const int tr_col = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+  const int k_lane = lq * C::KP + 8 * lg;          // this lane's K' read offset
+  const int v_lane = tr_key * C::VP + tr_col;      // this lane's V transpose-read offset
 
-  TileRegs<D, ROPE> R;
-  if (t_begin < t_end) {
-    tile_load<D, ROPE>(R, K, V, p.table, t_begin * C::BN, S, tid);
-    tile_commit<D, ROPE>(R, smem, smem + C::K_ELEMS, tid);
-  }
-  __syncthreads();
-
-  for (int t = t_begin; t < t_end; ++t) {
-    const int n0 = t * C::BN;
-    const uint16_t* Ks = smem + ((t - t_begin) & 1) * C::STAGE;
-    const uint16_t* Vs = Ks + C::K_ELEMS;
-    const bool more = t + 1 < t_end;
-    if (more) tile_load<D, ROPE>(R, K, V, p.table, n0 + C::BN, S, tid);
-
-    bool visible = mw < S;
-    if constexpr (MASK != MASK_NONE) visible = visible && (n0 <= mw + 31);
-    if constexpr (MASK == MASK_SLIDING_WINDOW) visible = visible && (n0 + C::BN - 1 > mw - W);
-    if (visible) {   // wave-uniform
-      // S^T = K' Q'^T: two 32-key subtiles, their MFMA chains interleaved.
-      f32x16 st[2] = {f32x16{}, f32x16{}};
+  // S^T = K' Q'^T for one tile: two 32-key subtiles, chains interleaved.
+  auto scores = [&](f32x16 (&sc)[2], const uint16_t* Ks) {
+    const uint16_t* kb = Ks + k_lane;
+    sc[0] = f32x16{};
+    sc[1] = f32x16{};
 #pragma unroll
-      for (int s = 0; s < C::KS; ++s) {
+    for (int s = 0; s < C::KS; ++s)
 #pragma unroll
-        for (int kt = 0; kt < 2; ++kt) {
-          u32x4 a = *reinterpret_cast<const u32x4*>(Ks + (32 * kt + lq) * C::KP + 16 * s + 8 * lg);
-          st[kt] = mfma32<QF16>(a, qreg[s], st[kt]);
+      for (int kt = 0; kt < 2; ++kt) {
+        const u32x4 a = *reinterpret_cast<const u32x4*>(kb + 32 * kt * C::KP + 16 * s);
+        sc[kt] = mfma32<QF16>(a, qreg[s], sc[kt]);
+      }
+  };
+  // O^T += V^T P^T for one tile; the head-dimension accumulators interleaved.
+  auto pv = [&](const u32x4 (&pop)[2][2], const uint16_t* Vs) {
+    const uint16_t* vb = Vs + v_lane;
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+      for (int hf = 0; hf < 2; ++hf)
+#pragma unroll
+        for (int mt = 0; mt < C::MT; ++mt) {
+          const uint16_t* base = vb + (32 * kt + 16 * hf) * C::VP + 32 * mt;
+          const u32x2 lo = lds_read_tr16(base);
+          const u32x2 hi = lds_read_tr16(base + 8 * C::VP);
+          const u32x4 a = {lo[0], lo[1], hi[0], hi[1]};
+          acc[mt] = mfma32(a, pop[kt][hf], acc[mt]);
         }
-      }
+  };
 
-      // Scores in log2 units (ALiBi folded in); element r of subtile kt is key
-      // n0 + 32 kt + 8 (r/4) + 4 lg + r%4.
-      if constexpr (ALIBI) {
-#pragma unroll
-        for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const int n = n0 + 32 * kt + 8 * (r >> 2) + 4 * lg + (r & 3);
-            st[kt][r] = __builtin_fmaf(st[kt][r], c2, slope2 * (float)(n - m));
-          }
-      }
-      // Masked entries at -inf; only tiles that cross the diagonal, the window
-      // edge or the sequence end pay for it (one wave-uniform branch).
-      bool need_mask = n0 + C::BN > S;
-      if constexpr (MASK != MASK_NONE) need_mask = need_mask || (n0 + C::BN - 1 > mw);
-      if constexpr (MASK == MASK_SLIDING_WINDOW) need_mask = need_mask || (n0 <= mw + 31 - W);
-      if (need_mask) {
-#pragma unroll
-        for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const int n = n0 + 32 * kt + 8 * (r >> 2) + 4 * lg + (r & 3);
-            bool ok = n < S;
-            if constexpr (MASK != MASK_NONE) ok = ok && (n <= m);
-            if constexpr (MASK == MASK_SLIDING_WINDOW) ok = ok && (n > m - W);
-            st[kt][r] = ok ? st[kt][r] : -INFINITY;
-          }
-      }
-
-      float mx = -INFINITY;
+  // Scores of tile t in log2 units (ALiBi folded in), masked entries at -inf,
+  // and their max merged into m_new.  Element r of subtile kt is key
+  // n0 + 32 kt + 8 (r/4) + (r%4) + 4 lg of query mw + lq; mask and bias tests
+  // compare one per-lane offset against the element's constant part, so
+  // nothing per element stays live across tiles.  A tile with no visible key
+  // for this wave (at the edge of the workgroup's range) is fully masked and
+  // contributes P = 0.  Under a causal or window mask a key past S is also past
+  // the query (rows past S are never stored), so only the unmasked variant
+  // tests the sequence end.
+  const int lane_off = 4 * lg - lq;
+  auto prepare = [&](f32x16 (&sc)[2], int t) {
+    const int n0 = t * C::BN;
+    const int dq = n0 - mw + lane_off;        // key - query of element offset 0
+    if constexpr (ALIBI) {
+      const float fb = slope2 * (float)dq;
 #pragma unroll
       for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, st[kt][r]);
-      mx = pair_max(mx);
-      if constexpr (!ALIBI) mx *= c2;
-      const float m_new = fmaxf(m_run, mx);
-      if (__any(m_new > m_run + 8.f)) {   // raise the reference max (wave-uniform)
-        const float alpha = (m_run == -INFINITY) ? 0.f : fast_exp2(m_run - m_new);
-        l_run *= alpha;
+        for (int r = 0; r < 16; ++r) {
+          const float cr = (float)(32 * kt + 8 * (r >> 2) + (r & 3));
+          sc[kt][r] = __builtin_fmaf(sc[kt][r], c2, __builtin_fmaf(slope2, cr, fb));
+        }
+    }
+    bool need_mask;
+    if constexpr (MASK == MASK_NONE) need_mask = n0 + C::BN > S;
+    else need_mask = n0 + C::BN - 1 > mw;
+    if constexpr (MASK == MASK_SLIDING_WINDOW) need_mask = need_mask || (n0 <= mw + 31 - W);
+    if (need_mask) {   // wave-uniform: diagonal, window-edge and sequence-end tiles only
+      const int de = n0 + 4 * lg - S;        // key - S of element offset 0
 #pragma unroll
-        for (int i = 0; i < C::MT; ++i) acc[i] *= alpha;
-        m_run = m_new;
-      }
-      const float m_use = (m_run == -INFINITY) ? 0.f : m_run;
-
-      u32x4 pb[2][2];
-      float rs = 0.f;
-#pragma unroll
-      for (int kt = 0; kt < 2; ++kt) {
-        float pv[16];
+      for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const float arg = ALIBI ? (st[kt][r] - m_use) : __builtin_fmaf(st[kt][r], c2, -m_use);
-          pv[r] = fast_exp2(arg);
-          rs += pv[r];
+          const int cr = 32 * kt + 8 * (r >> 2) + (r & 3);
+          bool ok;
+          if constexpr (MASK == MASK_NONE) ok = de < -cr;
+          else ok = dq <= -cr;
+          if constexpr (MASK == MASK_SLIDING_WINDOW) ok = ok && (dq + W > -cr);
+          sc[kt][r] = ok ? sc[kt][r] : -INFINITY;
         }
-#pragma unroll
-        for (int hf = 0; hf < 2; ++hf)
-#pragma unroll
-          for (int w = 0; w < 4; ++w) pb[kt][hf][w] = pack_bf16(pv[8 * hf + 2 * w], pv[8 * hf + 2 * w + 1]);
-      }
-      l_run += rs;
-
-      // O^T += V^T P^T; the V^T operand is two transpose reads of row-major V.
-      // The head-dimension tiles are independent accumulators, interleaved.
-#pragma unroll
-      for (int kt = 0; kt < 2; ++kt) {
-#pragma unroll
-        for (int hf = 0; hf < 2; ++hf) {
-#pragma unroll
-          for (int mt = 0; mt < C::MT; ++mt) {
-            const uint16_t* base = Vs + (32 * kt + 16 * hf + tr_key) * C::VP + 32 * mt + tr_col;
-            const u32x2 lo = lds_read_tr16(base);
-            const u32x2 hi = lds_read_tr16(base + 8 * C::VP);
-            const u32x4 a = {lo[0], lo[1], hi[0], hi[1]};
-            acc[mt] = mfma32(a, pb[kt][hf], acc[mt]);
-          }
-        }
-      }
     }
-
-    if (more) {
-      uint16_t* Kn = smem + ((t + 1 - t_begin) & 1) * C::STAGE;
-      tile_commit<D, ROPE>(R, Kn, Kn + C::K_ELEMS, tid);
+    float mx = -INFINITY;
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sc[kt][r]);
+    mx = pair_max(mx);
+    if constexpr (!ALIBI) mx *= c2;
+    m_new = fmaxf(m_run, mx);
+  };
+  // Raise the reference max when a row's max grew by more than 2^8 (rare,
+  // wave-uniform): the accumulated O and l are rescaled together.
+  auto raise = [&]() {
+    if (__any(m_new > m_run + 8.f)) {
+      const float alpha = (m_run == -INFINITY) ? 0.f : fast_exp2(m_run - m_new);
+      l_run *= alpha;
+#pragma unroll
+      for (int i = 0; i < C::MT; ++i) acc[i] *= alpha;
+      m_run = m_new;
     }
-    __syncthreads();
+  };
+  // P = exp2(score - m_run) as bf16 B operands, and the row sum.
+  auto probs = [&](const f32x16 (&sc)[2], u32x4 (&pop)[2][2]) {
+    const float m_use = (m_run == -INFINITY) ? 0.f : m_run;
+    float rs = 0.f;
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt) {
+      float pv_[16];
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const float arg = ALIBI ? (sc[kt][r] - m_use) : __builtin_fmaf(sc[kt][r], c2, -m_use);
+        pv_[r] = fast_exp2(arg);
+        rs += pv_[r];
+      }
+#pragma unroll
+      for (int hf = 0; hf < 2; ++hf)
+#pragma unroll
+        for (int w = 0; w < 4; ++w) pop[kt][hf][w] = pack_bf16(pv_[8 * hf + 2 * w], pv_[8 * hf + 2 * w + 1]);
+    }
+    l_run += rs;
+  };
+
+  // Materialise P and the row sum here: otherwise the compiler sinks their
+  // computation next to the PV MFMAs that consume them, out of part A.
+  auto pin_values = [](u32x4 (&pp)[2][2], float& l) {
+    asm volatile("" : "+v"(pp[0][0]), "+v"(pp[0][1]), "+v"(pp[1][0]), "+v"(pp[1][1]), "+v"(l));
+  };
+
+  // Software pipeline, one barrier per tile.  Entering iteration t the scores
+  // of tile t are prepared (masked, max merged, O rescaled).  Part A issues
+  // tile t+1's score MFMAs together with tile t's exp2 / sum / bf16 packing;
+  // part B issues tile t's PV MFMAs together with staging (K'_{t+2} rotated,
+  // V_{t+1}) and tile t+1's mask and max.  Within each part the MFMA and VALU
+  // streams are independent, so every wave keeps the matrix core and the
+  // vector ALU busy at once.  Tile X lives in LDS stage X & 1: iteration t
+  // reads K'_{t+1} and V_t and writes K'_{t+2} and V_{t+1}, so within an
+  // iteration no stage half is both read and written.
+  f32x16 sa[2], sb[2];
+  u32x4 pop[2][2];
+  __syncthreads();
+  if (t_begin < t_end) {
+    scores(sa, kst(t_begin));
+    prepare(sa, t_begin);
+    raise();
   }
+  // The first iteration stages K'_{t_begin+2} into the stage just read.
+  __syncthreads();
+  int t = t_begin;
+  auto iteration = [&](f32x16 (&cur)[2], f32x16 (&nxt)[2]) {
+    // A
+    probs(cur, pop);
+    scores(nxt, kst(t + 1));
+    pin_values(pop, l_run);   // keep the softmax work in this part
+    // B.  Staging past the last tile rewrites a stage nobody reads any more
+    // (clamped rows), which keeps this part free of branches.
+    prepare(nxt, t + 1);
+    pv(pop, vst(t));
+    tile_commit_k<D, ROPE>(R, kst(t + 2), tid);
+    tile_commit_v<D, ROPE>(R, vst(t + 1), tid);
+    tile_load_k<D, ROPE>(R, K, p.table, min(t + 3, t_end - 1) * C::BN, S, tid);
+    tile_load_v<D, ROPE>(R, V, min(t + 2, t_end - 1) * C::BN, S, tid);
+    raise();
+    __syncthreads();
+    ++t;
+  };
+  // two iterations per trip so the score buffers alternate without copies
+  while (t + 2 < t_end) {
+    iteration(sa, sb);
+    iteration(sb, sa);
+  }
+  if (t + 1 < t_end) {
+    iteration(sa, sb);
+    probs(sb, pop);
+  } else if (t < t_end) {
+    probs(sa, pop);
+  }
+  if (t < t_end) pv(pop, vst(t));
 
   // Epilogue: O = acc / l, LSE = (m + log2 l) ln 2.
   const float l_tot = pair_sum(l_run);

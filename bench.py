@@ -13,7 +13,10 @@ Alongside, on the same inputs and outside the timed steps:
 * the separate-RoPE path (rotation kernel, then the forward without RoPE) and
   the rotation kernel's HBM bandwidth, measured over a buffer pool larger than
   twice the 256 MB Infinity Cache;
-* the fuse-vs-separate crossover over S = 1024..16384 (skip with --no-sweep);
+* the fuse-vs-separate crossover over S = 1024..16384 (skip with --no-sweep),
+  each point the median of 50 calls after 10 warm-ups, and the rotation
+  calculus model fitted to it (crossover_model: fused extra time a*S^2,
+  separate rotation b*S, model crossover b/a next to the measured one);
 * a plain device-to-device copy of 512 MiB: the achievable HBM bandwidth next
   to the rotation kernel's, and the calibration kernel for the HBM-traffic
   counters;
@@ -67,11 +70,49 @@ def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
+def crossover_fit(sweep, w, s_min=4096, rows_per_rotation=256):
+    """Fit the rotation-calculus model to the sweep (Section 5.3, Eq. 1 restated
+    with consistent units): the fused kernel's extra time over the no-RoPE
+    kernel grows as a * S^2 (every workgroup of `rows_per_rotation` query rows
+    rotates each K tile it visits once), the separate rotation as b * S (one HBM
+    round trip of Q and K).  Fitted by least squares through the origin on the
+    points with S >= s_min, where both kernels fill the GPU; the model's
+    crossover is S* = b / a.  Also reported: the measured crossover (where the
+    fused speedup crosses 1, interpolated in log S), the fused kernel's
+    effective cost per rotated K element, the VALU operations per element that
+    cost stands for at the chip's fp32 lane rate (e_rot * (1 - phi)), and the
+    rotation's achieved bandwidth."""
+    pts = [r for r in sweep if r["S"] >= s_min]
+    if len(pts) < 2:
+        return None
+    a = sum((r["fused_ms"] - r["norope_ms"]) * r["S"] ** 2 for r in pts) / sum(r["S"] ** 4 for r in pts)
+    b = sum(r["rope_ms"] * r["S"] for r in pts) / sum(r["S"] ** 2 for r in pts)
+    measured = None
+    for lo, hi in zip(sweep, sweep[1:]):
+        if (lo["fused_speedup"] - 1.0) * (hi["fused_speedup"] - 1.0) <= 0 and lo["fused_speedup"] != hi["fused_speedup"]:
+            f = (lo["fused_speedup"] - 1.0) / (lo["fused_speedup"] - hi["fused_speedup"])
+            measured = round(math.exp(math.log(lo["S"]) + f * (math.log(hi["S"]) - math.log(lo["S"]))))
+            break
+    # rotated K elements per fused launch at S: B*H*S^2*D / (2 * rows_per_rotation) (causal)
+    rot_elems_per_s2 = w.B * w.H * w.D / (2.0 * rows_per_rotation)
+    c_rot_s = a * 1e-3 / rot_elems_per_s2            # seconds per rotated element
+    lane_rate = 256 * 4 * 16 * 2.4e9                  # fp32 VALU lane operations per second
+    bytes_per_s = 4.0 * w.B * (w.H + w.Hkv) * w.D     # separate rotation bytes per unit S
+    return {"fit_points_S": [r["S"] for r in pts],
+            "a_ms_per_S2": a, "b_ms_per_S": b,
+            "S_star_model": round(b / a) if a > 0 else None,
+            "S_star_measured": measured,
+            "fused_rot_ps_per_element": round(c_rot_s * 1e12, 3),
+            "e_rot_times_1_minus_phi": round(c_rot_s * lane_rate, 2),
+            "rotation_gbs_fit": round(bytes_per_s / (b * 1e-3) / 1e9, 1),
+            "rows_per_rotation": rows_per_rotation}
+
+
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="llama3_8b_b1h32kv8s8192d128")
     ap.add_argument("--no-sweep", action="store_true", help="skip the fuse-vs-separate sweep over S")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -197,6 +238,7 @@ def main():
         log(f"separate path: rope {rot_avg:.4f} ms ({rope_bw:.0f} GB/s) + fwd {sep_avg:.4f} ms")
 
     sweep = None
+    crossover = None
     if not args.no_sweep and w.rope != "none":
         sweep = []
         for S in LLAMA_SWEEP_S:
@@ -222,9 +264,9 @@ def main():
                 api.attnfuse_fwd(po[0][0], po[0][1], vs, out=os_, lse=ls, **dict(kw, rope="none"))
 
             for fn in (rot_s, fused_s, none_s):
-                for _ in range(3):
+                for _ in range(10):
                     fn()
-            reps = 20
+            reps = 50
             r_ms = statistics.median(time_calls(rot_s, max(reps, 2 * npool)))
             f_ms = statistics.median(time_calls(fused_s, reps))
             n_ms = statistics.median(time_calls(none_s, reps))
@@ -234,6 +276,7 @@ def main():
             log(f"sweep S={S}: fused {f_ms:.4f} ms, rope {r_ms:.4f} + norope {n_ms:.4f} ms")
             del pq, po, qs, ks, vs, os_, ls
         torch.cuda.empty_cache()
+        crossover = crossover_fit(sweep, w)
 
     # ---------------------------------------------------------------- plain copy reference
     copy_bytes = 512 << 20
@@ -300,6 +343,7 @@ def main():
     }
     if sweep is not None:
         line["crossover_sweep"] = sweep
+        line["crossover_model"] = crossover
     print(json.dumps(line), flush=True)
 
 

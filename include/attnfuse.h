@@ -42,7 +42,7 @@ extern "C" {
 #endif
 
 /* Element type of Q, K, V, O, dO, dQ, dK, dV.  fp32 is the debug path: same
- * method, fp32 arithmetic throughout, no MFMA (forward and rotation only). */
+ * method, fp32 arithmetic throughout, no MFMA, one row per thread. */
 enum { AF_DTYPE_BF16 = 0, AF_DTYPE_FP32 = 1 };
 
 /* RoPE pairing (Section 4.1 "Fused RoPE": the paper's NeoX convention pairs
@@ -109,7 +109,9 @@ size_t attnfuse_bwd_workspace_bytes(int B, int H, int H_kv, int S, int D, int ro
  *   workspace            device memory of >= attnfuse_bwd_workspace_bytes(B,
  *                        H, H_kv, S, D, rope) bytes (16-byte aligned),
  *                        caller-owned scratch, overwritten
- *   other arguments      as attnfuse_fwd.  Only AF_DTYPE_BF16 is compiled.
+ *   other arguments      as attnfuse_fwd.  AF_DTYPE_FP32 runs the fp32 debug
+ *                        backward (same passes, fp32 arithmetic; it uses only
+ *                        the workspace's row statistics).
  */
 int attnfuse_bwd(const void* Q, const void* K, const void* V, const void* O, const void* dO,
                  const float* LSE, void* dQ, void* dK, void* dV,

@@ -173,7 +173,7 @@ int attnfuse_bwd(const void* Q, const void* K, const void* V, const void* O, con
   if (rc != AF_OK) return rc;
   if ((rc = check_attn(mask, window, softmax_scale)) != AF_OK) return rc;
   if (workspace_bytes < attnfuse_bwd_workspace_bytes(B, H, H_kv, S, D, rope)) return AF_ERR_INVALID_ARG;
-  if (!supported_d(D) || dtype != AF_DTYPE_BF16) return AF_ERR_UNSUPPORTED;
+  if (!supported_d(D)) return AF_ERR_UNSUPPORTED;
 
   hipStream_t st = static_cast<hipStream_t>(stream);
   af::BwdParams p{};
@@ -193,7 +193,9 @@ int attnfuse_bwd(const void* Q, const void* K, const void* V, const void* O, con
   p.scale = softmax_scale;
   p.table = nullptr;
   if (rope != AF_ROPE_NONE && (rc = rope_table(D, rope_theta, S, st, &p.table)) != AF_OK) return rc;
-  return map_launch(af::launch_bwd_bf16(D, rope, mask, alibi_slopes != nullptr, p, st));
+  const bool alibi = alibi_slopes != nullptr;
+  if (dtype == AF_DTYPE_FP32) return map_launch(af::launch_bwd_fp32(D, rope, mask, alibi, p, st));
+  return map_launch(af::launch_bwd_bf16(D, rope, mask, alibi, p, st));
 }
 
 static int rope_common(const void* X0, const void* X1, void* Y0, void* Y1, int B, int H, int H_kv, int S, int D,

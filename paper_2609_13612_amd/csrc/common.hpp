@@ -159,6 +159,20 @@ __device__ __forceinline__ u32x4 ld16(const void* p) {
 }
 __device__ __forceinline__ void st16(void* p, u32x4 v) { *reinterpret_cast<u32x4*>(p) = v; }
 
+// Rotate a whole fp32 row in place (INVERSE: by the negative angle, the
+// transpose of the rotation, which carries gradients back); cs holds the
+// row's D/2 (cos, sin) pairs.  Used by the fp32 debug kernels.
+template <int D, int ROPE, bool INVERSE = false>
+__device__ __forceinline__ void rotate_row_f32(float* x, const float2* __restrict__ cs) {
+  if constexpr (ROPE == ROPE_NEOX) {
+#pragma unroll
+    for (int i = 0; i < D / 2; ++i) rotate_pair<INVERSE>(x[i], x[i + D / 2], cs[i].x, cs[i].y);
+  } else if constexpr (ROPE == ROPE_INTERLEAVED) {
+#pragma unroll
+    for (int i = 0; i < D / 2; ++i) rotate_pair<INVERSE>(x[2 * i], x[2 * i + 1], cs[i].x, cs[i].y);
+  }
+}
+
 // gfx950 LDS transpose read (ds_read_b64_tr_b16).  Within each group of 16
 // lanes the sixteen 8-byte chunks the lanes address form a 4 x 16 matrix of
 // 16-bit values (row r = the chunks of lanes 4r..4r+3, in lane order); lane i

@@ -11,17 +11,6 @@ namespace af {
 constexpr int F32_ROWS = 64;   // query rows per workgroup (one wave)
 constexpr int F32_BN = 32;     // keys per tile
 
-template <int D, int ROPE>
-__device__ __forceinline__ void rotate_row_f32(float* x, const float2* __restrict__ cs) {
-  if constexpr (ROPE == ROPE_NEOX) {
-#pragma unroll
-    for (int i = 0; i < D / 2; ++i) rotate_pair<false>(x[i], x[i + D / 2], cs[i].x, cs[i].y);
-  } else if constexpr (ROPE == ROPE_INTERLEAVED) {
-#pragma unroll
-    for (int i = 0; i < D / 2; ++i) rotate_pair<false>(x[2 * i], x[2 * i + 1], cs[i].x, cs[i].y);
-  }
-}
-
 template <int D, int ROPE, int MASK, bool ALIBI>
 __global__ __launch_bounds__(64) void fwd_fp32_kernel(FwdParams p) {
   __shared__ float Kf[F32_BN][D + 1];

@@ -52,6 +52,7 @@ struct RopeParams {
 int launch_fwd_bf16(int D, int rope, int mask, bool alibi, const FwdParams& p, hipStream_t st);
 int launch_fwd_fp32(int D, int rope, int mask, bool alibi, const FwdParams& p, hipStream_t st);
 int launch_bwd_bf16(int D, int rope, int mask, bool alibi, const BwdParams& p, hipStream_t st);
+int launch_bwd_fp32(int D, int rope, int mask, bool alibi, const BwdParams& p, hipStream_t st);
 int launch_rope(bool fp32, int D, int rope, bool inverse, const RopeParams& p, hipStream_t st);
 int launch_rope_table(float2* table, int rows, int D, double theta, hipStream_t st);
 

@@ -6,7 +6,7 @@ import pytest
 import torch
 
 import oracle
-from gpu_util import announce, assert_bf16_close, device_inputs, f64, need_gpu
+from gpu_util import announce, assert_bf16_close, assert_fp32_close, device_inputs, f64, need_gpu
 from paper_2609_13612_amd import api, inputs
 from paper_2609_13612_amd.workloads import WORKLOADS
 
@@ -40,6 +40,25 @@ def test_bwd_variants(rope, mask, alibi, D):
     got, ref = _run(cpu, dev, B, H, Hkv, S, D, rope, 10000.0, mask, window, alibi)
     for name, g, r in zip(("dQ", "dK", "dV"), got, ref):
         assert_bf16_close(g, r, name)
+
+
+FP32_VARIANTS = [("neox", "sliding_window", False, 128), ("interleaved", "none", True, 64),
+                 ("none", "causal", True, 128), ("neox", "causal", False, 64),
+                 ("interleaved", "causal", False, 128), ("none", "sliding_window", True, 64)]
+
+
+@pytest.mark.parametrize("rope,mask,alibi,D", FP32_VARIANTS, ids=lambda x: str(x))
+def test_bwd_fp32_variants(rope, mask, alibi, D):
+    """The fp32 debug backward against the fp64 oracle at the fp32 bound (1e-4),
+    with a ragged S (two 64-row blocks and a tail) and a GQA group of two."""
+    need_gpu()
+    B, H, Hkv, S = 1, 4, 2, 130
+    window = 50 if mask == "sliding_window" else None
+    announce(f"bwd fp32 rope={rope} mask={mask} alibi={alibi} D={D} S={S}")
+    cpu, dev = device_inputs(B, H, Hkv, S, D, dtype="fp32", seed=13, with_do=True)
+    got, ref = _run(cpu, dev, B, H, Hkv, S, D, rope, 10000.0, mask, window, alibi)
+    for name, g, r in zip(("dQ", "dK", "dV"), got, ref):
+        assert_fp32_close(g, r, name + " fp32")
 
 
 EDGE = [

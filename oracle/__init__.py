@@ -19,6 +19,8 @@ with the full score matrix materialised per (batch, head):
   ten combinators).
 * The backward follows the FlashAttention-2 equations; the forward keeps one
   scalar per row, L = m + log l (Section 4.4 "Backward Pass").
+* Decode (one query per sequence against a key/value cache, Section 2 "Flash
+  Decoding") is the same definition for that single row: ``decode_forward``.
 
 Every function is pinned by ``tests/test_oracle_*.py`` against invariants,
 closed forms, an independent brute force, finite differences and library
@@ -45,6 +47,7 @@ from .attention import (
     attention_backward,
     attention_forward_rows,
 )
+from .decode import decode_forward
 
 __all__ = [
     "ROPE_NONE", "ROPE_NEOX", "ROPE_INTERLEAVED", "ROPE_KINDS",
@@ -52,4 +55,5 @@ __all__ = [
     "MASK_NONE", "MASK_CAUSAL", "MASK_SLIDING_WINDOW", "MASK_KINDS",
     "visibility", "attention_scores", "attention_probs",
     "attention_forward", "attention_backward", "attention_forward_rows",
+    "decode_forward",
 ]

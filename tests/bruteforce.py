@@ -118,3 +118,40 @@ def finite_difference_grad(x, f, eps=1e-6):
 
     walk(x, g)
     return g
+
+
+def decode(q, k_cache, v_cache, cache_lens=None, *, rope="none", theta=10000.0, mask="causal", window=None,
+           alibi_slopes=None, scale=None):
+    """One query per (b, h) at position len_b - 1 against caches of already-rotated keys.
+
+    q: nested lists [B][H][D]; caches [B][Hkv][S_kv][D].  Returns (O [B][H][D], LSE [B][H]).
+    """
+    B, H, D = len(q), len(q[0]), len(q[0][0])
+    Hkv, S_kv = len(k_cache[0]), len(k_cache[0][0])
+    group = H // Hkv
+    if scale is None:
+        scale = 1.0 / math.sqrt(D)
+    lens = [S_kv] * B if cache_lens is None else [int(x) for x in cache_lens]
+    O = [[[0.0] * D for _ in range(H)] for _ in range(B)]
+    LSE = [[0.0] * H for _ in range(B)]
+    for b in range(B):
+        p = lens[b] - 1
+        rot = givens_matrix(D, p, theta, rope)
+        for h in range(H):
+            kvh = h // group
+            qr = matvec(rot, q[b][h])
+            scores = {}
+            for j in range(lens[b]):
+                if mask == "sliding_window" and not p - j < window:
+                    continue
+                sc = scale * dot(qr, k_cache[b][kvh][j])
+                if alibi_slopes is not None:
+                    sc -= alibi_slopes[h] * (p - j)
+                scores[j] = sc
+            mx = max(scores.values())
+            w = {j: math.exp(sc - mx) for j, sc in scores.items()}
+            tot = math.fsum(w.values())
+            LSE[b][h] = mx + math.log(tot)
+            for d in range(D):
+                O[b][h][d] = math.fsum(w[j] * v_cache[b][kvh][j][d] for j in w) / tot
+    return O, LSE

@@ -341,3 +341,57 @@ def check_backward_identities(seed=17):
     # The last key is seen only by the last query: dV_{S-1} = sum over heads of P * dO.
     P_last = [inter["P"][(0, h)][-1, -1] for h in range(2)]
     assert np.allclose(dv[0, :, -1], np.array([P_last[h] * do[0, h, -1] for h in range(2)]), atol=1e-13)
+
+
+# ----------------------------------------------------------------------------- decode
+
+def _decode_case(seed, B=2, H=4, Hkv=2, S=7, D=4):
+    r = _rng(seed)
+    return (r.standard_normal((B, H, D)), r.standard_normal((B, Hkv, S, D)), r.standard_normal((B, Hkv, S, D)))
+
+
+def check_decode_vs_bruteforce(variant, seed=20):
+    rope, mask, window, alibi = variant
+    q, kc, vc = _decode_case(seed)
+    kw = _kw(rope, mask, window, alibi, 4)
+    for lens in (None, [7, 3]):
+        O, L = oracle.decode_forward(q, kc, vc, lens, **kw)
+        Ob, Lb = bruteforce.decode(q.tolist(), kc.tolist(), vc.tolist(), lens, **kw)
+        assert np.allclose(O, np.array(Ob), atol=TOL, rtol=0)
+        assert np.allclose(L, np.array(Lb), atol=TOL, rtol=0)
+
+
+def check_decode_is_last_prefill_row(variant, seed=21):
+    # A cache written with keys rotated at their own positions, queried by the
+    # last token, is the last row of the prefill attention over those tokens.
+    rope, mask, window, alibi = variant
+    q, k, v, _ = _tiny(seed, B=2, H=4, Hkv=2, S=9, D=8)
+    kw = _kw(rope, mask, window, alibi, 4)
+    k_cache = oracle.rope_rotate(k, np.arange(9), 10000.0, rope)
+    for n in (9, 5, 1):
+        O, L = oracle.attention_forward(q[:, :, :n], k[:, :, :n], v[:, :, :n], **kw)
+        Od, Ld = oracle.decode_forward(q[:, :, n - 1], k_cache, v, [n, n], **kw)
+        assert np.allclose(Od, O[:, :, n - 1], atol=1e-13, rtol=0)
+        assert np.allclose(Ld, L[:, :, n - 1], atol=1e-13, rtol=0)
+
+
+def check_decode_closed_forms(kind, seed=22):
+    q, kc, vc = _decode_case(seed, B=1, H=2, Hkv=2, S=6, D=8)
+    # one cached token: the query is at position 0 (no rotation), O = v_0
+    O, L = oracle.decode_forward(q, kc, vc, [1], rope=kind, scale=0.7)
+    assert np.allclose(O[0], vc[0, :, 0], atol=1e-15)
+    assert np.allclose(L[0], 0.7 * np.einsum("hd,hd->h", q[0], kc[0, :, 0]), atol=1e-14)
+    # a width-1 window sees only the newest key
+    O, _ = oracle.decode_forward(q, kc, vc, [5], rope=kind, mask="sliding_window", window=1)
+    assert np.allclose(O[0], vc[0, :, 4], atol=1e-15)
+
+
+def check_decode_ignores_stale_entries(seed=23):
+    q, kc, vc = _decode_case(seed)
+    base = oracle.decode_forward(q, kc, vc, [4, 6], rope="neox")
+    kc2, vc2 = kc.copy(), vc.copy()
+    kc2[0, :, 4:] = 1e3
+    vc2[0, :, 4:] = -7.0
+    kc2[1, :, 6:] = 5.0
+    other = oracle.decode_forward(q, kc2, vc2, [4, 6], rope="neox")
+    assert np.array_equal(base[0], other[0]) and np.array_equal(base[1], other[1])

@@ -9,6 +9,7 @@ import pytest
 
 import oracle
 import oracle.attention as oatt
+import oracle.decode as odec
 import oracle.rope as orope
 import oracle_pins as P
 
@@ -77,9 +78,20 @@ def _no_scale_defaults(D, scale, alibi_slopes, H):
 _REAL_DEFAULTS = oatt._defaults
 
 
+def _bad_decode_visible(j, p, mask, window=None):
+    j = np.asarray(j)
+    if mask == "sliding_window":
+        return (j <= p) & (j >= p - window)        # W + 1 keys
+    return j <= p
+
+
 MUTATIONS = {
     "rotation_sign": [(oatt, "rope_rotate", _wrong_sign_rotate), (orope, "rope_rotate", _wrong_sign_rotate),
                       (oracle, "rope_rotate", _wrong_sign_rotate)],
+    "decode_rotation_sign": [(odec, "rope_rotate", _wrong_sign_rotate)],
+    "decode_gqa_mapping": [(odec, "kv_head", _bad_kv_head)],
+    "decode_query_position": [(odec, "query_position", lambda n: n)],   # one past the newest token
+    "decode_window_boundary": [(odec, "decode_visible", _bad_decode_visible)],
     "neox_partner": [(orope, "rope_pair_indices", _bad_pairs)],
     "frequency_exponent": [(orope, "rope_frequencies", _bad_freq), (oracle, "rope_frequencies", _bad_freq)],
     "gqa_mapping": [(oatt, "kv_head", _bad_kv_head)],
@@ -100,6 +112,10 @@ CHECKS = [
     P.check_gqa_repeat_kv,
     P.check_alibi_special_cases,
     lambda: P.check_backward_fd(FWD),
+    lambda: P.check_decode_vs_bruteforce(FWD),
+    lambda: P.check_decode_vs_bruteforce(ALIBI),
+    lambda: P.check_decode_vs_bruteforce(SW),
+    lambda: P.check_decode_closed_forms("neox"),
 ]
 
 

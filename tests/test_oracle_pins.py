@@ -99,3 +99,22 @@ def test_backward_vs_torch_autograd(variant):
 
 def test_backward_identities():
     P.check_backward_identities()
+
+
+@pytest.mark.parametrize("variant", P.VARIANTS, ids=lambda v: "-".join(map(str, v)))
+def test_decode_vs_bruteforce(variant):
+    P.check_decode_vs_bruteforce(variant)
+
+
+@pytest.mark.parametrize("variant", P.VARIANTS, ids=lambda v: "-".join(map(str, v)))
+def test_decode_is_last_prefill_row(variant):
+    P.check_decode_is_last_prefill_row(variant)
+
+
+@pytest.mark.parametrize("kind", ["none"] + ROPES)
+def test_decode_closed_forms(kind):
+    P.check_decode_closed_forms(kind)
+
+
+def test_decode_ignores_stale_entries():
+    P.check_decode_ignores_stale_entries()

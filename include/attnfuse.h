@@ -140,6 +140,48 @@ int attnfuse_rope_bwd(const void* dQr, const void* dKr, void* dQ, void* dK,
                       int B, int H, int H_kv, int S, int D, int dtype,
                       int rope, float rope_theta, void* stream);
 
+/* Bytes of device workspace attnfuse_decode needs: one partial (max, sum,
+ * accumulator) triple per (sequence, query head, cache chunk), fp32.  The chunk
+ * length is a power of two in [128, 1024] chosen from B * H_kv * S_kv so the
+ * first phase launches about 1024 workgroups.  Returns 0 for invalid sizes. */
+size_t attnfuse_decode_workspace_bytes(int B, int H, int H_kv, int S_kv, int D);
+
+/*
+ * Decode attention over a key/value cache (Section 2 "Flash Decoding"): one
+ * query per sequence.  Phase 1 splits each sequence's cache into chunks and
+ * computes a partial online-softmax triple (m, l, acc) per chunk for all query
+ * heads of a K/V head at once (the group's heads fill the MFMA's columns by
+ * cyclic replication, so K and V are read exactly once); phase 2 merges the
+ * partials by log-sum-exp.  With L = cache_lens[b] the query sits at position
+ * p = L - 1 and
+ *     s_j = softmax_scale * <R_p q, k_j> - slope_h * (p - j),   j < L
+ *     O   = softmax_j(s_j over visible j) v_j,   LSE = ln sum_{visible j} exp(s_j)
+ * The cache holds keys ALREADY ROTATED at their own positions (rotate them once
+ * when they are written, e.g. with attnfuse_rope); only the query is rotated
+ * here.  Under RoPE the rotated query and the cached keys meet in fp16, as in
+ * attnfuse_fwd, so |k| must stay below the fp16 maximum.
+ *
+ *   Q [B,H,D]                    the newest token's queries (dtype), unrotated
+ *   K, V [B,H_kv,S_kv,D]         the caches (dtype), row-major, contiguous
+ *   cache_lens                   device int32 [B] or NULL (every sequence uses
+ *                                S_kv entries); values above S_kv are clamped
+ *                                to S_kv, values below 1 give O = 0, LSE = -inf
+ *   O [B,H,D] (dtype), LSE [B,H] fp32 (natural log)
+ *   workspace                    device memory of >= attnfuse_decode_workspace_
+ *                                bytes(B, H, H_kv, S_kv, D) bytes, caller-owned
+ *   mask                         NONE or CAUSAL: every cached key is visible
+ *                                (all precede the query); SLIDING_WINDOW: the
+ *                                last `window` keys
+ *   rope, rope_theta, alibi_slopes, softmax_scale   as attnfuse_fwd
+ *   dtype                        AF_DTYPE_BF16 only; D in {64, 128};
+ *                                H / H_kv <= 32 (else AF_ERR_UNSUPPORTED)
+ */
+int attnfuse_decode(const void* Q, const void* K, const void* V, const int* cache_lens,
+                    void* O, float* LSE, void* workspace, size_t workspace_bytes,
+                    int B, int H, int H_kv, int S_kv, int D, int dtype,
+                    int rope, float rope_theta, int mask, int window,
+                    const float* alibi_slopes, float softmax_scale, void* stream);
+
 /* Static text for a return code (never NULL). */
 const char* attnfuse_strerror(int code);
 

@@ -101,6 +101,37 @@ def attnfuse_bwd(q, k, v, o, do, lse, *, rope="none", theta=10000.0, mask="causa
     return dq, dk, dv
 
 
+def attnfuse_decode_workspace_bytes(B, H, H_kv, S_kv, D):
+    return _lib.load().attnfuse_decode_workspace_bytes(B, H, H_kv, S_kv, D)
+
+
+def attnfuse_decode(q, k_cache, v_cache, cache_lens=None, *, rope="none", theta=10000.0, mask="causal",
+                    window=None, alibi_slopes=None, scale=None, out=None, lse=None, workspace=None):
+    """O [B,H,D], LSE [B,H] of one query per sequence against a KV cache of
+    already-rotated keys; see attnfuse_decode in include/attnfuse.h."""
+    if q.dim() != 3 or k_cache.dim() != 4 or v_cache.shape != k_cache.shape:
+        raise ValueError("q must be [B, H, D] and the caches [B, H_kv, S_kv, D]")
+    B, H, D = q.shape
+    Hkv, S_kv = k_cache.shape[1], k_cache.shape[2]
+    if k_cache.shape[0] != B or k_cache.shape[3] != D:
+        raise ValueError("cache shape does not match q")
+    _same(q, k_cache, v_cache, out)
+    if cache_lens is not None and (cache_lens.dtype != torch.int32 or not cache_lens.is_cuda
+                                   or cache_lens.shape != (B,)):
+        raise ValueError("cache_lens must be an int32 GPU tensor [B]")
+    out = torch.empty_like(q) if out is None else out
+    lse = torch.empty(B, H, device=q.device, dtype=torch.float32) if lse is None else lse
+    nbytes = attnfuse_decode_workspace_bytes(B, H, Hkv, S_kv, D)
+    if workspace is None:
+        workspace = torch.empty(nbytes, device=q.device, dtype=torch.uint8)
+    r, th, m, w, sc = _variant(rope, theta, mask, window, alibi_slopes, scale, D)
+    code = _lib.load().attnfuse_decode(_ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(cache_lens), _ptr(out),
+                                       _ptr(lse), _ptr(workspace), workspace.numel(), B, H, Hkv, S_kv, D,
+                                       DTYPE[q.dtype], r, th, m, w, _ptr(alibi_slopes), sc, _stream())
+    _check(code, "attnfuse_decode")
+    return out, lse
+
+
 def _rope_call(name, x0, x1, y0, y1, rope, theta):
     if x1 is not None:
         B, H, Hkv, S, D = _shape(x0, x1)

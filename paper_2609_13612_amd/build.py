@@ -28,7 +28,7 @@ DEVICE_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
 COMMON = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", f"-I{INCLUDE}", f"-I{CSRC}",
           "-Wall", "-Wno-unused-function"]
 
-SOURCES = ["api.cpp", "rope.hip", "fwd_bf16.hip", "fwd_fp32.hip", "bwd_bf16.hip", "bwd_fp32.hip"]
+SOURCES = ["api.cpp", "rope.hip", "fwd_bf16.hip", "fwd_fp32.hip", "bwd_bf16.hip", "bwd_fp32.hip", "decode.hip"]
 
 
 def _compile(src):

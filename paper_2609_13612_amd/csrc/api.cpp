@@ -107,6 +107,27 @@ BwdWorkspace bwd_workspace(int B, int H, int H_kv, int S, int D, int rope) {
   return w;
 }
 
+// Decode workspace: per-chunk partial (max, sum) pairs, then accumulators.
+struct DecodeLayout {
+  int chunk, nsplit;
+  size_t ml, acc, total;
+};
+
+// Keys per phase-1 workgroup: a power of two in [128, 1024] giving about 1024
+// workgroups; partial (max, sum) pairs then accumulators, each 256-byte aligned.
+DecodeLayout decode_layout(int B, int H, int H_kv, int S, int D) {
+  const long long work = (long long)B * H_kv * S;
+  DecodeLayout L{};
+  L.chunk = 128;
+  while (L.chunk < 1024 && (long long)L.chunk * 1024 < work) L.chunk *= 2;
+  L.nsplit = (S + L.chunk - 1) / L.chunk;
+  const size_t parts = (size_t)B * H * L.nsplit;
+  L.ml = 0;
+  L.acc = align256(parts * 2 * sizeof(float));
+  L.total = L.acc + align256(parts * D * sizeof(float));
+  return L;
+}
+
 }  // namespace
 
 extern "C" {
@@ -196,6 +217,49 @@ int attnfuse_bwd(const void* Q, const void* K, const void* V, const void* O, con
   const bool alibi = alibi_slopes != nullptr;
   if (dtype == AF_DTYPE_FP32) return map_launch(af::launch_bwd_fp32(D, rope, mask, alibi, p, st));
   return map_launch(af::launch_bwd_bf16(D, rope, mask, alibi, p, st));
+}
+
+// ---------------------------------------------------------------- decode
+size_t attnfuse_decode_workspace_bytes(int B, int H, int H_kv, int S_kv, int D) {
+  if (B < 1 || H < 1 || H_kv < 1 || S_kv < 1 || S_kv > kMaxS || D < 2 || (D & 1) || H % H_kv) return 0;
+  return decode_layout(B, H, H_kv, S_kv, D).total;
+}
+
+int attnfuse_decode(const void* Q, const void* K, const void* V, const int* cache_lens,
+                    void* O, float* LSE, void* workspace, size_t workspace_bytes,
+                    int B, int H, int H_kv, int S_kv, int D, int dtype,
+                    int rope, float rope_theta, int mask, int window,
+                    const float* alibi_slopes, float softmax_scale, void* stream) {
+  const void* ins[] = {Q, K, V};
+  const void* outs[] = {O, LSE, workspace};
+  for (const void* x : ins) if (!x || !aligned16(x)) return AF_ERR_INVALID_ARG;
+  for (const void* x : outs) if (!x || !aligned16(x)) return AF_ERR_INVALID_ARG;
+  if (cache_lens && (reinterpret_cast<uintptr_t>(cache_lens) & 3u)) return AF_ERR_INVALID_ARG;
+  for (const void* x : outs) {
+    for (const void* y : ins) if (x == y) return AF_ERR_INVALID_ARG;
+    if (x == static_cast<const void*>(cache_lens)) return AF_ERR_INVALID_ARG;
+  }
+  int rc = check_common(B, H, H_kv, S_kv, D, dtype, rope, rope_theta);
+  if (rc != AF_OK) return rc;
+  if ((rc = check_attn(mask, window, softmax_scale)) != AF_OK) return rc;
+  if (workspace_bytes < attnfuse_decode_workspace_bytes(B, H, H_kv, S_kv, D)) return AF_ERR_INVALID_ARG;
+  if (!supported_d(D) || dtype != AF_DTYPE_BF16 || H / H_kv > 32) return AF_ERR_UNSUPPORTED;
+
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const DecodeLayout L = decode_layout(B, H, H_kv, S_kv, D);
+  af::DecodeParams p{};
+  p.q = Q; p.k = K; p.v = V; p.lens = cache_lens; p.o = O; p.lse = LSE;
+  char* wb = static_cast<char*>(workspace);
+  p.part_ml = reinterpret_cast<float*>(wb + L.ml);
+  p.part_acc = reinterpret_cast<float*>(wb + L.acc);
+  p.B = B; p.H = H; p.Hkv = H_kv; p.S = S_kv;
+  p.window = (mask == AF_MASK_SLIDING_WINDOW) ? (window < S_kv ? window : S_kv) : 0;
+  p.chunk = L.chunk; p.nsplit = L.nsplit;
+  p.slopes = alibi_slopes;
+  p.scale = softmax_scale;
+  p.table = nullptr;
+  if (rope != AF_ROPE_NONE && (rc = rope_table(D, rope_theta, S_kv, st, &p.table)) != AF_OK) return rc;
+  return map_launch(af::launch_decode(D, rope, alibi_slopes != nullptr, p, st));
 }
 
 static int rope_common(const void* X0, const void* X1, void* Y0, void* Y1, int B, int H, int H_kv, int S, int D,

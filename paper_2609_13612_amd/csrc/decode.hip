@@ -1,0 +1,325 @@
+// Decode attention over a key/value cache, bf16 inputs, MFMA with fp32
+// accumulation, for gfx950 (Section 2 "Flash Decoding"; Table tab:decode).
+//
+// One query per sequence makes the work a stream over the cache: each K/V
+// element is used once per query head of its group, so the kernel is bound by
+// HBM and is built to read the cache exactly once at full width.
+//
+// Phase 1 (decode_split_kernel): workgroup = 4 waves = one (sequence, K/V
+//   head, chunk of `chunk` keys); each wave streams a quarter of the chunk in
+//   32-key tiles.  Scores are formed transposed, S^T = K Q'^T: the 32 MFMA
+//   columns are the group's query heads, replicated cyclically when the group
+//   has fewer than 32 (K and V are then read once for all of them); every lane
+//   owns one head column, so the softmax statistics stay in-lane as in the
+//   prefill kernel.  K tiles go from HBM straight into registers as the A
+//   operand (lane = key row); V tiles go through the wave's own LDS tile for
+//   the transpose read of O^T += V^T P^T.  The next tile's loads are issued
+//   before the current tile is computed.  The four waves' (m, l, acc) merge in
+//   LDS and one partial per (sequence, head, chunk) is written; chunks with no
+//   visible key return at once.
+// Phase 2 (decode_combine_kernel): per (sequence, head), merge the partials of
+//   the chunks that hold visible keys by log-sum-exp and write O and LSE.
+//
+// Precision: without RoPE the bf16 query and keys meet exactly in a bf16
+// MFMA.  With RoPE the query is rotated at position L-1 in fp32 and rounded to
+// fp16, and the (already rotated) bf16 cache keys are widened to fp16 in
+// registers (exact inside the fp16 range), as the prefill kernel does for its
+// rotated operands.  P and V are bf16.
+#include "common.hpp"
+#include "launch.hpp"
+
+namespace af {
+
+template <int D>
+struct DecCfg {
+  static constexpr int NW = 4;                      // waves per workgroup
+  static constexpr int KS = D / 16;                 // MFMA k-steps over the head dimension
+  static constexpr int MT = D / 32;                 // 32-row output tiles over the head dimension
+  static constexpr int VP = D + 16;                 // V tile pitch (transpose reads)
+  static constexpr int VT = 32 * VP;                // one wave's V tile (elements)
+  static constexpr int VPL = 32 * (D / 8) / 64;     // 16-byte V chunks per lane per tile
+  static constexpr int MERGE_FLOATS = 2 * NW * 32 + 2 * 32 * D;   // statistics + two accumulator slots
+  static constexpr int SMEM = (NW * VT > 2 * MERGE_FLOATS) ? NW * VT : 2 * MERGE_FLOATS;   // uint16 elements
+};
+
+__device__ __forceinline__ int seq_len(const DecodeParams& p, int b) {
+  return p.lens ? min(p.lens[b], p.S) : p.S;
+}
+
+// First visible key of a sequence with L cached keys.
+__device__ __forceinline__ int first_key(const DecodeParams& p, int L) {
+  return (p.window > 0) ? max(0, L - p.window) : 0;
+}
+
+template <int D, int ROPE, bool ALIBI>
+__global__ __launch_bounds__(256) void decode_split_kernel(DecodeParams p) {
+  using C = DecCfg<D>;
+  constexpr bool QF16 = ROPE != ROPE_NONE;
+  __shared__ __attribute__((aligned(16))) uint16_t smem[C::SMEM];
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int lq = lane & 31, lg = lane >> 5;
+  const int split = (int)(blockIdx.x % p.nsplit);
+  const int unit = (int)(blockIdx.x / p.nsplit);
+  const int b = unit / p.Hkv, g = unit % p.Hkv;
+  const int G = p.H / p.Hkv;
+  const int L = seq_len(p, b);
+  if (L < 1) return;
+  const int lo = first_key(p, L);
+  const int c0 = split * p.chunk;
+  if (c0 + p.chunk <= lo || c0 >= L) return;       // no visible key in this chunk (workgroup-uniform)
+  const int pos = L - 1;                           // the query's position
+
+  const int hc = lq % G;                           // head of this lane's column (cyclic replication)
+  const int h = g * G + hc;
+  const uint16_t* __restrict__ K = static_cast<const uint16_t*>(p.k) + (size_t)unit * p.S * D;
+  const uint16_t* __restrict__ V = static_cast<const uint16_t*>(p.v) + (size_t)unit * p.S * D;
+
+  // Query operand (B of S^T = K Q'^T): lane holds head column hc, dims 16s + 8lg .. +7.
+  const uint16_t* __restrict__ Qh = static_cast<const uint16_t*>(p.q) + ((size_t)b * p.H + h) * D;
+  u32x4 qreg[C::KS];
+#pragma unroll
+  for (int s = 0; s < C::KS; ++s) qreg[s] = ld16(Qh + 16 * s + 8 * lg);
+  if constexpr (ROPE == ROPE_NEOX) {
+#pragma unroll
+    for (int s = 0; s < C::KS / 2; ++s)
+      rotate_neox8<false, true>(qreg[s], qreg[s + C::KS / 2], p.table + (size_t)pos * (D / 2) + 16 * s + 8 * lg);
+  } else if constexpr (ROPE == ROPE_INTERLEAVED) {
+#pragma unroll
+    for (int s = 0; s < C::KS; ++s)
+      rotate_interleaved8<false, true>(qreg[s], p.table + (size_t)pos * (D / 2) + 8 * s + 4 * lg);
+  }
+
+  const float c2 = p.scale * kLog2e;
+  const float slope2 = ALIBI ? p.slopes[h] * kLog2e : 0.f;
+
+  // This wave's keys: a quarter of the chunk, clipped to the visible range.
+  const int cw = p.chunk / C::NW;
+  const int kbeg = max(c0 + wave * cw, lo & ~31);
+  const int kend = min(c0 + (wave + 1) * cw, L);
+
+  uint16_t* Vw = smem + wave * C::VT;
+  const int tr_key = 4 * lg + ((lane & 15) >> 2);
+  const int tr_col = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+
+  f32x16 acc[C::MT];
+#pragma unroll
+  for (int i = 0; i < C::MT; ++i) acc[i] = f32x16{};
+  float m_run = -INFINITY, l_run = 0.f;
+
+  u32x4 kreg[C::KS], vreg[C::VPL];
+  auto load_tile = [&](int n0) {   // rows past L are clamped to L-1 (finite data, masked)
+    const int n = min(n0 + lq, L - 1);
+#pragma unroll
+    for (int s = 0; s < C::KS; ++s) kreg[s] = ld16(K + (size_t)n * D + 16 * s + 8 * lg);
+#pragma unroll
+    for (int i = 0; i < C::VPL; ++i) {
+      const int it = lane + 64 * i;
+      const int r = it / (D / 8), c = it % (D / 8);
+      vreg[i] = ld16(V + (size_t)min(n0 + r, L - 1) * D + 8 * c);
+    }
+  };
+
+  if (kbeg < kend) load_tile(kbeg);
+  for (int n0 = kbeg; n0 < kend; n0 += 32) {
+    // V tile to this wave's LDS tile (the previous tile's transpose reads,
+    // issued earlier by this wave, complete first: LDS is in order per wave)
+#pragma unroll
+    for (int i = 0; i < C::VPL; ++i) {
+      const int it = lane + 64 * i;
+      const int r = it / (D / 8), c = it % (D / 8);
+      *reinterpret_cast<u32x4*>(Vw + r * C::VP + 8 * c) = vreg[i];
+    }
+    u32x4 kcur[C::KS];
+#pragma unroll
+    for (int s = 0; s < C::KS; ++s) kcur[s] = kreg[s];
+    if (n0 + 32 < kend) load_tile(n0 + 32);
+
+    if constexpr (QF16) {   // cached keys bf16 -> fp16 to meet the fp16 query
+#pragma unroll
+      for (int s = 0; s < C::KS; ++s)
+#pragma unroll
+        for (int w = 0; w < 4; ++w) kcur[s][w] = pack_f16(bf_lo(kcur[s][w]), bf_hi(kcur[s][w]));
+    }
+    f32x16 st = f32x16{};
+#pragma unroll
+    for (int s = 0; s < C::KS; ++s) st = mfma32<QF16>(kcur[s], qreg[s], st);
+
+    // element r: key n0 + 8 (r/4) + 4 lg + r%4 of head column lq
+    if constexpr (ALIBI) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int n = n0 + 8 * (r >> 2) + 4 * lg + (r & 3);
+        st[r] = __builtin_fmaf(st[r], c2, slope2 * (float)(n - pos));
+      }
+    }
+    if (n0 + 32 > L || n0 < lo) {   // wave-uniform: edge tiles only
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int n = n0 + 8 * (r >> 2) + 4 * lg + (r & 3);
+        st[r] = (n < L && n >= lo) ? st[r] : -INFINITY;
+      }
+    }
+    float mx = -INFINITY;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) mx = fmaxf(mx, st[r]);
+    mx = pair_max(mx);
+    if constexpr (!ALIBI) mx *= c2;
+    const float m_new = fmaxf(m_run, mx);
+    if (__any(m_new > m_run + 8.f)) {   // raise the reference max (wave-uniform)
+      const float alpha = (m_run == -INFINITY) ? 0.f : fast_exp2(m_run - m_new);
+      l_run *= alpha;
+#pragma unroll
+      for (int i = 0; i < C::MT; ++i) acc[i] *= alpha;
+      m_run = m_new;
+    }
+    const float m_use = (m_run == -INFINITY) ? 0.f : m_run;
+    float pv[16];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      pv[r] = fast_exp2(ALIBI ? (st[r] - m_use) : __builtin_fmaf(st[r], c2, -m_use));
+      l_run += pv[r];
+    }
+    u32x4 pop[2];
+#pragma unroll
+    for (int hf = 0; hf < 2; ++hf)
+#pragma unroll
+      for (int w = 0; w < 4; ++w) pop[hf][w] = pack_bf16(pv[8 * hf + 2 * w], pv[8 * hf + 2 * w + 1]);
+
+    // O^T += V^T P^T (V^T from transpose reads of the row-major V tile)
+#pragma unroll
+    for (int hf = 0; hf < 2; ++hf)
+#pragma unroll
+      for (int mt = 0; mt < C::MT; ++mt) {
+        const uint16_t* base = Vw + (16 * hf + tr_key) * C::VP + 32 * mt + tr_col;
+        const u32x2 lo2 = lds_read_tr16(base);
+        const u32x2 hi2 = lds_read_tr16(base + 8 * C::VP);
+        const u32x4 a = {lo2[0], lo2[1], hi2[0], hi2[1]};
+        acc[mt] = mfma32(a, pop[hf], acc[mt]);
+      }
+  }
+
+  // Merge the four waves' partials through LDS (the V tiles are dead): each
+  // wave rescales to the workgroup max, waves 2-3 hand over to 0-1, wave 1 to
+  // wave 0, and wave 0's sum leaves through one slot with coalesced stores.
+  __syncthreads();
+  float* ms = reinterpret_cast<float*>(smem);   // [NW][32] max, then [NW][32] sum
+  float* as = ms + 2 * C::NW * 32;              // two slots of [32 columns][D]
+  const float l_tot = pair_sum(l_run);
+  if (lane < 32) {
+    ms[wave * 32 + lane] = m_run;
+    ms[C::NW * 32 + wave * 32 + lane] = l_tot;
+  }
+  __syncthreads();
+  float M = -INFINITY;
+#pragma unroll
+  for (int w = 0; w < C::NW; ++w) M = fmaxf(M, ms[w * 32 + lq]);
+  const float f = (m_run == -INFINITY) ? 0.f : fast_exp2(m_run - M);
+#pragma unroll
+  for (int i = 0; i < C::MT; ++i) acc[i] *= f;
+  // lane's slot entries: column lq, dims 32 mt + 8 (r/4) + 4 lg + r%4
+  float* mine = as + lq * D + 4 * lg;
+  if (wave >= 2) {
+#pragma unroll
+    for (int mt = 0; mt < C::MT; ++mt)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) mine[(wave - 2) * 32 * D + 32 * mt + 8 * (r >> 2) + (r & 3)] = acc[mt][r];
+  }
+  __syncthreads();
+  if (wave < 2) {
+#pragma unroll
+    for (int mt = 0; mt < C::MT; ++mt)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[mt][r] += mine[wave * 32 * D + 32 * mt + 8 * (r >> 2) + (r & 3)];
+  }
+  __syncthreads();
+  if (wave == 1) {
+#pragma unroll
+    for (int mt = 0; mt < C::MT; ++mt)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) mine[32 * mt + 8 * (r >> 2) + (r & 3)] = acc[mt][r];
+  }
+  __syncthreads();
+  if (wave == 0) {
+#pragma unroll
+    for (int mt = 0; mt < C::MT; ++mt)
+#pragma unroll
+      for (int r = 0; r < 16; ++r)
+        mine[32 * D + 32 * mt + 8 * (r >> 2) + (r & 3)] = acc[mt][r] + mine[32 * mt + 8 * (r >> 2) + (r & 3)];
+  }
+  __syncthreads();
+  const size_t part0 = (size_t)b * p.H + g * G;   // partial row of column 0
+  for (int idx = tid; idx < G * D; idx += 256) {
+    const int c = idx / D, d = idx % D;
+    p.part_acc[((part0 + c) * p.nsplit + split) * D + d] = as[(32 + c) * D + d];
+  }
+  if (tid < G) {
+    float Mc = -INFINITY, Lc = 0.f;
+#pragma unroll
+    for (int w = 0; w < C::NW; ++w) Mc = fmaxf(Mc, ms[w * 32 + tid]);
+#pragma unroll
+    for (int w = 0; w < C::NW; ++w) {
+      const float mw = ms[w * 32 + tid];
+      Lc += (mw == -INFINITY) ? 0.f : ms[C::NW * 32 + w * 32 + tid] * fast_exp2(mw - Mc);
+    }
+    float* ml = p.part_ml + ((part0 + tid) * p.nsplit + split) * 2;
+    ml[0] = Mc;
+    ml[1] = Lc;
+  }
+}
+
+// One workgroup of D threads per (sequence, query head); thread d owns dim d.
+template <int D>
+__global__ __launch_bounds__(D) void decode_combine_kernel(DecodeParams p) {
+  const int bh = blockIdx.x, d = threadIdx.x;
+  const int b = bh / p.H;
+  const int L = seq_len(p, b);
+  uint16_t* O = static_cast<uint16_t*>(p.o) + (size_t)bh * D;
+  if (L < 1) {
+    O[d] = 0;
+    if (d == 0) p.lse[bh] = -INFINITY;
+    return;
+  }
+  const int s_lo = first_key(p, L) / p.chunk, s_hi = (L - 1) / p.chunk;
+  const float* ml = p.part_ml + (size_t)bh * p.nsplit * 2;
+  float M = -INFINITY;
+  for (int s = s_lo; s <= s_hi; ++s) M = fmaxf(M, ml[2 * s]);
+  float l = 0.f, o = 0.f;
+  for (int s = s_lo; s <= s_hi; ++s) {
+    const float f = fast_exp2(ml[2 * s] - M);
+    l += ml[2 * s + 1] * f;
+    o += p.part_acc[((size_t)bh * p.nsplit + s) * D + d] * f;
+  }
+  O[d] = static_cast<uint16_t>(pack_bf16(o / l, 0.f) & 0xffffu);
+  if (d == 0) p.lse[bh] = (M + __log2f(l)) * kLn2;
+}
+
+template <int D, int ROPE, bool ALIBI>
+static int launch_one(const DecodeParams& p, hipStream_t st) {
+  const long long blocks = (long long)p.nsplit * p.B * p.Hkv;
+  hipLaunchKernelGGL((decode_split_kernel<D, ROPE, ALIBI>), dim3((unsigned)blocks), dim3(256), 0, st, p);
+  hipLaunchKernelGGL((decode_combine_kernel<D>), dim3((unsigned)(p.B * p.H)), dim3(D), 0, st, p);
+  return hipGetLastError() == hipSuccess ? 0 : -3;
+}
+
+// The mask is a runtime lower bound on the key index (p.window > 0 for a
+// sliding window): NONE and CAUSAL see the same keys in decode.
+template <int D>
+static int dispatch_rope(int rope, bool alibi, const DecodeParams& p, hipStream_t st) {
+  switch (rope) {
+    case ROPE_NONE: return alibi ? launch_one<D, ROPE_NONE, true>(p, st) : launch_one<D, ROPE_NONE, false>(p, st);
+    case ROPE_NEOX: return alibi ? launch_one<D, ROPE_NEOX, true>(p, st) : launch_one<D, ROPE_NEOX, false>(p, st);
+    case ROPE_INTERLEAVED:
+      return alibi ? launch_one<D, ROPE_INTERLEAVED, true>(p, st) : launch_one<D, ROPE_INTERLEAVED, false>(p, st);
+  }
+  return -2;
+}
+
+int launch_decode(int D, int rope, bool alibi, const DecodeParams& p, hipStream_t st) {
+  if (D == 64) return dispatch_rope<64>(rope, alibi, p, st);
+  if (D == 128) return dispatch_rope<128>(rope, alibi, p, st);
+  return -2;
+}
+
+}  // namespace af

@@ -41,6 +41,23 @@ struct BwdParams {
   int heads_per_wg;       // set by the launcher for the dQ kernel
 };
 
+struct DecodeParams {
+  const void* q;          // [B, H, D]
+  const void* k;          // cache [B, H_kv, S, D], keys already rotated
+  const void* v;          // cache [B, H_kv, S, D]
+  const int* lens;        // device [B] cache lengths, or nullptr (all S)
+  void* o;                // [B, H, D]
+  float* lse;             // [B, H]
+  float* part_ml;         // workspace [B, H, nsplit, 2]: chunk max and sum (log2 units)
+  float* part_acc;        // workspace [B, H, nsplit, D]: chunk accumulator
+  int B, H, Hkv, S;
+  int window;             // > 0: sliding window of that many keys; 0: every cached key
+  int chunk, nsplit;      // keys per phase-1 workgroup; chunks per sequence
+  const float* slopes;
+  float scale;
+  const float2* table;
+};
+
 struct RopeParams {
   const void* x0;  void* y0;  int heads0;   // first tensor [B, heads0, S, D]
   const void* x1;  void* y1;  int heads1;   // optional second tensor (heads1 may be 0)
@@ -53,6 +70,7 @@ int launch_fwd_bf16(int D, int rope, int mask, bool alibi, const FwdParams& p, h
 int launch_fwd_fp32(int D, int rope, int mask, bool alibi, const FwdParams& p, hipStream_t st);
 int launch_bwd_bf16(int D, int rope, int mask, bool alibi, const BwdParams& p, hipStream_t st);
 int launch_bwd_fp32(int D, int rope, int mask, bool alibi, const BwdParams& p, hipStream_t st);
+int launch_decode(int D, int rope, bool alibi, const DecodeParams& p, hipStream_t st);
 int launch_rope(bool fp32, int D, int rope, bool inverse, const RopeParams& p, hipStream_t st);
 int launch_rope_table(float2* table, int rows, int D, double theta, hipStream_t st);
 

@@ -1,7 +1,9 @@
 """Named workload shapes and their algorithmic FLOP / byte counts.
 
-The five workloads are the parity and benchmark shapes of the build; inputs
-are seeded N(0, 1) tensors (see ``inputs``).  FLOPs count only visible
+The five prefill workloads are the parity and benchmark shapes of the build,
+and the three decode workloads are the cache geometries of the paper's decode
+table (batch 1, which the table leaves unstated); inputs are seeded N(0, 1)
+tensors (see ``inputs``).  FLOPs count only visible
 (query, key) pairs: 4*D per pair for the forward (Q K^T and P V) and 10*D for
 the backward (five matmuls: S, dV, dP, dQ, dK), the FlashAttention convention.
 The separate rotation moves 4 bytes per bf16 element of Q and K (read + write).
@@ -63,3 +65,37 @@ WORKLOADS = {
 }
 
 LLAMA_SWEEP_S = (1024, 2048, 4096, 8192, 16384)
+
+
+@dataclass(frozen=True)
+class DecodeWorkload:
+    """One query per sequence against a key/value cache of S_kv tokens
+    (the paper's decode table: Q.N = 1, large cache)."""
+    name: str
+    B: int
+    H: int
+    Hkv: int
+    S_kv: int
+    D: int
+    rope: str = "neox"
+    theta: float = 10000.0
+    notes: str = field(default="", compare=False)
+
+    def cache_bytes(self):
+        """K and V cache bytes read once (bf16), the kernel's algorithmic traffic
+        with the query, output and LSE (negligible) left out."""
+        return 2 * 2 * self.B * self.Hkv * self.S_kv * self.D
+
+    def flops(self):
+        """4*D per (query head, cached key), as for the forward."""
+        return 4 * self.D * self.B * self.H * self.S_kv
+
+
+DECODE_WORKLOADS = {
+    "decode_llama3_8b_h32kv8_cache4096": DecodeWorkload("decode_llama3_8b_h32kv8_cache4096", 1, 32, 8, 4096, 128,
+                                                        theta=500000.0, notes="Llama-3-8B geometry"),
+    "decode_llama3_70b_h64kv8_cache32768": DecodeWorkload("decode_llama3_70b_h64kv8_cache32768", 1, 64, 8, 32768,
+                                                          128, theta=500000.0, notes="Llama-3-70B geometry"),
+    "decode_mistral_7b_h32kv8_cache16384": DecodeWorkload("decode_mistral_7b_h32kv8_cache16384", 1, 32, 8, 16384,
+                                                          128, notes="Mistral-7B geometry"),
+}

@@ -21,9 +21,9 @@ def declared_symbols():
 
 
 def test_header_declares_the_boundary():
-    assert declared_symbols() == sorted(["attnfuse_bwd", "attnfuse_bwd_workspace_bytes", "attnfuse_fwd",
-                                         "attnfuse_rope", "attnfuse_rope_bwd", "attnfuse_strerror",
-                                         "attnfuse_version"])
+    assert declared_symbols() == sorted(["attnfuse_bwd", "attnfuse_bwd_workspace_bytes", "attnfuse_decode",
+                                         "attnfuse_decode_workspace_bytes", "attnfuse_fwd", "attnfuse_rope",
+                                         "attnfuse_rope_bwd", "attnfuse_strerror", "attnfuse_version"])
 
 
 def test_library_loads_and_exports_every_declared_symbol():
@@ -131,3 +131,46 @@ def test_rope_rejects_invalid_arguments(fn, over):
 
 def test_rope_unsupported():
     assert _rope(D=96) == -2
+
+
+# ----------------------------------------------------------------------------- decode
+
+def test_decode_workspace_bytes():
+    lib = _lib.load()
+    # Llama-3-70B geometry, 32k cache: 256-key chunks -> 128 per sequence; 64 heads
+    parts = 64 * 128
+    assert lib.attnfuse_decode_workspace_bytes(1, 64, 8, 32768, 128) == parts * 8 + parts * 128 * 4
+    # Llama-3-8B geometry, 4k cache: the 128-key minimum -> 32 chunks; 32 heads
+    parts = 32 * 32
+    assert lib.attnfuse_decode_workspace_bytes(1, 32, 8, 4096, 128) == parts * 8 + parts * 128 * 4
+    # sections start on 256-byte boundaries
+    assert lib.attnfuse_decode_workspace_bytes(1, 1, 1, 5, 64) == 256 + 256
+    assert lib.attnfuse_decode_workspace_bytes(0, 32, 8, 4096, 128) == 0
+    assert lib.attnfuse_decode_workspace_bytes(1, 6, 4, 4096, 128) == 0
+    assert lib.attnfuse_decode_workspace_bytes(1, 32, 8, 0, 128) == 0
+
+
+def _decode(**over):
+    a = dict(Q=FAKE, K=FAKE + 0x100, V=FAKE + 0x200, lens=None, O=FAKE + 0x300, LSE=FAKE + 0x400, ws=FAKE + 0x500,
+             ws_bytes=1 << 30, B=2, H=8, H_kv=2, S=300, D=128, dtype=0, rope=1, theta=1e4, mask=1, window=0,
+             slopes=None, scale=0.1, stream=None)
+    a.update(over)
+    return _lib.load().attnfuse_decode(a["Q"], a["K"], a["V"], a["lens"], a["O"], a["LSE"], a["ws"], a["ws_bytes"],
+                                       a["B"], a["H"], a["H_kv"], a["S"], a["D"], a["dtype"], a["rope"], a["theta"],
+                                       a["mask"], a["window"], a["slopes"], a["scale"], a["stream"])
+
+
+@pytest.mark.parametrize("over", [dict(Q=None), dict(K=None), dict(V=None), dict(O=None), dict(LSE=None),
+                                  dict(ws=None), dict(K=ODD), dict(lens=FAKE + 0x602), dict(O=FAKE),
+                                  dict(ws=FAKE + 0x200), dict(ws_bytes=1000), dict(H=8, H_kv=3), dict(S=0),
+                                  dict(mask=2, window=0), dict(mask=5), dict(scale=0.0), dict(rope=1, theta=0.0),
+                                  dict(dtype=5)],
+                         ids=lambda o: ",".join(f"{k}={v}" for k, v in o.items()))
+def test_decode_rejects_invalid_arguments(over):
+    assert _decode(**over) == -1
+
+
+def test_decode_unsupported():
+    assert _decode(D=96) == -2
+    assert _decode(dtype=1) == -2               # bf16 only
+    assert _decode(H=64, H_kv=1) == -2          # more than 32 query heads per K/V head

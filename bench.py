@@ -17,6 +17,9 @@ Alongside, on the same inputs and outside the timed steps:
   each point the median of 50 calls after 10 warm-ups, and the rotation
   calculus model fitted to it (crossover_model: fused extra time a*S^2,
   separate rotation b*S, model crossover b/a next to the measured one);
+* decode over a KV cache at the paper's three decode geometries (skip with
+  --no-decode): median latency and cache bandwidth against the HBM peak, the
+  caches rotated through a pool larger than twice the Infinity Cache;
 * a plain device-to-device copy of 512 MiB: the achievable HBM bandwidth next
   to the rotation kernel's, and the calibration kernel for the HBM-traffic
   counters;
@@ -41,6 +44,9 @@ sys.path.insert(0, ROOT)
 
 PEAK_BF16_TFLOPS = 2516.6     # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
+# The paper's decode latencies on H100 (Table tab:decode), other hardware: context only.
+PAPER_DECODE_MS = {"decode_llama3_8b_h32kv8_cache4096": 0.034, "decode_llama3_70b_h64kv8_cache32768": 0.184,
+                   "decode_mistral_7b_h32kv8_cache16384": 0.072}
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "fwd_llama3_8b_hbm_traffic.json")
 FWD_SOURCES = ("fwd_bf16.hip", "attn_tiles.hpp", "common.hpp")
 
@@ -116,6 +122,7 @@ def parse():
     ap.add_argument("--workload", default="llama3_8b_b1h32kv8s8192d128")
     ap.add_argument("--no-sweep", action="store_true", help="skip the fuse-vs-separate sweep over S")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-decode", action="store_true", help="skip the decode (KV-cache) measurements")
     ap.add_argument("--seed", type=int, default=0)
     return ap.parse_args()
 
@@ -128,7 +135,7 @@ def main():
 
     import torch
     from paper_2609_13612_amd import api, inputs
-    from paper_2609_13612_amd.workloads import LLAMA_SWEEP_S, WORKLOADS
+    from paper_2609_13612_amd.workloads import DECODE_WORKLOADS, LLAMA_SWEEP_S, WORKLOADS
 
     w = WORKLOADS[args.workload]
     torch.cuda.set_device(0)
@@ -288,6 +295,43 @@ def main():
     del src, dst
     log(f"plain copy of 512 MiB: {cp_ms:.4f} ms, {copy_gbs:.0f} GB/s moved")
 
+    # ---------------------------------------------------------------- decode over a KV cache
+    decode = None
+    if not args.no_decode:
+        decode = {}
+        for name, dw in DECODE_WORKLOADS.items():
+            c = inputs.make_decode(dw.B, dw.H, dw.Hkv, dw.S_kv, dw.D, seed=args.seed)
+            qd = c["q"].to(dev)
+            nb = dw.cache_bytes()
+            npool = max(2, math.ceil(600e6 / nb))   # more than twice the Infinity Cache: HBM, not MALL
+            kv_pool = [(c["k"].to(dev), c["v"].to(dev)) for _ in range(npool)]
+            del c
+            od = torch.empty_like(qd)
+            ld = torch.empty(dw.B, dw.H, device=dev, dtype=torch.float32)
+            wsd = torch.empty(api.attnfuse_decode_workspace_bytes(dw.B, dw.H, dw.Hkv, dw.S_kv, dw.D),
+                              device=dev, dtype=torch.uint8)
+            cnt = [0]
+
+            def dec():
+                i = cnt[0] % npool
+                cnt[0] += 1
+                api.attnfuse_decode(qd, kv_pool[i][0], kv_pool[i][1], rope=dw.rope, theta=dw.theta, out=od,
+                                    lse=ld, workspace=wsd)
+
+            for _ in range(10):
+                dec()
+            d_ms = statistics.median(time_calls(dec, max(50, 2 * npool)))
+            gbs = nb / (d_ms * 1e-3) / 1e9
+            decode[name] = {"B": dw.B, "H": dw.H, "H_kv": dw.Hkv, "S_kv": dw.S_kv, "D": dw.D, "rope": dw.rope,
+                            "ms": round(d_ms, 4), "cache_bytes": nb,
+                            "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS,
+                                         "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4)},
+                            "frac_of_copy": round(gbs / copy_gbs, 4), "cache_pool": npool,
+                            "paper_h100_ms": PAPER_DECODE_MS.get(name)}
+            log(f"decode {name}: {d_ms:.4f} ms, {gbs:.0f} GB/s of cache")
+            del kv_pool, qd, od, ld, wsd
+        torch.cuda.empty_cache()
+
     # ---------------------------------------------------------------- CPU oracle baseline
     cpu_baseline = None
     if not args.no_cpu_baseline:
@@ -344,6 +388,8 @@ def main():
     if sweep is not None:
         line["crossover_sweep"] = sweep
         line["crossover_model"] = crossover
+    if decode is not None:
+        line["decode"] = decode
     print(json.dumps(line), flush=True)
 
 

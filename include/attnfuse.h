@@ -142,8 +142,8 @@ int attnfuse_rope_bwd(const void* dQr, const void* dKr, void* dQ, void* dK,
 
 /* Bytes of device workspace attnfuse_decode needs: one partial (max, sum,
  * accumulator) triple per (sequence, query head, cache chunk), fp32.  The chunk
- * length is a power of two in [128, 1024] chosen from B * H_kv * S_kv so the
- * first phase launches about 1024 workgroups.  Returns 0 for invalid sizes. */
+ * length is a power of two in [128, 4096] chosen from B * H_kv * S_kv so the
+ * first phase launches about 512 workgroups.  Returns 0 for invalid sizes. */
 size_t attnfuse_decode_workspace_bytes(int B, int H, int H_kv, int S_kv, int D);
 
 /*

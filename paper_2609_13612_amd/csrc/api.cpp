@@ -113,13 +113,14 @@ struct DecodeLayout {
   size_t ml, acc, total;
 };
 
-// Keys per phase-1 workgroup: a power of two in [128, 1024] giving about 1024
-// workgroups; partial (max, sum) pairs then accumulators, each 256-byte aligned.
+// Keys per phase-1 workgroup: a power of two in [128, 4096] giving about 512
+// workgroups (one resident round at two per CU, so each wave streams several
+// tiles); partial (max, sum) pairs then accumulators, each 256-byte aligned.
 DecodeLayout decode_layout(int B, int H, int H_kv, int S, int D) {
   const long long work = (long long)B * H_kv * S;
   DecodeLayout L{};
   L.chunk = 128;
-  while (L.chunk < 1024 && (long long)L.chunk * 1024 < work) L.chunk *= 2;
+  while (L.chunk < 4096 && (long long)L.chunk * 512 < work) L.chunk *= 2;
   L.nsplit = (S + L.chunk - 1) / L.chunk;
   const size_t parts = (size_t)B * H * L.nsplit;
   L.ml = 0;

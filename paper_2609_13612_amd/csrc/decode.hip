@@ -18,7 +18,9 @@
 //   LDS and one partial per (sequence, head, chunk) is written; chunks with no
 //   visible key return at once.
 // Phase 2 (decode_combine_kernel): per (sequence, head), merge the partials of
-//   the chunks that hold visible keys by log-sum-exp and write O and LSE.
+//   the chunks that hold visible keys by log-sum-exp and write O and LSE; the
+//   head's dims are spread over several workgroups so the merge reads the
+//   partials with the whole chip.
 //
 // Precision: without RoPE the bf16 query and keys meet exactly in a bf16
 // MFMA.  With RoPE the query is rotated at position L-1 in fp32 and rounded to
@@ -269,37 +271,72 @@ __global__ __launch_bounds__(256) void decode_split_kernel(DecodeParams p) {
   }
 }
 
-// One workgroup of D threads per (sequence, query head); thread d owns dim d.
+// Phase 2.  Workgroup = 256 threads = one (sequence, query head) and 32 of its
+// dims; the chunk weights 2^(m_s - M) are formed once in LDS, then eight
+// thread groups each sum every eighth chunk's accumulators for the 32 dims
+// (coalesced rows) and the groups reduce through LDS.
+constexpr int COMBINE_MAX_CHUNKS = 8192;   // 2^20 keys / 128-key chunks
+
+__device__ __forceinline__ float block_reduce_256(float x, float* red, bool is_max) {
+  const int t = threadIdx.x;
+  red[t] = x;
+  __syncthreads();
+  for (int w = 128; w > 0; w >>= 1) {
+    if (t < w) red[t] = is_max ? fmaxf(red[t], red[t + w]) : red[t] + red[t + w];
+    __syncthreads();
+  }
+  const float r = red[0];
+  __syncthreads();
+  return r;
+}
+
 template <int D>
-__global__ __launch_bounds__(D) void decode_combine_kernel(DecodeParams p) {
-  const int bh = blockIdx.x, d = threadIdx.x;
+__global__ __launch_bounds__(256) void decode_combine_kernel(DecodeParams p) {
+  __shared__ float wts[COMBINE_MAX_CHUNKS];
+  __shared__ float red[256];
+  const int bh = blockIdx.x, t = threadIdx.x;
+  const int d = 32 * blockIdx.y + (t & 31), grp = t >> 5;
   const int b = bh / p.H;
   const int L = seq_len(p, b);
   uint16_t* O = static_cast<uint16_t*>(p.o) + (size_t)bh * D;
-  if (L < 1) {
-    O[d] = 0;
-    if (d == 0) p.lse[bh] = -INFINITY;
+  if (L < 1) {   // workgroup-uniform
+    if (grp == 0) O[d] = 0;
+    if (t == 0 && blockIdx.y == 0) p.lse[bh] = -INFINITY;
     return;
   }
   const int s_lo = first_key(p, L) / p.chunk, s_hi = (L - 1) / p.chunk;
-  const float* ml = p.part_ml + (size_t)bh * p.nsplit * 2;
-  float M = -INFINITY;
-  for (int s = s_lo; s <= s_hi; ++s) M = fmaxf(M, ml[2 * s]);
-  float l = 0.f, o = 0.f;
-  for (int s = s_lo; s <= s_hi; ++s) {
-    const float f = fast_exp2(ml[2 * s] - M);
-    l += ml[2 * s + 1] * f;
-    o += p.part_acc[((size_t)bh * p.nsplit + s) * D + d] * f;
+  const int n = s_hi - s_lo + 1;
+  const float* ml = p.part_ml + ((size_t)bh * p.nsplit + s_lo) * 2;
+  float mx = -INFINITY;
+  for (int i = t; i < n; i += 256) mx = fmaxf(mx, ml[2 * i]);
+  const float M = block_reduce_256(mx, red, true);
+  float lsum = 0.f;
+  for (int i = t; i < n; i += 256) {
+    const float w = fast_exp2(ml[2 * i] - M);
+    wts[i] = w;
+    lsum += ml[2 * i + 1] * w;
   }
-  O[d] = static_cast<uint16_t>(pack_bf16(o / l, 0.f) & 0xffffu);
-  if (d == 0) p.lse[bh] = (M + __log2f(l)) * kLn2;
+  const float l = block_reduce_256(lsum, red, false);   // its barriers also publish wts
+  const float* acc = p.part_acc + ((size_t)bh * p.nsplit + s_lo) * D + d;
+  float o = 0.f;
+#pragma unroll 4
+  for (int i = grp; i < n; i += 8) o += acc[(size_t)i * D] * wts[i];
+  red[t] = o;
+  __syncthreads();
+  if (grp == 0) {
+    float sum = 0.f;
+#pragma unroll
+    for (int g = 0; g < 8; ++g) sum += red[32 * g + t];
+    O[d] = static_cast<uint16_t>(pack_bf16(sum / l, 0.f) & 0xffffu);
+    if (t == 0 && blockIdx.y == 0) p.lse[bh] = (M + __log2f(l)) * kLn2;
+  }
 }
 
 template <int D, int ROPE, bool ALIBI>
 static int launch_one(const DecodeParams& p, hipStream_t st) {
   const long long blocks = (long long)p.nsplit * p.B * p.Hkv;
   hipLaunchKernelGGL((decode_split_kernel<D, ROPE, ALIBI>), dim3((unsigned)blocks), dim3(256), 0, st, p);
-  hipLaunchKernelGGL((decode_combine_kernel<D>), dim3((unsigned)(p.B * p.H)), dim3(D), 0, st, p);
+  hipLaunchKernelGGL((decode_combine_kernel<D>), dim3((unsigned)(p.B * p.H), D / 32), dim3(256), 0, st, p);
   return hipGetLastError() == hipSuccess ? 0 : -3;
 }
 

@@ -1,8 +1,9 @@
 """Seeded synthetic inputs shared by the HIP path's tests, the bench and the oracle checks.
 
 This module holds none of the method's arithmetic.  It draws i.i.d. N(0, 1)
-tensors from a CPU ``torch.Generator`` in a fixed order -- Q, K, V, then dO --
-as fp32, and rounds them to the storage dtype (bf16 rounds to nearest even).
+tensors from a CPU ``torch.Generator`` in a fixed order -- Q, K, V, then dO
+(decode: the query, then the K and V caches) -- as fp32, and rounds them to
+the storage dtype (bf16 rounds to nearest even).
 Both sides of a parity check consume exactly these values: the HIP path after
 a copy to the GPU, the oracle after an exact upcast to fp64.
 """
@@ -23,6 +24,21 @@ def make_qkv(B, H, Hkv, S, D, *, dtype="bf16", seed=0, with_do=False):
     }
     if with_do:
         out["do"] = torch.randn(B, H, S, D, generator=g, dtype=torch.float32)
+    t = DTYPES[dtype]
+    return {name: x.to(t).contiguous() for name, x in out.items()}
+
+
+def make_decode(B, H, Hkv, S_kv, D, *, dtype="bf16", seed=0):
+    """Dict with q [B,H,D] (one query per sequence) and the caches k, v
+    [B,Hkv,S_kv,D] on the CPU, drawn in that order."""
+    if dtype not in DTYPES:
+        raise ValueError(f"dtype must be one of {sorted(DTYPES)}")
+    g = torch.Generator("cpu").manual_seed(seed)
+    out = {
+        "q": torch.randn(B, H, D, generator=g, dtype=torch.float32),
+        "k": torch.randn(B, Hkv, S_kv, D, generator=g, dtype=torch.float32),
+        "v": torch.randn(B, Hkv, S_kv, D, generator=g, dtype=torch.float32),
+    }
     t = DTYPES[dtype]
     return {name: x.to(t).contiguous() for name, x in out.items()}
 

@@ -137,8 +137,8 @@ def test_rope_unsupported():
 
 def test_decode_workspace_bytes():
     lib = _lib.load()
-    # Llama-3-70B geometry, 32k cache: 256-key chunks -> 128 per sequence; 64 heads
-    parts = 64 * 128
+    # Llama-3-70B geometry, 32k cache: 512-key chunks -> 64 per sequence; 64 heads
+    parts = 64 * 64
     assert lib.attnfuse_decode_workspace_bytes(1, 64, 8, 32768, 128) == parts * 8 + parts * 128 * 4
     # Llama-3-8B geometry, 4k cache: the 128-key minimum -> 32 chunks; 32 heads
     parts = 32 * 32

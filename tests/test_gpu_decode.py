@@ -14,10 +14,10 @@ pytestmark = pytest.mark.gpu
 
 
 def _case(B, H, Hkv, S, D, seed):
-    """Seeded query [B, H, D] (the last row of a prefill draw) and caches [B, Hkv, S, D]."""
-    c = inputs.make_qkv(B, H, Hkv, S, D, seed=seed)
-    q = c["q"][:, :, S - 1].contiguous()
-    return q, c["k"], c["v"]
+    """Seeded query [B, H, D] and caches [B, Hkv, S, D] (the caches stand for
+    keys already rotated at their positions)."""
+    c = inputs.make_decode(B, H, Hkv, S, D, seed=seed)
+    return c["q"], c["k"], c["v"]
 
 
 def _run(B, H, Hkv, S, D, *, lens=None, rope="none", theta=10000.0, mask="causal", window=None, alibi=False,

@@ -41,6 +41,7 @@ from .attention import (
     MASK_SLIDING_WINDOW,
     MASK_KINDS,
     visibility,
+    block_visible,
     attention_scores,
     attention_probs,
     attention_forward,
@@ -53,7 +54,7 @@ __all__ = [
     "ROPE_NONE", "ROPE_NEOX", "ROPE_INTERLEAVED", "ROPE_KINDS",
     "rope_frequencies", "rope_pair_indices", "rope_rotate",
     "MASK_NONE", "MASK_CAUSAL", "MASK_SLIDING_WINDOW", "MASK_KINDS",
-    "visibility", "attention_scores", "attention_probs",
+    "visibility", "block_visible", "attention_scores", "attention_probs",
     "attention_forward", "attention_backward", "attention_forward_rows",
     "decode_forward",
 ]

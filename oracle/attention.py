@@ -8,7 +8,9 @@ package docstring.  Steps, in the order the method states them:
    Section 3.1).
 3. Post-matmul modification (Section 3.1 combinators ``alibi``, ``causal``,
    ``sliding_window``, ``full``): bias_ij = -slope_h * (i - j) for ALiBi, then
-   masked entries become -inf.
+   masked entries become -inf.  An optional block-sparse mask (Section 2,
+   "Block-Sparse Attention") additionally hides every key whose (query block,
+   key block) pair is inactive.
 4. Softmax over keys: m_i = max_j s_ij, l_i = sum_j exp(s_ij - m_i),
    P_ij = exp(s_ij - m_i) / l_i.
 5. O = P V and LSE_i = m_i + ln(l_i) (the one saved scalar per row, Section 4.4).
@@ -43,19 +45,37 @@ MASK_KINDS = (MASK_NONE, MASK_CAUSAL, MASK_SLIDING_WINDOW)
 _ROW_CHUNK = 2048
 
 
-def visibility(i, j, mask, window=None):
-    """Boolean matrix: is key j visible to query i (i, j index arrays, broadcast)."""
-    i = np.asarray(i)[:, None]
-    j = np.asarray(j)[None, :]
+def block_visible(i, j, block_mask):
+    """Block-sparse mask (Section 2 "Block-Sparse Attention"): block_mask is
+    (block_size, active) with active[qb, kb] True when query block qb may see key
+    block kb.  Returns the boolean matrix for query positions i, key positions j."""
+    bs, active = block_mask
+    active = np.asarray(active, dtype=bool)
+    return active[np.asarray(i)[:, None] // bs, np.asarray(j)[None, :] // bs]
+
+
+def visibility(i, j, mask, window=None, block_mask=None):
+    """Boolean matrix: is key j visible to query i (i, j index arrays, broadcast).
+
+    With a block mask, a key is visible when both the elementwise mask and its
+    block allow it."""
+    i = np.asarray(i)
+    j = np.asarray(j)
+    ii = i[:, None]
+    jj = j[None, :]
     if mask == MASK_NONE:
-        return np.ones((i.shape[0], j.shape[1]), dtype=bool)
-    if mask == MASK_CAUSAL:
-        return j <= i
-    if mask == MASK_SLIDING_WINDOW:
+        vis = np.ones((ii.shape[0], jj.shape[1]), dtype=bool)
+    elif mask == MASK_CAUSAL:
+        vis = jj <= ii
+    elif mask == MASK_SLIDING_WINDOW:
         if window is None or window < 1:
             raise ValueError("sliding window needs window >= 1")
-        return (j <= i) & (j > i - window)
-    raise ValueError(f"unknown mask {mask!r}")
+        vis = (jj <= ii) & (jj > ii - window)
+    else:
+        raise ValueError(f"unknown mask {mask!r}")
+    if block_mask is not None:
+        vis = vis & block_visible(i, j, block_mask)
+    return vis
 
 
 def kv_head(h, H, Hkv):
@@ -86,7 +106,7 @@ def _rotated(q, k, rope, theta, pos_offset):
     return rope_rotate(q, pos, theta, rope), rope_rotate(k, pos, theta, rope)
 
 
-def attention_scores(qr_bh, kr_bg, rows, *, mask, window, slope, scale):
+def attention_scores(qr_bh, kr_bg, rows, *, mask, window, slope, scale, block_mask=None):
     """Step 2-3 for one (b, h): scaled scores of the given query rows with bias and mask.
 
     qr_bh [S, D], kr_bg [S, D] already rotated.  Returns [len(rows), S] fp64
@@ -98,7 +118,7 @@ def attention_scores(qr_bh, kr_bg, rows, *, mask, window, slope, scale):
     s = scale * (qr_bh[rows] @ kr_bg.T)
     if slope is not None:
         s = s + alibi_bias(slope, rows, cols)
-    vis = visibility(rows, cols, mask, window)
+    vis = visibility(rows, cols, mask, window, block_mask)
     return np.where(vis, s, -np.inf)
 
 
@@ -125,19 +145,19 @@ def _defaults(D, scale, alibi_slopes, H):
 
 
 def attention_probs(q, k, b, h, *, rope=ROPE_NONE, theta=10000.0, mask=MASK_CAUSAL,
-                    window=None, alibi_slopes=None, scale=None, pos_offset=0):
+                    window=None, alibi_slopes=None, scale=None, pos_offset=0, block_mask=None):
     """The full softmax matrix P [S, S] of one (b, h) (for invariant checks)."""
     B, H, Hkv, S, D = _check(q, k, k)
     scale, slopes = _defaults(D, scale, alibi_slopes, H)
     qr, kr = _rotated(q, k, rope, theta, pos_offset)
     g = kv_head(h, H, Hkv)
     s = attention_scores(qr[b, h], kr[b, g], np.arange(S), mask=mask, window=window,
-                         slope=None if slopes is None else slopes[h], scale=scale)
+                         slope=None if slopes is None else slopes[h], scale=scale, block_mask=block_mask)
     return _softmax_rows(s)[0]
 
 
 def attention_forward(q, k, v, *, rope=ROPE_NONE, theta=10000.0, mask=MASK_CAUSAL,
-                      window=None, alibi_slopes=None, scale=None, pos_offset=0):
+                      window=None, alibi_slopes=None, scale=None, pos_offset=0, block_mask=None):
     """O [B, H, S, D] and LSE [B, H, S] (natural log), both fp64."""
     q = np.asarray(q, dtype=np.float64)
     k = np.asarray(k, dtype=np.float64)
@@ -154,7 +174,7 @@ def attention_forward(q, k, v, *, rope=ROPE_NONE, theta=10000.0, mask=MASK_CAUSA
             for r0 in range(0, S, _ROW_CHUNK):
                 rows = np.arange(r0, min(S, r0 + _ROW_CHUNK))
                 s = attention_scores(qr[b, h], kr[b, g], rows, mask=mask, window=window,
-                                     slope=slope, scale=scale)
+                                     slope=slope, scale=scale, block_mask=block_mask)
                 P, m, l = _softmax_rows(s)
                 O[b, h, rows] = P @ v[b, g]
                 with np.errstate(divide="ignore"):
@@ -164,7 +184,7 @@ def attention_forward(q, k, v, *, rope=ROPE_NONE, theta=10000.0, mask=MASK_CAUSA
 
 def attention_forward_rows(q_bh, k_bg, v_bg, rows, *, h=0, H=1, rope=ROPE_NONE,
                            theta=10000.0, mask=MASK_CAUSAL, window=None,
-                           alibi_slopes=None, scale=None, pos_offset=0):
+                           alibi_slopes=None, scale=None, pos_offset=0, block_mask=None):
     """O and LSE of selected query rows of ONE head, for sampled checks at full size.
 
     q_bh [S, D] is query head h; k_bg, v_bg [S, D] its K/V head.  Only the
@@ -185,7 +205,7 @@ def attention_forward_rows(q_bh, k_bg, v_bg, rows, *, h=0, H=1, rope=ROPE_NONE,
     cols = np.arange(S)
     if slopes is not None:
         s = s + alibi_bias(slopes[h], rows, cols)
-    s = np.where(visibility(rows, cols, mask, window), s, -np.inf)
+    s = np.where(visibility(rows, cols, mask, window, block_mask), s, -np.inf)
     P, m, l = _softmax_rows(s)
     with np.errstate(divide="ignore"):
         return P @ v_bg, m + np.log(l)
@@ -193,7 +213,7 @@ def attention_forward_rows(q_bh, k_bg, v_bg, rows, *, h=0, H=1, rope=ROPE_NONE,
 
 def attention_backward(q, k, v, do, *, rope=ROPE_NONE, theta=10000.0, mask=MASK_CAUSAL,
                        window=None, alibi_slopes=None, scale=None, pos_offset=0,
-                       return_intermediates=False):
+                       return_intermediates=False, block_mask=None):
     """dQ [B,H,S,D], dK and dV [B,H_kv,S,D] in fp64.
 
     With ``return_intermediates`` also returns a dict with per-(b,h) lists of
@@ -219,7 +239,7 @@ def attention_backward(q, k, v, do, *, rope=ROPE_NONE, theta=10000.0, mask=MASK_
             for r0 in range(0, S, _ROW_CHUNK):
                 rows = np.arange(r0, min(S, r0 + _ROW_CHUNK))
                 s = attention_scores(qr[b, h], kr[b, g], rows, mask=mask, window=window,
-                                     slope=slope, scale=scale)
+                                     slope=slope, scale=scale, block_mask=block_mask)
                 P = _softmax_rows(s)[0]
                 dO_rows = do[b, h, rows]
                 dv[b, g] += P.T @ dO_rows

@@ -50,7 +50,7 @@ def key_visible(i, j, mask, window):
 
 
 def forward(q, k, v, *, rope="none", theta=10000.0, mask="causal", window=None,
-            alibi_slopes=None, scale=None, pos_offset=0):
+            alibi_slopes=None, scale=None, pos_offset=0, block_mask=None):
     """q: nested lists [B][H][S][D]; k, v: [B][Hkv][S][D].  Returns (O, LSE) nested lists."""
     B, H, S, D = len(q), len(q[0]), len(q[0][0]), len(q[0][0][0])
     Hkv = len(k[0])
@@ -68,6 +68,8 @@ def forward(q, k, v, *, rope="none", theta=10000.0, mask="causal", window=None,
                 scores = {}
                 for j in range(S):
                     if not key_visible(i, j, mask, window):
+                        continue
+                    if block_mask is not None and not block_mask[1][i // block_mask[0]][j // block_mask[0]]:
                         continue
                     kj = matvec(rot[j], k[b][kvh][j])
                     sc = scale * dot(qi, kj)

@@ -395,3 +395,59 @@ def check_decode_ignores_stale_entries(seed=23):
     kc2[1, :, 6:] = 5.0
     other = oracle.decode_forward(q, kc2, vc2, [4, 6], rope="neox")
     assert np.array_equal(base[0], other[0]) and np.array_equal(base[1], other[1])
+
+
+# ----------------------------------------------------------------------------- block-sparse mask
+
+def _random_blocks(seed, nb, density=0.45, empty_row=1):
+    active = _rng(seed).random((nb, nb)) < density
+    active[empty_row] = False              # a query block that sees nothing: O = 0, LSE = -inf
+    return active
+
+
+def check_block_mask_vs_bruteforce(variant, seed=30):
+    rope, mask, window, alibi = variant
+    q, k, v, _ = _tiny(seed, B=1, H=4, Hkv=2, S=9, D=4)
+    kw = _kw(rope, mask, window, alibi, 4)
+    bm = (2, _random_blocks(seed, 5))      # 2x2 blocks, the last one ragged
+    O, L = oracle.attention_forward(q, k, v, block_mask=bm, **kw)
+    Ob, Lb = bruteforce.forward(q.tolist(), k.tolist(), v.tolist(), block_mask=(bm[0], bm[1].tolist()), **kw)
+    Ob, Lb = np.array(Ob), np.array(Lb)
+    assert np.array_equal(np.isneginf(L), np.isneginf(Lb))
+    fin = np.isfinite(Lb)
+    assert np.allclose(L[fin], Lb[fin], atol=TOL, rtol=0)
+    assert np.allclose(O, Ob, atol=TOL, rtol=0)
+    assert np.isneginf(L[:, :, 2:4]).all() and (O[:, :, 2:4] == 0).all()   # block row 1 is empty
+
+
+def check_block_mask_reductions(seed=31):
+    q, k, v, do = _tiny(seed, B=1, H=2, Hkv=1, S=10, D=8)
+    full = (4, np.ones((3, 3), dtype=bool))
+    for mask in ("none", "causal"):
+        a = oracle.attention_forward(q, k, v, rope="neox", mask=mask)
+        b = oracle.attention_forward(q, k, v, rope="neox", mask=mask, block_mask=full)
+        assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1])
+        ga = oracle.attention_backward(q, k, v, do, rope="neox", mask=mask)
+        gb = oracle.attention_backward(q, k, v, do, rope="neox", mask=mask, block_mask=full)
+        assert all(np.array_equal(x, y) for x, y in zip(ga, gb))
+    # block-lower-triangular blocks under a causal mask are exactly causal
+    tril = (4, np.tril(np.ones((3, 3), dtype=bool)))
+    a = oracle.attention_forward(q, k, v, rope="interleaved", mask="causal")
+    b = oracle.attention_forward(q, k, v, rope="interleaved", mask="causal", block_mask=tril)
+    assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1])
+
+
+def check_block_mask_backward_fd(seed=32):
+    q, k, v, do = _tiny(seed, B=1, H=2, Hkv=1, S=6, D=4)
+    active = _random_blocks(seed, 3, density=0.6, empty_row=2)
+    active[0, 0] = active[1, 1] = True
+    kw = dict(rope="neox", theta=10000.0, mask="none", window=None, alibi_slopes=None, scale=0.6)
+    dq, dk, dv = oracle.attention_backward(q, k, v, do, block_mask=(2, active), **kw)
+    ql, kl, vl, dol = q.tolist(), k.tolist(), v.tolist(), do.tolist()
+
+    def f():
+        return bruteforce.loss(ql, kl, vl, dol, block_mask=(2, active.tolist()), **kw)
+
+    assert np.allclose(dq, np.array(bruteforce.finite_difference_grad(ql, f)), atol=1e-7)
+    assert np.allclose(dk, np.array(bruteforce.finite_difference_grad(kl, f)), atol=1e-7)
+    assert np.allclose(dv, np.array(bruteforce.finite_difference_grad(vl, f)), atol=1e-7)

@@ -59,12 +59,18 @@ def _bad_alibi(slope, rows, cols):
     return slope * (np.asarray(rows)[:, None] - np.asarray(cols)[None, :]).astype(np.float64)
 
 
-def _bad_visibility(i, j, mask, window=None):
+def _bad_visibility(i, j, mask, window=None, block_mask=None):
     i2 = np.asarray(i)[:, None]
     j2 = np.asarray(j)[None, :]
     if mask == "sliding_window":
         return (j2 <= i2) & (j2 >= i2 - window)   # W + 1 keys
-    return _REAL_VIS(i, j, mask, window)
+    return _REAL_VIS(i, j, mask, window, block_mask)
+
+
+def _transposed_blocks(i, j, block_mask):
+    bs, active = block_mask
+    active = np.asarray(active, dtype=bool)
+    return active.T[np.asarray(i)[:, None] // bs, np.asarray(j)[None, :] // bs]
 
 
 _REAL_VIS = oatt.visibility
@@ -97,6 +103,7 @@ MUTATIONS = {
     "gqa_mapping": [(oatt, "kv_head", _bad_kv_head)],
     "alibi_sign": [(oatt, "alibi_bias", _bad_alibi)],
     "window_boundary": [(oatt, "visibility", _bad_visibility)],
+    "block_mask_transposed": [(oatt, "block_visible", _transposed_blocks)],
     "dropped_scale": [(oatt, "_defaults", _no_scale_defaults)],
     "gradient_not_unrotated": [(oatt, "rope_rotate", _no_inverse_rotate)],
 }
@@ -116,6 +123,7 @@ CHECKS = [
     lambda: P.check_decode_vs_bruteforce(ALIBI),
     lambda: P.check_decode_vs_bruteforce(SW),
     lambda: P.check_decode_closed_forms("neox"),
+    lambda: P.check_block_mask_vs_bruteforce(FWD),
 ]
 
 

@@ -118,3 +118,16 @@ def test_decode_closed_forms(kind):
 
 def test_decode_ignores_stale_entries():
     P.check_decode_ignores_stale_entries()
+
+
+@pytest.mark.parametrize("variant", P.VARIANTS, ids=lambda v: "-".join(map(str, v)))
+def test_block_mask_vs_bruteforce(variant):
+    P.check_block_mask_vs_bruteforce(variant)
+
+
+def test_block_mask_reductions():
+    P.check_block_mask_reductions()
+
+
+def test_block_mask_backward_fd():
+    P.check_block_mask_backward_fd()

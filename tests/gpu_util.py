@@ -3,12 +3,14 @@
 Tolerances are the ones the contract states: bf16 outputs max-abs 2e-2 and
 mean-abs 2e-3; the fp32 debug path 1e-4; LSE 1e-3 absolute.
 
-Reading of the bf16 bound: a bf16 output x carries up to 2^-9 |x| of rounding
-that the format itself imposes (half an ulp; 0.031 at |x| = 16), which no
-implementation with bf16 outputs can avoid.  The max-abs bound is therefore
-applied per element as 2e-2 + 2^-9 |ref|: exactly the stated 2e-2 for the
-O(1) values it was written for (at most +0.0078 below |ref| = 4), and the
-format's own resolution for large gradients.  The mean-abs bound is unchanged.
+Reading of the bf16 bound: bf16 has an 8-bit significand, so rounding a value
+x to it can move it by up to half an ulp, 2^-8 |x| (the format's unit
+roundoff: up to 0.0039 just above |x| = 1, 0.0625 just above |x| = 16), which no
+implementation with bf16 outputs can avoid -- from |x| = 8 on even the
+correctly rounded exact value can miss a flat 2e-2.  The max-abs bound is
+therefore applied per element as 2e-2 + 2^-8 |ref|: the stated 2e-2 plus at
+most 0.0039 for the O(1) values it was written for, and the format's own
+resolution for large gradients.  The mean-abs bound is unchanged.
 """
 import sys
 
@@ -41,7 +43,7 @@ def f64(t):
     return inputs.to_f64(t)
 
 
-BF16_HALF_ULP = 2.0 ** -9
+BF16_HALF_ULP = 2.0 ** -8   # bf16 unit roundoff
 
 
 def assert_bf16_close(gpu, ref, what, max_tol=BF16_MAX, mean_tol=BF16_MEAN):
@@ -51,7 +53,7 @@ def assert_bf16_close(gpu, ref, what, max_tol=BF16_MAX, mean_tol=BF16_MEAN):
     excess = err - (max_tol + BF16_HALF_ULP * np.abs(ref))
     i = np.unravel_index(np.argmax(excess), err.shape) if err.size else None
     assert err.size == 0 or excess.max() <= 0, \
-        f"{what}: error {err[i]:.3e} at |ref| {abs(ref[i]):.3f} exceeds {max_tol} + 2^-9|ref| (max-abs {err.max():.3e})"
+        f"{what}: error {err[i]:.3e} at |ref| {abs(ref[i]):.3f} exceeds {max_tol} + 2^-8|ref| (max-abs {err.max():.3e})"
     assert err.mean() <= mean_tol, f"{what}: mean-abs {err.mean():.3e} > {mean_tol}"
     return float(err.max()), float(err.mean())
 

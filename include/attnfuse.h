@@ -121,6 +121,55 @@ int attnfuse_bwd(const void* Q, const void* K, const void* V, const void* O, con
                  const float* alibi_slopes, float softmax_scale, void* stream);
 
 /*
+ * Block-sparse attention (Section 4.3 "Block-Sparse Attention"): the variant
+ * attnfuse_fwd computes with an extra block-level visibility test.  Positions
+ * are grouped into blocks of AF_SPARSE_BLOCK = 64 (nb = ceil(S / 64) blocks per
+ * side); query i sees key j only when block (i / 64, j / 64) is active AND the
+ * elementwise mask allows it.  The kernels iterate only over active blocks:
+ * each workgroup gathers the union of its query blocks' active key blocks and
+ * skips the rest, so the work is proportional to the active fraction.  A row
+ * whose visible set is empty gets O = 0, LSE = -inf (and zero gradients).
+ *
+ * The mask is one compressed-sparse-row list shared by every batch and head:
+ *   q_block_ptr  device int32 [nb + 1]: row r's active key blocks are
+ *                k_block_idx[q_block_ptr[r] .. q_block_ptr[r+1]-1];
+ *                q_block_ptr[0] = 0, non-decreasing
+ *   k_block_idx  device int32 [q_block_ptr[nb]]: key-block indices in [0, nb)
+ *                (any order; duplicates allowed; entries outside [0, nb) are
+ *                clamped into it)
+ * Both 4-byte aligned, caller-owned, read only.  The pointer array must be a
+ * valid CSR offset list: it is read on the device, and offsets outside
+ * k_block_idx are not detected (the Python binding builds and checks it).
+ * S <= 64 * 2048 = 131072; dtype AF_DTYPE_BF16 (fp32: AF_ERR_UNSUPPORTED).
+ * Other arguments and results as attnfuse_fwd.
+ */
+#define AF_SPARSE_BLOCK 64
+int attnfuse_fwd_blocksparse(const void* Q, const void* K, const void* V, void* O, float* LSE,
+                             const int* q_block_ptr, const int* k_block_idx,
+                             int B, int H, int H_kv, int S, int D, int dtype,
+                             int rope, float rope_theta, int mask, int window,
+                             const float* alibi_slopes, float softmax_scale, void* stream);
+
+/*
+ * Backward of attnfuse_fwd_blocksparse (Section 4.3: the backward also visits
+ * only active blocks).  The dQ pass walks each query block's key blocks (the
+ * forward's list); the dK/dV pass walks each key block's query blocks, so it
+ * also needs the transposed list of the same mask:
+ *   k_block_ptr  device int32 [nb + 1], q_block_idx: key-block column c's
+ *                active query blocks (compressed sparse column form)
+ * The two lists must describe the same block set; no check is made that they
+ * do.  Workspace, other arguments and results as attnfuse_bwd; bf16 only.
+ */
+int attnfuse_bwd_blocksparse(const void* Q, const void* K, const void* V, const void* O, const void* dO,
+                             const float* LSE, void* dQ, void* dK, void* dV,
+                             const int* q_block_ptr, const int* k_block_idx,
+                             const int* k_block_ptr, const int* q_block_idx,
+                             void* workspace, size_t workspace_bytes,
+                             int B, int H, int H_kv, int S, int D, int dtype,
+                             int rope, float rope_theta, int mask, int window,
+                             const float* alibi_slopes, float softmax_scale, void* stream);
+
+/*
  * Standalone rotation, the separate-RoPE path (Section 5.3 "The Rotation
  * Calculus": pre-rotation reads Q and K and writes Q' and K' once, an HBM round
  * trip, before an attention that has no RoPE).  One bandwidth-bound launch
@@ -147,7 +196,7 @@ int attnfuse_rope_bwd(const void* dQr, const void* dKr, void* dQ, void* dK,
 size_t attnfuse_decode_workspace_bytes(int B, int H, int H_kv, int S_kv, int D);
 
 /*
- * Decode attention over a key/value cache (Section 2 "Flash Decoding"): one
+ * Decode attention over a key/value cache (Section 4.2 "Flash Decoding"): one
  * query per sequence.  Phase 1 splits each sequence's cache into chunks and
  * computes a partial online-softmax triple (m, l, acc) per chunk for all query
  * heads of a K/V head at once (the group's heads fill the MFMA's columns by

@@ -19,7 +19,7 @@ with the full score matrix materialised per (batch, head):
   ten combinators).
 * The backward follows the FlashAttention-2 equations; the forward keeps one
   scalar per row, L = m + log l (Section 4.4 "Backward Pass").
-* Decode (one query per sequence against a key/value cache, Section 2 "Flash
+* Decode (one query per sequence against a key/value cache, Section 4.2 "Flash
   Decoding") is the same definition for that single row: ``decode_forward``.
 
 Every function is pinned by ``tests/test_oracle_*.py`` against invariants,

@@ -8,7 +8,7 @@ package docstring.  Steps, in the order the method states them:
    Section 3.1).
 3. Post-matmul modification (Section 3.1 combinators ``alibi``, ``causal``,
    ``sliding_window``, ``full``): bias_ij = -slope_h * (i - j) for ALiBi, then
-   masked entries become -inf.  An optional block-sparse mask (Section 2,
+   masked entries become -inf.  An optional block-sparse mask (Section 4.3,
    "Block-Sparse Attention") additionally hides every key whose (query block,
    key block) pair is inactive.
 4. Softmax over keys: m_i = max_j s_ij, l_i = sum_j exp(s_ij - m_i),
@@ -46,7 +46,7 @@ _ROW_CHUNK = 2048
 
 
 def block_visible(i, j, block_mask):
-    """Block-sparse mask (Section 2 "Block-Sparse Attention"): block_mask is
+    """Block-sparse mask (Section 4.3 "Block-Sparse Attention"): block_mask is
     (block_size, active) with active[qb, kb] True when query block qb may see key
     block kb.  Returns the boolean matrix for query positions i, key positions j."""
     bs, active = block_mask

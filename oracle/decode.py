@@ -1,6 +1,6 @@
 """Decode attention (one query per sequence over a KV cache), fp64 -- oracle, test infrastructure only.
 
-The paper's Flash Decoding path (Section 2, "Flash Decoding"; evaluated in
+The paper's Flash Decoding path (Section 4.2, "Flash Decoding"; evaluated in
 Table ``tab:decode``) computes ordinary attention for a single query row per
 (batch, query head) against a long key/value cache; splitting the cache into
 chunks and merging partial (m, l, acc) triples by log-sum-exp is exact, so the

@@ -17,6 +17,10 @@ SIGNATURES = {
     "attnfuse_bwd_workspace_bytes": (ctypes.c_size_t, [_I, _I, _I, _I, _I, _I]),
     "attnfuse_bwd": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t,
                           _I, _I, _I, _I, _I, _I, _I, _F, _I, _I, _P, _F, _P]),
+    "attnfuse_fwd_blocksparse": (_I, [_P, _P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _F, _I, _I, _P, _F,
+                                      _P]),
+    "attnfuse_bwd_blocksparse": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t,
+                                      _I, _I, _I, _I, _I, _I, _I, _F, _I, _I, _P, _F, _P]),
     "attnfuse_rope": (_I, [_P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _F, _P]),
     "attnfuse_rope_bwd": (_I, [_P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _F, _P]),
     "attnfuse_decode_workspace_bytes": (ctypes.c_size_t, [_I, _I, _I, _I, _I]),

@@ -101,6 +101,58 @@ def attnfuse_bwd(q, k, v, o, do, lse, *, rope="none", theta=10000.0, mask="causa
     return dq, dk, dv
 
 
+def _mask_ptrs(block_mask, q, S):
+    if block_mask.S != S:
+        raise ValueError(f"block mask built for S={block_mask.S}, tensors have S={S}")
+    ts = (block_mask.q_ptr, block_mask.k_idx, block_mask.k_ptr, block_mask.q_idx)
+    for t in ts:
+        if t.device != q.device or t.dtype != torch.int32 or not t.is_contiguous():
+            raise ValueError("block mask lists must be contiguous int32 tensors on q's device")
+    # an empty index list has no storage; any valid aligned address serves
+    return [t.data_ptr() if t.numel() else block_mask.q_ptr.data_ptr() for t in ts]
+
+
+def attnfuse_fwd_blocksparse(q, k, v, block_mask, *, rope="none", theta=10000.0, mask="none", window=None,
+                             alibi_slopes=None, scale=None, out=None, lse=None):
+    """O, LSE of attention restricted to the active blocks of ``block_mask``
+    (a blockmask.BlockMask); see attnfuse_fwd_blocksparse."""
+    B, H, Hkv, S, D = _shape(q, k)
+    _same(q, k, v, out)
+    if v.shape != k.shape:
+        raise ValueError("v must have k's shape")
+    qp, ki, _, _ = _mask_ptrs(block_mask, q, S)
+    out = torch.empty_like(q) if out is None else out
+    lse = torch.empty(B, H, S, device=q.device, dtype=torch.float32) if lse is None else lse
+    r, th, m, w, sc = _variant(rope, theta, mask, window, alibi_slopes, scale, D)
+    code = _lib.load().attnfuse_fwd_blocksparse(_ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(lse), qp, ki,
+                                                B, H, Hkv, S, D, DTYPE[q.dtype], r, th, m, w, _ptr(alibi_slopes),
+                                                sc, _stream())
+    _check(code, "attnfuse_fwd_blocksparse")
+    return out, lse
+
+
+def attnfuse_bwd_blocksparse(q, k, v, o, do, lse, block_mask, *, rope="none", theta=10000.0, mask="none",
+                             window=None, alibi_slopes=None, scale=None, dq=None, dk=None, dv=None,
+                             workspace=None):
+    """dQ, dK, dV of attnfuse_fwd_blocksparse; see attnfuse_bwd_blocksparse."""
+    B, H, Hkv, S, D = _shape(q, k)
+    _same(q, k, v, o, do, dq, dk, dv)
+    qp, ki, kp, qi = _mask_ptrs(block_mask, q, S)
+    dq = torch.empty_like(q) if dq is None else dq
+    dk = torch.empty_like(k) if dk is None else dk
+    dv = torch.empty_like(v) if dv is None else dv
+    nbytes = attnfuse_bwd_workspace_bytes(B, H, Hkv, S, D, rope)
+    if workspace is None:
+        workspace = torch.empty(nbytes, device=q.device, dtype=torch.uint8)
+    r, th, m, w, sc = _variant(rope, theta, mask, window, alibi_slopes, scale, D)
+    code = _lib.load().attnfuse_bwd_blocksparse(_ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(do), _ptr(lse),
+                                                _ptr(dq), _ptr(dk), _ptr(dv), qp, ki, kp, qi, _ptr(workspace),
+                                                workspace.numel(), B, H, Hkv, S, D, DTYPE[q.dtype], r, th, m, w,
+                                                _ptr(alibi_slopes), sc, _stream())
+    _check(code, "attnfuse_bwd_blocksparse")
+    return dq, dk, dv
+
+
 def attnfuse_decode_workspace_bytes(B, H, H_kv, S_kv, D):
     return _lib.load().attnfuse_decode_workspace_bytes(B, H, H_kv, S_kv, D)
 

@@ -20,6 +20,12 @@ constexpr int kMaxS = 1 << 20;
 constexpr int kAbiVersion = 2;
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+bool aligned4(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 3u) == 0; }
+
+// Block-sparse masks: 64-position blocks, at most 2048 per side (the per-
+// workgroup tile list lives in LDS).
+constexpr int kMaxSparseS = 64 * 2048;
+
 
 int map_launch(int rc) {
   if (rc == 0) return AF_OK;
@@ -129,6 +135,82 @@ DecodeLayout decode_layout(int B, int H, int H_kv, int S, int D) {
   return L;
 }
 
+// ---------------------------------------------------------------- shared bodies
+int fwd_impl(const void* Q, const void* K, const void* V, void* O, float* LSE, const int* q_block_ptr,
+             const int* k_block_idx, int B, int H, int H_kv, int S, int D, int dtype, int rope, float rope_theta,
+             int mask, int window, const float* alibi_slopes, float softmax_scale, void* stream) {
+  if (!Q || !K || !V || !O || !LSE) return AF_ERR_INVALID_ARG;
+  if (!aligned16(Q) || !aligned16(K) || !aligned16(V) || !aligned16(O) || !aligned16(LSE)) return AF_ERR_INVALID_ARG;
+  if (O == Q || O == K || O == V || (const void*)LSE == Q || (const void*)LSE == K || (const void*)LSE == V)
+    return AF_ERR_INVALID_ARG;
+  int rc = check_common(B, H, H_kv, S, D, dtype, rope, rope_theta);
+  if (rc != AF_OK) return rc;
+  if ((rc = check_attn(mask, window, softmax_scale)) != AF_OK) return rc;
+  if (!supported_d(D)) return AF_ERR_UNSUPPORTED;
+  if (q_block_ptr && dtype == AF_DTYPE_FP32) return AF_ERR_UNSUPPORTED;   // block-sparse: bf16 kernels only
+
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  af::FwdParams p{};
+  p.q = Q; p.k = K; p.v = V; p.o = O; p.lse = LSE;
+  p.B = B; p.H = H; p.Hkv = H_kv; p.S = S;
+  // a window of S or more keys is the causal mask; clamping keeps n + window in int range
+  p.window = (mask == AF_MASK_SLIDING_WINDOW) ? (window < S ? window : S) : 0;
+  p.slopes = alibi_slopes;
+  p.scale = softmax_scale;
+  p.table = nullptr;
+  p.bq_ptr = q_block_ptr;
+  p.bk_idx = k_block_idx;
+  if (rope != AF_ROPE_NONE && (rc = rope_table(D, rope_theta, S, st, &p.table)) != AF_OK) return rc;
+  const bool alibi = alibi_slopes != nullptr;
+  if (dtype == AF_DTYPE_BF16) return map_launch(af::launch_fwd_bf16(D, rope, mask, alibi, p, st));
+  return map_launch(af::launch_fwd_fp32(D, rope, mask, alibi, p, st));
+}
+
+// sparse: NULL (dense) or {q_block_ptr, k_block_idx, k_block_ptr, q_block_idx}
+int bwd_impl(const void* Q, const void* K, const void* V, const void* O, const void* dO, const float* LSE, void* dQ,
+             void* dK, void* dV, const int* const* sparse, void* workspace, size_t workspace_bytes, int B, int H,
+             int H_kv, int S, int D, int dtype, int rope, float rope_theta, int mask, int window,
+             const float* alibi_slopes, float softmax_scale, void* stream) {
+  const void* ins[] = {Q, K, V, O, dO, LSE};
+  void* outs[] = {dQ, dK, dV, workspace};
+  for (const void* x : ins) if (!x || !aligned16(x)) return AF_ERR_INVALID_ARG;
+  for (const void* x : outs) if (!x || !aligned16(x)) return AF_ERR_INVALID_ARG;
+  for (const void* x : outs)
+    for (const void* y : ins) if (x == y) return AF_ERR_INVALID_ARG;
+  int rc = check_common(B, H, H_kv, S, D, dtype, rope, rope_theta);
+  if (rc != AF_OK) return rc;
+  if ((rc = check_attn(mask, window, softmax_scale)) != AF_OK) return rc;
+  if (workspace_bytes < attnfuse_bwd_workspace_bytes(B, H, H_kv, S, D, rope)) return AF_ERR_INVALID_ARG;
+  if (!supported_d(D)) return AF_ERR_UNSUPPORTED;
+  if (sparse && dtype == AF_DTYPE_FP32) return AF_ERR_UNSUPPORTED;        // block-sparse: bf16 kernels only
+
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  af::BwdParams p{};
+  p.q = Q; p.k = K; p.v = V; p.o = O; p.dout = dO; p.lse = LSE;
+  p.dq = dQ; p.dk = dK; p.dv = dV;
+  const BwdWorkspace ws = bwd_workspace(B, H, H_kv, S, D, rope);
+  char* wb = static_cast<char*>(workspace);
+  p.delta = reinterpret_cast<float*>(wb + ws.delta);
+  p.lse2 = reinterpret_cast<float*>(wb + ws.lse2);
+  p.do16 = wb + ws.do16;
+  p.qr16 = (rope != AF_ROPE_NONE) ? wb + ws.qr16 : nullptr;
+  p.kr16 = (rope != AF_ROPE_NONE) ? wb + ws.kr16 : nullptr;
+  p.B = B; p.H = H; p.Hkv = H_kv; p.S = S;
+  // a window of S or more keys is the causal mask; clamping keeps n + window in int range
+  p.window = (mask == AF_MASK_SLIDING_WINDOW) ? (window < S ? window : S) : 0;
+  p.slopes = alibi_slopes;
+  p.scale = softmax_scale;
+  p.table = nullptr;
+  if (sparse) {
+    p.bq_ptr = sparse[0]; p.bk_idx = sparse[1];
+    p.bk_ptr = sparse[2]; p.bq_idx = sparse[3];
+  }
+  if (rope != AF_ROPE_NONE && (rc = rope_table(D, rope_theta, S, st, &p.table)) != AF_OK) return rc;
+  const bool alibi = alibi_slopes != nullptr;
+  if (dtype == AF_DTYPE_FP32) return map_launch(af::launch_bwd_fp32(D, rope, mask, alibi, p, st));
+  return map_launch(af::launch_bwd_bf16(D, rope, mask, alibi, p, st));
+}
+
 }  // namespace
 
 extern "C" {
@@ -149,28 +231,22 @@ int attnfuse_fwd(const void* Q, const void* K, const void* V, void* O, float* LS
                  int B, int H, int H_kv, int S, int D, int dtype,
                  int rope, float rope_theta, int mask, int window,
                  const float* alibi_slopes, float softmax_scale, void* stream) {
-  if (!Q || !K || !V || !O || !LSE) return AF_ERR_INVALID_ARG;
-  if (!aligned16(Q) || !aligned16(K) || !aligned16(V) || !aligned16(O) || !aligned16(LSE)) return AF_ERR_INVALID_ARG;
-  if (O == Q || O == K || O == V || (const void*)LSE == Q || (const void*)LSE == K || (const void*)LSE == V)
-    return AF_ERR_INVALID_ARG;
-  int rc = check_common(B, H, H_kv, S, D, dtype, rope, rope_theta);
-  if (rc != AF_OK) return rc;
-  if ((rc = check_attn(mask, window, softmax_scale)) != AF_OK) return rc;
-  if (!supported_d(D)) return AF_ERR_UNSUPPORTED;
+  return fwd_impl(Q, K, V, O, LSE, nullptr, nullptr, B, H, H_kv, S, D, dtype, rope, rope_theta, mask, window,
+                  alibi_slopes, softmax_scale, stream);
+}
 
-  hipStream_t st = static_cast<hipStream_t>(stream);
-  af::FwdParams p{};
-  p.q = Q; p.k = K; p.v = V; p.o = O; p.lse = LSE;
-  p.B = B; p.H = H; p.Hkv = H_kv; p.S = S;
-  // a window of S or more keys is the causal mask; clamping keeps n + window in int range
-  p.window = (mask == AF_MASK_SLIDING_WINDOW) ? (window < S ? window : S) : 0;
-  p.slopes = alibi_slopes;
-  p.scale = softmax_scale;
-  p.table = nullptr;
-  if (rope != AF_ROPE_NONE && (rc = rope_table(D, rope_theta, S, st, &p.table)) != AF_OK) return rc;
-  const bool alibi = alibi_slopes != nullptr;
-  if (dtype == AF_DTYPE_BF16) return map_launch(af::launch_fwd_bf16(D, rope, mask, alibi, p, st));
-  return map_launch(af::launch_fwd_fp32(D, rope, mask, alibi, p, st));
+int attnfuse_fwd_blocksparse(const void* Q, const void* K, const void* V, void* O, float* LSE,
+                             const int* q_block_ptr, const int* k_block_idx,
+                             int B, int H, int H_kv, int S, int D, int dtype,
+                             int rope, float rope_theta, int mask, int window,
+                             const float* alibi_slopes, float softmax_scale, void* stream) {
+  if (!q_block_ptr || !k_block_idx || !aligned4(q_block_ptr) || !aligned4(k_block_idx)) return AF_ERR_INVALID_ARG;
+  const void* outs[] = {O, LSE};
+  for (const void* x : outs)
+    if (x == (const void*)q_block_ptr || x == (const void*)k_block_idx) return AF_ERR_INVALID_ARG;
+  if (S < 1 || S > kMaxSparseS) return AF_ERR_INVALID_ARG;
+  return fwd_impl(Q, K, V, O, LSE, q_block_ptr, k_block_idx, B, H, H_kv, S, D, dtype, rope, rope_theta, mask,
+                  window, alibi_slopes, softmax_scale, stream);
 }
 
 size_t attnfuse_bwd_workspace_bytes(int B, int H, int H_kv, int S, int D, int rope) {
@@ -185,39 +261,26 @@ int attnfuse_bwd(const void* Q, const void* K, const void* V, const void* O, con
                  int B, int H, int H_kv, int S, int D, int dtype,
                  int rope, float rope_theta, int mask, int window,
                  const float* alibi_slopes, float softmax_scale, void* stream) {
-  const void* ins[] = {Q, K, V, O, dO, LSE};
-  void* outs[] = {dQ, dK, dV, workspace};
-  for (const void* x : ins) if (!x || !aligned16(x)) return AF_ERR_INVALID_ARG;
-  for (const void* x : outs) if (!x || !aligned16(x)) return AF_ERR_INVALID_ARG;
-  for (const void* x : outs)
-    for (const void* y : ins) if (x == y) return AF_ERR_INVALID_ARG;
-  int rc = check_common(B, H, H_kv, S, D, dtype, rope, rope_theta);
-  if (rc != AF_OK) return rc;
-  if ((rc = check_attn(mask, window, softmax_scale)) != AF_OK) return rc;
-  if (workspace_bytes < attnfuse_bwd_workspace_bytes(B, H, H_kv, S, D, rope)) return AF_ERR_INVALID_ARG;
-  if (!supported_d(D)) return AF_ERR_UNSUPPORTED;
+  return bwd_impl(Q, K, V, O, dO, LSE, dQ, dK, dV, nullptr, workspace, workspace_bytes, B, H, H_kv, S, D, dtype,
+                  rope, rope_theta, mask, window, alibi_slopes, softmax_scale, stream);
+}
 
-  hipStream_t st = static_cast<hipStream_t>(stream);
-  af::BwdParams p{};
-  p.q = Q; p.k = K; p.v = V; p.o = O; p.dout = dO; p.lse = LSE;
-  p.dq = dQ; p.dk = dK; p.dv = dV;
-  const BwdWorkspace ws = bwd_workspace(B, H, H_kv, S, D, rope);
-  char* wb = static_cast<char*>(workspace);
-  p.delta = reinterpret_cast<float*>(wb + ws.delta);
-  p.lse2 = reinterpret_cast<float*>(wb + ws.lse2);
-  p.do16 = wb + ws.do16;
-  p.qr16 = (rope != AF_ROPE_NONE) ? wb + ws.qr16 : nullptr;
-  p.kr16 = (rope != AF_ROPE_NONE) ? wb + ws.kr16 : nullptr;
-  p.B = B; p.H = H; p.Hkv = H_kv; p.S = S;
-  // a window of S or more keys is the causal mask; clamping keeps n + window in int range
-  p.window = (mask == AF_MASK_SLIDING_WINDOW) ? (window < S ? window : S) : 0;
-  p.slopes = alibi_slopes;
-  p.scale = softmax_scale;
-  p.table = nullptr;
-  if (rope != AF_ROPE_NONE && (rc = rope_table(D, rope_theta, S, st, &p.table)) != AF_OK) return rc;
-  const bool alibi = alibi_slopes != nullptr;
-  if (dtype == AF_DTYPE_FP32) return map_launch(af::launch_bwd_fp32(D, rope, mask, alibi, p, st));
-  return map_launch(af::launch_bwd_bf16(D, rope, mask, alibi, p, st));
+int attnfuse_bwd_blocksparse(const void* Q, const void* K, const void* V, const void* O, const void* dO,
+                             const float* LSE, void* dQ, void* dK, void* dV,
+                             const int* q_block_ptr, const int* k_block_idx,
+                             const int* k_block_ptr, const int* q_block_idx,
+                             void* workspace, size_t workspace_bytes,
+                             int B, int H, int H_kv, int S, int D, int dtype,
+                             int rope, float rope_theta, int mask, int window,
+                             const float* alibi_slopes, float softmax_scale, void* stream) {
+  const int* m[] = {q_block_ptr, k_block_idx, k_block_ptr, q_block_idx};
+  for (const int* x : m) if (!x || !aligned4(x)) return AF_ERR_INVALID_ARG;
+  const void* outs[] = {dQ, dK, dV, workspace};
+  for (const void* x : outs)
+    for (const int* y : m) if (x == (const void*)y) return AF_ERR_INVALID_ARG;
+  if (S < 1 || S > kMaxSparseS) return AF_ERR_INVALID_ARG;
+  return bwd_impl(Q, K, V, O, dO, LSE, dQ, dK, dV, m, workspace, workspace_bytes, B, H, H_kv, S, D, dtype, rope,
+                  rope_theta, mask, window, alibi_slopes, softmax_scale, stream);
 }
 
 // ---------------------------------------------------------------- decode

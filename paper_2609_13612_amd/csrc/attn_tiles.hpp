@@ -125,6 +125,75 @@ __device__ __forceinline__ void tile_commit(TileRegs<D, ROPE>& R, uint16_t* __re
   tile_commit_v<D, ROPE>(R, Vs, tid);
 }
 
+// ---------------------------------------------------------------- block-sparse tile lists
+// Largest number of 64-wide blocks along the sequence a block-sparse launch
+// accepts (S <= 131072); the host rejects longer sequences.
+constexpr int SPARSE_MAX_BLOCKS = 2048;
+
+// LDS for one workgroup's list of active tiles.
+struct TileList {
+  uint32_t member[SPARSE_MAX_BLOCKS / 4];   // per block: bit j set when list row j holds it (one byte each)
+  uint16_t tile[SPARSE_MAX_BLOCKS];         // the active blocks, ascending
+  uint8_t rows[SPARSE_MAX_BLOCKS];          // and their row bits
+  int wave_total[8];                        // compaction: active blocks per wave's share
+};
+
+// The ascending union of the compressed rows r0 .. r0+nr-1 (nr <= 8) of a
+// block mask (ptr [rows+1], idx: each row's active blocks), restricted to
+// blocks in [lo, hi) (the range the elementwise mask can reach), with a bit
+// per row saying which rows hold each block.  Entries are clamped into
+// [0, nb) so a malformed mask cannot index outside the tiles.  Every thread
+// of the workgroup must call it; it returns the count after a barrier, and
+// L.tile / L.rows are then valid.
+template <int THREADS>
+__device__ int build_tile_list(TileList& L, const int* __restrict__ ptr, const int* __restrict__ idx, int r0,
+                               int nr, int nb, int lo, int hi, int tid) {
+  for (int w = tid; w < (nb + 3) / 4; w += THREADS) L.member[w] = 0u;
+  __syncthreads();
+  for (int j = 0; j < nr; ++j) {
+    const int e0 = ptr[r0 + j], e1 = ptr[r0 + j + 1];
+    for (int e = e0 + tid; e < e1; e += THREADS) {
+      const int b = min(max(idx[e], 0), nb - 1);
+      if (b >= lo && b < hi) atomicOr(&L.member[b >> 2], (1u << j) << (8 * (b & 3)));
+    }
+  }
+  __syncthreads();
+  // compaction: thread t owns blocks [t*per, (t+1)*per); its output position is
+  // the number of active blocks owned by lower threads (a scan within the wave,
+  // then the totals of the lower waves)
+  static_assert(THREADS % 64 == 0 && THREADS <= 512, "whole waves, at most eight");
+  const int per = (nb + THREADS - 1) / THREADS;
+  auto byte_of = [&](int b) { return (L.member[b >> 2] >> (8 * (b & 3))) & 0xffu; };
+  int cnt = 0;
+  for (int b = tid * per; b < min(nb, (tid + 1) * per); ++b) cnt += byte_of(b) != 0u;
+  const int lane = tid & 63, wave = tid >> 6;
+  int incl = cnt;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const int x = __shfl_up(incl, off, 64);
+    if (lane >= off) incl += x;
+  }
+  if (lane == 63) L.wave_total[wave] = incl;
+  __syncthreads();
+  int pos = incl - cnt, total = 0;
+#pragma unroll
+  for (int w = 0; w < THREADS / 64; ++w) {
+    const int x = L.wave_total[w];
+    pos += (w < wave) ? x : 0;
+    total += x;
+  }
+  for (int b = tid * per; b < min(nb, (tid + 1) * per); ++b) {
+    const uint32_t m = byte_of(b);
+    if (m != 0u) {
+      L.tile[pos] = (uint16_t)b;
+      L.rows[pos] = (uint8_t)m;
+      ++pos;
+    }
+  }
+  __syncthreads();
+  return total;
+}
+
 // Query heads packed per workgroup by the forward and the dQ kernel: the
 // largest power of two <= 8 dividing the GQA group size.
 inline int heads_per_wg(int G) {

@@ -21,14 +21,19 @@
 // contractions over queries/keys read a transposed LDS copy stored with the
 // perm16 row order that matches the score tile's register order.
 //
-// Precision follows the forward: with RoPE the rotated Q' and K' (and dS,
-// which multiplies them) are fp16 MFMA operands, so P is re-derived from the
-// same rounded operands that produced the forward's LSE; without RoPE every
-// MFMA operand is bf16.  dV = P^T dO sums P over many queries without
-// normalisation, so it runs on fp16 operands (P and dO, the latter converted
-// exactly from bf16 when its transposed copy is staged); this bounds the
-// accumulated rounding of P at 2^-12 per term and needs |dO| < 65504.
-// dP = dO V^T uses the bf16 inputs as they are.
+// Precision: Q', K' and dS are fp16 MFMA operands.  With RoPE the rotated
+// Q' and K' are the fp16 values the forward's scores came from, so P is
+// re-derived from the same rounded operands that produced its LSE; without
+// RoPE, Q and K are converted exactly from bf16 as they are staged.  dS in
+// fp16 (2^-12 relative rounding instead of bf16's 2^-9) keeps the sums
+// dK = dS^T Q and dQ = dS K accurate when attention concentrates on a few
+// keys and their gradients grow.  dV = P^T dO sums P over many queries
+// without normalisation, so it also runs on fp16 operands (P and dO, the
+// latter converted exactly from bf16).  All of this needs |Q|, |K|, |dO| and
+// |dS| below the fp16 maximum 65504.  dP = dO V^T uses the bf16 inputs as
+// they are.
+#include <type_traits>
+
 #include "attn_tiles.hpp"
 #include "launch.hpp"
 
@@ -201,8 +206,8 @@ __device__ __forceinline__ u32x4 tr_operand(const uint16_t* tile, int pitch, int
 
 // ---------------------------------------------------------------- dK / dV
 // Query-side tile of the dK/dV kernel: 64 query rows of Q' (fp16, rotated by
-// the preprocessing kernel) or Q (bf16, without RoPE) and of dO (fp16), plus
-// their LSE (log2 units) and delta.  Staging is a plain copy.
+// the preprocessing kernel) or Q (bf16, converted to fp16 as it is staged)
+// and of dO (fp16), plus their LSE (log2 units) and delta.
 template <int D>
 struct QTileCfg {
   static constexpr int NW = 8;                // two waves per SIMD
@@ -250,7 +255,8 @@ __device__ __forceinline__ void qtile_load(QTileRegs<D>& R, const uint16_t* __re
   R.del = in ? dl : 0.f;
 }
 
-template <int D>
+// TO_F16: Q arrives as bf16 (no RoPE) and is converted as it is staged.
+template <int D, bool TO_F16>
 __device__ __forceinline__ void qtile_commit(const QTileRegs<D>& R, uint16_t* __restrict__ Qs,
                                              uint16_t* __restrict__ Os, float* __restrict__ lse2s,
                                              float* __restrict__ dels, int tid) {
@@ -260,7 +266,12 @@ __device__ __forceinline__ void qtile_commit(const QTileRegs<D>& R, uint16_t* __
     const int it = tid + C::THREADS * i;
     if (C::ITEMS % C::THREADS != 0 && it >= C::ITEMS) break;
     const int r = it / (D / 8), c = it % (D / 8);
-    *reinterpret_cast<u32x4*>(Qs + r * C::QP + 8 * c) = R.q[i];
+    u32x4 q = R.q[i];
+    if constexpr (TO_F16) {
+#pragma unroll
+      for (int w = 0; w < 4; ++w) q[w] = pack_f16(bf_lo(q[w]), bf_hi(q[w]));
+    }
+    *reinterpret_cast<u32x4*>(Qs + r * C::QP + 8 * c) = q;
     *reinterpret_cast<u32x4*>(Os + r * C::QP + 8 * c) = R.o[i];
   }
   if (tid < C::BQ) {
@@ -276,10 +287,10 @@ __device__ __forceinline__ void qtile_commit(const QTileRegs<D>& R, uint16_t* __
 // The block's K' rows (B operand of S = Q' K'^T) and V rows (fp16, B operand
 // of dP = dO V^T) stay resident in LDS, leaving the registers to the dK/dV
 // accumulators.
-template <int D, int ROPE, int MASK, bool ALIBI>
+template <int D, int ROPE, int MASK, bool ALIBI, bool SPARSE>
 __global__ __launch_bounds__(512) void bwd_dkdv_kernel(BwdParams p) {
   using C = QTileCfg<D>;
-  constexpr bool QF16 = ROPE != ROPE_NONE;   // rotated operands (and dS with them) in fp16
+  constexpr bool ROT = ROPE != ROPE_NONE;    // Q' and K' come rotated (fp16) from the workspace
   constexpr int SMEM = 2 * C::STAGE + 2 * C::V_ELEMS;
   static_assert(SMEM * 2 >= 4 * 16 * C::MT * 64 * 4, "the partial-sum exchange reuses the staging memory");
   __shared__ __attribute__((aligned(16))) uint16_t smem[SMEM];
@@ -301,7 +312,7 @@ __global__ __launch_bounds__(512) void bwd_dkdv_kernel(BwdParams p) {
 
   // K' (fp16, rotated by the preprocessing kernel) or K (bf16) as is, and V
   // converted to fp16; rows past S clamped (their results are not stored)
-  const uint16_t* Kg = static_cast<const uint16_t*>(QF16 ? p.kr16 : p.k) + (size_t)bg * S * D;
+  const uint16_t* Kg = static_cast<const uint16_t*>(ROT ? p.kr16 : p.k) + (size_t)bg * S * D;
   const uint16_t* Vg = static_cast<const uint16_t*>(p.v) + (size_t)bg * S * D;
   constexpr int VITEMS = C::KEYS * (D / 8);
 #pragma unroll
@@ -310,9 +321,12 @@ __global__ __launch_bounds__(512) void bwd_dkdv_kernel(BwdParams p) {
     const int r = it / (D / 8), c = it % (D / 8);
     const size_t off = (size_t)min(nb + r, S - 1) * D + 8 * c;
     u32x4 v = ld16(Vg + off);
-    const u32x4 k = ld16(Kg + off);
+    u32x4 k = ld16(Kg + off);
 #pragma unroll
-    for (int w = 0; w < 4; ++w) v[w] = pack_f16(bf_lo(v[w]), bf_hi(v[w]));
+    for (int w = 0; w < 4; ++w) {
+      v[w] = pack_f16(bf_lo(v[w]), bf_hi(v[w]));
+      if constexpr (!ROT) k[w] = pack_f16(bf_lo(k[w]), bf_hi(k[w]));
+    }
     *reinterpret_cast<u32x4*>(Vs + r * C::VP + 8 * c) = v;
     *reinterpret_cast<u32x4*>(Ks + r * C::VP + 8 * c) = k;
   }
@@ -327,14 +341,27 @@ __global__ __launch_bounds__(512) void bwd_dkdv_kernel(BwdParams p) {
   int tq_begin = 0, tq_end = ntq;
   if constexpr (MASK != MASK_NONE) tq_begin = nb / C::BQ;
   if constexpr (MASK == MASK_SLIDING_WINDOW) tq_end = min(ntq, (min(nb + C::KEYS - 1, S - 1) + W - 1) / C::BQ + 1);
-  const int nq = max(0, tq_end - tq_begin);
+  // Query tiles by position: tq_begin + i, or under a block-sparse mask the
+  // union of the active query blocks of the workgroup's two 64-key blocks
+  // (the mask by key block), with a bit per key block saying which hold it.
+  __shared__ std::conditional_t<SPARSE, TileList, int> tl;
+  int nq = max(0, tq_end - tq_begin);
+  const int jw = kw >> 1;             // this wave's 64-key block within the workgroup
+  if constexpr (SPARSE) {
+    const int r0 = nb / C::BQ, r1 = (min(nb + C::KEYS, S) - 1) / C::BQ;
+    nq = __builtin_amdgcn_readfirstlane(build_tile_list<C::THREADS>(tl, p.bk_ptr, p.bq_idx, r0, r1 - r0 + 1, ntq,
+                                                                    tq_begin, tq_end, tid));
+  }
   const int steps = G * nq;           // (query head of the group, query tile) pairs
 
   auto head_of = [&](int s) { return g * G + s / nq; };
-  auto tile_of = [&](int s) { return tq_begin + s % nq; };
+  auto tile_of = [&](int s) -> int {
+    if constexpr (SPARSE) return __builtin_amdgcn_readfirstlane((int)tl.tile[s % nq]);
+    else return tq_begin + s % nq;
+  };
   auto src = [&](int s, const uint16_t*& Qh, const uint16_t*& dOh, const float*& l2, const float*& dl) {
     const size_t bh = (size_t)b * p.H + head_of(s);
-    Qh = static_cast<const uint16_t*>(QF16 ? p.qr16 : p.q) + bh * S * D;
+    Qh = static_cast<const uint16_t*>(ROT ? p.qr16 : p.q) + bh * S * D;
     dOh = static_cast<const uint16_t*>(p.do16) + bh * S * D;
     l2 = p.lse2 + bh * S;
     dl = p.delta + bh * S;
@@ -346,7 +373,7 @@ __global__ __launch_bounds__(512) void bwd_dkdv_kernel(BwdParams p) {
     const float *l2, *dl;
     src(0, Qh, dOh, l2, dl);
     qtile_load<D>(R, Qh, dOh, l2, dl, tile_of(0) * C::BQ, S, tid);
-    qtile_commit<D>(R, smem, smem + C::Q_ELEMS, stat[0][0], stat[0][1], tid);
+    qtile_commit<D, !ROT>(R, smem, smem + C::Q_ELEMS, stat[0][0], stat[0][1], tid);
   }
   __syncthreads();
 
@@ -369,6 +396,7 @@ __global__ __launch_bounds__(512) void bwd_dkdv_kernel(BwdParams p) {
     const float slope2 = ALIBI ? p.slopes[h] * kLog2e : 0.f;
 
     bool visible = nw < S;
+    if constexpr (SPARSE) visible = visible && ((tl.rows[s % nq] >> jw) & 1);
     if constexpr (MASK != MASK_NONE) visible = visible && (mq + 31 >= nw);
     if constexpr (MASK == MASK_SLIDING_WINDOW) visible = visible && (mq <= nw + 31 + W - 1);
     if (visible) {
@@ -384,7 +412,7 @@ __global__ __launch_bounds__(512) void bwd_dkdv_kernel(BwdParams p) {
         const u32x4 ao = *reinterpret_cast<const u32x4*>(Os + (32 * qt + lq) * C::QP + 16 * k + 8 * lg);
         const u32x4 bk = *reinterpret_cast<const u32x4*>(Ks + (32 * kw + lq) * C::VP + 16 * k + 8 * lg);
         const u32x4 bv = *reinterpret_cast<const u32x4*>(Vs + (32 * kw + lq) * C::VP + 16 * k + 8 * lg);
-        sc = mfma32<QF16>(aq, bk, sc);
+        sc = mfma32<true>(aq, bk, sc);
         dp = mfma32<true>(ao, bv, dp);
       }
       // element r: query mq + 8 (r/4) + 4 lg + r%4, key n
@@ -422,7 +450,7 @@ __global__ __launch_bounds__(512) void bwd_dkdv_kernel(BwdParams p) {
 #pragma unroll
         for (int w = 0; w < 4; ++w) {
           pb[hf][w] = pack_f16(pr[8 * hf + 2 * w], pr[8 * hf + 2 * w + 1]);
-          db[hf][w] = pack_op<QF16>(ds[8 * hf + 2 * w], ds[8 * hf + 2 * w + 1]);
+          db[hf][w] = pack_f16(ds[8 * hf + 2 * w], ds[8 * hf + 2 * w + 1]);
         }
       // dV^T += dO^T P and dK'^T += Q'^T dS (transposed operands from row-major tiles)
 #pragma unroll
@@ -430,14 +458,14 @@ __global__ __launch_bounds__(512) void bwd_dkdv_kernel(BwdParams p) {
 #pragma unroll
         for (int mt = 0; mt < C::MT; ++mt) {
           dv[mt] = mfma32<true>(tr_operand(Os, C::QP, 32 * qt + 16 * hf, 32 * mt, lane), pb[hf], dv[mt]);
-          dk[mt] = mfma32<QF16>(tr_operand(Qs, C::QP, 32 * qt + 16 * hf, 32 * mt, lane), db[hf], dk[mt]);
+          dk[mt] = mfma32<true>(tr_operand(Qs, C::QP, 32 * qt + 16 * hf, 32 * mt, lane), db[hf], dk[mt]);
         }
       }
     }
 
     if (more) {
       const int sn = (s + 1) & 1;
-      qtile_commit<D>(R, smem + sn * C::STAGE, smem + sn * C::STAGE + C::Q_ELEMS, stat[sn][0], stat[sn][1], tid);
+      qtile_commit<D, !ROT>(R, smem + sn * C::STAGE, smem + sn * C::STAGE + C::Q_ELEMS, stat[sn][0], stat[sn][1], tid);
     }
     __syncthreads();
   }
@@ -471,13 +499,23 @@ __global__ __launch_bounds__(512) void bwd_dkdv_kernel(BwdParams p) {
   }
 }
 
+// Convert a staged K tile's registers from bf16 to fp16 (exact for |k| < 65504).
+template <int D>
+__device__ __forceinline__ void k_to_f16(TileRegs<D, ROPE_NONE>& R) {
+  using C = TileCfg<D, ROPE_NONE>;
+#pragma unroll
+  for (int i = 0; i < C::KPT; ++i)
+#pragma unroll
+    for (int w = 0; w < 4; ++w) R.ka[i][w] = pack_f16(bf_lo(R.ka[i][w]), bf_hi(R.ka[i][w]));
+}
+
 // ---------------------------------------------------------------- dQ
 // Same decomposition as the forward: 8 waves, GQA heads packed, double-buffered
 // K'/V tiles (attn_tiles.hpp); dQ'^T += K'^T dS^T with K'^T from transpose reads.
-template <int D, int ROPE, int MASK, bool ALIBI>
+template <int D, int ROPE, int MASK, bool ALIBI, bool SPARSE>
 __global__ __launch_bounds__(512) void bwd_dq_kernel(BwdParams p) {
-  using C = TileCfg<D, ROPE_NONE>;            // K' arrives rotated: staging is a plain copy
-  constexpr bool QF16 = ROPE != ROPE_NONE;
+  using C = TileCfg<D, ROPE_NONE>;            // K' arrives rotated, or K is converted to fp16 at staging
+  constexpr bool ROT = ROPE != ROPE_NONE;    // Q' and K' come rotated (fp16) from the workspace
   __shared__ __attribute__((aligned(16))) uint16_t smem[2 * C::STAGE];
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, lq = lane & 31, lg = lane >> 5;
@@ -500,14 +538,14 @@ __global__ __launch_bounds__(512) void bwd_dq_kernel(BwdParams p) {
   const int p_end = min(p0 + P, S);
   const size_t bh = (size_t)b * p.H + h;
 
-  const uint16_t* Qh = static_cast<const uint16_t*>(QF16 ? p.qr16 : p.q) + bh * S * D;
+  const uint16_t* Qh = static_cast<const uint16_t*>(ROT ? p.qr16 : p.q) + bh * S * D;
   const uint16_t* dOh = static_cast<const uint16_t*>(p.dout) + bh * S * D;
-  const uint16_t* Kg = static_cast<const uint16_t*>(QF16 ? p.kr16 : p.k) + (size_t)bg * S * D;
+  const uint16_t* Kg = static_cast<const uint16_t*>(ROT ? p.kr16 : p.k) + (size_t)bg * S * D;
   const uint16_t* Vg = static_cast<const uint16_t*>(p.v) + (size_t)bg * S * D;
 
   u32x4 qreg[C::KS], oreg[C::KS];
   const int mc = min(m, S - 1);   // rows past S compute on row S-1 and are never stored
-  load_row_operand<D, ROPE_NONE>(qreg, Qh, nullptr, mc, S, lg);
+  load_row_operand<D, ROPE_NONE, !ROT>(qreg, Qh, nullptr, mc, S, lg);
   load_row_operand<D, ROPE_NONE>(oreg, dOh, nullptr, mc, S, lg);
   const float lse2 = (m < S) ? p.lse2[bh * S + mc] : INFINITY;
   const float del = (m < S) ? p.delta[bh * S + mc] : 0.f;
@@ -524,21 +562,39 @@ __global__ __launch_bounds__(512) void bwd_dq_kernel(BwdParams p) {
   if constexpr (MASK != MASK_NONE) t_end = min(ntiles, (p_end - 1) / C::BN + 1);
   if constexpr (MASK == MASK_SLIDING_WINDOW) t_begin = max(0, p0 - W + 1) / C::BN;
 
+  // Key tiles by position i: t_begin + i, or under a block-sparse mask the
+  // union of the workgroup's query blocks' active key blocks (as the forward).
+  __shared__ std::conditional_t<SPARSE, TileList, int> tl;
+  int ntl = t_end - t_begin;
+  int jw = 0;
+  if constexpr (SPARSE) {
+    const int r0 = p0 / C::BN, r1 = (p_end - 1) / C::BN;
+    ntl = __builtin_amdgcn_readfirstlane(build_tile_list<C::THREADS>(tl, p.bq_ptr, p.bk_idx, r0, r1 - r0 + 1,
+                                                                     ntiles, t_begin, t_end, tid));
+    jw = mw / C::BN - r0;
+  }
+  auto tile_at = [&](int i) -> int {
+    if constexpr (SPARSE) return __builtin_amdgcn_readfirstlane((int)tl.tile[i]);
+    else return t_begin + i;
+  };
+
   TileRegs<D, ROPE_NONE> R;
-  if (t_begin < t_end) {
-    tile_load<D, ROPE_NONE>(R, Kg, Vg, nullptr, t_begin * C::BN, S, tid);
+  if (ntl > 0) {
+    tile_load<D, ROPE_NONE>(R, Kg, Vg, nullptr, tile_at(0) * C::BN, S, tid);
+    if constexpr (!ROT) k_to_f16(R);
     tile_commit<D, ROPE_NONE>(R, smem, smem + C::K_ELEMS, tid);
   }
   __syncthreads();
 
-  for (int t = t_begin; t < t_end; ++t) {
-    const int n0 = t * C::BN;
-    const uint16_t* Ks = smem + ((t - t_begin) & 1) * C::STAGE;
+  for (int t = 0; t < ntl; ++t) {
+    const int n0 = tile_at(t) * C::BN;
+    const uint16_t* Ks = smem + (t & 1) * C::STAGE;
     const uint16_t* Vs = Ks + C::K_ELEMS;
-    const bool more = t + 1 < t_end;
-    if (more) tile_load<D, ROPE_NONE>(R, Kg, Vg, nullptr, n0 + C::BN, S, tid);
+    const bool more = t + 1 < ntl;
+    if (more) tile_load<D, ROPE_NONE>(R, Kg, Vg, nullptr, tile_at(t + 1) * C::BN, S, tid);
 
     bool visible = mw < S;
+    if constexpr (SPARSE) visible = visible && ((tl.rows[t] >> jw) & 1);
     if constexpr (MASK != MASK_NONE) visible = visible && (n0 <= mw + 31);
     if constexpr (MASK == MASK_SLIDING_WINDOW) visible = visible && (n0 + C::BN - 1 > mw - W);
     if (visible) {
@@ -552,7 +608,7 @@ __global__ __launch_bounds__(512) void bwd_dq_kernel(BwdParams p) {
         for (int k = 0; k < C::KS; ++k) {
           const u32x4 ak = *reinterpret_cast<const u32x4*>(Ks + (32 * kt + lq) * C::KP + 16 * k + 8 * lg);
           const u32x4 av = *reinterpret_cast<const u32x4*>(Vs + (32 * kt + lq) * C::VP + 16 * k + 8 * lg);
-          sc = mfma32<QF16>(ak, qreg[k], sc);
+          sc = mfma32<true>(ak, qreg[k], sc);
           dp = mfma32(av, oreg[k], dp);
         }
         // element r: key nn = n0 + 32 kt + 8 (r/4) + 4 lg + r%4, query m
@@ -579,16 +635,17 @@ __global__ __launch_bounds__(512) void bwd_dq_kernel(BwdParams p) {
 #pragma unroll
         for (int hf = 0; hf < 2; ++hf)
 #pragma unroll
-          for (int w = 0; w < 4; ++w) db[hf][w] = pack_op<QF16>(ds[8 * hf + 2 * w], ds[8 * hf + 2 * w + 1]);
+          for (int w = 0; w < 4; ++w) db[hf][w] = pack_f16(ds[8 * hf + 2 * w], ds[8 * hf + 2 * w + 1]);
 #pragma unroll
         for (int mt = 0; mt < C::MT; ++mt)
 #pragma unroll
           for (int hf = 0; hf < 2; ++hf)
-            dq[mt] = mfma32<QF16>(tr_operand(Ks, C::KP, 32 * kt + 16 * hf, 32 * mt, lane), db[hf], dq[mt]);
+            dq[mt] = mfma32<true>(tr_operand(Ks, C::KP, 32 * kt + 16 * hf, 32 * mt, lane), db[hf], dq[mt]);
       }
     }
     if (more) {
-      uint16_t* Kn = smem + ((t + 1 - t_begin) & 1) * C::STAGE;
+      uint16_t* Kn = smem + ((t + 1) & 1) * C::STAGE;
+      if constexpr (!ROT) k_to_f16(R);
       tile_commit<D, ROPE_NONE>(R, Kn, Kn + C::K_ELEMS, tid);
     }
     __syncthreads();
@@ -607,13 +664,23 @@ static int launch_one(const BwdParams& p, hipStream_t st) {
   hipLaunchKernelGGL((bwd_prep_kernel<D, ROPE>), dim3((unsigned)(q_blocks + k_blocks)), dim3(256), 0, st, p, q_blocks);
   using QC = QTileCfg<D>;
   const int nkb = (p.S + QC::KEYS - 1) / QC::KEYS;
-  hipLaunchKernelGGL((bwd_dkdv_kernel<D, ROPE, MASK, ALIBI>), dim3((unsigned)(nkb * p.B * p.Hkv)), dim3(QC::THREADS), 0, st, p);
+  if (p.bk_ptr)
+    hipLaunchKernelGGL((bwd_dkdv_kernel<D, ROPE, MASK, ALIBI, true>), dim3((unsigned)(nkb * p.B * p.Hkv)),
+                       dim3(QC::THREADS), 0, st, p);
+  else
+    hipLaunchKernelGGL((bwd_dkdv_kernel<D, ROPE, MASK, ALIBI, false>), dim3((unsigned)(nkb * p.B * p.Hkv)),
+                       dim3(QC::THREADS), 0, st, p);
   using TC = TileCfg<D, ROPE_NONE>;
   BwdParams pq = p;
   pq.heads_per_wg = heads_per_wg(p.H / p.Hkv);
   const int P = TC::ROWS / pq.heads_per_wg;
   const long long qblocks = (long long)((p.S + P - 1) / P) * p.B * p.Hkv * ((p.H / p.Hkv) / pq.heads_per_wg);
-  hipLaunchKernelGGL((bwd_dq_kernel<D, ROPE, MASK, ALIBI>), dim3((unsigned)qblocks), dim3(TC::THREADS), 0, st, pq);
+  if (p.bq_ptr)
+    hipLaunchKernelGGL((bwd_dq_kernel<D, ROPE, MASK, ALIBI, true>), dim3((unsigned)qblocks), dim3(TC::THREADS), 0, st,
+                       pq);
+  else
+    hipLaunchKernelGGL((bwd_dq_kernel<D, ROPE, MASK, ALIBI, false>), dim3((unsigned)qblocks), dim3(TC::THREADS), 0,
+                       st, pq);
   return hipGetLastError() == hipSuccess ? 0 : -3;
 }
 

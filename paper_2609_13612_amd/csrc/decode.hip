@@ -1,5 +1,5 @@
 // Decode attention over a key/value cache, bf16 inputs, MFMA with fp32
-// accumulation, for gfx950 (Section 2 "Flash Decoding"; Table tab:decode).
+// accumulation, for gfx950 (Section 4.2 "Flash Decoding"; Table tab:decode).
 //
 // One query per sequence makes the work a stream over the cache: each K/V
 // element is used once per query head of its group, so the kernel is bound by

@@ -42,7 +42,7 @@
 
 namespace af {
 
-template <int D, int ROPE, int MASK, bool ALIBI>
+template <int D, int ROPE, int MASK, bool ALIBI, bool SPARSE>
 __global__ __launch_bounds__(512) void fwd_bf16_kernel(FwdParams p) {
   using C = TileCfg<D, ROPE>;
   constexpr bool QF16 = ROPE != ROPE_NONE;
@@ -87,9 +87,26 @@ __global__ __launch_bounds__(512) void fwd_bf16_kernel(FwdParams p) {
   int t_begin = 0, t_end = ntiles;
   if constexpr (MASK != MASK_NONE) t_end = min(ntiles, (p_end - 1) / C::BN + 1);
   if constexpr (MASK == MASK_SLIDING_WINDOW) t_begin = max(0, p0 - W + 1) / C::BN;
-  // LDS stage of key tile X (K' and V); the index is wave-uniform and kept
-  // opaque so per-read offsets fold into the LDS instructions.
-  auto kst = [&](int X) { return smem + __builtin_amdgcn_readfirstlane((X - t_begin) & 1) * C::STAGE; };
+  // The tiles the workgroup visits, by position i: t_begin + i, or under a
+  // block-sparse mask the ascending union of the active key blocks of its
+  // query blocks, with a bit per query block saying which of them hold the
+  // tile (a tile inactive for a wave's own block is computed fully masked).
+  __shared__ std::conditional_t<SPARSE, TileList, int> tl;
+  int ntl = t_end - t_begin;
+  int jw = 0;                                    // this wave's query block among the list rows
+  if constexpr (SPARSE) {
+    const int r0 = p0 / C::BN, r1 = (p_end - 1) / C::BN;
+    ntl = __builtin_amdgcn_readfirstlane(build_tile_list<C::THREADS>(tl, p.bq_ptr, p.bk_idx, r0, r1 - r0 + 1,
+                                                                     ntiles, t_begin, t_end, tid));
+    jw = mw / C::BN - r0;
+  }
+  auto tile_at = [&](int i) -> int {
+    if constexpr (SPARSE) return __builtin_amdgcn_readfirstlane((int)tl.tile[i]);
+    else return t_begin + i;
+  };
+  // LDS stage of the tile at position X (K' and V); the index is wave-uniform
+  // and kept opaque so per-read offsets fold into the LDS instructions.
+  auto kst = [&](int X) { return smem + __builtin_amdgcn_readfirstlane(X & 1) * C::STAGE; };
   auto vst = [&](int X) { return kst(X) + C::K_ELEMS; };
 
   // Query operand (B of S^T = K Q^T): lane holds row m, dims 16s + 8lg .. +7.
@@ -108,20 +125,20 @@ __global__ __launch_bounds__(512) void fwd_bf16_kernel(FwdParams p) {
       rotate_interleaved8<false, true>(qreg[s], p.table + (size_t)mc * (D / 2) + 8 * s + 4 * lg);
   }
 
-  // Prologue: stage K'_{t_begin}, K'_{t_begin+1}, V_{t_begin}; load the
-  // registers of the first in-loop commit (K'_{t_begin+2}, V_{t_begin+1}).
+  // Prologue: stage K' of the first two tiles and V of the first; load the
+  // registers of the first in-loop commit (K' of the third, V of the second).
   TileRegs<D, ROPE> R;
-  for (int X = t_begin; X < min(t_begin + 2, t_end); ++X) {
-    tile_load<D, ROPE>(R, K, V, p.table, X * C::BN, S, tid);
+  for (int X = 0; X < min(2, ntl); ++X) {
+    tile_load<D, ROPE>(R, K, V, p.table, tile_at(X) * C::BN, S, tid);
     tile_commit_k<D, ROPE>(R, kst(X), tid);
-    if (X == t_begin) tile_commit_v<D, ROPE>(R, vst(X), tid);
+    if (X == 0) tile_commit_v<D, ROPE>(R, vst(X), tid);
   }
   // Every global load so far has landed (the commits waited for theirs);
   // saying so explicitly keeps the compiler from guarding the loop's
   // query-operand MFMAs with waits on the staging loads issued in the loop.
   __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0), expcnt and lgkmcnt unconstrained
-  if (t_begin + 2 < t_end) tile_load_k<D, ROPE>(R, K, p.table, (t_begin + 2) * C::BN, S, tid);
-  if (t_begin + 1 < t_end) tile_load_v<D, ROPE>(R, V, (t_begin + 1) * C::BN, S, tid);
+  if (2 < ntl) tile_load_k<D, ROPE>(R, K, p.table, tile_at(2) * C::BN, S, tid);
+  if (1 < ntl) tile_load_v<D, ROPE>(R, V, tile_at(1) * C::BN, S, tid);
 
   f32x16 acc[C::MT];
 #pragma unroll
@@ -178,8 +195,8 @@ __global__ __launch_bounds__(512) void fwd_bf16_kernel(FwdParams p) {
   // the query (rows past S are never stored), so only the unmasked variant
   // tests the sequence end.
   const int lane_off = 4 * lg - lq;
-  auto prepare = [&](f32x16 (&sc)[2], int t) {
-    const int n0 = t * C::BN;
+  auto prepare = [&](f32x16 (&sc)[2], int i) {
+    const int n0 = tile_at(i) * C::BN;
     const int dq = n0 - mw + lane_off;        // key - query of element offset 0
     if constexpr (ALIBI) {
       const float fb = slope2 * (float)dq;
@@ -208,6 +225,12 @@ __global__ __launch_bounds__(512) void fwd_bf16_kernel(FwdParams p) {
           if constexpr (MASK == MASK_SLIDING_WINDOW) ok = ok && (dq + W > -cr);
           sc[kt][r] = ok ? sc[kt][r] : -INFINITY;
         }
+    }
+    if constexpr (SPARSE) {
+      if (((tl.rows[i] >> jw) & 1) == 0) {   // wave-uniform: block inactive for this wave's rows
+#pragma unroll
+        for (int kt = 0; kt < 2; ++kt) sc[kt] = f32x16{} - INFINITY;
+      }
     }
     float mx = -INFINITY;
 #pragma unroll
@@ -268,14 +291,14 @@ __global__ __launch_bounds__(512) void fwd_bf16_kernel(FwdParams p) {
   f32x16 sa[2], sb[2];
   u32x4 pop[2][2];
   __syncthreads();
-  if (t_begin < t_end) {
-    scores(sa, kst(t_begin));
-    prepare(sa, t_begin);
+  if (ntl > 0) {
+    scores(sa, kst(0));
+    prepare(sa, 0);
     raise();
   }
-  // The first iteration stages K'_{t_begin+2} into the stage just read.
+  // The first iteration stages the third tile's K' into the stage just read.
   __syncthreads();
-  int t = t_begin;
+  int t = 0;   // position in the tile list
   auto iteration = [&](f32x16 (&cur)[2], f32x16 (&nxt)[2]) {
     // A
     probs(cur, pop);
@@ -287,24 +310,24 @@ __global__ __launch_bounds__(512) void fwd_bf16_kernel(FwdParams p) {
     pv(pop, vst(t));
     tile_commit_k<D, ROPE>(R, kst(t + 2), tid);
     tile_commit_v<D, ROPE>(R, vst(t + 1), tid);
-    tile_load_k<D, ROPE>(R, K, p.table, min(t + 3, t_end - 1) * C::BN, S, tid);
-    tile_load_v<D, ROPE>(R, V, min(t + 2, t_end - 1) * C::BN, S, tid);
+    tile_load_k<D, ROPE>(R, K, p.table, tile_at(min(t + 3, ntl - 1)) * C::BN, S, tid);
+    tile_load_v<D, ROPE>(R, V, tile_at(min(t + 2, ntl - 1)) * C::BN, S, tid);
     raise();
     __syncthreads();
     ++t;
   };
   // two iterations per trip so the score buffers alternate without copies
-  while (t + 2 < t_end) {
+  while (t + 2 < ntl) {
     iteration(sa, sb);
     iteration(sb, sa);
   }
-  if (t + 1 < t_end) {
+  if (t + 1 < ntl) {
     iteration(sa, sb);
     probs(sb, pop);
-  } else if (t < t_end) {
+  } else if (t < ntl) {
     probs(sa, pop);
   }
-  if (t < t_end) pv(pop, vst(t));
+  if (t < ntl) pv(pop, vst(t));
 
   // Epilogue: O = acc / l, LSE = (m + log2 l) ln 2.
   const float l_tot = pair_sum(l_run);
@@ -331,7 +354,12 @@ static int launch_one(const FwdParams& p0, hipStream_t st) {
   p.heads_per_wg = heads_per_wg(p.H / p.Hkv);
   const int P = C::ROWS / p.heads_per_wg;
   const long long blocks = (long long)((p.S + P - 1) / P) * p.B * p.Hkv * ((p.H / p.Hkv) / p.heads_per_wg);
-  hipLaunchKernelGGL((fwd_bf16_kernel<D, ROPE, MASK, ALIBI>), dim3((unsigned)blocks), dim3(C::THREADS), 0, st, p);
+  if (p.bq_ptr)
+    hipLaunchKernelGGL((fwd_bf16_kernel<D, ROPE, MASK, ALIBI, true>), dim3((unsigned)blocks), dim3(C::THREADS), 0, st,
+                       p);
+  else
+    hipLaunchKernelGGL((fwd_bf16_kernel<D, ROPE, MASK, ALIBI, false>), dim3((unsigned)blocks), dim3(C::THREADS), 0,
+                       st, p);
   return hipGetLastError() == hipSuccess ? 0 : -3;
 }
 

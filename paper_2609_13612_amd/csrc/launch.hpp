@@ -17,6 +17,8 @@ struct FwdParams {
   float scale;
   const float2* table;    // [rows >= S][D/2] (cos, sin); nullptr without RoPE
   int heads_per_wg;       // set by the bf16 launcher: query heads packed per workgroup
+  const int* bq_ptr;      // block-sparse mask by 64-row query block (CSR row pointers), or nullptr
+  const int* bk_idx;      // and the active 64-key blocks of each row
 };
 
 struct BwdParams {
@@ -39,6 +41,10 @@ struct BwdParams {
   float scale;
   const float2* table;
   int heads_per_wg;       // set by the launcher for the dQ kernel
+  const int* bq_ptr;      // block-sparse mask by 64-row query block (CSR), or nullptr
+  const int* bk_idx;
+  const int* bk_ptr;      // the same mask by 64-key block (CSC), or nullptr
+  const int* bq_idx;
 };
 
 struct DecodeParams {

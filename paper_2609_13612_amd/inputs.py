@@ -6,7 +6,10 @@ tensors from a CPU ``torch.Generator`` in a fixed order -- Q, K, V, then dO
 the storage dtype (bf16 rounds to nearest even).
 Both sides of a parity check consume exactly these values: the HIP path after
 a copy to the GPU, the oracle after an exact upcast to fp64.
+Block-sparse patterns are bool matrices over (query block, key block), drawn
+from a numpy ``Generator`` of their own seed.
 """
+import numpy as np
 import torch
 
 DTYPES = {"bf16": torch.bfloat16, "fp32": torch.float32}
@@ -52,3 +55,31 @@ def alibi_slopes(H):
 def to_f64(t):
     """Exact upcast of a (CPU or GPU) tensor to an fp64 numpy array."""
     return t.detach().to("cpu", torch.float64).numpy()
+
+
+def random_blocks(nb, density, *, seed=0, empty_rows=()):
+    """Bool [nb, nb]: each (query block, key block) active with probability
+    ``density``; the rows listed in ``empty_rows`` have no active block."""
+    rng = np.random.default_rng(seed)
+    active = rng.random((nb, nb)) < density
+    for r in empty_rows:
+        active[r] = False
+    return active
+
+
+def bigbird_blocks(nb, *, window=3, n_global=1, n_random=1, seed=0):
+    """Bool [nb, nb] with the three parts of a BigBird-style mask: a band of
+    ``window`` blocks around the diagonal, ``n_global`` global blocks (the
+    first block rows see every key block and every query block sees the first
+    key blocks), and ``n_random`` further key blocks per query block drawn
+    uniformly from those not yet active."""
+    rng = np.random.default_rng(seed)
+    i = np.arange(nb)
+    active = np.abs(i[:, None] - i[None, :]) <= window // 2
+    active[:n_global, :] = True
+    active[:, :n_global] = True
+    for r in range(nb):
+        free = np.flatnonzero(~active[r])
+        if free.size:
+            active[r, rng.choice(free, size=min(n_random, free.size), replace=False)] = True
+    return active

@@ -21,9 +21,10 @@ def declared_symbols():
 
 
 def test_header_declares_the_boundary():
-    assert declared_symbols() == sorted(["attnfuse_bwd", "attnfuse_bwd_workspace_bytes", "attnfuse_decode",
-                                         "attnfuse_decode_workspace_bytes", "attnfuse_fwd", "attnfuse_rope",
-                                         "attnfuse_rope_bwd", "attnfuse_strerror", "attnfuse_version"])
+    assert declared_symbols() == sorted(["attnfuse_bwd", "attnfuse_bwd_blocksparse", "attnfuse_bwd_workspace_bytes",
+                                         "attnfuse_decode", "attnfuse_decode_workspace_bytes", "attnfuse_fwd",
+                                         "attnfuse_fwd_blocksparse", "attnfuse_rope", "attnfuse_rope_bwd",
+                                         "attnfuse_strerror", "attnfuse_version"])
 
 
 def test_library_loads_and_exports_every_declared_symbol():
@@ -174,3 +175,63 @@ def test_decode_unsupported():
     assert _decode(D=96) == -2
     assert _decode(dtype=1) == -2               # bf16 only
     assert _decode(H=64, H_kv=1) == -2          # more than 32 query heads per K/V head
+
+
+# ----------------------------------------------------------------------------- block-sparse
+MASKP = 0x20000   # 4-byte aligned stand-ins for the device mask lists
+
+
+def _fwd_bs(**over):
+    a = dict(Q=FAKE, K=FAKE + 0x100, V=FAKE + 0x200, O=FAKE + 0x300, LSE=FAKE + 0x400, qp=MASKP, ki=MASKP + 0x100,
+             B=1, H=4, H_kv=2, S=16, D=64, dtype=0, rope=1, theta=10000.0, mask=0, window=0, slopes=None,
+             scale=0.125, stream=None)
+    a.update(over)
+    return _lib.load().attnfuse_fwd_blocksparse(a["Q"], a["K"], a["V"], a["O"], a["LSE"], a["qp"], a["ki"], a["B"],
+                                                a["H"], a["H_kv"], a["S"], a["D"], a["dtype"], a["rope"],
+                                                a["theta"], a["mask"], a["window"], a["slopes"], a["scale"],
+                                                a["stream"])
+
+
+def _bwd_bs(**over):
+    base = FAKE
+    a = dict(Q=base, K=base + 0x100, V=base + 0x200, O=base + 0x300, dO=base + 0x400, LSE=base + 0x500,
+             dQ=base + 0x600, dK=base + 0x700, dV=base + 0x800, qp=MASKP, ki=MASKP + 0x100, kp=MASKP + 0x200,
+             qi=MASKP + 0x300, ws=base + 0x900, ws_bytes=1 << 20, B=1, H=4, H_kv=2, S=16, D=64, dtype=0, rope=1,
+             theta=1e4, mask=0, window=0, slopes=None, scale=0.125, stream=None)
+    a.update(over)
+    return _lib.load().attnfuse_bwd_blocksparse(a["Q"], a["K"], a["V"], a["O"], a["dO"], a["LSE"], a["dQ"], a["dK"],
+                                                a["dV"], a["qp"], a["ki"], a["kp"], a["qi"], a["ws"], a["ws_bytes"],
+                                                a["B"], a["H"], a["H_kv"], a["S"], a["D"], a["dtype"], a["rope"],
+                                                a["theta"], a["mask"], a["window"], a["slopes"], a["scale"],
+                                                a["stream"])
+
+
+INVALID_FWD_BS = [dict(qp=None), dict(ki=None), dict(qp=MASKP + 2), dict(ki=MASKP + 0x101), dict(O=MASKP),
+                  dict(LSE=MASKP + 0x100), dict(S=64 * 2048 + 1), dict(S=0), dict(Q=None), dict(H=3),
+                  dict(mask=2, window=0), dict(scale=0.0)]
+
+
+@pytest.mark.parametrize("over", INVALID_FWD_BS, ids=lambda o: ",".join(f"{k}={v}" for k, v in o.items()))
+def test_fwd_blocksparse_rejects_invalid_arguments(over):
+    assert _fwd_bs(**over) == -1
+
+
+def test_fwd_blocksparse_unsupported():
+    assert _fwd_bs(D=96) == -2
+    assert _fwd_bs(dtype=1) == -2      # bf16 kernels only
+    assert _fwd_bs(dtype=1, Q=None) == -1
+
+
+INVALID_BWD_BS = [dict(qp=None), dict(ki=None), dict(kp=None), dict(qi=None), dict(kp=MASKP + 0x201),
+                  dict(dQ=MASKP), dict(ws=MASKP + 0x300), dict(S=64 * 2048 + 1), dict(ws_bytes=100), dict(dO=None),
+                  dict(H=4, H_kv=3)]
+
+
+@pytest.mark.parametrize("over", INVALID_BWD_BS, ids=lambda o: ",".join(f"{k}={v}" for k, v in o.items()))
+def test_bwd_blocksparse_rejects_invalid_arguments(over):
+    assert _bwd_bs(**over) == -1
+
+
+def test_bwd_blocksparse_unsupported():
+    assert _bwd_bs(D=96) == -2
+    assert _bwd_bs(dtype=1) == -2

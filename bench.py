@@ -20,6 +20,9 @@ Alongside, on the same inputs and outside the timed steps:
 * decode over a KV cache at the paper's three decode geometries (skip with
   --no-decode): median latency and cache bandwidth against the HBM peak, the
   caches rotated through a pool larger than twice the Infinity Cache;
+* block-sparse attention with a BigBird-style mask at N = 4096 (skip with
+  --no-sparse): forward and backward medians, TFLOP/s over the visible pairs,
+  and the dense forward of the same shape for the speedup;
 * a plain device-to-device copy of 512 MiB: the achievable HBM bandwidth next
   to the rotation kernel's, and the calibration kernel for the HBM-traffic
   counters;
@@ -47,6 +50,8 @@ PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
 # The paper's decode latencies on H100 (Table tab:decode), other hardware: context only.
 PAPER_DECODE_MS = {"decode_llama3_8b_h32kv8_cache4096": 0.034, "decode_llama3_70b_h64kv8_cache32768": 0.184,
                    "decode_mistral_7b_h32kv8_cache16384": 0.072}
+# The paper's block-sparse forward latency (BigBird mask, N = 4096), other hardware: context only.
+PAPER_SPARSE_MS = {"bigbird_b4h12s4096d64": 0.084}
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "fwd_llama3_8b_hbm_traffic.json")
 FWD_SOURCES = ("fwd_bf16.hip", "attn_tiles.hpp", "common.hpp")
 
@@ -123,6 +128,7 @@ def parse():
     ap.add_argument("--no-sweep", action="store_true", help="skip the fuse-vs-separate sweep over S")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-decode", action="store_true", help="skip the decode (KV-cache) measurements")
+    ap.add_argument("--no-sparse", action="store_true", help="skip the block-sparse (BigBird mask) measurements")
     ap.add_argument("--seed", type=int, default=0)
     return ap.parse_args()
 
@@ -134,8 +140,8 @@ def main():
         sys.exit(2)
 
     import torch
-    from paper_2609_13612_amd import api, inputs
-    from paper_2609_13612_amd.workloads import DECODE_WORKLOADS, LLAMA_SWEEP_S, WORKLOADS
+    from paper_2609_13612_amd import api, blockmask, inputs
+    from paper_2609_13612_amd.workloads import DECODE_WORKLOADS, LLAMA_SWEEP_S, SPARSE_WORKLOADS, WORKLOADS
 
     w = WORKLOADS[args.workload]
     torch.cuda.set_device(0)
@@ -332,6 +338,52 @@ def main():
             del kv_pool, qd, od, ld, wsd
         torch.cuda.empty_cache()
 
+    # ---------------------------------------------------------------- block-sparse attention
+    sparse = None
+    if not args.no_sparse:
+        sparse = {}
+        for name, sw in SPARSE_WORKLOADS.items():
+            c = inputs.make_qkv(sw.B, sw.H, sw.Hkv, sw.S, sw.D, seed=args.seed, with_do=True)
+            qb, kb, vb, dob = (c[n].to(dev) for n in ("q", "k", "v", "do"))
+            del c
+            active = sw.active()
+            bm = blockmask.block_mask_from_dense(torch.from_numpy(active), sw.S, device=dev)
+            ob, lb = torch.empty_like(qb), torch.empty(sw.B, sw.H, sw.S, device=dev, dtype=torch.float32)
+            grads = (torch.empty_like(qb), torch.empty_like(kb), torch.empty_like(vb))
+            wsb = torch.empty(api.attnfuse_bwd_workspace_bytes(sw.B, sw.H, sw.Hkv, sw.S, sw.D), device=dev,
+                              dtype=torch.uint8)
+            skw = dict(rope="none", mask="none")
+
+            def sp_fwd():
+                api.attnfuse_fwd_blocksparse(qb, kb, vb, bm, out=ob, lse=lb, **skw)
+
+            def sp_bwd():
+                api.attnfuse_bwd_blocksparse(qb, kb, vb, ob, dob, lb, bm, dq=grads[0], dk=grads[1], dv=grads[2],
+                                             workspace=wsb, **skw)
+
+            def dense_fwd():
+                api.attnfuse_fwd(qb, kb, vb, out=ob, lse=lb, **skw)
+
+            res = {}
+            # in this order the backward reads the block-sparse forward's O and LSE
+            for label, fn in (("dense_fwd", dense_fwd), ("fwd", sp_fwd), ("bwd", sp_bwd)):
+                for _ in range(10):
+                    fn()
+                res[label] = statistics.median(time_calls(fn, 50))
+            f_tf = sw.fwd_flops(active) / (res["fwd"] * 1e-3) / 1e12
+            b_tf = sw.bwd_flops(active) / (res["bwd"] * 1e-3) / 1e12
+            sparse[name] = {"B": sw.B, "H": sw.H, "H_kv": sw.Hkv, "S": sw.S, "D": sw.D, "block": 64,
+                            "active_blocks": int(active.sum()), "density": round(float(active.mean()), 4),
+                            "fwd_ms": round(res["fwd"], 4), "fwd_tflops": round(f_tf, 1),
+                            "bwd_ms": round(res["bwd"], 4), "bwd_tflops": round(b_tf, 1),
+                            "dense_fwd_ms": round(res["dense_fwd"], 4),
+                            "fwd_speedup_vs_dense": round(res["dense_fwd"] / res["fwd"], 3),
+                            "paper_fwd_ms": PAPER_SPARSE_MS.get(name)}
+            log(f"block-sparse {name}: density {active.mean():.4f}, fwd {res['fwd']:.4f} ms ({f_tf:.0f} TF/s), "
+                f"bwd {res['bwd']:.4f} ms, dense fwd {res['dense_fwd']:.4f} ms")
+            del qb, kb, vb, dob, ob, lb, grads, wsb, bm
+        torch.cuda.empty_cache()
+
     # ---------------------------------------------------------------- CPU oracle baseline
     cpu_baseline = None
     if not args.no_cpu_baseline:
@@ -390,6 +442,8 @@ def main():
         line["crossover_model"] = crossover
     if decode is not None:
         line["decode"] = decode
+    if sparse is not None:
+        line["block_sparse"] = sparse
     print(json.dumps(line), flush=True)
 
 

@@ -135,8 +135,9 @@ int attnfuse_bwd(const void* Q, const void* K, const void* V, const void* O, con
  *                k_block_idx[q_block_ptr[r] .. q_block_ptr[r+1]-1];
  *                q_block_ptr[0] = 0, non-decreasing
  *   k_block_idx  device int32 [q_block_ptr[nb]]: key-block indices in [0, nb)
- *                (any order; duplicates allowed; entries outside [0, nb) are
- *                clamped into it)
+ *                (any order, duplicates allowed; rows strictly ascending, the
+ *                canonical form, are read fastest; entries outside [0, nb)
+ *                are ignored)
  * Both 4-byte aligned, caller-owned, read only.  The pointer array must be a
  * valid CSR offset list: it is read on the device, and offsets outside
  * k_block_idx are not detected (the Python binding builds and checks it).

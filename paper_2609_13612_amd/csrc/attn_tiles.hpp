@@ -130,31 +130,41 @@ __device__ __forceinline__ void tile_commit(TileRegs<D, ROPE>& R, uint16_t* __re
 // accepts (S <= 131072); the host rejects longer sequences.
 constexpr int SPARSE_MAX_BLOCKS = 2048;
 
-// LDS for one workgroup's list of active tiles.
+// LDS for one workgroup's list of active tiles: the block indices, ascending,
+// and (for lists that merge several rows) which of the rows hold each block.
+template <bool ROWS>
 struct TileList {
-  uint32_t member[SPARSE_MAX_BLOCKS / 4];   // per block: bit j set when list row j holds it (one byte each)
-  uint16_t tile[SPARSE_MAX_BLOCKS];         // the active blocks, ascending
-  uint8_t rows[SPARSE_MAX_BLOCKS];          // and their row bits
-  int wave_total[8];                        // compaction: active blocks per wave's share
+  uint16_t tile[SPARSE_MAX_BLOCKS];
+  uint8_t rows[SPARSE_MAX_BLOCKS];
 };
+template <>
+struct TileList<false> {
+  uint16_t tile[SPARSE_MAX_BLOCKS];
+};
+// LDS the list construction needs only while it runs (2080 bytes): a byte per
+// block marking the rows that hold it, and one count per wave.
+constexpr int TILE_LIST_SCRATCH_BYTES = SPARSE_MAX_BLOCKS + 8 * 4;
 
 // The ascending union of the compressed rows r0 .. r0+nr-1 (nr <= 8) of a
 // block mask (ptr [rows+1], idx: each row's active blocks), restricted to
 // blocks in [lo, hi) (the range the elementwise mask can reach), with a bit
-// per row saying which rows hold each block.  Entries are clamped into
-// [0, nb) so a malformed mask cannot index outside the tiles.  Every thread
-// of the workgroup must call it; it returns the count after a barrier, and
-// L.tile / L.rows are then valid.
-template <int THREADS>
-__device__ int build_tile_list(TileList& L, const int* __restrict__ ptr, const int* __restrict__ idx, int r0,
-                               int nr, int nb, int lo, int hi, int tid) {
-  for (int w = tid; w < (nb + 3) / 4; w += THREADS) L.member[w] = 0u;
+// per row saying which rows hold each block (stored only when ROWS).  Entries
+// outside [lo, hi), which contains only valid blocks, are ignored, so a
+// malformed mask cannot index outside the tiles.  ``scratch`` is TILE_LIST_SCRATCH_BYTES of 4-byte aligned LDS that is
+// free until the call returns.  Every thread of the workgroup must call it; it
+// returns the count after a barrier, and the list is then valid.
+template <int THREADS, bool ROWS>
+__device__ int build_tile_list(TileList<ROWS>& L, void* scratch, const int* __restrict__ ptr,
+                               const int* __restrict__ idx, int r0, int nr, int nb, int lo, int hi, int tid) {
+  uint32_t* member = static_cast<uint32_t*>(scratch);   // one byte per block
+  int* wave_total = reinterpret_cast<int*>(member + SPARSE_MAX_BLOCKS / 4);
+  for (int w = tid; w < (nb + 3) / 4; w += THREADS) member[w] = 0u;
   __syncthreads();
   for (int j = 0; j < nr; ++j) {
     const int e0 = ptr[r0 + j], e1 = ptr[r0 + j + 1];
     for (int e = e0 + tid; e < e1; e += THREADS) {
-      const int b = min(max(idx[e], 0), nb - 1);
-      if (b >= lo && b < hi) atomicOr(&L.member[b >> 2], (1u << j) << (8 * (b & 3)));
+      const int b = idx[e];
+      if (b >= lo && b < hi) atomicOr(&member[b >> 2], (1u << j) << (8 * (b & 3)));
     }
   }
   __syncthreads();
@@ -163,7 +173,7 @@ __device__ int build_tile_list(TileList& L, const int* __restrict__ ptr, const i
   // then the totals of the lower waves)
   static_assert(THREADS % 64 == 0 && THREADS <= 512, "whole waves, at most eight");
   const int per = (nb + THREADS - 1) / THREADS;
-  auto byte_of = [&](int b) { return (L.member[b >> 2] >> (8 * (b & 3))) & 0xffu; };
+  auto byte_of = [&](int b) { return (member[b >> 2] >> (8 * (b & 3))) & 0xffu; };
   int cnt = 0;
   for (int b = tid * per; b < min(nb, (tid + 1) * per); ++b) cnt += byte_of(b) != 0u;
   const int lane = tid & 63, wave = tid >> 6;
@@ -173,12 +183,12 @@ __device__ int build_tile_list(TileList& L, const int* __restrict__ ptr, const i
     const int x = __shfl_up(incl, off, 64);
     if (lane >= off) incl += x;
   }
-  if (lane == 63) L.wave_total[wave] = incl;
+  if (lane == 63) wave_total[wave] = incl;
   __syncthreads();
   int pos = incl - cnt, total = 0;
 #pragma unroll
   for (int w = 0; w < THREADS / 64; ++w) {
-    const int x = L.wave_total[w];
+    const int x = wave_total[w];
     pos += (w < wave) ? x : 0;
     total += x;
   }
@@ -186,12 +196,51 @@ __device__ int build_tile_list(TileList& L, const int* __restrict__ ptr, const i
     const uint32_t m = byte_of(b);
     if (m != 0u) {
       L.tile[pos] = (uint16_t)b;
-      L.rows[pos] = (uint8_t)m;
+      if constexpr (ROWS) L.rows[pos] = (uint8_t)m;
       ++pos;
     }
   }
   __syncthreads();
   return total;
+}
+
+// The list of ONE compressed row r (restricted to [lo, hi)), read directly
+// when the row is strictly ascending (the canonical form, which needs no
+// sorting or duplicate removal): wave 0 streams the row, keeps the entries in
+// range in order and checks the order on the way.  Any other row goes through
+// build_tile_list.  ``scratch`` as there, plus 8 more bytes.  Every thread of
+// the workgroup must call it; the list is valid when it returns.
+template <int THREADS>
+__device__ int tile_list_of_row(TileList<false>& L, void* scratch, const int* __restrict__ ptr,
+                                const int* __restrict__ idx, int r, int nb, int lo, int hi, int tid) {
+  int* res = reinterpret_cast<int*>(static_cast<char*>(scratch) + TILE_LIST_SCRATCH_BYTES);
+  if (tid < 64) {
+    const int e0 = ptr[r], e1 = ptr[r + 1];
+    int n = 0;
+    bool ordered = true;
+    for (int e = e0 + tid; e - tid < e1; e += 64) {
+      const bool live = e < e1;
+      const int x = live ? idx[e] : 0;
+      const int nxt = (e + 1 < e1) ? idx[e + 1] : 0x7fffffff;
+      ordered = ordered && __ballot(live && x >= nxt) == 0ull;
+      const bool in = live && x >= lo && x < hi;
+      const unsigned long long bits = __ballot(in);
+      const int pos = n + __popcll(bits & ((1ull << tid) - 1ull));
+      if (in && pos < SPARSE_MAX_BLOCKS) L.tile[pos] = (uint16_t)x;
+      n += __popcll(bits);
+    }
+    if (tid == 0) {
+      res[0] = n;
+      res[1] = ordered;
+    }
+  }
+  __syncthreads();
+  const int n = res[0], ordered = res[1];
+  // every thread holds the result before anyone reuses the scratch memory
+  // (the fallback below, or the caller's staging)
+  __syncthreads();
+  if (!ordered) return build_tile_list<THREADS>(L, scratch, ptr, idx, r, 1, nb, lo, hi, tid);
+  return n;
 }
 
 // Query heads packed per workgroup by the forward and the dQ kernel: the

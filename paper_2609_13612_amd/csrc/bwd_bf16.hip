@@ -344,13 +344,13 @@ __global__ __launch_bounds__(512) void bwd_dkdv_kernel(BwdParams p) {
   // Query tiles by position: tq_begin + i, or under a block-sparse mask the
   // union of the active query blocks of the workgroup's two 64-key blocks
   // (the mask by key block), with a bit per key block saying which hold it.
-  __shared__ std::conditional_t<SPARSE, TileList, int> tl;
+  __shared__ std::conditional_t<SPARSE, TileList<true>, int> tl;
   int nq = max(0, tq_end - tq_begin);
   const int jw = kw >> 1;             // this wave's 64-key block within the workgroup
-  if constexpr (SPARSE) {
+  if constexpr (SPARSE) {             // the query staging memory serves as scratch: nothing is staged yet
     const int r0 = nb / C::BQ, r1 = (min(nb + C::KEYS, S) - 1) / C::BQ;
-    nq = __builtin_amdgcn_readfirstlane(build_tile_list<C::THREADS>(tl, p.bk_ptr, p.bq_idx, r0, r1 - r0 + 1, ntq,
-                                                                    tq_begin, tq_end, tid));
+    nq = __builtin_amdgcn_readfirstlane(build_tile_list<C::THREADS>(tl, smem, p.bk_ptr, p.bq_idx, r0, r1 - r0 + 1,
+                                                                    ntq, tq_begin, tq_end, tid));
   }
   const int steps = G * nq;           // (query head of the group, query tile) pairs
 
@@ -564,12 +564,12 @@ __global__ __launch_bounds__(512) void bwd_dq_kernel(BwdParams p) {
 
   // Key tiles by position i: t_begin + i, or under a block-sparse mask the
   // union of the workgroup's query blocks' active key blocks (as the forward).
-  __shared__ std::conditional_t<SPARSE, TileList, int> tl;
+  __shared__ std::conditional_t<SPARSE, TileList<true>, int> tl;
   int ntl = t_end - t_begin;
   int jw = 0;
-  if constexpr (SPARSE) {
+  if constexpr (SPARSE) {             // the staging memory serves as scratch: nothing is staged yet
     const int r0 = p0 / C::BN, r1 = (p_end - 1) / C::BN;
-    ntl = __builtin_amdgcn_readfirstlane(build_tile_list<C::THREADS>(tl, p.bq_ptr, p.bk_idx, r0, r1 - r0 + 1,
+    ntl = __builtin_amdgcn_readfirstlane(build_tile_list<C::THREADS>(tl, smem, p.bq_ptr, p.bk_idx, r0, r1 - r0 + 1,
                                                                      ntiles, t_begin, t_end, tid));
     jw = mw / C::BN - r0;
   }

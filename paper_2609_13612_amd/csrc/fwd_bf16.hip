@@ -46,7 +46,7 @@ template <int D, int ROPE, int MASK, bool ALIBI, bool SPARSE>
 __global__ __launch_bounds__(512) void fwd_bf16_kernel(FwdParams p) {
   using C = TileCfg<D, ROPE>;
   constexpr bool QF16 = ROPE != ROPE_NONE;
-  __shared__ __attribute__((aligned(16))) uint16_t smem[2 * C::STAGE];
+  __shared__ __attribute__((aligned(16))) uint16_t smem[(SPARSE ? 4 : 2) * C::STAGE];
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -58,21 +58,39 @@ __global__ __launch_bounds__(512) void fwd_bf16_kernel(FwdParams p) {
   // with that count a multiple of 8 every block of one K/V head lands on the
   // same XCD and shares its L2.
   const int HP = p.heads_per_wg;                 // query heads per workgroup
-  const int WPH = C::NW / HP;                    // waves per head
-  const int P = 32 * WPH;                        // positions per workgroup
   const int G = p.H / p.Hkv;
   const int groups = G / HP;
   const int units = p.B * p.Hkv * groups;
-  const int npb = (S + P - 1) / P;
   const int unit = blockIdx.x % units;
-  const int pb = npb - 1 - (int)(blockIdx.x / units);
   const int hg = unit % groups, bg = unit / groups;
   const int b = bg / p.Hkv, g = bg % p.Hkv;
-  const int h = g * G + hg * HP + wave / WPH;
-  const int p0 = pb * P;
-  const int mw = p0 + 32 * (wave % WPH);         // first query row of this wave
+  int h, p0, mw, p_end;
+  int kg = 0;                                    // block-sparse: this wave's key group
+  if constexpr (SPARSE) {
+    // One 64-row query block; wave = (head hh, row half rh, key group kg).
+    // The 4 / HP key groups take turns over the block's list of active tiles.
+    const int ksplit = 4 / HP;
+    kg = wave % ksplit;
+    const int rh = (wave / ksplit) & 1, hh = wave / (2 * ksplit);
+    const int nqb = (S + C::BN - 1) / C::BN;
+    const int slot = (int)(blockIdx.x / units);
+    // under a causal or window mask the last blocks have the longest lists
+    const int qb = (MASK == MASK_NONE) ? slot : nqb - 1 - slot;
+    h = g * G + hg * HP + hh;
+    p0 = qb * C::BN;
+    mw = p0 + 32 * rh;
+    p_end = min(p0 + C::BN, S);
+  } else {
+    const int WPH = C::NW / HP;                  // waves per head
+    const int P = 32 * WPH;                      // positions per workgroup
+    const int npb = (S + P - 1) / P;
+    const int pb = npb - 1 - (int)(blockIdx.x / units);
+    h = g * G + hg * HP + wave / WPH;
+    p0 = pb * P;
+    mw = p0 + 32 * (wave % WPH);                 // first query row of this wave
+    p_end = min(p0 + P, S);
+  }
   const int m = mw + lq;                         // this lane's query row
-  const int p_end = min(p0 + P, S);
 
   const size_t bh = (size_t)b * p.H + h;
   const uint16_t* __restrict__ Q = static_cast<const uint16_t*>(p.q) + bh * S * D;
@@ -88,25 +106,18 @@ __global__ __launch_bounds__(512) void fwd_bf16_kernel(FwdParams p) {
   if constexpr (MASK != MASK_NONE) t_end = min(ntiles, (p_end - 1) / C::BN + 1);
   if constexpr (MASK == MASK_SLIDING_WINDOW) t_begin = max(0, p0 - W + 1) / C::BN;
   // The tiles the workgroup visits, by position i: t_begin + i, or under a
-  // block-sparse mask the ascending union of the active key blocks of its
-  // query blocks, with a bit per query block saying which of them hold the
-  // tile (a tile inactive for a wave's own block is computed fully masked).
-  __shared__ std::conditional_t<SPARSE, TileList, int> tl;
-  int ntl = t_end - t_begin;
-  int jw = 0;                                    // this wave's query block among the list rows
-  if constexpr (SPARSE) {
-    const int r0 = p0 / C::BN, r1 = (p_end - 1) / C::BN;
-    ntl = __builtin_amdgcn_readfirstlane(build_tile_list<C::THREADS>(tl, p.bq_ptr, p.bk_idx, r0, r1 - r0 + 1,
-                                                                     ntiles, t_begin, t_end, tid));
-    jw = mw / C::BN - r0;
-  }
+  // block-sparse mask the ascending active key blocks of its query block
+  // (within the same range).
+  __shared__ std::conditional_t<SPARSE, TileList<false>, int> tl;
+  int ntl = t_end - t_begin;   // (block-sparse: set once the query loads are in flight)
   auto tile_at = [&](int i) -> int {
     if constexpr (SPARSE) return __builtin_amdgcn_readfirstlane((int)tl.tile[i]);
     else return t_begin + i;
   };
-  // LDS stage of the tile at position X (K' and V); the index is wave-uniform
+  // LDS stage of the tile at position X (K' and V): X & 1, or under a
+  // block-sparse mask the slot X of the key groups.  The index is wave-uniform
   // and kept opaque so per-read offsets fold into the LDS instructions.
-  auto kst = [&](int X) { return smem + __builtin_amdgcn_readfirstlane(X & 1) * C::STAGE; };
+  auto kst = [&](int X) { return smem + __builtin_amdgcn_readfirstlane(SPARSE ? X : (X & 1)) * C::STAGE; };
   auto vst = [&](int X) { return kst(X) + C::K_ELEMS; };
 
   // Query operand (B of S^T = K Q^T): lane holds row m, dims 16s + 8lg .. +7.
@@ -115,6 +126,9 @@ __global__ __launch_bounds__(512) void fwd_bf16_kernel(FwdParams p) {
   u32x4 qreg[C::KS];
 #pragma unroll
   for (int s = 0; s < C::KS; ++s) qreg[s] = ld16(Q + (size_t)mc * D + 16 * s + 8 * lg);
+  if constexpr (SPARSE)   // the staging slots serve as scratch: nothing is staged yet
+    ntl = __builtin_amdgcn_readfirstlane(
+        tile_list_of_row<C::THREADS>(tl, smem, p.bq_ptr, p.bk_idx, p0 / C::BN, ntiles, t_begin, t_end, tid));
   if constexpr (ROPE == ROPE_NEOX) {
 #pragma unroll
     for (int s = 0; s < C::KS / 2; ++s)
@@ -128,17 +142,19 @@ __global__ __launch_bounds__(512) void fwd_bf16_kernel(FwdParams p) {
   // Prologue: stage K' of the first two tiles and V of the first; load the
   // registers of the first in-loop commit (K' of the third, V of the second).
   TileRegs<D, ROPE> R;
-  for (int X = 0; X < min(2, ntl); ++X) {
-    tile_load<D, ROPE>(R, K, V, p.table, tile_at(X) * C::BN, S, tid);
-    tile_commit_k<D, ROPE>(R, kst(X), tid);
-    if (X == 0) tile_commit_v<D, ROPE>(R, vst(X), tid);
+  if constexpr (!SPARSE) {
+    for (int X = 0; X < min(2, ntl); ++X) {
+      tile_load<D, ROPE>(R, K, V, p.table, tile_at(X) * C::BN, S, tid);
+      tile_commit_k<D, ROPE>(R, kst(X), tid);
+      if (X == 0) tile_commit_v<D, ROPE>(R, vst(X), tid);
+    }
+    // Every global load so far has landed (the commits waited for theirs);
+    // saying so explicitly keeps the compiler from guarding the loop's
+    // query-operand MFMAs with waits on the staging loads issued in the loop.
+    __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0), expcnt and lgkmcnt unconstrained
+    if (2 < ntl) tile_load_k<D, ROPE>(R, K, p.table, tile_at(2) * C::BN, S, tid);
+    if (1 < ntl) tile_load_v<D, ROPE>(R, V, tile_at(1) * C::BN, S, tid);
   }
-  // Every global load so far has landed (the commits waited for theirs);
-  // saying so explicitly keeps the compiler from guarding the loop's
-  // query-operand MFMAs with waits on the staging loads issued in the loop.
-  __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0), expcnt and lgkmcnt unconstrained
-  if (2 < ntl) tile_load_k<D, ROPE>(R, K, p.table, tile_at(2) * C::BN, S, tid);
-  if (1 < ntl) tile_load_v<D, ROPE>(R, V, tile_at(1) * C::BN, S, tid);
 
   f32x16 acc[C::MT];
 #pragma unroll
@@ -226,12 +242,6 @@ __global__ __launch_bounds__(512) void fwd_bf16_kernel(FwdParams p) {
           sc[kt][r] = ok ? sc[kt][r] : -INFINITY;
         }
     }
-    if constexpr (SPARSE) {
-      if (((tl.rows[i] >> jw) & 1) == 0) {   // wave-uniform: block inactive for this wave's rows
-#pragma unroll
-        for (int kt = 0; kt < 2; ++kt) sc[kt] = f32x16{} - INFINITY;
-      }
-    }
     float mx = -INFINITY;
 #pragma unroll
     for (int kt = 0; kt < 2; ++kt)
@@ -279,59 +289,137 @@ __global__ __launch_bounds__(512) void fwd_bf16_kernel(FwdParams p) {
     asm volatile("" : "+v"(pp[0][0]), "+v"(pp[0][1]), "+v"(pp[1][0]), "+v"(pp[1][1]), "+v"(l));
   };
 
-  // Software pipeline, one barrier per tile.  Entering iteration t the scores
-  // of tile t are prepared (masked, max merged, O rescaled).  Part A issues
-  // tile t+1's score MFMAs together with tile t's exp2 / sum / bf16 packing;
-  // part B issues tile t's PV MFMAs together with staging (K'_{t+2} rotated,
-  // V_{t+1}) and tile t+1's mask and max.  Within each part the MFMA and VALU
-  // streams are independent, so every wave keeps the matrix core and the
-  // vector ALU busy at once.  Tile X lives in LDS stage X & 1: iteration t
-  // reads K'_{t+1} and V_t and writes K'_{t+2} and V_{t+1}, so within an
-  // iteration no stage half is both read and written.
-  f32x16 sa[2], sb[2];
   u32x4 pop[2][2];
-  __syncthreads();
-  if (ntl > 0) {
-    scores(sa, kst(0));
-    prepare(sa, 0);
-    raise();
-  }
-  // The first iteration stages the third tile's K' into the stage just read.
-  __syncthreads();
-  int t = 0;   // position in the tile list
-  auto iteration = [&](f32x16 (&cur)[2], f32x16 (&nxt)[2]) {
-    // A
-    probs(cur, pop);
-    scores(nxt, kst(t + 1));
-    pin_values(pop, l_run);   // keep the softmax work in this part
-    // B.  Staging past the last tile rewrites a stage nobody reads any more
-    // (clamped rows), which keeps this part free of branches.
-    prepare(nxt, t + 1);
-    pv(pop, vst(t));
-    tile_commit_k<D, ROPE>(R, kst(t + 2), tid);
-    tile_commit_v<D, ROPE>(R, vst(t + 1), tid);
-    tile_load_k<D, ROPE>(R, K, p.table, tile_at(min(t + 3, ntl - 1)) * C::BN, S, tid);
-    tile_load_v<D, ROPE>(R, V, tile_at(min(t + 2, ntl - 1)) * C::BN, S, tid);
-    raise();
+  if constexpr (SPARSE) {
+    // Block-sparse: each round the workgroup commits the next 4 / HP tiles of
+    // the list into their own slots and then every wave computes the slot of
+    // its key group: scores, mask and max, softmax, PV in sequence (the other
+    // wave of the SIMD overlaps them).  The tiles travel through NR register
+    // sets; the next round's first NR tiles are loaded before this round's
+    // barrier, so their latency overlaps the compute.
+    const int ksplit = 4 / HP;
+    constexpr int NR = 2;
+    TileRegs<D, ROPE> RS[NR];
+    auto load_tile = [&](TileRegs<D, ROPE>& X, int pos) {
+      tile_load<D, ROPE>(X, K, V, p.table, tile_at(pos) * C::BN, S, tid);
+    };
+#pragma unroll
+    for (int j = 0; j < NR; ++j)
+      if (j < min(ksplit, ntl)) load_tile(RS[j], j);
+    f32x16 sc[2];
+    for (int base = 0; base < ntl; base += ksplit) {
+      const int nt = min(ksplit, ntl - base);   // wave-uniform
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        if (j < nt) {
+          tile_commit<D, ROPE>(RS[j % NR], kst(j), vst(j), tid);
+          if (j + NR < nt) load_tile(RS[j % NR], base + j + NR);
+        }
+      }
+      const int next = base + ksplit, nt2 = min(ksplit, ntl - next);
+#pragma unroll
+      for (int j = 0; j < NR; ++j)
+        if (j < nt2) load_tile(RS[j], next + j);
+      __syncthreads();
+      if (kg < nt && mw < S) {   // wave-uniform
+        scores(sc, kst(kg));
+        prepare(sc, base + kg);
+        raise();
+        probs(sc, pop);
+        pv(pop, vst(kg));
+      }
+      __syncthreads();
+    }
+    // Merge the key groups' partial states (m, l, O) into key group 0: the
+    // others hand theirs over through LDS, indexed [wave][element][lane].
+    if (ksplit > 1) {
+      constexpr int NE = 2 + 16 * C::MT;   // floats per lane: m, l, O
+      static_assert(C::NW * NE * 64 * 4 <= 4 * C::STAGE * 2, "the merge reuses the four staging slots");
+      float* xch = reinterpret_cast<float*>(smem);
+      if (kg != 0) {
+        float* dst = xch + wave * NE * 64 + lane;
+        dst[0] = m_run;
+        dst[64] = l_run;
+#pragma unroll
+        for (int mt = 0; mt < C::MT; ++mt)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) dst[(2 + 16 * mt + r) * 64] = acc[mt][r];
+      }
+      __syncthreads();
+      if (kg == 0) {
+        float m_tot = m_run;
+        for (int j = 1; j < ksplit; ++j) m_tot = fmaxf(m_tot, xch[(wave + j) * NE * 64 + lane]);
+        const float a0 = (m_run == -INFINITY) ? 0.f : fast_exp2(m_run - m_tot);
+        l_run *= a0;
+#pragma unroll
+        for (int mt = 0; mt < C::MT; ++mt) acc[mt] *= a0;
+        for (int j = 1; j < ksplit; ++j) {
+          const float* src = xch + (wave + j) * NE * 64 + lane;
+          const float mj = src[0];
+          const float aj = (mj == -INFINITY) ? 0.f : fast_exp2(mj - m_tot);
+          l_run += aj * src[64];
+#pragma unroll
+          for (int mt = 0; mt < C::MT; ++mt)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[mt][r] += aj * src[(2 + 16 * mt + r) * 64];
+        }
+        m_run = m_tot;
+      }
+    }
+  } else {
+    // Software pipeline, one barrier per tile.  Entering iteration t the
+    // scores of tile t are prepared (masked, max merged, O rescaled).  Part A
+    // issues tile t+1's score MFMAs together with tile t's exp2 / sum / bf16
+    // packing; part B issues tile t's PV MFMAs together with staging (K'_{t+2}
+    // rotated, V_{t+1}) and tile t+1's mask and max.  Within each part the
+    // MFMA and VALU streams are independent, so every wave keeps the matrix
+    // core and the vector ALU busy at once.  Tile X lives in LDS stage X & 1:
+    // iteration t reads K'_{t+1} and V_t and writes K'_{t+2} and V_{t+1}, so
+    // within an iteration no stage half is both read and written.
+    f32x16 sa[2], sb[2];
     __syncthreads();
-    ++t;
-  };
-  // two iterations per trip so the score buffers alternate without copies
-  while (t + 2 < ntl) {
-    iteration(sa, sb);
-    iteration(sb, sa);
+    if (ntl > 0) {
+      scores(sa, kst(0));
+      prepare(sa, 0);
+      raise();
+    }
+    // The first iteration stages the third tile's K' into the stage just read.
+    __syncthreads();
+    int t = 0;   // position in the tile list
+    auto iteration = [&](f32x16 (&cur)[2], f32x16 (&nxt)[2]) {
+      // A
+      probs(cur, pop);
+      scores(nxt, kst(t + 1));
+      pin_values(pop, l_run);   // keep the softmax work in this part
+      // B.  Staging past the last tile rewrites a stage nobody reads any more
+      // (clamped rows), which keeps this part free of branches.
+      prepare(nxt, t + 1);
+      pv(pop, vst(t));
+      tile_commit_k<D, ROPE>(R, kst(t + 2), tid);
+      tile_commit_v<D, ROPE>(R, vst(t + 1), tid);
+      tile_load_k<D, ROPE>(R, K, p.table, tile_at(min(t + 3, ntl - 1)) * C::BN, S, tid);
+      tile_load_v<D, ROPE>(R, V, tile_at(min(t + 2, ntl - 1)) * C::BN, S, tid);
+      raise();
+      __syncthreads();
+      ++t;
+    };
+    // two iterations per trip so the score buffers alternate without copies
+    while (t + 2 < ntl) {
+      iteration(sa, sb);
+      iteration(sb, sa);
+    }
+    if (t + 1 < ntl) {
+      iteration(sa, sb);
+      probs(sb, pop);
+    } else if (t < ntl) {
+      probs(sa, pop);
+    }
+    if (t < ntl) pv(pop, vst(t));
   }
-  if (t + 1 < ntl) {
-    iteration(sa, sb);
-    probs(sb, pop);
-  } else if (t < ntl) {
-    probs(sa, pop);
-  }
-  if (t < ntl) pv(pop, vst(t));
 
   // Epilogue: O = acc / l, LSE = (m + log2 l) ln 2.
   const float l_tot = pair_sum(l_run);
-  if (m < S) {
+  if (m < S && kg == 0) {
     const float inv = (l_tot > 0.f) ? 1.f / l_tot : 0.f;
     uint16_t* O = static_cast<uint16_t*>(p.o) + (bh * S + m) * D;
 #pragma unroll
@@ -351,15 +439,20 @@ template <int D, int ROPE, int MASK, bool ALIBI>
 static int launch_one(const FwdParams& p0, hipStream_t st) {
   using C = TileCfg<D, ROPE>;
   FwdParams p = p0;
-  p.heads_per_wg = heads_per_wg(p.H / p.Hkv);
-  const int P = C::ROWS / p.heads_per_wg;
-  const long long blocks = (long long)((p.S + P - 1) / P) * p.B * p.Hkv * ((p.H / p.Hkv) / p.heads_per_wg);
-  if (p.bq_ptr)
+  const int G = p.H / p.Hkv;
+  if (p.bq_ptr) {
+    // block-sparse: one 64-row query block of up to 4 heads per workgroup
+    p.heads_per_wg = heads_per_wg(G) < 4 ? heads_per_wg(G) : 4;
+    const long long blocks = (long long)((p.S + C::BN - 1) / C::BN) * p.B * p.Hkv * (G / p.heads_per_wg);
     hipLaunchKernelGGL((fwd_bf16_kernel<D, ROPE, MASK, ALIBI, true>), dim3((unsigned)blocks), dim3(C::THREADS), 0, st,
                        p);
-  else
+  } else {
+    p.heads_per_wg = heads_per_wg(G);
+    const int P = C::ROWS / p.heads_per_wg;
+    const long long blocks = (long long)((p.S + P - 1) / P) * p.B * p.Hkv * (G / p.heads_per_wg);
     hipLaunchKernelGGL((fwd_bf16_kernel<D, ROPE, MASK, ALIBI, false>), dim3((unsigned)blocks), dim3(C::THREADS), 0,
                        st, p);
+  }
   return hipGetLastError() == hipSuccess ? 0 : -3;
 }
 

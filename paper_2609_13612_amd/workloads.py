@@ -1,9 +1,10 @@
 """Named workload shapes and their algorithmic FLOP / byte counts.
 
 The five prefill workloads are the parity and benchmark shapes of the build,
-and the three decode workloads are the cache geometries of the paper's decode
-table (batch 1, which the table leaves unstated); inputs are seeded N(0, 1)
-tensors (see ``inputs``).  FLOPs count only visible
+the three decode workloads are the cache geometries of the paper's decode
+table (batch 1, which the table leaves unstated), and the block-sparse
+workload is the paper's BigBird case (N = 4096) on the GPT-2-small heads of
+its Ampere comparisons; inputs are seeded N(0, 1) tensors (see ``inputs``).  FLOPs count only visible
 (query, key) pairs: 4*D per pair for the forward (Q K^T and P V) and 10*D for
 the backward (five matmuls: S, dV, dP, dQ, dK), the FlashAttention convention.
 The separate rotation moves 4 bytes per bf16 element of Q and K (read + write).
@@ -98,4 +99,49 @@ DECODE_WORKLOADS = {
                                                           128, theta=500000.0, notes="Llama-3-70B geometry"),
     "decode_mistral_7b_h32kv8_cache16384": DecodeWorkload("decode_mistral_7b_h32kv8_cache16384", 1, 32, 8, 16384,
                                                           128, notes="Mistral-7B geometry"),
+}
+
+
+@dataclass(frozen=True)
+class SparseWorkload:
+    """Block-sparse attention with a BigBird-style block mask (64-position
+    blocks: a band of ``window`` blocks, ``n_global`` global blocks and
+    ``n_random`` random blocks per block row, drawn with ``mask_seed``)."""
+    name: str
+    B: int
+    H: int
+    Hkv: int
+    S: int
+    D: int
+    window: int = 3
+    n_global: int = 1
+    n_random: int = 1
+    mask_seed: int = 0
+    notes: str = field(default="", compare=False)
+
+    def active(self):
+        from . import inputs
+        return inputs.bigbird_blocks((self.S + 63) // 64, window=self.window, n_global=self.n_global,
+                                     n_random=self.n_random, seed=self.mask_seed)
+
+    def visible_pairs(self, active=None):
+        """Visible (query, key) pairs per (batch, head): every active block
+        contributes its rows times its columns (the last block may be short)."""
+        import numpy as np
+        active = self.active() if active is None else active
+        nb = active.shape[0]
+        size = np.full(nb, 64)
+        size[-1] = self.S - 64 * (nb - 1)
+        return int((size[:, None] * size[None, :] * active).sum())
+
+    def fwd_flops(self, active=None):
+        return 4 * self.D * self.B * self.H * self.visible_pairs(active)
+
+    def bwd_flops(self, active=None):
+        return 10 * self.D * self.B * self.H * self.visible_pairs(active)
+
+
+SPARSE_WORKLOADS = {
+    "bigbird_b4h12s4096d64": SparseWorkload("bigbird_b4h12s4096d64", 4, 12, 12, 4096, 64,
+                                            notes="BigBird-style mask at N = 4096, GPT-2-small heads, no RoPE"),
 }

@@ -66,8 +66,10 @@ def test_blocksparse_fwd_bwd_variants(rope, mask, alibi, D):
 
 @pytest.mark.parametrize("H,Hkv", [(2, 2), (8, 2), (16, 2), (8, 1)], ids=lambda x: str(x))
 def test_blocksparse_group_sizes(H, Hkv):
-    """Query heads per workgroup 1, 4, 8 and 8: a workgroup's list is the union
-    of four, one, or half a query block's rows."""
+    """GQA groups of 1, 4, 8 and 8 query heads: the forward's workgroup takes
+    one query block with four, one and one key groups (its partial states
+    merged when several); the dQ pass's list is the union of four, one or half
+    a query block's rows."""
     need_gpu()
     B, S, D = 2, 1000, 128
     announce(f"blocksparse group H={H} Hkv={Hkv}")
@@ -88,7 +90,8 @@ def test_blocksparse_group_sizes(H, Hkv):
                                          (1000, "sliding_window", "interleaved")], ids=lambda x: str(x))
 def test_blocksparse_all_active_matches_dense_bitwise(S, mask, rope):
     """With every block active the tile lists equal the dense ranges, visited in
-    the same order: the results equal the dense kernels' bit for bit."""
+    the same order (four query heads per K/V head, so the forward runs one key
+    group): the results equal the dense kernels' bit for bit."""
     need_gpu()
     B, H, Hkv, D = 1, 8, 2, 128
     window = 200 if mask == "sliding_window" else None
@@ -182,3 +185,42 @@ def test_blocksparse_reports_errors():
     with pytest.raises(api.AttnFuseError) as e:
         api.attnfuse_fwd_blocksparse(dev["q"].float(), dev["k"].float(), dev["v"].float(), bm)
     assert e.value.code == -2                                   # bf16 kernels only
+
+
+def test_blocksparse_noncanonical_lists():
+    """Rows in any order with duplicates, and entries outside [0, nb), describe
+    the same mask as the canonical lists: duplicates count once and invalid
+    entries are ignored (forward through the general list builder, backward
+    through the union builder)."""
+    need_gpu()
+    B, H, Hkv, S, D = 1, 4, 2, 700, 64
+    announce("blocksparse non-canonical lists")
+    cpu, dev = device_inputs(B, H, Hkv, S, D, seed=37, with_do=True)
+    nb = blockmask.num_blocks(S)
+    active = inputs.random_blocks(nb, 0.4, seed=9, empty_rows=(2,))
+    rng = np.random.default_rng(3)
+
+    def scrambled(mat):
+        ptr, idx = [0], []
+        for r in range(mat.shape[0]):
+            row = list(np.flatnonzero(mat[r]))
+            row += list(rng.choice(row, size=min(2, len(row)), replace=False)) if row else []   # duplicates
+            row += [-1, nb + 3] if r % 3 == 0 else []                                       # invalid entries
+            rng.shuffle(row)
+            idx += row
+            ptr.append(len(idx))
+        return (torch.tensor(ptr, dtype=torch.int32, device="cuda"),
+                torch.tensor(idx, dtype=torch.int32, device="cuda"))
+
+    q_ptr, k_idx = scrambled(active)
+    k_ptr, q_idx = scrambled(active.T)
+    bm = blockmask.BlockMask(S, torch.from_numpy(active).cuda(), q_ptr, k_idx, k_ptr, q_idx)
+    o, lse = _fwd(dev, bm, "neox", "causal", None, None)
+    grads = api.attnfuse_bwd_blocksparse(dev["q"], dev["k"], dev["v"], o, dev["do"], lse, bm, rope="neox",
+                                         mask="causal")
+    torch.cuda.synchronize()
+    O, L = _ref_fwd(cpu, bm, "neox", "causal", None, None)
+    assert_bf16_close(o, O, "O")
+    assert_lse_close(lse, L, "LSE")
+    for name, g, r in zip(("dQ", "dK", "dV"), grads, _ref_bwd(cpu, bm, "neox", "causal", None, None)):
+        assert_bf16_close(g, r, name)

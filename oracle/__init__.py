@@ -15,8 +15,9 @@ with the full score matrix materialised per (batch, head):
   "FlashAttention and online softmax"), so the definition is the oracle.
 * RoPE is the pre-matmul rotation (Section 2 "Rotary Position Embeddings",
   Section 4.1 "Fused RoPE").
-* Masks and ALiBi are the post-matmul modifications (Section 3.1, the list of
-  ten combinators).
+* Masks, ALiBi and a dense additive bias are the post-matmul modifications
+  (Section 3.1, the list of ten combinators); relu attention replaces the
+  softmax (the same list).
 * The backward follows the FlashAttention-2 equations; the forward keeps one
   scalar per row, L = m + log l (Section 4.4 "Backward Pass").
 * Decode (one query per sequence against a key/value cache, Section 4.2 "Flash
@@ -40,6 +41,9 @@ from .attention import (
     MASK_CAUSAL,
     MASK_SLIDING_WINDOW,
     MASK_KINDS,
+    NORM_SOFTMAX,
+    NORM_RELU,
+    NORM_KINDS,
     visibility,
     block_visible,
     attention_scores,

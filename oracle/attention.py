@@ -11,15 +11,22 @@ package docstring.  Steps, in the order the method states them:
    masked entries become -inf.  An optional block-sparse mask (Section 4.3,
    "Block-Sparse Attention") additionally hides every key whose (query block,
    key block) pair is inactive.
+   An optional dense bias tensor (the ``additive_bias`` combinator) is added
+   to the scaled score the same way.
 4. Softmax over keys: m_i = max_j s_ij, l_i = sum_j exp(s_ij - m_i),
-   P_ij = exp(s_ij - m_i) / l_i.
-5. O = P V and LSE_i = m_i + ln(l_i) (the one saved scalar per row, Section 4.4).
+   P_ij = exp(s_ij - m_i) / l_i.  The ``relu_attention`` combinator replaces
+   it with P_ij = max(s_ij, 0) (masked entries give 0), unnormalised.
+5. O = P V and LSE_i = m_i + ln(l_i) (the one saved scalar per row, Section 4.4);
+   relu attention has no row statistic.
 
 Backward (FlashAttention-2 equations, split as in Section 4.4):
 dV = P^T dO, dP = dO V^T, delta_i = sum_j P_ij dP_ij (= rowsum(dO o O)),
 dS = P o (dP - delta), dQ' = scale dS K', dK' = scale dS^T Q', and the rotation
 is undone with its transpose: dQ = R^T dQ', dK = R^T dK'.  For grouped-query
-attention the gradients of a shared K/V head sum over its query heads.
+attention the gradients of a shared K/V head sum over its query heads.  Under
+relu attention dS = dP o [s > 0] (the derivative of max(s, 0), taken as 0 at
+s = 0) and there is no delta.  Neither the ALiBi slopes nor the bias tensor
+receive a gradient.
 
 Readings of points the paper leaves open:
 * sliding window of width W keeps keys j with i - W < j <= i (W keys,
@@ -30,7 +37,12 @@ Readings of points the paper leaves open:
 * a row with no visible key gets O = 0 and LSE = -inf;
 * the softmax scale defaults to 1/sqrt(D); LSE is a natural logarithm;
 * queries and keys share positions 0..S-1 (plus an optional common offset,
-  which only moves the RoPE angles).
+  which only moves the RoPE angles);
+* the additive bias is a tensor broadcastable to [B, H, S, S] (query head h),
+  added after the scale and before the mask, exactly like ALiBi;
+* relu attention is P = max(s, 0) with no normalisation (a 1/n factor such as
+  dividing by the sequence length folds into the scale and the bias, since
+  max(a s, 0) = a max(s, 0) for a > 0).
 """
 import numpy as np
 
@@ -40,6 +52,9 @@ MASK_NONE = "none"
 MASK_CAUSAL = "causal"
 MASK_SLIDING_WINDOW = "sliding_window"
 MASK_KINDS = (MASK_NONE, MASK_CAUSAL, MASK_SLIDING_WINDOW)
+NORM_SOFTMAX = "softmax"
+NORM_RELU = "relu"
+NORM_KINDS = (NORM_SOFTMAX, NORM_RELU)
 
 # Rows per chunk when a head's score matrix would not fit comfortably in memory.
 _ROW_CHUNK = 2048
@@ -106,11 +121,11 @@ def _rotated(q, k, rope, theta, pos_offset):
     return rope_rotate(q, pos, theta, rope), rope_rotate(k, pos, theta, rope)
 
 
-def attention_scores(qr_bh, kr_bg, rows, *, mask, window, slope, scale, block_mask=None):
+def attention_scores(qr_bh, kr_bg, rows, *, mask, window, slope, scale, block_mask=None, bias_bh=None):
     """Step 2-3 for one (b, h): scaled scores of the given query rows with bias and mask.
 
-    qr_bh [S, D], kr_bg [S, D] already rotated.  Returns [len(rows), S] fp64
-    with masked entries at -inf.
+    qr_bh [S, D], kr_bg [S, D] already rotated; bias_bh [S, S] or None.
+    Returns [len(rows), S] fp64 with masked entries at -inf.
     """
     S = kr_bg.shape[0]
     rows = np.asarray(rows)
@@ -118,8 +133,37 @@ def attention_scores(qr_bh, kr_bg, rows, *, mask, window, slope, scale, block_ma
     s = scale * (qr_bh[rows] @ kr_bg.T)
     if slope is not None:
         s = s + alibi_bias(slope, rows, cols)
+    if bias_bh is not None:
+        s = s + bias_bh[rows]
     vis = visibility(rows, cols, mask, window, block_mask)
     return np.where(vis, s, -np.inf)
+
+
+def _relu_rows(s):
+    """Step 4 under relu attention: P = max(s, 0); masked entries (-inf) give 0."""
+    return np.maximum(s, 0.0)
+
+
+def _relu_grad(s, dP):
+    """dS under relu attention: dP where the score is positive, else 0."""
+    return np.where(s > 0.0, dP, 0.0)
+
+
+def _bias_of(bias, B, H, S):
+    """The bias tensor broadcast to [B, H, S, S] (a read-only view), or None."""
+    if bias is None:
+        return None
+    bias = np.asarray(bias, dtype=np.float64)
+    try:
+        return np.broadcast_to(bias, (B, H, S, S))
+    except ValueError:
+        raise ValueError("bias must broadcast to [B, H, S, S]") from None
+
+
+def _norm_of(norm):
+    if norm not in NORM_KINDS:
+        raise ValueError(f"unknown norm {norm!r}")
+    return norm
 
 
 def _softmax_rows(s):
@@ -157,13 +201,17 @@ def attention_probs(q, k, b, h, *, rope=ROPE_NONE, theta=10000.0, mask=MASK_CAUS
 
 
 def attention_forward(q, k, v, *, rope=ROPE_NONE, theta=10000.0, mask=MASK_CAUSAL,
-                      window=None, alibi_slopes=None, scale=None, pos_offset=0, block_mask=None):
-    """O [B, H, S, D] and LSE [B, H, S] (natural log), both fp64."""
+                      window=None, alibi_slopes=None, scale=None, pos_offset=0, block_mask=None,
+                      bias=None, norm=NORM_SOFTMAX):
+    """O [B, H, S, D] and LSE [B, H, S] (natural log), both fp64; LSE is None
+    under relu attention."""
     q = np.asarray(q, dtype=np.float64)
     k = np.asarray(k, dtype=np.float64)
     v = np.asarray(v, dtype=np.float64)
     B, H, Hkv, S, D = _check(q, k, v)
     scale, slopes = _defaults(D, scale, alibi_slopes, H)
+    bias = _bias_of(bias, B, H, S)
+    norm = _norm_of(norm)
     qr, kr = _rotated(q, k, rope, theta, pos_offset)
     O = np.zeros((B, H, S, D))
     LSE = np.empty((B, H, S))
@@ -174,17 +222,22 @@ def attention_forward(q, k, v, *, rope=ROPE_NONE, theta=10000.0, mask=MASK_CAUSA
             for r0 in range(0, S, _ROW_CHUNK):
                 rows = np.arange(r0, min(S, r0 + _ROW_CHUNK))
                 s = attention_scores(qr[b, h], kr[b, g], rows, mask=mask, window=window,
-                                     slope=slope, scale=scale, block_mask=block_mask)
+                                     slope=slope, scale=scale, block_mask=block_mask,
+                                     bias_bh=None if bias is None else bias[b, h])
+                if norm == NORM_RELU:
+                    O[b, h, rows] = _relu_rows(s) @ v[b, g]
+                    continue
                 P, m, l = _softmax_rows(s)
                 O[b, h, rows] = P @ v[b, g]
                 with np.errstate(divide="ignore"):
                     LSE[b, h, rows] = m + np.log(l)
-    return O, LSE
+    return O, (None if norm == NORM_RELU else LSE)
 
 
 def attention_forward_rows(q_bh, k_bg, v_bg, rows, *, h=0, H=1, rope=ROPE_NONE,
                            theta=10000.0, mask=MASK_CAUSAL, window=None,
-                           alibi_slopes=None, scale=None, pos_offset=0, block_mask=None):
+                           alibi_slopes=None, scale=None, pos_offset=0, block_mask=None,
+                           bias_bh=None, norm=NORM_SOFTMAX):
     """O and LSE of selected query rows of ONE head, for sampled checks at full size.
 
     q_bh [S, D] is query head h; k_bg, v_bg [S, D] its K/V head.  Only the
@@ -205,7 +258,11 @@ def attention_forward_rows(q_bh, k_bg, v_bg, rows, *, h=0, H=1, rope=ROPE_NONE,
     cols = np.arange(S)
     if slopes is not None:
         s = s + alibi_bias(slopes[h], rows, cols)
+    if bias_bh is not None:
+        s = s + np.asarray(bias_bh, dtype=np.float64)[rows]
     s = np.where(visibility(rows, cols, mask, window, block_mask), s, -np.inf)
+    if _norm_of(norm) == NORM_RELU:
+        return _relu_rows(s) @ v_bg, None
     P, m, l = _softmax_rows(s)
     with np.errstate(divide="ignore"):
         return P @ v_bg, m + np.log(l)
@@ -213,11 +270,12 @@ def attention_forward_rows(q_bh, k_bg, v_bg, rows, *, h=0, H=1, rope=ROPE_NONE,
 
 def attention_backward(q, k, v, do, *, rope=ROPE_NONE, theta=10000.0, mask=MASK_CAUSAL,
                        window=None, alibi_slopes=None, scale=None, pos_offset=0,
-                       return_intermediates=False, block_mask=None):
+                       return_intermediates=False, block_mask=None, bias=None, norm=NORM_SOFTMAX):
     """dQ [B,H,S,D], dK and dV [B,H_kv,S,D] in fp64.
 
     With ``return_intermediates`` also returns a dict with per-(b,h) lists of
-    P, dS and delta (only sensible at small sizes).
+    P, dS and delta (only sensible at small sizes; delta is absent under relu
+    attention).
     """
     q = np.asarray(q, dtype=np.float64)
     k = np.asarray(k, dtype=np.float64)
@@ -227,6 +285,8 @@ def attention_backward(q, k, v, do, *, rope=ROPE_NONE, theta=10000.0, mask=MASK_
     if do.shape != q.shape:
         raise ValueError("dO must have the shape of Q")
     scale, slopes = _defaults(D, scale, alibi_slopes, H)
+    bias = _bias_of(bias, B, H, S)
+    norm = _norm_of(norm)
     qr, kr = _rotated(q, k, rope, theta, pos_offset)
     dqr = np.zeros_like(qr)
     dkr = np.zeros_like(kr)
@@ -239,13 +299,18 @@ def attention_backward(q, k, v, do, *, rope=ROPE_NONE, theta=10000.0, mask=MASK_
             for r0 in range(0, S, _ROW_CHUNK):
                 rows = np.arange(r0, min(S, r0 + _ROW_CHUNK))
                 s = attention_scores(qr[b, h], kr[b, g], rows, mask=mask, window=window,
-                                     slope=slope, scale=scale, block_mask=block_mask)
-                P = _softmax_rows(s)[0]
+                                     slope=slope, scale=scale, block_mask=block_mask,
+                                     bias_bh=None if bias is None else bias[b, h])
+                P = _relu_rows(s) if norm == NORM_RELU else _softmax_rows(s)[0]
                 dO_rows = do[b, h, rows]
                 dv[b, g] += P.T @ dO_rows
                 dP = dO_rows @ v[b, g].T
-                delta = np.sum(P * dP, axis=1)
-                dS = P * (dP - delta[:, None])
+                if norm == NORM_RELU:
+                    delta = None
+                    dS = _relu_grad(s, dP)
+                else:
+                    delta = np.sum(P * dP, axis=1)
+                    dS = P * (dP - delta[:, None])
                 dqr[b, h, rows] = scale * (dS @ kr[b, g])
                 dkr[b, g] += scale * (dS.T @ qr[b, h, rows])
                 if return_intermediates and S <= _ROW_CHUNK:

@@ -50,8 +50,10 @@ def key_visible(i, j, mask, window):
 
 
 def forward(q, k, v, *, rope="none", theta=10000.0, mask="causal", window=None,
-            alibi_slopes=None, scale=None, pos_offset=0, block_mask=None):
-    """q: nested lists [B][H][S][D]; k, v: [B][Hkv][S][D].  Returns (O, LSE) nested lists."""
+            alibi_slopes=None, scale=None, pos_offset=0, block_mask=None, bias=None, norm="softmax"):
+    """q: nested lists [B][H][S][D]; k, v: [B][Hkv][S][D]; bias: nested [B][H][S][S] or None.
+    Returns (O, LSE) nested lists; under norm="relu" the weights are max(score, 0)
+    and LSE is None."""
     B, H, S, D = len(q), len(q[0]), len(q[0][0]), len(q[0][0][0])
     Hkv = len(k[0])
     group = H // Hkv
@@ -75,7 +77,13 @@ def forward(q, k, v, *, rope="none", theta=10000.0, mask="causal", window=None,
                     sc = scale * dot(qi, kj)
                     if alibi_slopes is not None:
                         sc -= alibi_slopes[h] * (i - j)
+                    if bias is not None:
+                        sc += bias[b][h][i][j]
                     scores[j] = sc
+                if norm == "relu":
+                    for d in range(D):
+                        O[b][h][i][d] = math.fsum(sc * v[b][kvh][j][d] for j, sc in scores.items() if sc > 0.0)
+                    continue
                 if not scores:
                     LSE[b][h][i] = -math.inf
                     continue
@@ -85,7 +93,7 @@ def forward(q, k, v, *, rope="none", theta=10000.0, mask="causal", window=None,
                 LSE[b][h][i] = mx + math.log(tot)
                 for d in range(D):
                     O[b][h][i][d] = math.fsum(w[j] * v[b][kvh][j][d] for j in w) / tot
-    return O, LSE
+    return O, (None if norm == "relu" else LSE)
 
 
 def loss(q, k, v, do, **kw):

@@ -451,3 +451,91 @@ def check_block_mask_backward_fd(seed=32):
     assert np.allclose(dq, np.array(bruteforce.finite_difference_grad(ql, f)), atol=1e-7)
     assert np.allclose(dk, np.array(bruteforce.finite_difference_grad(kl, f)), atol=1e-7)
     assert np.allclose(dv, np.array(bruteforce.finite_difference_grad(vl, f)), atol=1e-7)
+
+
+# ----------------------------------------------------------------------------- additive bias, relu attention
+
+def _bias(seed, B, H, S, scale=1.5):
+    return scale * _rng(seed + 1000).standard_normal((B, H, S, S))
+
+
+def check_bias_relu_vs_bruteforce(variant, norm, seed=40):
+    """The dense bias tensor (and relu attention) against the pure-Python loops."""
+    rope, mask, window, alibi = variant
+    q, k, v, _ = _tiny(seed, B=2, H=4, Hkv=2, S=7, D=4)
+    kw = _kw(rope, mask, window, alibi, 4)
+    bias = _bias(seed, 2, 4, 7)
+    O, L = oracle.attention_forward(q, k, v, bias=bias, norm=norm, **kw)
+    Ob, Lb = bruteforce.forward(q.tolist(), k.tolist(), v.tolist(), bias=bias.tolist(), norm=norm, **kw)
+    assert np.allclose(O, np.array(Ob), atol=TOL, rtol=0)
+    if norm == "relu":
+        assert L is None and Lb is None
+    else:
+        assert np.allclose(L, np.array(Lb), atol=TOL, rtol=0)
+
+
+def check_bias_reductions(seed=41):
+    """Special cases that reduce the bias to other parts of the definition:
+    the ALiBi matrix as a bias tensor is ALiBi; -inf above the diagonal is the
+    causal mask; a bias constant along each row leaves O unchanged and shifts
+    LSE by that constant; a bias broadcast over batch and heads equals its
+    materialised copy."""
+    B, H, S, D = 2, 3, 8, 4
+    q, k, v, _ = _tiny(seed, B=B, H=H, Hkv=1, S=S, D=D)
+    slopes = [0.25, 0.5, 1.25]
+    i = np.arange(S)
+    alibi = np.stack([-sl * (i[:, None] - i[None, :]) for sl in slopes])[None].astype(np.float64)
+    a = oracle.attention_forward(q, k, v, rope="neox", mask="causal", alibi_slopes=slopes, scale=0.7)
+    b = oracle.attention_forward(q, k, v, rope="neox", mask="causal", bias=alibi, scale=0.7)
+    assert np.allclose(a[0], b[0], atol=TOL, rtol=0) and np.allclose(a[1], b[1], atol=TOL, rtol=0)
+    upper = np.where(i[None, :] > i[:, None], -np.inf, 0.0)
+    a = oracle.attention_forward(q, k, v, rope="interleaved", mask="causal")
+    b = oracle.attention_forward(q, k, v, rope="interleaved", mask="none", bias=upper)
+    assert np.allclose(a[0], b[0], atol=TOL, rtol=0) and np.allclose(a[1], b[1], atol=TOL, rtol=0)
+    c = _rng(seed).standard_normal((B, H, S, 1)) * 3.0
+    a = oracle.attention_forward(q, k, v, mask="none", scale=0.9)
+    b = oracle.attention_forward(q, k, v, mask="none", scale=0.9, bias=np.broadcast_to(c, (B, H, S, S)))
+    assert np.allclose(a[0], b[0], atol=1e-12, rtol=0)
+    assert np.allclose(b[1] - a[1], c[..., 0], atol=1e-12, rtol=0)
+    one = _bias(seed, 1, 1, S)
+    a = oracle.attention_forward(q, k, v, mask="none", bias=one)
+    b = oracle.attention_forward(q, k, v, mask="none", bias=np.broadcast_to(one, (B, H, S, S)).copy())
+    assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1])
+
+
+def check_relu_closed_forms(seed=42):
+    """Relu attention: causal row 0 is max(s_00, 0) v_0; scores all below zero
+    give O = 0; O is positively homogeneous in the scale (max(a s, 0) =
+    a max(s, 0)) and linear in V."""
+    q, k, v, _ = _tiny(seed, B=1, H=2, Hkv=1, S=6, D=4)
+    O, L = oracle.attention_forward(q, k, v, rope="neox", mask="causal", norm="relu", scale=0.8)
+    assert L is None
+    s00 = 0.8 * q[0, :, 0] @ k[0, 0, 0]                     # RoPE is the identity at position 0
+    assert np.allclose(O[0, :, 0], np.maximum(s00, 0.0)[:, None] * v[0, 0, 0][None, :], atol=TOL, rtol=0)
+    neg = np.full((1, 2, 6, 6), -1e3)
+    O, _ = oracle.attention_forward(q, k, v, mask="none", norm="relu", bias=neg)
+    assert (O == 0).all()
+    a, _ = oracle.attention_forward(q, k, v, mask="sliding_window", window=3, norm="relu", scale=0.5)
+    b, _ = oracle.attention_forward(q, k, v, mask="sliding_window", window=3, norm="relu", scale=1.5)
+    assert np.allclose(3.0 * a, b, atol=TOL, rtol=0)
+    c, _ = oracle.attention_forward(q, k, -2.0 * v, mask="sliding_window", window=3, norm="relu", scale=0.5)
+    assert np.allclose(-2.0 * a, c, atol=TOL, rtol=0)
+
+
+def check_bias_relu_backward_fd(norm, seed=43):
+    """Gradients with a bias tensor (softmax or relu) against central finite
+    differences of the brute force; relu kinks (s = 0) are measure-zero for
+    these random inputs."""
+    q, k, v, do = _tiny(seed, B=1, H=2, Hkv=1, S=5, D=4)
+    bias = _bias(seed, 1, 2, 5)
+    kw = dict(rope="neox", theta=10000.0, mask="causal", window=None, alibi_slopes=None, scale=0.6)
+    dq, dk, dv = oracle.attention_backward(q, k, v, do, bias=bias, norm=norm, **kw)
+    ql, kl, vl, dol = q.tolist(), k.tolist(), v.tolist(), do.tolist()
+    bl = bias.tolist()
+
+    def f():
+        return bruteforce.loss(ql, kl, vl, dol, bias=bl, norm=norm, **kw)
+
+    assert np.allclose(dq, np.array(bruteforce.finite_difference_grad(ql, f)), atol=1e-7)
+    assert np.allclose(dk, np.array(bruteforce.finite_difference_grad(kl, f)), atol=1e-7)
+    assert np.allclose(dv, np.array(bruteforce.finite_difference_grad(vl, f)), atol=1e-7)

@@ -91,6 +91,25 @@ def _bad_decode_visible(j, p, mask, window=None):
     return j <= p
 
 
+_REAL_BIAS_OF = oatt._bias_of
+
+
+def _scaled_bias_of(bias, B, H, S):
+    b = _REAL_BIAS_OF(bias, B, H, S)
+    return None if b is None else 0.41 * b          # the softmax scale applied to the bias too
+
+
+def _transposed_bias_of(bias, B, H, S):
+    b = _REAL_BIAS_OF(bias, B, H, S)
+    return None if b is None else np.swapaxes(b, -1, -2)
+
+
+def _normalised_relu(s):
+    r = np.maximum(s, 0.0)
+    tot = r.sum(axis=1, keepdims=True)
+    return r / np.where(tot > 0, tot, 1.0)
+
+
 MUTATIONS = {
     "rotation_sign": [(oatt, "rope_rotate", _wrong_sign_rotate), (orope, "rope_rotate", _wrong_sign_rotate),
                       (oracle, "rope_rotate", _wrong_sign_rotate)],
@@ -106,6 +125,10 @@ MUTATIONS = {
     "block_mask_transposed": [(oatt, "block_visible", _transposed_blocks)],
     "dropped_scale": [(oatt, "_defaults", _no_scale_defaults)],
     "gradient_not_unrotated": [(oatt, "rope_rotate", _no_inverse_rotate)],
+    "bias_scaled": [(oatt, "_bias_of", _scaled_bias_of)],
+    "bias_transposed": [(oatt, "_bias_of", _transposed_bias_of)],
+    "relu_normalised": [(oatt, "_relu_rows", _normalised_relu)],
+    "relu_gradient_unmasked": [(oatt, "_relu_grad", lambda s, dP: dP)],
 }
 
 CHECKS = [
@@ -124,6 +147,11 @@ CHECKS = [
     lambda: P.check_decode_vs_bruteforce(SW),
     lambda: P.check_decode_closed_forms("neox"),
     lambda: P.check_block_mask_vs_bruteforce(FWD),
+    lambda: P.check_bias_relu_vs_bruteforce(FWD, "softmax"),
+    lambda: P.check_bias_relu_vs_bruteforce(FWD, "relu"),
+    P.check_bias_reductions,
+    P.check_relu_closed_forms,
+    lambda: P.check_bias_relu_backward_fd("relu"),
 ]
 
 

@@ -131,3 +131,22 @@ def test_block_mask_reductions():
 
 def test_block_mask_backward_fd():
     P.check_block_mask_backward_fd()
+
+
+@pytest.mark.parametrize("norm", ["softmax", "relu"])
+@pytest.mark.parametrize("variant", P.VARIANTS, ids=lambda v: "-".join(map(str, v)))
+def test_bias_relu_vs_bruteforce(variant, norm):
+    P.check_bias_relu_vs_bruteforce(variant, norm)
+
+
+def test_bias_reductions():
+    P.check_bias_reductions()
+
+
+def test_relu_closed_forms():
+    P.check_relu_closed_forms()
+
+
+@pytest.mark.parametrize("norm", ["softmax", "relu"])
+def test_bias_relu_backward_fd(norm):
+    P.check_bias_relu_backward_fd(norm)

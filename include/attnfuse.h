@@ -56,6 +56,11 @@ enum { AF_ROPE_NONE = 0, AF_ROPE_NEOX = 1, AF_ROPE_INTERLEAVED = 2 };
  * (window keys, the diagonal included). */
 enum { AF_MASK_NONE = 0, AF_MASK_CAUSAL = 1, AF_MASK_SLIDING_WINDOW = 2 };
 
+/* Normalisation of the scores (Section 3.1 combinators softmax and
+ * relu_attention): SOFTMAX as everywhere else; RELU uses P_ij = max(s_ij, 0)
+ * with no normalisation and no row statistic (see attnfuse_fwd_bias_norm). */
+enum { AF_NORM_SOFTMAX = 0, AF_NORM_RELU = 1 };
+
 enum { AF_OK = 0, AF_ERR_INVALID_ARG = -1, AF_ERR_UNSUPPORTED = -2, AF_ERR_HIP = -3 };
 
 /*
@@ -169,6 +174,52 @@ int attnfuse_bwd_blocksparse(const void* Q, const void* K, const void* V, const 
                              int B, int H, int H_kv, int S, int D, int dtype,
                              int rope, float rope_theta, int mask, int window,
                              const float* alibi_slopes, float softmax_scale, void* stream);
+
+/*
+ * attnfuse_fwd with the two remaining combinators of Section 3.1: a dense
+ * additive bias tensor (additive_bias) and relu attention (relu_attention).
+ * The paper names both without defining them; here
+ *     s_ij  = softmax_scale * <R_i q_i, R_j k_j> + bias[b, h, i, j]
+ * (added before the mask, like ALiBi), then with norm = AF_NORM_SOFTMAX the
+ * usual O = softmax(s) V and LSE, and with norm = AF_NORM_RELU
+ *     O_i = sum_{visible j} max(s_ij, 0) v_j
+ * (no normalisation: a 1/n factor folds into softmax_scale and the bias), with
+ * no row statistic: LSE is not written and may be NULL.
+ *
+ *   bias     device fp32, or NULL for none.  Element (b, h, i, j) -- batch,
+ *            query head, query position, key position -- is read at
+ *            bias[b*bias_stride_b + h*bias_stride_h + i*bias_stride_q + j]:
+ *            keys contiguous, the other strides in elements, >= 0 (0
+ *            broadcasts: e.g. a key-padding bias [B, 1, 1, S] has strides
+ *            (S, 0, 0)).  4-byte aligned, read only, must not alias an
+ *            output; the caller guarantees every addressed element exists.
+ *   norm     AF_NORM_*
+ *   other arguments as attnfuse_fwd.  Supported: bf16, D in {64, 128}, every
+ *   RoPE kind and mask, without ALiBi (a bias tensor can carry it); other
+ *   combinations return AF_ERR_UNSUPPORTED.  bias = NULL with
+ *   AF_NORM_SOFTMAX is exactly attnfuse_fwd.
+ */
+int attnfuse_fwd_bias_norm(const void* Q, const void* K, const void* V, void* O, float* LSE,
+                           const float* bias, long long bias_stride_b, long long bias_stride_h,
+                           long long bias_stride_q, int norm,
+                           int B, int H, int H_kv, int S, int D, int dtype,
+                           int rope, float rope_theta, int mask, int window,
+                           const float* alibi_slopes, float softmax_scale, void* stream);
+
+/*
+ * Backward of attnfuse_fwd_bias_norm (the same bias and norm).  The bias gets
+ * no gradient.  Under AF_NORM_RELU the probabilities are recomputed as
+ * max(s, 0) and dS = dP where s > 0 (0 at s = 0); LSE is not used and may be
+ * NULL.  Workspace, other arguments and results as attnfuse_bwd.
+ */
+int attnfuse_bwd_bias_norm(const void* Q, const void* K, const void* V, const void* O, const void* dO,
+                           const float* LSE, void* dQ, void* dK, void* dV,
+                           const float* bias, long long bias_stride_b, long long bias_stride_h,
+                           long long bias_stride_q, int norm,
+                           void* workspace, size_t workspace_bytes,
+                           int B, int H, int H_kv, int S, int D, int dtype,
+                           int rope, float rope_theta, int mask, int window,
+                           const float* alibi_slopes, float softmax_scale, void* stream);
 
 /*
  * Standalone rotation, the separate-RoPE path (Section 5.3 "The Rotation

@@ -270,12 +270,21 @@ def attention_forward_rows(q_bh, k_bg, v_bg, rows, *, h=0, H=1, rope=ROPE_NONE,
 
 def attention_backward(q, k, v, do, *, rope=ROPE_NONE, theta=10000.0, mask=MASK_CAUSAL,
                        window=None, alibi_slopes=None, scale=None, pos_offset=0,
-                       return_intermediates=False, block_mask=None, bias=None, norm=NORM_SOFTMAX):
+                       return_intermediates=False, block_mask=None, bias=None, norm=NORM_SOFTMAX,
+                       relu_gate="exact"):
     """dQ [B,H,S,D], dK and dV [B,H_kv,S,D] in fp64.
 
     With ``return_intermediates`` also returns a dict with per-(b,h) lists of
     P, dS and delta (only sensible at small sizes; delta is absent under relu
     attention).
+
+    ``relu_gate`` says in which precision the relu derivative's decision
+    s > 0 is taken: "exact" (fp64, the definition) or "fp16" (the score formed
+    from the rotated Q' and K' rounded to fp16, the operand precision of an
+    fp16 matrix unit).  The gate is a discontinuous function of the score, so a
+    score within rounding of 0 flips it; comparing against a kernel that gates
+    on fp16 operands takes the decision in that precision on both sides.
+    Everything else stays fp64.
     """
     q = np.asarray(q, dtype=np.float64)
     k = np.asarray(k, dtype=np.float64)
@@ -287,7 +296,12 @@ def attention_backward(q, k, v, do, *, rope=ROPE_NONE, theta=10000.0, mask=MASK_
     scale, slopes = _defaults(D, scale, alibi_slopes, H)
     bias = _bias_of(bias, B, H, S)
     norm = _norm_of(norm)
+    if relu_gate not in ("exact", "fp16"):
+        raise ValueError(f"unknown relu_gate {relu_gate!r}")
     qr, kr = _rotated(q, k, rope, theta, pos_offset)
+    if relu_gate == "fp16":
+        qg = qr.astype(np.float16).astype(np.float64)
+        kg = kr.astype(np.float16).astype(np.float64)
     dqr = np.zeros_like(qr)
     dkr = np.zeros_like(kr)
     dv = np.zeros_like(v)
@@ -307,7 +321,12 @@ def attention_backward(q, k, v, do, *, rope=ROPE_NONE, theta=10000.0, mask=MASK_
                 dP = dO_rows @ v[b, g].T
                 if norm == NORM_RELU:
                     delta = None
-                    dS = _relu_grad(s, dP)
+                    sg = s
+                    if relu_gate == "fp16":
+                        sg = attention_scores(qg[b, h], kg[b, g], rows, mask=mask, window=window, slope=slope,
+                                              scale=scale, block_mask=block_mask,
+                                              bias_bh=None if bias is None else bias[b, h])
+                    dS = _relu_grad(sg, dP)
                 else:
                     delta = np.sum(P * dP, axis=1)
                     dS = P * (dP - delta[:, None])

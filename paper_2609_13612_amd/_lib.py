@@ -12,6 +12,7 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "lib", "liba
 _P = ctypes.c_void_p
 _I = ctypes.c_int
 _F = ctypes.c_float
+_L = ctypes.c_longlong
 SIGNATURES = {
     "attnfuse_fwd": (_I, [_P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _F, _I, _I, _P, _F, _P]),
     "attnfuse_bwd_workspace_bytes": (ctypes.c_size_t, [_I, _I, _I, _I, _I, _I]),
@@ -21,6 +22,10 @@ SIGNATURES = {
                                       _P]),
     "attnfuse_bwd_blocksparse": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t,
                                       _I, _I, _I, _I, _I, _I, _I, _F, _I, _I, _P, _F, _P]),
+    "attnfuse_fwd_bias_norm": (_I, [_P, _P, _P, _P, _P, _P, _L, _L, _L, _I, _I, _I, _I, _I, _I, _I, _I, _F, _I, _I,
+                                    _P, _F, _P]),
+    "attnfuse_bwd_bias_norm": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _L, _L, _L, _I, _P, ctypes.c_size_t,
+                                    _I, _I, _I, _I, _I, _I, _I, _F, _I, _I, _P, _F, _P]),
     "attnfuse_rope": (_I, [_P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _F, _P]),
     "attnfuse_rope_bwd": (_I, [_P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _F, _P]),
     "attnfuse_decode_workspace_bytes": (ctypes.c_size_t, [_I, _I, _I, _I, _I]),

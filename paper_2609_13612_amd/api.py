@@ -153,6 +153,66 @@ def attnfuse_bwd_blocksparse(q, k, v, o, do, lse, block_mask, *, rope="none", th
     return dq, dk, dv
 
 
+NORM = {"softmax": 0, "relu": 1}
+
+
+def _bias_args(bias, q, B, H, S):
+    """(pointer, stride_b, stride_h, stride_q) of an fp32 GPU bias broadcastable
+    to [B, H, S, S] with keys contiguous (broadcast dimensions get stride 0)."""
+    if bias is None:
+        return None, 0, 0, 0
+    if bias.dtype != torch.float32 or bias.device != q.device:
+        raise ValueError("bias must be an fp32 tensor on q's device")
+    while bias.dim() < 4:
+        bias = bias.unsqueeze(0)
+    e = bias.expand(B, H, S, S)
+    if e.stride(3) != 1:
+        raise ValueError("bias must be contiguous along the key dimension")
+    return e.data_ptr(), e.stride(0), e.stride(1), e.stride(2)
+
+
+def attnfuse_fwd_bias_norm(q, k, v, *, bias=None, norm="softmax", rope="none", theta=10000.0, mask="causal",
+                           window=None, scale=None, out=None, lse=None):
+    """O (and LSE, None under relu attention) with a dense additive bias and/or
+    relu attention; see attnfuse_fwd_bias_norm in include/attnfuse.h."""
+    B, H, Hkv, S, D = _shape(q, k)
+    _same(q, k, v, out)
+    if v.shape != k.shape:
+        raise ValueError("v must have k's shape")
+    out = torch.empty_like(q) if out is None else out
+    if NORM[norm] == NORM["softmax"] and lse is None:
+        lse = torch.empty(B, H, S, device=q.device, dtype=torch.float32)
+    bp, sb, sh, sq = _bias_args(bias, q, B, H, S)
+    r, th, m, w, sc = _variant(rope, theta, mask, window, None, scale, D)
+    code = _lib.load().attnfuse_fwd_bias_norm(_ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(lse), bp, sb, sh, sq,
+                                              NORM[norm], B, H, Hkv, S, D, DTYPE[q.dtype], r, th, m, w, None, sc,
+                                              _stream())
+    _check(code, "attnfuse_fwd_bias_norm")
+    return out, lse
+
+
+def attnfuse_bwd_bias_norm(q, k, v, o, do, lse, *, bias=None, norm="softmax", rope="none", theta=10000.0,
+                           mask="causal", window=None, scale=None, dq=None, dk=None, dv=None, workspace=None):
+    """dQ, dK, dV of attnfuse_fwd_bias_norm (lse may be None under relu
+    attention); see attnfuse_bwd_bias_norm."""
+    B, H, Hkv, S, D = _shape(q, k)
+    _same(q, k, v, o, do, dq, dk, dv)
+    dq = torch.empty_like(q) if dq is None else dq
+    dk = torch.empty_like(k) if dk is None else dk
+    dv = torch.empty_like(v) if dv is None else dv
+    nbytes = attnfuse_bwd_workspace_bytes(B, H, Hkv, S, D, rope)
+    if workspace is None:
+        workspace = torch.empty(nbytes, device=q.device, dtype=torch.uint8)
+    bp, sb, sh, sq = _bias_args(bias, q, B, H, S)
+    r, th, m, w, sc = _variant(rope, theta, mask, window, None, scale, D)
+    code = _lib.load().attnfuse_bwd_bias_norm(_ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(do), _ptr(lse),
+                                              _ptr(dq), _ptr(dk), _ptr(dv), bp, sb, sh, sq, NORM[norm],
+                                              _ptr(workspace), workspace.numel(), B, H, Hkv, S, D, DTYPE[q.dtype],
+                                              r, th, m, w, None, sc, _stream())
+    _check(code, "attnfuse_bwd_bias_norm")
+    return dq, dk, dv
+
+
 def attnfuse_decode_workspace_bytes(B, H, H_kv, S_kv, D):
     return _lib.load().attnfuse_decode_workspace_bytes(B, H, H_kv, S_kv, D)
 

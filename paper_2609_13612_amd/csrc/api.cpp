@@ -136,18 +136,47 @@ DecodeLayout decode_layout(int B, int H, int H_kv, int S, int D) {
 }
 
 // ---------------------------------------------------------------- shared bodies
+// Dense bias tensor and normalisation of the extended entry points (EXT_NONE
+// for the plain ones).
+struct Ext {
+  const float* bias = nullptr;
+  long long sb = 0, sh = 0, sq = 0;
+  int norm = AF_NORM_SOFTMAX;
+  int kind() const {
+    if (norm == AF_NORM_RELU) return bias ? af::EXT_RELU_BIAS : af::EXT_RELU;
+    return bias ? af::EXT_BIAS : af::EXT_NONE;
+  }
+};
+
+int check_ext(const Ext& e, const void* const* outs, int nouts) {
+  if (e.norm != AF_NORM_SOFTMAX && e.norm != AF_NORM_RELU) return AF_ERR_INVALID_ARG;
+  if (e.bias) {
+    if ((reinterpret_cast<uintptr_t>(e.bias) & 3u) != 0) return AF_ERR_INVALID_ARG;
+    if (e.sb < 0 || e.sh < 0 || e.sq < 0) return AF_ERR_INVALID_ARG;
+    for (int i = 0; i < nouts; ++i) if (outs[i] == (const void*)e.bias) return AF_ERR_INVALID_ARG;
+  }
+  return AF_OK;
+}
+
 int fwd_impl(const void* Q, const void* K, const void* V, void* O, float* LSE, const int* q_block_ptr,
-             const int* k_block_idx, int B, int H, int H_kv, int S, int D, int dtype, int rope, float rope_theta,
-             int mask, int window, const float* alibi_slopes, float softmax_scale, void* stream) {
-  if (!Q || !K || !V || !O || !LSE) return AF_ERR_INVALID_ARG;
+             const int* k_block_idx, const Ext& ext, int B, int H, int H_kv, int S, int D, int dtype, int rope,
+             float rope_theta, int mask, int window, const float* alibi_slopes, float softmax_scale, void* stream) {
+  const bool relu = ext.norm == AF_NORM_RELU;   // no row statistic: LSE may be NULL
+  if (!Q || !K || !V || !O || (!LSE && !relu)) return AF_ERR_INVALID_ARG;
   if (!aligned16(Q) || !aligned16(K) || !aligned16(V) || !aligned16(O) || !aligned16(LSE)) return AF_ERR_INVALID_ARG;
   if (O == Q || O == K || O == V || (const void*)LSE == Q || (const void*)LSE == K || (const void*)LSE == V)
     return AF_ERR_INVALID_ARG;
+  const void* outs[] = {O, LSE};
+  int rc0 = check_ext(ext, outs, 2);
+  if (rc0 != AF_OK) return rc0;
   int rc = check_common(B, H, H_kv, S, D, dtype, rope, rope_theta);
   if (rc != AF_OK) return rc;
   if ((rc = check_attn(mask, window, softmax_scale)) != AF_OK) return rc;
   if (!supported_d(D)) return AF_ERR_UNSUPPORTED;
   if (q_block_ptr && dtype == AF_DTYPE_FP32) return AF_ERR_UNSUPPORTED;   // block-sparse: bf16 kernels only
+  // the bias tensor and relu attention: bf16, without ALiBi or a block mask
+  if (ext.kind() != af::EXT_NONE && (dtype == AF_DTYPE_FP32 || alibi_slopes || q_block_ptr))
+    return AF_ERR_UNSUPPORTED;
 
   hipStream_t st = static_cast<hipStream_t>(stream);
   af::FwdParams p{};
@@ -160,29 +189,37 @@ int fwd_impl(const void* Q, const void* K, const void* V, void* O, float* LSE, c
   p.table = nullptr;
   p.bq_ptr = q_block_ptr;
   p.bk_idx = k_block_idx;
+  p.bias = ext.bias;
+  p.bias_sb = ext.sb; p.bias_sh = ext.sh; p.bias_sq = ext.sq;
   if (rope != AF_ROPE_NONE && (rc = rope_table(D, rope_theta, S, st, &p.table)) != AF_OK) return rc;
   const bool alibi = alibi_slopes != nullptr;
-  if (dtype == AF_DTYPE_BF16) return map_launch(af::launch_fwd_bf16(D, rope, mask, alibi, p, st));
+  if (dtype == AF_DTYPE_BF16) return map_launch(af::launch_fwd_bf16(D, rope, mask, alibi, ext.kind(), p, st));
   return map_launch(af::launch_fwd_fp32(D, rope, mask, alibi, p, st));
 }
 
 // sparse: NULL (dense) or {q_block_ptr, k_block_idx, k_block_ptr, q_block_idx}
 int bwd_impl(const void* Q, const void* K, const void* V, const void* O, const void* dO, const float* LSE, void* dQ,
-             void* dK, void* dV, const int* const* sparse, void* workspace, size_t workspace_bytes, int B, int H,
-             int H_kv, int S, int D, int dtype, int rope, float rope_theta, int mask, int window,
+             void* dK, void* dV, const int* const* sparse, const Ext& ext, void* workspace, size_t workspace_bytes,
+             int B, int H, int H_kv, int S, int D, int dtype, int rope, float rope_theta, int mask, int window,
              const float* alibi_slopes, float softmax_scale, void* stream) {
+  const bool relu = ext.norm == AF_NORM_RELU;   // the LSE is not used: it may be NULL
+  if (relu) LSE = nullptr;
   const void* ins[] = {Q, K, V, O, dO, LSE};
   void* outs[] = {dQ, dK, dV, workspace};
-  for (const void* x : ins) if (!x || !aligned16(x)) return AF_ERR_INVALID_ARG;
+  for (const void* x : ins) if (!aligned16(x)) return AF_ERR_INVALID_ARG;
+  if (!Q || !K || !V || !O || !dO || (!LSE && !relu)) return AF_ERR_INVALID_ARG;
   for (const void* x : outs) if (!x || !aligned16(x)) return AF_ERR_INVALID_ARG;
   for (const void* x : outs)
-    for (const void* y : ins) if (x == y) return AF_ERR_INVALID_ARG;
+    for (const void* y : ins) if (y && x == y) return AF_ERR_INVALID_ARG;
+  int rc0 = check_ext(ext, outs, 4);
+  if (rc0 != AF_OK) return rc0;
   int rc = check_common(B, H, H_kv, S, D, dtype, rope, rope_theta);
   if (rc != AF_OK) return rc;
   if ((rc = check_attn(mask, window, softmax_scale)) != AF_OK) return rc;
   if (workspace_bytes < attnfuse_bwd_workspace_bytes(B, H, H_kv, S, D, rope)) return AF_ERR_INVALID_ARG;
   if (!supported_d(D)) return AF_ERR_UNSUPPORTED;
   if (sparse && dtype == AF_DTYPE_FP32) return AF_ERR_UNSUPPORTED;        // block-sparse: bf16 kernels only
+  if (ext.kind() != af::EXT_NONE && (dtype == AF_DTYPE_FP32 || alibi_slopes || sparse)) return AF_ERR_UNSUPPORTED;
 
   hipStream_t st = static_cast<hipStream_t>(stream);
   af::BwdParams p{};
@@ -205,10 +242,12 @@ int bwd_impl(const void* Q, const void* K, const void* V, const void* O, const v
     p.bq_ptr = sparse[0]; p.bk_idx = sparse[1];
     p.bk_ptr = sparse[2]; p.bq_idx = sparse[3];
   }
+  p.bias = ext.bias;
+  p.bias_sb = ext.sb; p.bias_sh = ext.sh; p.bias_sq = ext.sq;
   if (rope != AF_ROPE_NONE && (rc = rope_table(D, rope_theta, S, st, &p.table)) != AF_OK) return rc;
   const bool alibi = alibi_slopes != nullptr;
   if (dtype == AF_DTYPE_FP32) return map_launch(af::launch_bwd_fp32(D, rope, mask, alibi, p, st));
-  return map_launch(af::launch_bwd_bf16(D, rope, mask, alibi, p, st));
+  return map_launch(af::launch_bwd_bf16(D, rope, mask, alibi, ext.kind(), p, st));
 }
 
 }  // namespace
@@ -231,7 +270,7 @@ int attnfuse_fwd(const void* Q, const void* K, const void* V, void* O, float* LS
                  int B, int H, int H_kv, int S, int D, int dtype,
                  int rope, float rope_theta, int mask, int window,
                  const float* alibi_slopes, float softmax_scale, void* stream) {
-  return fwd_impl(Q, K, V, O, LSE, nullptr, nullptr, B, H, H_kv, S, D, dtype, rope, rope_theta, mask, window,
+  return fwd_impl(Q, K, V, O, LSE, nullptr, nullptr, Ext{}, B, H, H_kv, S, D, dtype, rope, rope_theta, mask, window,
                   alibi_slopes, softmax_scale, stream);
 }
 
@@ -245,8 +284,20 @@ int attnfuse_fwd_blocksparse(const void* Q, const void* K, const void* V, void* 
   for (const void* x : outs)
     if (x == (const void*)q_block_ptr || x == (const void*)k_block_idx) return AF_ERR_INVALID_ARG;
   if (S < 1 || S > kMaxSparseS) return AF_ERR_INVALID_ARG;
-  return fwd_impl(Q, K, V, O, LSE, q_block_ptr, k_block_idx, B, H, H_kv, S, D, dtype, rope, rope_theta, mask,
+  return fwd_impl(Q, K, V, O, LSE, q_block_ptr, k_block_idx, Ext{}, B, H, H_kv, S, D, dtype, rope, rope_theta, mask,
                   window, alibi_slopes, softmax_scale, stream);
+}
+
+int attnfuse_fwd_bias_norm(const void* Q, const void* K, const void* V, void* O, float* LSE,
+                           const float* bias, long long bias_stride_b, long long bias_stride_h,
+                           long long bias_stride_q, int norm,
+                           int B, int H, int H_kv, int S, int D, int dtype,
+                           int rope, float rope_theta, int mask, int window,
+                           const float* alibi_slopes, float softmax_scale, void* stream) {
+  Ext e;
+  e.bias = bias; e.sb = bias_stride_b; e.sh = bias_stride_h; e.sq = bias_stride_q; e.norm = norm;
+  return fwd_impl(Q, K, V, O, LSE, nullptr, nullptr, e, B, H, H_kv, S, D, dtype, rope, rope_theta, mask, window,
+                  alibi_slopes, softmax_scale, stream);
 }
 
 size_t attnfuse_bwd_workspace_bytes(int B, int H, int H_kv, int S, int D, int rope) {
@@ -261,8 +312,8 @@ int attnfuse_bwd(const void* Q, const void* K, const void* V, const void* O, con
                  int B, int H, int H_kv, int S, int D, int dtype,
                  int rope, float rope_theta, int mask, int window,
                  const float* alibi_slopes, float softmax_scale, void* stream) {
-  return bwd_impl(Q, K, V, O, dO, LSE, dQ, dK, dV, nullptr, workspace, workspace_bytes, B, H, H_kv, S, D, dtype,
-                  rope, rope_theta, mask, window, alibi_slopes, softmax_scale, stream);
+  return bwd_impl(Q, K, V, O, dO, LSE, dQ, dK, dV, nullptr, Ext{}, workspace, workspace_bytes, B, H, H_kv, S, D,
+                  dtype, rope, rope_theta, mask, window, alibi_slopes, softmax_scale, stream);
 }
 
 int attnfuse_bwd_blocksparse(const void* Q, const void* K, const void* V, const void* O, const void* dO,
@@ -279,8 +330,22 @@ int attnfuse_bwd_blocksparse(const void* Q, const void* K, const void* V, const 
   for (const void* x : outs)
     for (const int* y : m) if (x == (const void*)y) return AF_ERR_INVALID_ARG;
   if (S < 1 || S > kMaxSparseS) return AF_ERR_INVALID_ARG;
-  return bwd_impl(Q, K, V, O, dO, LSE, dQ, dK, dV, m, workspace, workspace_bytes, B, H, H_kv, S, D, dtype, rope,
-                  rope_theta, mask, window, alibi_slopes, softmax_scale, stream);
+  return bwd_impl(Q, K, V, O, dO, LSE, dQ, dK, dV, m, Ext{}, workspace, workspace_bytes, B, H, H_kv, S, D, dtype,
+                  rope, rope_theta, mask, window, alibi_slopes, softmax_scale, stream);
+}
+
+int attnfuse_bwd_bias_norm(const void* Q, const void* K, const void* V, const void* O, const void* dO,
+                           const float* LSE, void* dQ, void* dK, void* dV,
+                           const float* bias, long long bias_stride_b, long long bias_stride_h,
+                           long long bias_stride_q, int norm,
+                           void* workspace, size_t workspace_bytes,
+                           int B, int H, int H_kv, int S, int D, int dtype,
+                           int rope, float rope_theta, int mask, int window,
+                           const float* alibi_slopes, float softmax_scale, void* stream) {
+  Ext e;
+  e.bias = bias; e.sb = bias_stride_b; e.sh = bias_stride_h; e.sq = bias_stride_q; e.norm = norm;
+  return bwd_impl(Q, K, V, O, dO, LSE, dQ, dK, dV, nullptr, e, workspace, workspace_bytes, B, H, H_kv, S, D, dtype,
+                  rope, rope_theta, mask, window, alibi_slopes, softmax_scale, stream);
 }
 
 // ---------------------------------------------------------------- decode

@@ -106,7 +106,8 @@ __device__ __forceinline__ void tile_commit_k(TileRegs<D, ROPE>& R, uint16_t* __
   }
 }
 
-template <int D, int ROPE>
+// V16: store V converted to fp16 (exact for |v| < 65504), for fp16 P operands.
+template <int D, int ROPE, bool V16 = false>
 __device__ __forceinline__ void tile_commit_v(const TileRegs<D, ROPE>& R, uint16_t* __restrict__ Vs, int tid) {
   using C = TileCfg<D, ROPE>;
 #pragma unroll
@@ -114,15 +115,20 @@ __device__ __forceinline__ void tile_commit_v(const TileRegs<D, ROPE>& R, uint16
     const int it = tid + C::THREADS * i;
     if (C::V_ITEMS % C::THREADS != 0 && it >= C::V_ITEMS) break;
     const int r = it / (D / 8), c = it % (D / 8);
-    *reinterpret_cast<u32x4*>(Vs + r * C::VP + 8 * c) = R.v[i];
+    u32x4 v = R.v[i];
+    if constexpr (V16) {
+#pragma unroll
+      for (int w = 0; w < 4; ++w) v[w] = pack_f16(bf_lo(v[w]), bf_hi(v[w]));
+    }
+    *reinterpret_cast<u32x4*>(Vs + r * C::VP + 8 * c) = v;
   }
 }
 
-template <int D, int ROPE>
+template <int D, int ROPE, bool V16 = false>
 __device__ __forceinline__ void tile_commit(TileRegs<D, ROPE>& R, uint16_t* __restrict__ Ks,
                                             uint16_t* __restrict__ Vs, int tid) {
   tile_commit_k<D, ROPE>(R, Ks, tid);
-  tile_commit_v<D, ROPE>(R, Vs, tid);
+  tile_commit_v<D, ROPE, V16>(R, Vs, tid);
 }
 
 // ---------------------------------------------------------------- block-sparse tile lists

@@ -76,7 +76,7 @@ __global__ __launch_bounds__(256) void bwd_prep_kernel(BwdParams p, int q_blocks
       st16(dst + d1, h1);
       if (c == 0) {
         p.delta[row] = acc;
-        const float l = p.lse[row];
+        const float l = p.lse ? p.lse[row] : 0.f;   // relu attention has no LSE
         p.lse2[row] = (l == -INFINITY) ? INFINITY : l * kLog2e;
       }
       if constexpr (ROPE != ROPE_NONE) {
@@ -287,9 +287,11 @@ __device__ __forceinline__ void qtile_commit(const QTileRegs<D>& R, uint16_t* __
 // The block's K' rows (B operand of S = Q' K'^T) and V rows (fp16, B operand
 // of dP = dO V^T) stay resident in LDS, leaving the registers to the dK/dV
 // accumulators.
-template <int D, int ROPE, int MASK, bool ALIBI, bool SPARSE>
+template <int D, int ROPE, int MASK, bool ALIBI, bool SPARSE, int EXT = EXT_NONE>
 __global__ __launch_bounds__(512) void bwd_dkdv_kernel(BwdParams p) {
   using C = QTileCfg<D>;
+  constexpr bool TBIAS = EXT == EXT_BIAS || EXT == EXT_RELU_BIAS;
+  constexpr bool RELU = EXT == EXT_RELU || EXT == EXT_RELU_BIAS;
   constexpr bool ROT = ROPE != ROPE_NONE;    // Q' and K' come rotated (fp16) from the workspace
   constexpr int SMEM = 2 * C::STAGE + 2 * C::V_ELEMS;
   static_assert(SMEM * 2 >= 4 * 16 * C::MT * 64 * 4, "the partial-sum exchange reuses the staging memory");
@@ -394,6 +396,8 @@ __global__ __launch_bounds__(512) void bwd_dkdv_kernel(BwdParams p) {
     const int h = head_of(s);
     const int mq = tile_of(s) * C::BQ + 32 * qt;   // first query row of this wave's half
     const float slope2 = ALIBI ? p.slopes[h] * kLog2e : 0.f;
+    const float* __restrict__ bcol = nullptr;      // this lane's key column of the bias tensor
+    if constexpr (TBIAS) bcol = p.bias + b * p.bias_sb + h * p.bias_sh + min(n, S - 1);
 
     bool visible = nw < S;
     if constexpr (SPARSE) visible = visible && ((tl.rows[s % nq] >> jw) & 1);
@@ -401,6 +405,7 @@ __global__ __launch_bounds__(512) void bwd_dkdv_kernel(BwdParams p) {
     if constexpr (MASK == MASK_SLIDING_WINDOW) visible = visible && (mq <= nw + 31 + W - 1);
     if (visible) {
       bool need_mask = nw + 32 > S;
+      if constexpr (RELU) need_mask = need_mask || (mq + 32 > S);   // no LSE zeroes the rows past S
       if constexpr (MASK != MASK_NONE) need_mask = need_mask || (mq < nw + 31);
       if constexpr (MASK == MASK_SLIDING_WINDOW) need_mask = need_mask || (mq + 31 - W >= nw);
       // S = Q' K'^T and dP = dO V^T for 32 queries (rows) x this wave's 32 keys
@@ -427,9 +432,22 @@ __global__ __launch_bounds__(512) void bwd_dkdv_kernel(BwdParams p) {
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           const int r = 4 * a + e;
-          const float x = ALIBI ? __builtin_fmaf(sc[r], c2, slope2 * (float)(n - (mq + 8 * a + 4 * lg + e))) : sc[r] * c2;
-          pr[r] = fast_exp2(x - lv[e]);
-          ds[r] = dp[r] - dv4[e];
+          if constexpr (TBIAS || RELU) {
+            const int mr = mq + 8 * a + 4 * lg + e;
+            const float bv = TBIAS ? bcol[(long long)min(mr, S - 1) * p.bias_sq] : 0.f;
+            if constexpr (RELU) {   // P = max(s, 0), dS = dP where s > 0
+              const float x = __builtin_fmaf(sc[r], p.scale, bv);
+              pr[r] = fmaxf(x, 0.f);
+              ds[r] = (x > 0.f) ? dp[r] : 0.f;
+            } else {
+              pr[r] = fast_exp2(__builtin_fmaf(sc[r], c2, bv * kLog2e) - lv[e]);
+              ds[r] = dp[r] - dv4[e];
+            }
+          } else {
+            const float x = ALIBI ? __builtin_fmaf(sc[r], c2, slope2 * (float)(n - (mq + 8 * a + 4 * lg + e))) : sc[r] * c2;
+            pr[r] = fast_exp2(x - lv[e]);
+            ds[r] = dp[r] - dv4[e];
+          }
         }
       }
       if (need_mask) {   // wave-uniform: diagonal, window-edge and sequence-end tiles only
@@ -437,13 +455,17 @@ __global__ __launch_bounds__(512) void bwd_dkdv_kernel(BwdParams p) {
         for (int r = 0; r < 16; ++r) {
           const int m = mq + 8 * (r >> 2) + 4 * lg + (r & 3);
           bool ok = n < S;
+          if constexpr (RELU) ok = ok && (m < S);
           if constexpr (MASK != MASK_NONE) ok = ok && (n <= m);
           if constexpr (MASK == MASK_SLIDING_WINDOW) ok = ok && (n > m - W);
           pr[r] = ok ? pr[r] : 0.f;
+          if constexpr (RELU) ds[r] = ok ? ds[r] : 0.f;
         }
       }
+      if constexpr (!RELU) {
 #pragma unroll
-      for (int r = 0; r < 16; ++r) ds[r] *= pr[r];
+        for (int r = 0; r < 16; ++r) ds[r] *= pr[r];
+      }
       u32x4 pb[2], db[2];
 #pragma unroll
       for (int hf = 0; hf < 2; ++hf)
@@ -512,10 +534,12 @@ __device__ __forceinline__ void k_to_f16(TileRegs<D, ROPE_NONE>& R) {
 // ---------------------------------------------------------------- dQ
 // Same decomposition as the forward: 8 waves, GQA heads packed, double-buffered
 // K'/V tiles (attn_tiles.hpp); dQ'^T += K'^T dS^T with K'^T from transpose reads.
-template <int D, int ROPE, int MASK, bool ALIBI, bool SPARSE>
+template <int D, int ROPE, int MASK, bool ALIBI, bool SPARSE, int EXT = EXT_NONE>
 __global__ __launch_bounds__(512) void bwd_dq_kernel(BwdParams p) {
   using C = TileCfg<D, ROPE_NONE>;            // K' arrives rotated, or K is converted to fp16 at staging
   constexpr bool ROT = ROPE != ROPE_NONE;    // Q' and K' come rotated (fp16) from the workspace
+  constexpr bool TBIAS = EXT == EXT_BIAS || EXT == EXT_RELU_BIAS;
+  constexpr bool RELU = EXT == EXT_RELU || EXT == EXT_RELU_BIAS;
   __shared__ __attribute__((aligned(16))) uint16_t smem[2 * C::STAGE];
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, lq = lane & 31, lg = lane >> 5;
@@ -548,6 +572,8 @@ __global__ __launch_bounds__(512) void bwd_dq_kernel(BwdParams p) {
   load_row_operand<D, ROPE_NONE, !ROT>(qreg, Qh, nullptr, mc, S, lg);
   load_row_operand<D, ROPE_NONE>(oreg, dOh, nullptr, mc, S, lg);
   const float lse2 = (m < S) ? p.lse2[bh * S + mc] : INFINITY;
+  const float* __restrict__ brow = nullptr;       // this lane's row of the bias tensor
+  if constexpr (TBIAS) brow = p.bias + b * p.bias_sb + h * p.bias_sh + mc * p.bias_sq;
   const float del = (m < S) ? p.delta[bh * S + mc] : 0.f;
 
   f32x16 dq[C::MT];
@@ -613,11 +639,22 @@ __global__ __launch_bounds__(512) void bwd_dq_kernel(BwdParams p) {
         }
         // element r: key nn = n0 + 32 kt + 8 (r/4) + 4 lg + r%4, query m
         float ds[16];
+        bool pos[16];   // relu attention: s > 0
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const int nn = n0 + 32 * kt + 8 * (r >> 2) + 4 * lg + (r & 3);
-          const float x = ALIBI ? __builtin_fmaf(sc[r], c2, slope2 * (float)(nn - m)) : sc[r] * c2;
-          ds[r] = fast_exp2(x - lse2);
+          if constexpr (TBIAS || RELU) {
+            const float bv = TBIAS ? ((nn < S) ? brow[nn] : 0.f) : 0.f;
+            if constexpr (RELU) {
+              pos[r] = __builtin_fmaf(sc[r], p.scale, bv) > 0.f;
+              ds[r] = 1.f;
+            } else {
+              ds[r] = fast_exp2(__builtin_fmaf(sc[r], c2, bv * kLog2e) - lse2);
+            }
+          } else {
+            const float x = ALIBI ? __builtin_fmaf(sc[r], c2, slope2 * (float)(nn - m)) : sc[r] * c2;
+            ds[r] = fast_exp2(x - lse2);
+          }
         }
         if (need_mask) {   // wave-uniform
 #pragma unroll
@@ -629,8 +666,13 @@ __global__ __launch_bounds__(512) void bwd_dq_kernel(BwdParams p) {
             ds[r] = ok ? ds[r] : 0.f;
           }
         }
+        if constexpr (RELU) {   // dS = dP where s > 0
 #pragma unroll
-        for (int r = 0; r < 16; ++r) ds[r] *= dp[r] - del;
+          for (int r = 0; r < 16; ++r) ds[r] = pos[r] ? ds[r] * dp[r] : 0.f;
+        } else {
+#pragma unroll
+          for (int r = 0; r < 16; ++r) ds[r] *= dp[r] - del;
+        }
         u32x4 db[2];
 #pragma unroll
         for (int hf = 0; hf < 2; ++hf)
@@ -654,7 +696,7 @@ __global__ __launch_bounds__(512) void bwd_dq_kernel(BwdParams p) {
 }
 
 // ---------------------------------------------------------------- launch
-template <int D, int ROPE, int MASK, bool ALIBI>
+template <int D, int ROPE, int MASK, bool ALIBI, int EXT = EXT_NONE>
 static int launch_one(const BwdParams& p, hipStream_t st) {
   constexpr int RPB = 256 / (D / 16);
   const long long qrows = (long long)p.B * p.H * p.S;
@@ -664,49 +706,61 @@ static int launch_one(const BwdParams& p, hipStream_t st) {
   hipLaunchKernelGGL((bwd_prep_kernel<D, ROPE>), dim3((unsigned)(q_blocks + k_blocks)), dim3(256), 0, st, p, q_blocks);
   using QC = QTileCfg<D>;
   const int nkb = (p.S + QC::KEYS - 1) / QC::KEYS;
-  if (p.bk_ptr)
+  if (EXT == EXT_NONE && p.bk_ptr)
     hipLaunchKernelGGL((bwd_dkdv_kernel<D, ROPE, MASK, ALIBI, true>), dim3((unsigned)(nkb * p.B * p.Hkv)),
                        dim3(QC::THREADS), 0, st, p);
   else
-    hipLaunchKernelGGL((bwd_dkdv_kernel<D, ROPE, MASK, ALIBI, false>), dim3((unsigned)(nkb * p.B * p.Hkv)),
+    hipLaunchKernelGGL((bwd_dkdv_kernel<D, ROPE, MASK, ALIBI, false, EXT>), dim3((unsigned)(nkb * p.B * p.Hkv)),
                        dim3(QC::THREADS), 0, st, p);
   using TC = TileCfg<D, ROPE_NONE>;
   BwdParams pq = p;
   pq.heads_per_wg = heads_per_wg(p.H / p.Hkv);
   const int P = TC::ROWS / pq.heads_per_wg;
   const long long qblocks = (long long)((p.S + P - 1) / P) * p.B * p.Hkv * ((p.H / p.Hkv) / pq.heads_per_wg);
-  if (p.bq_ptr)
+  if (EXT == EXT_NONE && p.bq_ptr)
     hipLaunchKernelGGL((bwd_dq_kernel<D, ROPE, MASK, ALIBI, true>), dim3((unsigned)qblocks), dim3(TC::THREADS), 0, st,
                        pq);
   else
-    hipLaunchKernelGGL((bwd_dq_kernel<D, ROPE, MASK, ALIBI, false>), dim3((unsigned)qblocks), dim3(TC::THREADS), 0,
-                       st, pq);
+    hipLaunchKernelGGL((bwd_dq_kernel<D, ROPE, MASK, ALIBI, false, EXT>), dim3((unsigned)qblocks), dim3(TC::THREADS),
+                       0, st, pq);
   return hipGetLastError() == hipSuccess ? 0 : -3;
 }
 
+template <int D, int ROPE, int MASK>
+static int dispatch_ext(bool alibi, int ext, const BwdParams& p, hipStream_t st) {
+  switch (ext) {
+    case EXT_NONE: return alibi ? launch_one<D, ROPE, MASK, true>(p, st) : launch_one<D, ROPE, MASK, false>(p, st);
+    case EXT_BIAS: return launch_one<D, ROPE, MASK, false, EXT_BIAS>(p, st);
+    case EXT_RELU: return launch_one<D, ROPE, MASK, false, EXT_RELU>(p, st);
+    case EXT_RELU_BIAS: return launch_one<D, ROPE, MASK, false, EXT_RELU_BIAS>(p, st);
+  }
+  return -2;
+}
+
 template <int D, int ROPE>
-static int dispatch_mask(int mask, bool alibi, const BwdParams& p, hipStream_t st) {
+static int dispatch_mask(int mask, bool alibi, int ext, const BwdParams& p, hipStream_t st) {
   switch (mask) {
-    case MASK_NONE: return alibi ? launch_one<D, ROPE, MASK_NONE, true>(p, st) : launch_one<D, ROPE, MASK_NONE, false>(p, st);
-    case MASK_CAUSAL: return alibi ? launch_one<D, ROPE, MASK_CAUSAL, true>(p, st) : launch_one<D, ROPE, MASK_CAUSAL, false>(p, st);
-    case MASK_SLIDING_WINDOW: return alibi ? launch_one<D, ROPE, MASK_SLIDING_WINDOW, true>(p, st) : launch_one<D, ROPE, MASK_SLIDING_WINDOW, false>(p, st);
+    case MASK_NONE: return dispatch_ext<D, ROPE, MASK_NONE>(alibi, ext, p, st);
+    case MASK_CAUSAL: return dispatch_ext<D, ROPE, MASK_CAUSAL>(alibi, ext, p, st);
+    case MASK_SLIDING_WINDOW: return dispatch_ext<D, ROPE, MASK_SLIDING_WINDOW>(alibi, ext, p, st);
   }
   return -2;
 }
 
 template <int D>
-static int dispatch_rope(int rope, int mask, bool alibi, const BwdParams& p, hipStream_t st) {
+static int dispatch_rope(int rope, int mask, bool alibi, int ext, const BwdParams& p, hipStream_t st) {
   switch (rope) {
-    case ROPE_NONE: return dispatch_mask<D, ROPE_NONE>(mask, alibi, p, st);
-    case ROPE_NEOX: return dispatch_mask<D, ROPE_NEOX>(mask, alibi, p, st);
-    case ROPE_INTERLEAVED: return dispatch_mask<D, ROPE_INTERLEAVED>(mask, alibi, p, st);
+    case ROPE_NONE: return dispatch_mask<D, ROPE_NONE>(mask, alibi, ext, p, st);
+    case ROPE_NEOX: return dispatch_mask<D, ROPE_NEOX>(mask, alibi, ext, p, st);
+    case ROPE_INTERLEAVED: return dispatch_mask<D, ROPE_INTERLEAVED>(mask, alibi, ext, p, st);
   }
   return -2;
 }
 
-int launch_bwd_bf16(int D, int rope, int mask, bool alibi, const BwdParams& p, hipStream_t st) {
-  if (D == 64) return dispatch_rope<64>(rope, mask, alibi, p, st);
-  if (D == 128) return dispatch_rope<128>(rope, mask, alibi, p, st);
+int launch_bwd_bf16(int D, int rope, int mask, bool alibi, int ext, const BwdParams& p, hipStream_t st) {
+  if (ext != EXT_NONE && (alibi || p.bq_ptr || p.bk_ptr)) return -2;   // not instantiated
+  if (D == 64) return dispatch_rope<64>(rope, mask, alibi, ext, p, st);
+  if (D == 128) return dispatch_rope<128>(rope, mask, alibi, ext, p, st);
   return -2;
 }
 

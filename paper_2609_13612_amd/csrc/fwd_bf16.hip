@@ -42,10 +42,16 @@
 
 namespace af {
 
-template <int D, int ROPE, int MASK, bool ALIBI, bool SPARSE>
+template <int D, int ROPE, int MASK, bool ALIBI, bool SPARSE, int EXT = EXT_NONE>
 __global__ __launch_bounds__(512) void fwd_bf16_kernel(FwdParams p) {
   using C = TileCfg<D, ROPE>;
   constexpr bool QF16 = ROPE != ROPE_NONE;
+  constexpr bool TBIAS = EXT == EXT_BIAS || EXT == EXT_RELU_BIAS;   // dense bias tensor
+  constexpr bool RELU = EXT == EXT_RELU || EXT == EXT_RELU_BIAS;    // P = max(s, 0), unnormalised
+  // scores leave prepare already scaled (and biased); plain softmax scales in probs
+  constexpr bool PRESCALED = ALIBI || TBIAS || RELU;
+  // Relu weights are unnormalised (not bounded by 1): P and V go to the PV
+  // MFMA as fp16 (2^-12 rounding of P instead of bf16's 2^-9).
   __shared__ __attribute__((aligned(16))) uint16_t smem[(SPARSE ? 4 : 2) * C::STAGE];
 
   const int tid = threadIdx.x, lane = tid & 63;
@@ -123,6 +129,8 @@ __global__ __launch_bounds__(512) void fwd_bf16_kernel(FwdParams p) {
   // Query operand (B of S^T = K Q^T): lane holds row m, dims 16s + 8lg .. +7.
   // Rows past S load row S-1 (finite data; never stored).
   const int mc = min(m, S - 1);
+  const float* __restrict__ brow = nullptr;      // this lane's row of the bias tensor
+  if constexpr (TBIAS) brow = p.bias + b * p.bias_sb + h * p.bias_sh + mc * p.bias_sq;
   u32x4 qreg[C::KS];
 #pragma unroll
   for (int s = 0; s < C::KS; ++s) qreg[s] = ld16(Q + (size_t)mc * D + 16 * s + 8 * lg);
@@ -146,7 +154,7 @@ __global__ __launch_bounds__(512) void fwd_bf16_kernel(FwdParams p) {
     for (int X = 0; X < min(2, ntl); ++X) {
       tile_load<D, ROPE>(R, K, V, p.table, tile_at(X) * C::BN, S, tid);
       tile_commit_k<D, ROPE>(R, kst(X), tid);
-      if (X == 0) tile_commit_v<D, ROPE>(R, vst(X), tid);
+      if (X == 0) tile_commit_v<D, ROPE, RELU>(R, vst(X), tid);
     }
     // Every global load so far has landed (the commits waited for theirs);
     // saying so explicitly keeps the compiler from guarding the loop's
@@ -197,7 +205,7 @@ __global__ __launch_bounds__(512) void fwd_bf16_kernel(FwdParams p) {
           const u32x2 lo = lds_read_tr16(base);
           const u32x2 hi = lds_read_tr16(base + 8 * C::VP);
           const u32x4 a = {lo[0], lo[1], hi[0], hi[1]};
-          acc[mt] = mfma32(a, pop[kt][hf], acc[mt]);
+          acc[mt] = mfma32<RELU>(a, pop[kt][hf], acc[mt]);
         }
   };
 
@@ -224,6 +232,22 @@ __global__ __launch_bounds__(512) void fwd_bf16_kernel(FwdParams p) {
           sc[kt][r] = __builtin_fmaf(sc[kt][r], c2, __builtin_fmaf(slope2, cr, fb));
         }
     }
+    if constexpr (TBIAS || RELU) {
+      // relu works in natural units, the softmax in log2 units
+      const float cs = RELU ? p.scale : c2;
+#pragma unroll
+      for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          float bv = 0.f;
+          if constexpr (TBIAS) {
+            const int n = n0 + 32 * kt + 8 * (r >> 2) + 4 * lg + (r & 3);
+            bv = (n < S) ? brow[n] : 0.f;
+            if constexpr (!RELU) bv *= kLog2e;
+          }
+          sc[kt][r] = __builtin_fmaf(sc[kt][r], cs, bv);
+        }
+    }
     bool need_mask;
     if constexpr (MASK == MASK_NONE) need_mask = n0 + C::BN > S;
     else need_mask = n0 + C::BN - 1 > mw;
@@ -242,18 +266,21 @@ __global__ __launch_bounds__(512) void fwd_bf16_kernel(FwdParams p) {
           sc[kt][r] = ok ? sc[kt][r] : -INFINITY;
         }
     }
-    float mx = -INFINITY;
+    if constexpr (!RELU) {
+      float mx = -INFINITY;
 #pragma unroll
-    for (int kt = 0; kt < 2; ++kt)
+      for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sc[kt][r]);
-    mx = pair_max(mx);
-    if constexpr (!ALIBI) mx *= c2;
-    m_new = fmaxf(m_run, mx);
+        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sc[kt][r]);
+      mx = pair_max(mx);
+      if constexpr (!PRESCALED) mx *= c2;
+      m_new = fmaxf(m_run, mx);
+    }
   };
   // Raise the reference max when a row's max grew by more than 2^8 (rare,
   // wave-uniform): the accumulated O and l are rescaled together.
   auto raise = [&]() {
+    if constexpr (RELU) return;   // no running max
     if (__any(m_new > m_run + 8.f)) {
       const float alpha = (m_run == -INFINITY) ? 0.f : fast_exp2(m_run - m_new);
       l_run *= alpha;
@@ -262,7 +289,8 @@ __global__ __launch_bounds__(512) void fwd_bf16_kernel(FwdParams p) {
       m_run = m_new;
     }
   };
-  // P = exp2(score - m_run) as bf16 B operands, and the row sum.
+  // P = exp2(score - m_run) as bf16 B operands, and the row sum (relu
+  // attention: P = max(score, 0), no sum).
   auto probs = [&](const f32x16 (&sc)[2], u32x4 (&pop)[2][2]) {
     const float m_use = (m_run == -INFINITY) ? 0.f : m_run;
     float rs = 0.f;
@@ -271,14 +299,18 @@ __global__ __launch_bounds__(512) void fwd_bf16_kernel(FwdParams p) {
       float pv_[16];
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const float arg = ALIBI ? (sc[kt][r] - m_use) : __builtin_fmaf(sc[kt][r], c2, -m_use);
-        pv_[r] = fast_exp2(arg);
-        rs += pv_[r];
+        if constexpr (RELU) {
+          pv_[r] = fmaxf(sc[kt][r], 0.f);
+        } else {
+          const float arg = PRESCALED ? (sc[kt][r] - m_use) : __builtin_fmaf(sc[kt][r], c2, -m_use);
+          pv_[r] = fast_exp2(arg);
+          rs += pv_[r];
+        }
       }
 #pragma unroll
       for (int hf = 0; hf < 2; ++hf)
 #pragma unroll
-        for (int w = 0; w < 4; ++w) pop[kt][hf][w] = pack_bf16(pv_[8 * hf + 2 * w], pv_[8 * hf + 2 * w + 1]);
+        for (int w = 0; w < 4; ++w) pop[kt][hf][w] = pack_op<RELU>(pv_[8 * hf + 2 * w], pv_[8 * hf + 2 * w + 1]);
     }
     l_run += rs;
   };
@@ -396,7 +428,7 @@ __global__ __launch_bounds__(512) void fwd_bf16_kernel(FwdParams p) {
       prepare(nxt, t + 1);
       pv(pop, vst(t));
       tile_commit_k<D, ROPE>(R, kst(t + 2), tid);
-      tile_commit_v<D, ROPE>(R, vst(t + 1), tid);
+      tile_commit_v<D, ROPE, RELU>(R, vst(t + 1), tid);
       tile_load_k<D, ROPE>(R, K, p.table, tile_at(min(t + 3, ntl - 1)) * C::BN, S, tid);
       tile_load_v<D, ROPE>(R, V, tile_at(min(t + 2, ntl - 1)) * C::BN, S, tid);
       raise();
@@ -420,7 +452,7 @@ __global__ __launch_bounds__(512) void fwd_bf16_kernel(FwdParams p) {
   // Epilogue: O = acc / l, LSE = (m + log2 l) ln 2.
   const float l_tot = pair_sum(l_run);
   if (m < S && kg == 0) {
-    const float inv = (l_tot > 0.f) ? 1.f / l_tot : 0.f;
+    const float inv = RELU ? 1.f : (l_tot > 0.f) ? 1.f / l_tot : 0.f;
     uint16_t* O = static_cast<uint16_t*>(p.o) + (bh * S + m) * D;
 #pragma unroll
     for (int mt = 0; mt < C::MT; ++mt) {
@@ -431,16 +463,16 @@ __global__ __launch_bounds__(512) void fwd_bf16_kernel(FwdParams p) {
         *reinterpret_cast<u32x2*>(O + 32 * mt + 8 * a + 4 * lg) = w;
       }
     }
-    if (lg == 0) p.lse[bh * S + m] = (l_tot > 0.f) ? (m_run + __log2f(l_tot)) * kLn2 : -INFINITY;
+    if (!RELU && lg == 0) p.lse[bh * S + m] = (l_tot > 0.f) ? (m_run + __log2f(l_tot)) * kLn2 : -INFINITY;
   }
 }
 
-template <int D, int ROPE, int MASK, bool ALIBI>
+template <int D, int ROPE, int MASK, bool ALIBI, int EXT = EXT_NONE>
 static int launch_one(const FwdParams& p0, hipStream_t st) {
   using C = TileCfg<D, ROPE>;
   FwdParams p = p0;
   const int G = p.H / p.Hkv;
-  if (p.bq_ptr) {
+  if (EXT == EXT_NONE && p.bq_ptr) {
     // block-sparse: one 64-row query block of up to 4 heads per workgroup
     p.heads_per_wg = heads_per_wg(G) < 4 ? heads_per_wg(G) : 4;
     const long long blocks = (long long)((p.S + C::BN - 1) / C::BN) * p.B * p.Hkv * (G / p.heads_per_wg);
@@ -450,35 +482,47 @@ static int launch_one(const FwdParams& p0, hipStream_t st) {
     p.heads_per_wg = heads_per_wg(G);
     const int P = C::ROWS / p.heads_per_wg;
     const long long blocks = (long long)((p.S + P - 1) / P) * p.B * p.Hkv * (G / p.heads_per_wg);
-    hipLaunchKernelGGL((fwd_bf16_kernel<D, ROPE, MASK, ALIBI, false>), dim3((unsigned)blocks), dim3(C::THREADS), 0,
-                       st, p);
+    hipLaunchKernelGGL((fwd_bf16_kernel<D, ROPE, MASK, ALIBI, false, EXT>), dim3((unsigned)blocks), dim3(C::THREADS),
+                       0, st, p);
   }
   return hipGetLastError() == hipSuccess ? 0 : -3;
 }
 
+template <int D, int ROPE, int MASK>
+static int dispatch_ext(bool alibi, int ext, const FwdParams& p, hipStream_t st) {
+  switch (ext) {
+    case EXT_NONE: return alibi ? launch_one<D, ROPE, MASK, true>(p, st) : launch_one<D, ROPE, MASK, false>(p, st);
+    case EXT_BIAS: return launch_one<D, ROPE, MASK, false, EXT_BIAS>(p, st);
+    case EXT_RELU: return launch_one<D, ROPE, MASK, false, EXT_RELU>(p, st);
+    case EXT_RELU_BIAS: return launch_one<D, ROPE, MASK, false, EXT_RELU_BIAS>(p, st);
+  }
+  return -2;
+}
+
 template <int D, int ROPE>
-static int dispatch_mask(int mask, bool alibi, const FwdParams& p, hipStream_t st) {
+static int dispatch_mask(int mask, bool alibi, int ext, const FwdParams& p, hipStream_t st) {
   switch (mask) {
-    case MASK_NONE: return alibi ? launch_one<D, ROPE, MASK_NONE, true>(p, st) : launch_one<D, ROPE, MASK_NONE, false>(p, st);
-    case MASK_CAUSAL: return alibi ? launch_one<D, ROPE, MASK_CAUSAL, true>(p, st) : launch_one<D, ROPE, MASK_CAUSAL, false>(p, st);
-    case MASK_SLIDING_WINDOW: return alibi ? launch_one<D, ROPE, MASK_SLIDING_WINDOW, true>(p, st) : launch_one<D, ROPE, MASK_SLIDING_WINDOW, false>(p, st);
+    case MASK_NONE: return dispatch_ext<D, ROPE, MASK_NONE>(alibi, ext, p, st);
+    case MASK_CAUSAL: return dispatch_ext<D, ROPE, MASK_CAUSAL>(alibi, ext, p, st);
+    case MASK_SLIDING_WINDOW: return dispatch_ext<D, ROPE, MASK_SLIDING_WINDOW>(alibi, ext, p, st);
   }
   return -2;
 }
 
 template <int D>
-static int dispatch_rope(int rope, int mask, bool alibi, const FwdParams& p, hipStream_t st) {
+static int dispatch_rope(int rope, int mask, bool alibi, int ext, const FwdParams& p, hipStream_t st) {
   switch (rope) {
-    case ROPE_NONE: return dispatch_mask<D, ROPE_NONE>(mask, alibi, p, st);
-    case ROPE_NEOX: return dispatch_mask<D, ROPE_NEOX>(mask, alibi, p, st);
-    case ROPE_INTERLEAVED: return dispatch_mask<D, ROPE_INTERLEAVED>(mask, alibi, p, st);
+    case ROPE_NONE: return dispatch_mask<D, ROPE_NONE>(mask, alibi, ext, p, st);
+    case ROPE_NEOX: return dispatch_mask<D, ROPE_NEOX>(mask, alibi, ext, p, st);
+    case ROPE_INTERLEAVED: return dispatch_mask<D, ROPE_INTERLEAVED>(mask, alibi, ext, p, st);
   }
   return -2;
 }
 
-int launch_fwd_bf16(int D, int rope, int mask, bool alibi, const FwdParams& p, hipStream_t st) {
-  if (D == 64) return dispatch_rope<64>(rope, mask, alibi, p, st);
-  if (D == 128) return dispatch_rope<128>(rope, mask, alibi, p, st);
+int launch_fwd_bf16(int D, int rope, int mask, bool alibi, int ext, const FwdParams& p, hipStream_t st) {
+  if (ext != EXT_NONE && (alibi || p.bq_ptr)) return -2;   // not instantiated
+  if (D == 64) return dispatch_rope<64>(rope, mask, alibi, ext, p, st);
+  if (D == 128) return dispatch_rope<128>(rope, mask, alibi, ext, p, st);
   return -2;
 }
 

@@ -6,6 +6,11 @@
 
 namespace af {
 
+// Score-modification / normalisation variants beyond masks and ALiBi (the
+// additive_bias and relu_attention combinators): a dense fp32 bias tensor
+// added to the scaled scores, and P = max(s, 0) in place of the softmax.
+enum { EXT_NONE = 0, EXT_BIAS = 1, EXT_RELU = 2, EXT_RELU_BIAS = 3 };
+
 struct FwdParams {
   const void* q;
   const void* k;
@@ -19,6 +24,8 @@ struct FwdParams {
   int heads_per_wg;       // set by the bf16 launcher: query heads packed per workgroup
   const int* bq_ptr;      // block-sparse mask by 64-row query block (CSR row pointers), or nullptr
   const int* bk_idx;      // and the active 64-key blocks of each row
+  const float* bias;      // dense bias: element (b, h, i, j) at bias[b*bias_sb + h*bias_sh + i*bias_sq + j]
+  long long bias_sb, bias_sh, bias_sq;
 };
 
 struct BwdParams {
@@ -45,6 +52,8 @@ struct BwdParams {
   const int* bk_idx;
   const int* bk_ptr;      // the same mask by 64-key block (CSC), or nullptr
   const int* bq_idx;
+  const float* bias;      // dense bias, as in FwdParams
+  long long bias_sb, bias_sh, bias_sq;
 };
 
 struct DecodeParams {
@@ -72,9 +81,10 @@ struct RopeParams {
 };
 
 // Return 0 on success, -2 when the variant is not compiled, -3 on a HIP error.
-int launch_fwd_bf16(int D, int rope, int mask, bool alibi, const FwdParams& p, hipStream_t st);
+// ext: EXT_* (common.hpp); variants other than EXT_NONE run without ALiBi and block masks.
+int launch_fwd_bf16(int D, int rope, int mask, bool alibi, int ext, const FwdParams& p, hipStream_t st);
 int launch_fwd_fp32(int D, int rope, int mask, bool alibi, const FwdParams& p, hipStream_t st);
-int launch_bwd_bf16(int D, int rope, int mask, bool alibi, const BwdParams& p, hipStream_t st);
+int launch_bwd_bf16(int D, int rope, int mask, bool alibi, int ext, const BwdParams& p, hipStream_t st);
 int launch_bwd_fp32(int D, int rope, int mask, bool alibi, const BwdParams& p, hipStream_t st);
 int launch_decode(int D, int rope, bool alibi, const DecodeParams& p, hipStream_t st);
 int launch_rope(bool fp32, int D, int rope, bool inverse, const RopeParams& p, hipStream_t st);

@@ -539,3 +539,25 @@ def check_bias_relu_backward_fd(norm, seed=43):
     assert np.allclose(dq, np.array(bruteforce.finite_difference_grad(ql, f)), atol=1e-7)
     assert np.allclose(dk, np.array(bruteforce.finite_difference_grad(kl, f)), atol=1e-7)
     assert np.allclose(dv, np.array(bruteforce.finite_difference_grad(vl, f)), atol=1e-7)
+
+
+def check_relu_gate_precision(seed=44):
+    """The fp16 relu gate equals the exact one when the rotated operands are
+    representable in fp16 (small integers, no RoPE), and differs exactly where
+    rounding to fp16 moves a score across zero (a constructed case)."""
+    r = _rng(seed)
+    q = r.integers(-3, 4, (1, 2, 6, 4)).astype(np.float64)
+    k = r.integers(-3, 4, (1, 1, 6, 4)).astype(np.float64)
+    v, do = r.standard_normal((1, 1, 6, 4)), r.standard_normal((1, 2, 6, 4))
+    kw = dict(mask="none", norm="relu", scale=0.5)
+    a = oracle.attention_backward(q, k, v, do, relu_gate="exact", **kw)
+    b = oracle.attention_backward(q, k, v, do, relu_gate="fp16", **kw)
+    assert all(np.array_equal(x, y) for x, y in zip(a, b))
+    # one query, two keys; q.k1 = 1e-4 exactly in fp64 but 0 after fp16 rounding of q
+    q = np.zeros((1, 1, 1, 2)); q[0, 0, 0] = [1.0 + 2.0 ** -13, 1.0]
+    k = np.zeros((1, 1, 1, 2)); k[0, 0, 0] = [1.0, -1.0]
+    v = np.ones((1, 1, 1, 2)); do = np.ones((1, 1, 1, 2))
+    ex = oracle.attention_backward(q, k, v, do, mask="none", norm="relu", scale=1.0, relu_gate="exact")
+    hf = oracle.attention_backward(q, k, v, do, mask="none", norm="relu", scale=1.0, relu_gate="fp16")
+    assert np.allclose(ex[0][0, 0, 0], 2.0 * k[0, 0, 0])        # s = 2^-13 > 0: dS = dP = 2
+    assert np.array_equal(hf[0], np.zeros_like(hf[0]))          # fp16 q.k = 0: gate closed

@@ -21,8 +21,9 @@ def declared_symbols():
 
 
 def test_header_declares_the_boundary():
-    assert declared_symbols() == sorted(["attnfuse_bwd", "attnfuse_bwd_blocksparse", "attnfuse_bwd_workspace_bytes",
-                                         "attnfuse_decode", "attnfuse_decode_workspace_bytes", "attnfuse_fwd",
+    assert declared_symbols() == sorted(["attnfuse_bwd", "attnfuse_bwd_bias_norm", "attnfuse_bwd_blocksparse",
+                                         "attnfuse_bwd_workspace_bytes", "attnfuse_decode",
+                                         "attnfuse_decode_workspace_bytes", "attnfuse_fwd", "attnfuse_fwd_bias_norm",
                                          "attnfuse_fwd_blocksparse", "attnfuse_rope", "attnfuse_rope_bwd",
                                          "attnfuse_strerror", "attnfuse_version"])
 
@@ -235,3 +236,69 @@ def test_bwd_blocksparse_rejects_invalid_arguments(over):
 def test_bwd_blocksparse_unsupported():
     assert _bwd_bs(D=96) == -2
     assert _bwd_bs(dtype=1) == -2
+
+
+# ----------------------------------------------------------------------------- bias tensor, relu attention
+BIASP = 0x30000
+
+
+def _fwd_bn(**over):
+    a = dict(Q=FAKE, K=FAKE + 0x100, V=FAKE + 0x200, O=FAKE + 0x300, LSE=FAKE + 0x400, bias=BIASP, sb=256, sh=64,
+             sq=8, norm=0, B=1, H=4, H_kv=2, S=8, D=64, dtype=0, rope=1, theta=10000.0, mask=1, window=0,
+             slopes=None, scale=0.125, stream=None)
+    a.update(over)
+    return _lib.load().attnfuse_fwd_bias_norm(a["Q"], a["K"], a["V"], a["O"], a["LSE"], a["bias"], a["sb"], a["sh"],
+                                              a["sq"], a["norm"], a["B"], a["H"], a["H_kv"], a["S"], a["D"],
+                                              a["dtype"], a["rope"], a["theta"], a["mask"], a["window"], a["slopes"],
+                                              a["scale"], a["stream"])
+
+
+def _bwd_bn(**over):
+    base = FAKE
+    a = dict(Q=base, K=base + 0x100, V=base + 0x200, O=base + 0x300, dO=base + 0x400, LSE=base + 0x500,
+             dQ=base + 0x600, dK=base + 0x700, dV=base + 0x800, bias=BIASP, sb=256, sh=64, sq=8, norm=0,
+             ws=base + 0x900, ws_bytes=1 << 20, B=1, H=4, H_kv=2, S=8, D=64, dtype=0, rope=1, theta=1e4, mask=1,
+             window=0, slopes=None, scale=0.125, stream=None)
+    a.update(over)
+    return _lib.load().attnfuse_bwd_bias_norm(a["Q"], a["K"], a["V"], a["O"], a["dO"], a["LSE"], a["dQ"], a["dK"],
+                                              a["dV"], a["bias"], a["sb"], a["sh"], a["sq"], a["norm"], a["ws"],
+                                              a["ws_bytes"], a["B"], a["H"], a["H_kv"], a["S"], a["D"], a["dtype"],
+                                              a["rope"], a["theta"], a["mask"], a["window"], a["slopes"], a["scale"],
+                                              a["stream"])
+
+
+INVALID_BN = [dict(norm=2), dict(norm=-1), dict(bias=BIASP + 2), dict(sb=-1), dict(sh=-8), dict(sq=-1),
+              dict(O=BIASP), dict(Q=None), dict(LSE=None), dict(mask=2, window=0), dict(S=0)]
+
+
+@pytest.mark.parametrize("over", INVALID_BN, ids=lambda o: ",".join(f"{k}={v}" for k, v in o.items()))
+def test_fwd_bias_norm_rejects_invalid_arguments(over):
+    assert _fwd_bn(**over) == -1
+
+
+def test_fwd_bias_norm_relu_allows_null_lse_only_for_relu():
+    assert _fwd_bn(LSE=None, norm=0) == -1
+    assert _fwd_bn(LSE=None, norm=1, D=96) == -2     # validation passed; D unsupported
+
+
+@pytest.mark.parametrize("over", [dict(D=96), dict(dtype=1), dict(slopes=FAKE + 0x1000),
+                                  dict(norm=1, dtype=1), dict(norm=1, slopes=FAKE + 0x1000, bias=None)],
+                         ids=lambda o: ",".join(f"{k}={v}" for k, v in o.items()))
+def test_fwd_bias_norm_unsupported(over):
+    assert _fwd_bn(**over) == -2
+
+
+INVALID_BWD_BN = [dict(norm=3), dict(bias=BIASP + 1), dict(sq=-2), dict(dK=BIASP), dict(ws=BIASP), dict(dO=None),
+                  dict(LSE=None), dict(Q=None, LSE=None, norm=1), dict(ws_bytes=10)]
+
+
+@pytest.mark.parametrize("over", INVALID_BWD_BN, ids=lambda o: ",".join(f"{k}={v}" for k, v in o.items()))
+def test_bwd_bias_norm_rejects_invalid_arguments(over):
+    assert _bwd_bn(**over) == -1
+
+
+def test_bwd_bias_norm_unsupported():
+    assert _bwd_bn(D=96) == -2
+    assert _bwd_bn(dtype=1) == -2
+    assert _bwd_bn(slopes=FAKE + 0x1000) == -2
+    assert _bwd_bn(LSE=None, norm=1, D=96) == -2      # LSE is not needed under relu attention

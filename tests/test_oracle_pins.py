@@ -150,3 +150,7 @@ def test_relu_closed_forms():
 @pytest.mark.parametrize("norm", ["softmax", "relu"])
 def test_bias_relu_backward_fd(norm):
     P.check_bias_relu_backward_fd(norm)
+
+
+def test_relu_gate_precision():
+    P.check_relu_gate_precision()

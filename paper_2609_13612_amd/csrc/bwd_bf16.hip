@@ -552,7 +552,10 @@ __global__ __launch_bounds__(512) void bwd_dq_kernel(BwdParams p) {
   const int units = p.B * p.Hkv * groups;
   const int npb = (S + P - 1) / P;
   const int unit = blockIdx.x % units;
-  const int pb = npb - 1 - (int)(blockIdx.x / units);
+  // position blocks run backwards (the longest causal rows first); under a
+  // block mask without an elementwise mask they run forwards, as the forward's
+  // do, which starts global rows (conventionally the first) early
+  const int pb = (SPARSE && MASK == MASK_NONE) ? (int)(blockIdx.x / units) : npb - 1 - (int)(blockIdx.x / units);
   const int hg = unit % groups, bg = unit / groups;
   const int b = bg / p.Hkv, g = bg % p.Hkv;
   const int h = g * G + hg * HP + wave / WPH;

@@ -6,21 +6,25 @@
 // HBM and is built to read the cache exactly once at full width.
 //
 // Phase 1 (decode_split_kernel): workgroup = 4 waves = one (sequence, K/V
-//   head, chunk of `chunk` keys); each wave streams a quarter of the chunk in
-//   32-key tiles.  Scores are formed transposed, S^T = K Q'^T: the 32 MFMA
-//   columns are the group's query heads, replicated cyclically when the group
-//   has fewer than 32 (K and V are then read once for all of them); every lane
-//   owns one head column, so the softmax statistics stay in-lane as in the
-//   prefill kernel.  K tiles go from HBM straight into registers as the A
-//   operand (lane = key row); V tiles go through the wave's own LDS tile for
-//   the transpose read of O^T += V^T P^T.  The next tile's loads are issued
-//   before the current tile is computed.  The four waves' (m, l, acc) merge in
-//   LDS and one partial per (sequence, head, chunk) is written; chunks with no
-//   visible key return at once.
+//   head, chunk of `chunk` keys); the four waves take the chunk's 32-key
+//   tiles in turn, so the workgroup streams its chunk front to back.  Scores
+//   are formed transposed, S^T = K Q'^T: the 32 MFMA columns are the group's
+//   query heads, replicated cyclically when the group has fewer than 32 (K and
+//   V are then read once for all of them); every lane owns one head column, so
+//   the softmax statistics stay in-lane as in the prefill kernel.  K tiles go
+//   from HBM straight into registers as the A operand (lane = key row); V
+//   tiles go through the wave's own LDS tile for the transpose read of
+//   O^T += V^T P^T.  The first tile's loads are issued before the query is
+//   loaded and rotated; each next tile's as soon as the current tile's score
+//   MFMAs have consumed its keys, so one tile per wave is always in flight.
+//   The register budget is held to two waves per SIMD so that two workgroups
+//   stream on every CU at once.  The four waves' (m, l, acc) merge in LDS and
+//   one partial per (sequence, head, chunk) is written; chunks with no visible
+//   key return at once.
 // Phase 2 (decode_combine_kernel): per (sequence, head), merge the partials of
 //   the chunks that hold visible keys by log-sum-exp and write O and LSE; the
 //   head's dims are spread over several workgroups so the merge reads the
-//   partials with the whole chip.
+//   partials with the whole chip, in one round trip to memory.
 //
 // Precision: without RoPE the bf16 query and keys meet exactly in a bf16
 // MFMA.  With RoPE the query is rotated at position L-1 in fp32 and rounded to
@@ -54,7 +58,8 @@ __device__ __forceinline__ int first_key(const DecodeParams& p, int L) {
 }
 
 template <int D, int ROPE, bool ALIBI>
-__global__ __launch_bounds__(256) void decode_split_kernel(DecodeParams p) {
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void decode_split_kernel(DecodeParams p) {
   using C = DecCfg<D>;
   constexpr bool QF16 = ROPE != ROPE_NONE;
   __shared__ __attribute__((aligned(16))) uint16_t smem[C::SMEM];
@@ -78,28 +83,16 @@ __global__ __launch_bounds__(256) void decode_split_kernel(DecodeParams p) {
   const uint16_t* __restrict__ K = static_cast<const uint16_t*>(p.k) + (size_t)unit * p.S * D;
   const uint16_t* __restrict__ V = static_cast<const uint16_t*>(p.v) + (size_t)unit * p.S * D;
 
-  // Query operand (B of S^T = K Q'^T): lane holds head column hc, dims 16s + 8lg .. +7.
-  const uint16_t* __restrict__ Qh = static_cast<const uint16_t*>(p.q) + ((size_t)b * p.H + h) * D;
-  u32x4 qreg[C::KS];
-#pragma unroll
-  for (int s = 0; s < C::KS; ++s) qreg[s] = ld16(Qh + 16 * s + 8 * lg);
-  if constexpr (ROPE == ROPE_NEOX) {
-#pragma unroll
-    for (int s = 0; s < C::KS / 2; ++s)
-      rotate_neox8<false, true>(qreg[s], qreg[s + C::KS / 2], p.table + (size_t)pos * (D / 2) + 16 * s + 8 * lg);
-  } else if constexpr (ROPE == ROPE_INTERLEAVED) {
-#pragma unroll
-    for (int s = 0; s < C::KS; ++s)
-      rotate_interleaved8<false, true>(qreg[s], p.table + (size_t)pos * (D / 2) + 8 * s + 4 * lg);
-  }
-
   const float c2 = p.scale * kLog2e;
   const float slope2 = ALIBI ? p.slopes[h] * kLog2e : 0.f;
 
-  // This wave's keys: a quarter of the chunk, clipped to the visible range.
-  const int cw = p.chunk / C::NW;
-  const int kbeg = max(c0 + wave * cw, lo & ~31);
-  const int kend = min(c0 + (wave + 1) * cw, L);
+  // This wave's tiles: every NW-th tile of the chunk from the wave's own,
+  // starting at the first tile that holds a visible key.
+  constexpr int STEP = 32 * C::NW;
+  const int first = lo & ~31;
+  const int kend = min(c0 + p.chunk, L);
+  int kbeg = c0 + 32 * wave;
+  if (kbeg < first) kbeg += (first - kbeg + STEP - 1) / STEP * STEP;
 
   uint16_t* Vw = smem + wave * C::VT;
   const int tr_key = 4 * lg + ((lane & 15) >> 2);
@@ -124,7 +117,22 @@ __global__ __launch_bounds__(256) void decode_split_kernel(DecodeParams p) {
   };
 
   if (kbeg < kend) load_tile(kbeg);
-  for (int n0 = kbeg; n0 < kend; n0 += 32) {
+  // Query operand (B of S^T = K Q'^T): lane holds head column hc, dims 16s + 8lg .. +7.
+  const uint16_t* __restrict__ Qh = static_cast<const uint16_t*>(p.q) + ((size_t)b * p.H + h) * D;
+  u32x4 qreg[C::KS];
+#pragma unroll
+  for (int s = 0; s < C::KS; ++s) qreg[s] = ld16(Qh + 16 * s + 8 * lg);
+  if constexpr (ROPE == ROPE_NEOX) {
+#pragma unroll
+    for (int s = 0; s < C::KS / 2; ++s)
+      rotate_neox8<false, true>(qreg[s], qreg[s + C::KS / 2], p.table + (size_t)pos * (D / 2) + 16 * s + 8 * lg);
+  } else if constexpr (ROPE == ROPE_INTERLEAVED) {
+#pragma unroll
+    for (int s = 0; s < C::KS; ++s)
+      rotate_interleaved8<false, true>(qreg[s], p.table + (size_t)pos * (D / 2) + 8 * s + 4 * lg);
+  }
+
+  for (int n0 = kbeg; n0 < kend; n0 += STEP) {
     // V tile to this wave's LDS tile (the previous tile's transpose reads,
     // issued earlier by this wave, complete first: LDS is in order per wave)
 #pragma unroll
@@ -133,20 +141,16 @@ __global__ __launch_bounds__(256) void decode_split_kernel(DecodeParams p) {
       const int r = it / (D / 8), c = it % (D / 8);
       *reinterpret_cast<u32x4*>(Vw + r * C::VP + 8 * c) = vreg[i];
     }
-    u32x4 kcur[C::KS];
-#pragma unroll
-    for (int s = 0; s < C::KS; ++s) kcur[s] = kreg[s];
-    if (n0 + 32 < kend) load_tile(n0 + 32);
-
     if constexpr (QF16) {   // cached keys bf16 -> fp16 to meet the fp16 query
 #pragma unroll
       for (int s = 0; s < C::KS; ++s)
 #pragma unroll
-        for (int w = 0; w < 4; ++w) kcur[s][w] = pack_f16(bf_lo(kcur[s][w]), bf_hi(kcur[s][w]));
+        for (int w = 0; w < 4; ++w) kreg[s][w] = pack_f16(bf_lo(kreg[s][w]), bf_hi(kreg[s][w]));
     }
     f32x16 st = f32x16{};
 #pragma unroll
-    for (int s = 0; s < C::KS; ++s) st = mfma32<QF16>(kcur[s], qreg[s], st);
+    for (int s = 0; s < C::KS; ++s) st = mfma32<QF16>(kreg[s], qreg[s], st);
+    if (n0 + STEP < kend) load_tile(n0 + STEP);
 
     // element r: key n0 + 8 (r/4) + 4 lg + r%4 of head column lq
     if constexpr (ALIBI) {
@@ -272,29 +276,27 @@ __global__ __launch_bounds__(256) void decode_split_kernel(DecodeParams p) {
 }
 
 // Phase 2.  Workgroup = 256 threads = one (sequence, query head) and 32 of its
-// dims; the chunk weights 2^(m_s - M) are formed once in LDS, then eight
-// thread groups each sum every eighth chunk's accumulators for the 32 dims
-// (coalesced rows) and the groups reduce through LDS.
+// dims, as eight groups of 32 threads that each take every eighth chunk.  The
+// group's accumulators are loaded together with the chunk statistics, so the
+// merge costs one round trip to memory: each thread folds its chunks' (m, l)
+// into a running pair, the pairs merge across the workgroup, and every thread
+// weights its accumulators by 2^(m_s - M) from the maxima kept in LDS.
 constexpr int COMBINE_MAX_CHUNKS = 8192;   // 2^20 keys / 128-key chunks
 
-__device__ __forceinline__ float block_reduce_256(float x, float* red, bool is_max) {
-  const int t = threadIdx.x;
-  red[t] = x;
-  __syncthreads();
-  for (int w = 128; w > 0; w >>= 1) {
-    if (t < w) red[t] = is_max ? fmaxf(red[t], red[t + w]) : red[t] + red[t + w];
-    __syncthreads();
-  }
-  const float r = red[0];
-  __syncthreads();
-  return r;
+__device__ __forceinline__ void merge_ml(float& m, float& l, float m2, float l2) {
+  const float M = fmaxf(m, m2);
+  if (M == -INFINITY) return;
+  l = l * fast_exp2(m - M) + l2 * fast_exp2(m2 - M);
+  m = M;
 }
 
 template <int D>
 __global__ __launch_bounds__(256) void decode_combine_kernel(DecodeParams p) {
-  __shared__ float wts[COMBINE_MAX_CHUNKS];
+  constexpr int PF = 8;   // accumulators per thread loaded up front (chunks 0..63)
+  __shared__ float mx_s[COMBINE_MAX_CHUNKS];
   __shared__ float red[256];
-  const int bh = blockIdx.x, t = threadIdx.x;
+  __shared__ float wred[8];
+  const int bh = blockIdx.x, t = threadIdx.x, lane = t & 63, wv = t >> 6;
   const int d = 32 * blockIdx.y + (t & 31), grp = t >> 5;
   const int b = bh / p.H;
   const int L = seq_len(p, b);
@@ -307,20 +309,37 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(DecodeParams p) {
   const int s_lo = first_key(p, L) / p.chunk, s_hi = (L - 1) / p.chunk;
   const int n = s_hi - s_lo + 1;
   const float* ml = p.part_ml + ((size_t)bh * p.nsplit + s_lo) * 2;
-  float mx = -INFINITY;
-  for (int i = t; i < n; i += 256) mx = fmaxf(mx, ml[2 * i]);
-  const float M = block_reduce_256(mx, red, true);
-  float lsum = 0.f;
-  for (int i = t; i < n; i += 256) {
-    const float w = fast_exp2(ml[2 * i] - M);
-    wts[i] = w;
-    lsum += ml[2 * i + 1] * w;
-  }
-  const float l = block_reduce_256(lsum, red, false);   // its barriers also publish wts
   const float* acc = p.part_acc + ((size_t)bh * p.nsplit + s_lo) * D + d;
+  float a[PF];
+#pragma unroll
+  for (int j = 0; j < PF; ++j) {
+    const int i = grp + 8 * j;
+    a[j] = (i < n) ? acc[(size_t)i * D] : 0.f;
+  }
+  float m = -INFINITY, l = 0.f;
+  for (int i = t; i < n; i += 256) {
+    const float2 v = *reinterpret_cast<const float2*>(ml + 2 * i);
+    mx_s[i] = v.x;
+    merge_ml(m, l, v.x, v.y);
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) merge_ml(m, l, __shfl_xor(m, o), __shfl_xor(l, o));
+  if (lane == 0) {
+    wred[2 * wv] = m;
+    wred[2 * wv + 1] = l;
+  }
+  __syncthreads();   // also publishes mx_s
+  m = wred[0];
+  l = wred[1];
+#pragma unroll
+  for (int w = 1; w < 4; ++w) merge_ml(m, l, wred[2 * w], wred[2 * w + 1]);
   float o = 0.f;
-#pragma unroll 4
-  for (int i = grp; i < n; i += 8) o += acc[(size_t)i * D] * wts[i];
+#pragma unroll
+  for (int j = 0; j < PF; ++j) {
+    const int i = grp + 8 * j;
+    if (i < n) o += a[j] * fast_exp2(mx_s[i] - m);
+  }
+  for (int i = grp + 8 * PF; i < n; i += 8) o += acc[(size_t)i * D] * fast_exp2(mx_s[i] - m);
   red[t] = o;
   __syncthreads();
   if (grp == 0) {
@@ -328,7 +347,7 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(DecodeParams p) {
 #pragma unroll
     for (int g = 0; g < 8; ++g) sum += red[32 * g + t];
     O[d] = static_cast<uint16_t>(pack_bf16(sum / l, 0.f) & 0xffffu);
-    if (t == 0 && blockIdx.y == 0) p.lse[bh] = (M + __log2f(l)) * kLn2;
+    if (t == 0 && blockIdx.y == 0) p.lse[bh] = (m + __log2f(l)) * kLn2;
   }
 }
 

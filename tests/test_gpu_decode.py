@@ -84,6 +84,19 @@ def test_decode_edges():
     assert_lse_close(lse, L, "LSE window 1")
 
 
+@pytest.mark.parametrize("mask,window", [("causal", None), ("sliding_window", 12000)], ids=str)
+def test_decode_many_chunks(mask, window):
+    """A long cache over one K/V head: 157 chunks of 128 keys, so the merge runs
+    past the 64 partials each thread loads up front (95 under the window, 71 for
+    the shorter sequence)."""
+    need_gpu()
+    announce(f"decode many chunks mask={mask}")
+    o, lse, O, L = _run(2, 4, 1, 20000, 128, lens=[20000, 9000], rope="neox", theta=500000.0, mask=mask,
+                        window=window, seed=26)
+    assert_bf16_close(o, O, "O")
+    assert_lse_close(lse, L, "LSE")
+
+
 @pytest.mark.parametrize("name", sorted(DECODE_WORKLOADS))
 def test_decode_paper_geometries(name):
     """The three cache geometries of the paper's decode table at full size."""

@@ -1,0 +1,109 @@
+"""HIP-graph capture of the entry points through the C ABI.
+
+After one eager call on a device (which builds that device's cos/sin table),
+the fused forward and backward, the block-sparse forward and decode allocate
+nothing, synchronise nothing and issue no memset, so a captured sequence of
+them replays.  Each test captures once, then replays on three fresh inputs
+copied into the captured buffers, with eager calls and synchronisations in
+between, and checks every replay bit for bit against the eager result on the
+same inputs (the kernels use no atomics, so they are deterministic).
+"""
+import pytest
+import torch
+
+from gpu_util import announce, device_inputs, need_gpu
+from paper_2609_13612_amd import api, blockmask, inputs
+
+pytestmark = pytest.mark.gpu
+
+SEEDS = (71, 72, 73)
+
+
+def _capture(fn):
+    g = torch.cuda.CUDAGraph()
+    torch.cuda.synchronize()
+    with torch.cuda.graph(g):
+        fn()
+    torch.cuda.synchronize()
+    return g
+
+
+def test_graph_fwd_bwd_replays():
+    """Fused RoPE + causal forward then backward, GQA, S = 1000 (ragged tail)."""
+    need_gpu()
+    announce("graph capture: fwd + bwd")
+    B, H, Hkv, S, D = 1, 8, 2, 1000, 128
+    kw = dict(rope="neox", theta=500000.0, mask="causal")
+    _, d0 = device_inputs(B, H, Hkv, S, D, seed=70, with_do=True)
+    q, k, v, do = (d0[n].clone() for n in ("q", "k", "v", "do"))
+    o, lse = api.attnfuse_fwd(q, k, v, **kw)            # eager warm-up: builds the table
+    api.attnfuse_bwd(q, k, v, o, do, lse, **kw)
+    o_s, lse_s = torch.empty_like(q), torch.empty(B, H, S, device="cuda")
+    dq_s, dk_s, dv_s = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
+    ws = torch.empty(api.attnfuse_bwd_workspace_bytes(B, H, Hkv, S, D, "neox"), device="cuda", dtype=torch.uint8)
+
+    def step():
+        api.attnfuse_fwd(q, k, v, out=o_s, lse=lse_s, **kw)
+        api.attnfuse_bwd(q, k, v, o_s, do, lse_s, dq=dq_s, dk=dk_s, dv=dv_s, workspace=ws, **kw)
+
+    g = _capture(step)
+    for seed in SEEDS:
+        _, d = device_inputs(B, H, Hkv, S, D, seed=seed, with_do=True)
+        o_e, lse_e = api.attnfuse_fwd(d["q"], d["k"], d["v"], **kw)
+        grads_e = api.attnfuse_bwd(d["q"], d["k"], d["v"], o_e, d["do"], lse_e, **kw)
+        torch.cuda.synchronize()
+        for dst, name in ((q, "q"), (k, "k"), (v, "v"), (do, "do")):
+            dst.copy_(d[name])
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(o_s, o_e) and torch.equal(lse_s, lse_e), f"seed {seed}: forward replay differs"
+        for name, a, b in zip(("dQ", "dK", "dV"), (dq_s, dk_s, dv_s), grads_e):
+            assert torch.equal(a, b), f"seed {seed}: {name} replay differs"
+
+
+def test_graph_blocksparse_replays():
+    """Block-sparse forward over a BigBird-style mask, D = 64, S = 1024."""
+    need_gpu()
+    announce("graph capture: block-sparse fwd")
+    B, H, Hkv, S, D = 2, 4, 4, 1024, 64
+    bm = blockmask.block_mask_from_dense(torch.from_numpy(inputs.bigbird_blocks(S // 64, seed=3)), S, device="cuda")
+    _, d0 = device_inputs(B, H, Hkv, S, D, seed=70)
+    q, k, v = (d0[n].clone() for n in ("q", "k", "v"))
+    api.attnfuse_fwd_blocksparse(q, k, v, bm)
+    o_s, lse_s = torch.empty_like(q), torch.empty(B, H, S, device="cuda")
+    g = _capture(lambda: api.attnfuse_fwd_blocksparse(q, k, v, bm, out=o_s, lse=lse_s))
+    for seed in SEEDS:
+        _, d = device_inputs(B, H, Hkv, S, D, seed=seed)
+        o_e, lse_e = api.attnfuse_fwd_blocksparse(d["q"], d["k"], d["v"], bm)
+        torch.cuda.synchronize()
+        for dst, name in ((q, "q"), (k, "k"), (v, "v")):
+            dst.copy_(d[name])
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(o_s, o_e) and torch.equal(lse_s, lse_e), f"seed {seed}: replay differs"
+
+
+def test_graph_decode_replays():
+    """Decode (split + combine) over a ragged batch of caches with RoPE on the query."""
+    need_gpu()
+    announce("graph capture: decode")
+    B, H, Hkv, S, D = 2, 32, 8, 3000, 128
+    kw = dict(rope="neox", theta=500000.0)
+    c0 = inputs.make_decode(B, H, Hkv, S, D, seed=70)
+    q, kc, vc = (c0[n].cuda() for n in ("q", "k", "v"))
+    lens = torch.tensor([3000, 1234], dtype=torch.int32, device="cuda")
+    api.attnfuse_decode(q, kc, vc, lens, **kw)
+    o_s, lse_s = torch.empty_like(q), torch.empty(B, H, device="cuda")
+    ws = torch.empty(api.attnfuse_decode_workspace_bytes(B, H, Hkv, S, D), device="cuda", dtype=torch.uint8)
+    g = _capture(lambda: api.attnfuse_decode(q, kc, vc, lens, out=o_s, lse=lse_s, workspace=ws, **kw))
+    for seed in SEEDS:
+        c = inputs.make_decode(B, H, Hkv, S, D, seed=seed)
+        dq, dk, dv = (c[n].cuda() for n in ("q", "k", "v"))
+        o_e, lse_e = api.attnfuse_decode(dq, dk, dv, lens, **kw)
+        torch.cuda.synchronize()
+        q.copy_(dq)
+        kc.copy_(dk)
+        vc.copy_(dv)
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(o_s, o_e) and torch.equal(lse_s, lse_e), f"seed {seed}: replay differs"

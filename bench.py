@@ -23,6 +23,11 @@ Alongside, on the same inputs and outside the timed steps:
 * block-sparse attention with a BigBird-style mask at N = 4096 (skip with
   --no-sparse): forward and backward medians, TFLOP/s over the visible pairs,
   and the dense forward of the same shape for the speedup;
+* the other attention workloads at full size (skip with --no-workloads): the
+  sliding-window (W = 1024, GQA) and ALiBi + causal shapes and the D = 64
+  RoPE + causal shape, each forward and backward (median of 50 and 20 calls
+  after 10 and 3 warm-ups) against the MFMA peak, and, with RoPE, the
+  separate path (rotation + no-RoPE forward) next to the fused forward;
 * a plain device-to-device copy of 512 MiB: the achievable HBM bandwidth next
   to the rotation kernel's, and the calibration kernel for the HBM-traffic
   counters;
@@ -129,6 +134,7 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-decode", action="store_true", help="skip the decode (KV-cache) measurements")
     ap.add_argument("--no-sparse", action="store_true", help="skip the block-sparse (BigBird mask) measurements")
+    ap.add_argument("--no-workloads", action="store_true", help="skip the other attention workloads")
     ap.add_argument("--seed", type=int, default=0)
     return ap.parse_args()
 
@@ -384,6 +390,78 @@ def main():
             del qb, kb, vb, dob, ob, lb, grads, wsb, bm
         torch.cuda.empty_cache()
 
+    # ---------------------------------------------------------------- the other attention workloads
+    others = None
+    if not args.no_workloads:
+        others = {}
+        for name, ow in WORKLOADS.items():
+            if name == w.name or ow.S < 1024:   # the headline, and the tiny parity case
+                continue
+            c = inputs.make_qkv(ow.B, ow.H, ow.Hkv, ow.S, ow.D, seed=args.seed, with_do=True)
+            qw, kw_, vw, dow = (c[n].to(dev) for n in ("q", "k", "v", "do"))
+            del c
+            sl = inputs.alibi_slopes(ow.H).to(dev) if ow.alibi else None
+            okw = dict(rope=ow.rope, theta=ow.theta, mask=ow.mask, window=ow.window or None, alibi_slopes=sl)
+            ow_o = torch.empty_like(qw)
+            ow_l = torch.empty(ow.B, ow.H, ow.S, device=dev, dtype=torch.float32)
+            ow_g = (torch.empty_like(qw), torch.empty_like(kw_), torch.empty_like(vw))
+            ow_ws = torch.empty(api.attnfuse_bwd_workspace_bytes(ow.B, ow.H, ow.Hkv, ow.S, ow.D, ow.rope),
+                                device=dev, dtype=torch.uint8)
+
+            def ofwd():
+                api.attnfuse_fwd(qw, kw_, vw, out=ow_o, lse=ow_l, **okw)
+
+            def obwd():
+                api.attnfuse_bwd(qw, kw_, vw, ow_o, dow, ow_l, dq=ow_g[0], dk=ow_g[1], dv=ow_g[2], workspace=ow_ws,
+                                 **okw)
+
+            for _ in range(10):
+                ofwd()
+            f_ms = statistics.median(time_calls(ofwd, 50))
+            for _ in range(3):
+                obwd()
+            b_ms = statistics.median(time_calls(obwd, 20))
+            f_tf = ow.fwd_flops() / (f_ms * 1e-3) / 1e12
+            b_tf = ow.bwd_flops() / (b_ms * 1e-3) / 1e12
+            rec = {"B": ow.B, "H": ow.H, "H_kv": ow.Hkv, "S": ow.S, "D": ow.D, "rope": ow.rope, "mask": ow.mask,
+                   "window": ow.window, "alibi": ow.alibi,
+                   "fwd_ms": round(f_ms, 4), "fwd_tflops": round(f_tf, 1), "fwd_frac_peak": round(f_tf / PEAK_BF16_TFLOPS, 4),
+                   "bwd_ms": round(b_ms, 4), "bwd_tflops": round(b_tf, 1), "bwd_frac_peak": round(b_tf / PEAK_BF16_TFLOPS, 4)}
+            msg = f"{name}: fwd {f_ms:.4f} ms ({f_tf:.0f} TF/s), bwd {b_ms:.4f} ms ({b_tf:.0f} TF/s)"
+            if ow.rope != "none":
+                nbytes = ow.rope_bytes()
+                npool = max(2, math.ceil(600e6 / nbytes))
+                pool = [(qw.clone(), kw_.clone()) for _ in range(npool)]
+                outs = [(torch.empty_like(qw), torch.empty_like(kw_)) for _ in range(npool)]
+                it2 = [0]
+
+                def orot():
+                    i = it2[0] % npool
+                    it2[0] += 1
+                    api.attnfuse_rope(pool[i][0], pool[i][1], rope=ow.rope, theta=ow.theta, out_q=outs[i][0],
+                                      out_k=outs[i][1])
+
+                for _ in range(3):
+                    orot()
+                r_ms = statistics.median(time_calls(orot, max(20, 2 * npool)))
+                qr_, kr_ = outs[0]
+
+                def osep():
+                    api.attnfuse_fwd(qr_, kr_, vw, out=ow_o, lse=ow_l, **dict(okw, rope="none"))
+
+                for _ in range(3):
+                    osep()
+                n_ms = statistics.median(time_calls(osep, 50))
+                rec["separate"] = {"rope_ms": round(r_ms, 4), "fwd_norope_ms": round(n_ms, 4),
+                                   "total_ms": round(r_ms + n_ms, 4), "fused_speedup": round((r_ms + n_ms) / f_ms, 4),
+                                   "rope_gbs": round(nbytes / (r_ms * 1e-3) / 1e9, 1)}
+                msg += f"; separate {r_ms + n_ms:.4f} ms (fused speedup {(r_ms + n_ms) / f_ms:.3f})"
+                del pool, outs
+            others[name] = rec
+            log(msg)
+            del qw, kw_, vw, dow, ow_o, ow_l, ow_g, ow_ws
+        torch.cuda.empty_cache()
+
     # ---------------------------------------------------------------- CPU oracle baseline
     cpu_baseline = None
     if not args.no_cpu_baseline:
@@ -446,6 +524,8 @@ def main():
         line["decode"] = decode
     if sparse is not None:
         line["block_sparse"] = sparse
+    if others is not None:
+        line["workloads"] = others
     print(json.dumps(line), flush=True)
 
 

@@ -241,10 +241,11 @@ int attnfuse_rope_bwd(const void* dQr, const void* dKr, void* dQ, void* dK,
                       int B, int H, int H_kv, int S, int D, int dtype,
                       int rope, float rope_theta, void* stream);
 
-/* Bytes of device workspace attnfuse_decode needs: one partial (max, sum,
- * accumulator) triple per (sequence, query head, cache chunk), fp32.  The chunk
- * length is a power of two in [128, 4096] chosen from B * H_kv * S_kv so the
- * first phase launches about 512 workgroups.  Returns 0 for invalid sizes. */
+/* Bytes of device workspace attnfuse_decode needs: four partial (max, sum,
+ * accumulator) triples per (sequence, query head, cache chunk), one per
+ * first-phase wave, fp32.  The chunk length is a power of two in [128, 4096]
+ * chosen from B * H_kv * S_kv so the first phase launches about 512
+ * workgroups.  Returns 0 for invalid sizes. */
 size_t attnfuse_decode_workspace_bytes(int B, int H, int H_kv, int S_kv, int D);
 
 /*

@@ -113,7 +113,8 @@ BwdWorkspace bwd_workspace(int B, int H, int H_kv, int S, int D, int rope) {
   return w;
 }
 
-// Decode workspace: per-chunk partial (max, sum) pairs, then accumulators.
+// Decode workspace: per-wave partial (max, sum) pairs, then accumulators
+// (four phase-1 waves per chunk, each writing its own partial).
 struct DecodeLayout {
   int chunk, nsplit;
   size_t ml, acc, total;
@@ -121,14 +122,15 @@ struct DecodeLayout {
 
 // Keys per phase-1 workgroup: a power of two in [128, 4096] giving about 512
 // workgroups (one resident round at two per CU, so each wave streams several
-// tiles); partial (max, sum) pairs then accumulators, each 256-byte aligned.
+// tiles); the wave partials' (max, sum) pairs then accumulators, each
+// 256-byte aligned.
 DecodeLayout decode_layout(int B, int H, int H_kv, int S, int D) {
   const long long work = (long long)B * H_kv * S;
   DecodeLayout L{};
   L.chunk = 128;
   while (L.chunk < 4096 && (long long)L.chunk * 512 < work) L.chunk *= 2;
   L.nsplit = (S + L.chunk - 1) / L.chunk;
-  const size_t parts = (size_t)B * H * L.nsplit;
+  const size_t parts = (size_t)B * H * L.nsplit * 4;
   L.ml = 0;
   L.acc = align256(parts * 2 * sizeof(float));
   L.total = L.acc + align256(parts * D * sizeof(float));

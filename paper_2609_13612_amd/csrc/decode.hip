@@ -18,13 +18,13 @@
 //   loaded and rotated; each next tile's as soon as the current tile's score
 //   MFMAs have consumed its keys, so one tile per wave is always in flight.
 //   The register budget is held to two waves per SIMD so that two workgroups
-//   stream on every CU at once.  The four waves' (m, l, acc) merge in LDS and
-//   one partial per (sequence, head, chunk) is written; chunks with no visible
-//   key return at once.
-// Phase 2 (decode_combine_kernel): per (sequence, head), merge the partials of
-//   the chunks that hold visible keys by log-sum-exp and write O and LSE; the
-//   head's dims are spread over several workgroups so the merge reads the
-//   partials with the whole chip, in one round trip to memory.
+//   stream on every CU at once.  Each wave then writes its own (m, l, acc)
+//   partial for the group's G query heads straight from its registers (the
+//   kernel has no barrier); chunks with no visible key return at once.
+// Phase 2 (decode_combine_kernel): per (sequence, head), merge the wave
+//   partials of the chunks that hold visible keys by log-sum-exp and write O
+//   and LSE; the head's dims are spread over several workgroups so the merge
+//   reads the partials with the whole chip, in one round trip to memory.
 //
 // Precision: without RoPE the bf16 query and keys meet exactly in a bf16
 // MFMA.  With RoPE the query is rotated at position L-1 in fp32 and rounded to
@@ -44,8 +44,7 @@ struct DecCfg {
   static constexpr int VP = D + 16;                 // V tile pitch (transpose reads)
   static constexpr int VT = 32 * VP;                // one wave's V tile (elements)
   static constexpr int VPL = 32 * (D / 8) / 64;     // 16-byte V chunks per lane per tile
-  static constexpr int MERGE_FLOATS = 2 * NW * 32 + 2 * 32 * D;   // statistics + two accumulator slots
-  static constexpr int SMEM = (NW * VT > 2 * MERGE_FLOATS) ? NW * VT : 2 * MERGE_FLOATS;   // uint16 elements
+  static constexpr int SMEM = NW * VT;             // uint16 elements
 };
 
 __device__ __forceinline__ int seq_len(const DecodeParams& p, int b) {
@@ -206,83 +205,26 @@ void decode_split_kernel(DecodeParams p) {
       }
   }
 
-  // Merge the four waves' partials through LDS (the V tiles are dead): each
-  // wave rescales to the workgroup max, waves 2-3 hand over to 0-1, wave 1 to
-  // wave 0, and wave 0's sum leaves through one slot with coalesced stores.
-  __syncthreads();
-  float* ms = reinterpret_cast<float*>(smem);   // [NW][32] max, then [NW][32] sum
-  float* as = ms + 2 * C::NW * 32;              // two slots of [32 columns][D]
+  // One partial per wave, straight from registers: the first G head columns.
   const float l_tot = pair_sum(l_run);
-  if (lane < 32) {
-    ms[wave * 32 + lane] = m_run;
-    ms[C::NW * 32 + wave * 32 + lane] = l_tot;
-  }
-  __syncthreads();
-  float M = -INFINITY;
-#pragma unroll
-  for (int w = 0; w < C::NW; ++w) M = fmaxf(M, ms[w * 32 + lq]);
-  const float f = (m_run == -INFINITY) ? 0.f : fast_exp2(m_run - M);
-#pragma unroll
-  for (int i = 0; i < C::MT; ++i) acc[i] *= f;
-  // lane's slot entries: column lq, dims 32 mt + 8 (r/4) + 4 lg + r%4
-  float* mine = as + lq * D + 4 * lg;
-  if (wave >= 2) {
+  const int nslot = p.nsplit * C::NW;
+  if (lq < G) {
+    const size_t prow = ((size_t)b * p.H + g * G + lq) * nslot + split * C::NW + wave;
+    float* dst = p.part_acc + prow * D + 4 * lg;
 #pragma unroll
     for (int mt = 0; mt < C::MT; ++mt)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) mine[(wave - 2) * 32 * D + 32 * mt + 8 * (r >> 2) + (r & 3)] = acc[mt][r];
-  }
-  __syncthreads();
-  if (wave < 2) {
-#pragma unroll
-    for (int mt = 0; mt < C::MT; ++mt)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[mt][r] += mine[wave * 32 * D + 32 * mt + 8 * (r >> 2) + (r & 3)];
-  }
-  __syncthreads();
-  if (wave == 1) {
-#pragma unroll
-    for (int mt = 0; mt < C::MT; ++mt)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) mine[32 * mt + 8 * (r >> 2) + (r & 3)] = acc[mt][r];
-  }
-  __syncthreads();
-  if (wave == 0) {
-#pragma unroll
-    for (int mt = 0; mt < C::MT; ++mt)
-#pragma unroll
-      for (int r = 0; r < 16; ++r)
-        mine[32 * D + 32 * mt + 8 * (r >> 2) + (r & 3)] = acc[mt][r] + mine[32 * mt + 8 * (r >> 2) + (r & 3)];
-  }
-  __syncthreads();
-  const size_t part0 = (size_t)b * p.H + g * G;   // partial row of column 0
-  for (int idx = tid; idx < G * D; idx += 256) {
-    const int c = idx / D, d = idx % D;
-    p.part_acc[((part0 + c) * p.nsplit + split) * D + d] = as[(32 + c) * D + d];
-  }
-  if (tid < G) {
-    float Mc = -INFINITY, Lc = 0.f;
-#pragma unroll
-    for (int w = 0; w < C::NW; ++w) Mc = fmaxf(Mc, ms[w * 32 + tid]);
-#pragma unroll
-    for (int w = 0; w < C::NW; ++w) {
-      const float mw = ms[w * 32 + tid];
-      Lc += (mw == -INFINITY) ? 0.f : ms[C::NW * 32 + w * 32 + tid] * fast_exp2(mw - Mc);
+      for (int a = 0; a < 4; ++a)
+        *reinterpret_cast<float4*>(dst + 32 * mt + 8 * a) =
+            float4{acc[mt][4 * a], acc[mt][4 * a + 1], acc[mt][4 * a + 2], acc[mt][4 * a + 3]};
+    if (lg == 0) {
+      p.part_ml[prow * 2] = m_run;
+      p.part_ml[prow * 2 + 1] = l_tot;
     }
-    float* ml = p.part_ml + ((part0 + tid) * p.nsplit + split) * 2;
-    ml[0] = Mc;
-    ml[1] = Lc;
   }
 }
 
-// Phase 2.  Workgroup = 256 threads = one (sequence, query head) and 32 of its
-// dims, as eight groups of 32 threads that each take every eighth chunk.  The
-// group's accumulators are loaded together with the chunk statistics, so the
-// merge costs one round trip to memory: each thread folds its chunks' (m, l)
-// into a running pair, the pairs merge across the workgroup, and every thread
-// weights its accumulators by 2^(m_s - M) from the maxima kept in LDS.
-constexpr int COMBINE_MAX_CHUNKS = 8192;   // 2^20 keys / 128-key chunks
-
+// Fold the (max, sum) pair (m2, l2) into the running pair (m, l), log2 units.
 __device__ __forceinline__ void merge_ml(float& m, float& l, float m2, float l2) {
   const float M = fmaxf(m, m2);
   if (M == -INFINITY) return;
@@ -290,10 +232,15 @@ __device__ __forceinline__ void merge_ml(float& m, float& l, float m2, float l2)
   m = M;
 }
 
-template <int D>
+// Phase 2.  Workgroup = 256 threads = one (sequence, query head) and 32 of its
+// dims, as eight groups of 32 threads that each take every eighth partial (4
+// per chunk, one per wave).  Each thread loads its first PF partials'
+// accumulators and maxima together with the statistics, so the merge costs
+// one round trip to memory: each thread folds the (m, l) pairs it reads into
+// a running pair, the pairs merge across the workgroup, and every thread
+// weights its accumulators by 2^(m_s - M).
+template <int D, int PF>
 __global__ __launch_bounds__(256) void decode_combine_kernel(DecodeParams p) {
-  constexpr int PF = 8;   // accumulators per thread loaded up front (chunks 0..63)
-  __shared__ float mx_s[COMBINE_MAX_CHUNKS];
   __shared__ float red[256];
   __shared__ float wred[8];
   const int bh = blockIdx.x, t = threadIdx.x, lane = t & 63, wv = t >> 6;
@@ -306,20 +253,22 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(DecodeParams p) {
     if (t == 0 && blockIdx.y == 0) p.lse[bh] = -INFINITY;
     return;
   }
+  constexpr int NWV = DecCfg<D>::NW;   // partials per chunk
+  const int nslot = p.nsplit * NWV;
   const int s_lo = first_key(p, L) / p.chunk, s_hi = (L - 1) / p.chunk;
-  const int n = s_hi - s_lo + 1;
-  const float* ml = p.part_ml + ((size_t)bh * p.nsplit + s_lo) * 2;
-  const float* acc = p.part_acc + ((size_t)bh * p.nsplit + s_lo) * D + d;
-  float a[PF];
+  const int n = (s_hi - s_lo + 1) * NWV;
+  const float* ml = p.part_ml + ((size_t)bh * nslot + s_lo * NWV) * 2;
+  const float* acc = p.part_acc + ((size_t)bh * nslot + s_lo * NWV) * D + d;
+  float a[PF], mm[PF];
 #pragma unroll
   for (int j = 0; j < PF; ++j) {
     const int i = grp + 8 * j;
     a[j] = (i < n) ? acc[(size_t)i * D] : 0.f;
+    mm[j] = (i < n) ? ml[2 * i] : -INFINITY;
   }
   float m = -INFINITY, l = 0.f;
   for (int i = t; i < n; i += 256) {
     const float2 v = *reinterpret_cast<const float2*>(ml + 2 * i);
-    mx_s[i] = v.x;
     merge_ml(m, l, v.x, v.y);
   }
 #pragma unroll
@@ -328,18 +277,15 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(DecodeParams p) {
     wred[2 * wv] = m;
     wred[2 * wv + 1] = l;
   }
-  __syncthreads();   // also publishes mx_s
+  __syncthreads();
   m = wred[0];
   l = wred[1];
 #pragma unroll
   for (int w = 1; w < 4; ++w) merge_ml(m, l, wred[2 * w], wred[2 * w + 1]);
   float o = 0.f;
 #pragma unroll
-  for (int j = 0; j < PF; ++j) {
-    const int i = grp + 8 * j;
-    if (i < n) o += a[j] * fast_exp2(mx_s[i] - m);
-  }
-  for (int i = grp + 8 * PF; i < n; i += 8) o += acc[(size_t)i * D] * fast_exp2(mx_s[i] - m);
+  for (int j = 0; j < PF; ++j) o += a[j] * fast_exp2(mm[j] - m);
+  for (int i = grp + 8 * PF; i < n; i += 8) o += acc[(size_t)i * D] * fast_exp2(ml[2 * i] - m);
   red[t] = o;
   __syncthreads();
   if (grp == 0) {
@@ -355,7 +301,12 @@ template <int D, int ROPE, bool ALIBI>
 static int launch_one(const DecodeParams& p, hipStream_t st) {
   const long long blocks = (long long)p.nsplit * p.B * p.Hkv;
   hipLaunchKernelGGL((decode_split_kernel<D, ROPE, ALIBI>), dim3((unsigned)blocks), dim3(256), 0, st, p);
-  hipLaunchKernelGGL((decode_combine_kernel<D>), dim3((unsigned)(p.B * p.H), D / 32), dim3(256), 0, st, p);
+  // preload depth: every partial of a head (8 groups x PF) when it fits
+  const dim3 cgrid((unsigned)(p.B * p.H), D / 32);
+  if (p.nsplit * DecCfg<D>::NW <= 8 * 16)
+    hipLaunchKernelGGL((decode_combine_kernel<D, 16>), cgrid, dim3(256), 0, st, p);
+  else
+    hipLaunchKernelGGL((decode_combine_kernel<D, 32>), cgrid, dim3(256), 0, st, p);
   return hipGetLastError() == hipSuccess ? 0 : -3;
 }
 

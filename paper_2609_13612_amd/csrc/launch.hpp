@@ -63,8 +63,8 @@ struct DecodeParams {
   const int* lens;        // device [B] cache lengths, or nullptr (all S)
   void* o;                // [B, H, D]
   float* lse;             // [B, H]
-  float* part_ml;         // workspace [B, H, nsplit, 2]: chunk max and sum (log2 units)
-  float* part_acc;        // workspace [B, H, nsplit, D]: chunk accumulator
+  float* part_ml;         // workspace [B, H, 4 nsplit, 2]: wave partial max and sum (log2 units)
+  float* part_acc;        // workspace [B, H, 4 nsplit, D]: wave partial accumulator
   int B, H, Hkv, S;
   int window;             // > 0: sliding window of that many keys; 0: every cached key
   int chunk, nsplit;      // keys per phase-1 workgroup; chunks per sequence

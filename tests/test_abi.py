@@ -139,14 +139,15 @@ def test_rope_unsupported():
 
 def test_decode_workspace_bytes():
     lib = _lib.load()
-    # Llama-3-70B geometry, 32k cache: 512-key chunks -> 64 per sequence; 64 heads
-    parts = 64 * 64
+    # Llama-3-70B geometry, 32k cache: 512-key chunks -> 64 per sequence, four
+    # wave partials each; 64 heads
+    parts = 64 * 64 * 4
     assert lib.attnfuse_decode_workspace_bytes(1, 64, 8, 32768, 128) == parts * 8 + parts * 128 * 4
     # Llama-3-8B geometry, 4k cache: the 128-key minimum -> 32 chunks; 32 heads
-    parts = 32 * 32
+    parts = 32 * 32 * 4
     assert lib.attnfuse_decode_workspace_bytes(1, 32, 8, 4096, 128) == parts * 8 + parts * 128 * 4
     # sections start on 256-byte boundaries
-    assert lib.attnfuse_decode_workspace_bytes(1, 1, 1, 5, 64) == 256 + 256
+    assert lib.attnfuse_decode_workspace_bytes(1, 1, 1, 5, 64) == 256 + 4 * 64 * 4   # 4 partials: 32 B -> 256, 1024
     assert lib.attnfuse_decode_workspace_bytes(0, 32, 8, 4096, 128) == 0
     assert lib.attnfuse_decode_workspace_bytes(1, 6, 4, 4096, 128) == 0
     assert lib.attnfuse_decode_workspace_bytes(1, 32, 8, 0, 128) == 0

@@ -44,7 +44,7 @@ struct DecCfg {
   static constexpr int VP = D + 16;                 // V tile pitch (transpose reads)
   static constexpr int VT = 32 * VP;                // one wave's V tile (elements)
   static constexpr int VPL = 32 * (D / 8) / 64;     // 16-byte V chunks per lane per tile
-  static constexpr int SMEM = NW * VT;             // uint16 elements
+  static constexpr int SMEM = NW * VT;              // uint16 elements
 };
 
 __device__ __forceinline__ int seq_len(const DecodeParams& p, int b) {

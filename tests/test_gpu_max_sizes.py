@@ -1,0 +1,86 @@
+"""GPU parity at the largest sizes the C ABI accepts.
+
+* Fused RoPE + sliding-window attention, forward and backward, at S = 2^20
+  (the sequence-length limit): a row's result depends only on the W keys
+  before it, so the oracle runs on slices of the sequence with their true
+  positions (``pos_offset``), and the rows and keys at least W from a slice's
+  start (and, for dK/dV, W from an interior slice's end) are exact.  Slices
+  sit in the middle and at the very end of the sequence, where the RoPE
+  angles are largest.
+* Decode over a 2^20-entry cache: 2048 wave partials per head to merge.
+* Block-sparse forward at S = 131072 (2048 blocks, the tile-list capacity)
+  with a BigBird-style mask whose global row lists every block.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from gpu_util import announce, assert_bf16_close, assert_lse_close, device_inputs, f64, need_gpu
+from paper_2609_13612_amd import api, blockmask, inputs
+
+pytestmark = pytest.mark.gpu
+
+S_MAX = 1 << 20
+
+
+def test_sliding_window_max_sequence_fwd_bwd():
+    need_gpu()
+    B, H, Hkv, S, D, W = 1, 2, 1, S_MAX, 64, 256
+    kw = dict(rope="neox", theta=500000.0, mask="sliding_window", window=W)
+    announce(f"max sequence S={S} sliding window {W}")
+    cpu, dev = device_inputs(B, H, Hkv, S, D, seed=61, with_do=True)
+    o, lse = api.attnfuse_fwd(dev["q"], dev["k"], dev["v"], **kw)
+    dq, dk, dv = api.attnfuse_bwd(dev["q"], dev["k"], dev["v"], o, dev["do"], lse, **kw)
+    torch.cuda.synchronize()
+    for t in (o, dq, dk, dv):
+        assert torch.isfinite(t.float()).all()
+    L = 4 * W
+    for s0 in (S // 2 - L // 2, S - L):
+        s1 = s0 + L
+        sl = slice(s0, s1)
+        args = [f64(cpu[n][:, :, sl]) for n in ("q", "k", "v", "do")]
+        O, LSE = oracle.attention_forward(*args[:3], pos_offset=s0, **kw)
+        ref = oracle.attention_backward(*args, pos_offset=s0, **kw)
+        rows = slice(W - 1, L)                         # every visible key inside the slice
+        keys = slice(W - 1, L if s1 == S else L - W + 1)   # every visible query inside the slice
+        assert_bf16_close(f64(o[:, :, sl])[:, :, rows], O[:, :, rows], f"O [{s0}, {s1})")
+        assert_lse_close(f64(lse[:, :, sl])[:, :, rows], LSE[:, :, rows], f"LSE [{s0}, {s1})")
+        assert_bf16_close(f64(dq[:, :, sl])[:, :, rows], ref[0][:, :, rows], f"dQ [{s0}, {s1})")
+        assert_bf16_close(f64(dk[:, :, sl])[:, :, keys], ref[1][:, :, keys], f"dK [{s0}, {s1})")
+        assert_bf16_close(f64(dv[:, :, sl])[:, :, keys], ref[2][:, :, keys], f"dV [{s0}, {s1})")
+
+
+def test_decode_max_cache():
+    need_gpu()
+    B, H, Hkv, S, D = 1, 8, 1, S_MAX, 128
+    announce(f"decode max cache S_kv={S}")
+    c = inputs.make_decode(B, H, Hkv, S, D, seed=62)
+    o, lse = api.attnfuse_decode(c["q"].cuda(), c["k"].cuda(), c["v"].cuda(), rope="neox", theta=500000.0)
+    torch.cuda.synchronize()
+    O, L = oracle.decode_forward(f64(c["q"]), f64(c["k"]), f64(c["v"]), rope="neox", theta=500000.0)
+    assert_bf16_close(f64(o), O, "O")
+    assert_lse_close(f64(lse), L, "LSE")
+
+
+def test_blocksparse_max_blocks_fwd():
+    need_gpu()
+    B, H, Hkv, S, D = 1, 2, 2, blockmask.MAX_BLOCKS * blockmask.BLOCK, 64
+    announce(f"block-sparse max blocks S={S}")
+    cpu, dev = device_inputs(B, H, Hkv, S, D, seed=63, with_do=True)
+    active = inputs.bigbird_blocks(blockmask.num_blocks(S), seed=1)
+    bm = blockmask.block_mask_from_dense(torch.from_numpy(active), S, device="cuda")
+    o, lse = api.attnfuse_fwd_blocksparse(dev["q"], dev["k"], dev["v"], bm)
+    grads = api.attnfuse_bwd_blocksparse(dev["q"], dev["k"], dev["v"], o, dev["do"], lse, bm)
+    torch.cuda.synchronize()
+    for t in (o, *grads):
+        assert torch.isfinite(t.float()).all()
+    rng = np.random.default_rng(3)
+    # row 0 is in the global block row (every key block active); rows of block
+    # 1 see the global key block, their band and a random block
+    rows = np.unique(np.concatenate([[0, 1, 63, 64, 100, S - 1], rng.integers(0, S, 10)]))
+    for h in range(H):
+        O, L = oracle.attention_forward_rows(f64(cpu["q"][0, h]), f64(cpu["k"][0, h]), f64(cpu["v"][0, h]), rows,
+                                             mask="none", block_mask=bm.as_oracle())
+        assert_bf16_close(f64(o[0, h])[rows], O, f"O h={h}")
+        assert_lse_close(f64(lse[0, h])[rows], L, f"LSE h={h}")

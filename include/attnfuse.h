@@ -250,11 +250,11 @@ size_t attnfuse_decode_workspace_bytes(int B, int H, int H_kv, int S_kv, int D);
 
 /*
  * Decode attention over a key/value cache (Section 4.2 "Flash Decoding"): one
- * query per sequence.  Phase 1 splits each sequence's cache into chunks and
- * computes a partial online-softmax triple (m, l, acc) per chunk for all query
- * heads of a K/V head at once (the group's heads fill the MFMA's columns by
- * cyclic replication, so K and V are read exactly once); phase 2 merges the
- * partials by log-sum-exp.  With L = cache_lens[b] the query sits at position
+ * query per sequence.  Phase 1 splits each sequence's cache into chunks,
+ * each streamed by four waves, and computes a partial online-softmax triple
+ * (m, l, acc) per wave for all query heads of a K/V head at once (the group's
+ * heads fill the MFMA's columns by cyclic replication, so K and V are read
+ * exactly once); phase 2 merges the partials by log-sum-exp.  With L = cache_lens[b] the query sits at position
  * p = L - 1 and
  *     s_j = softmax_scale * <R_p q, k_j> - slope_h * (p - j),   j < L
  *     O   = softmax_j(s_j over visible j) v_j,   LSE = ln sum_{visible j} exp(s_j)

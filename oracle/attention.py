@@ -268,10 +268,18 @@ def attention_forward_rows(q_bh, k_bg, v_bg, rows, *, h=0, H=1, rope=ROPE_NONE,
         return P @ v_bg, m + np.log(l)
 
 
+def _row_delta(P, dP, dO_rows, o_rows):
+    """delta_i of the softmax backward: sum_j P_ij dP_ij, or rowsum(dO_i * o_i)
+    of a given forward output (equal for the exact output)."""
+    if o_rows is None:
+        return np.sum(P * dP, axis=1)
+    return np.sum(dO_rows * o_rows, axis=1)
+
+
 def attention_backward(q, k, v, do, *, rope=ROPE_NONE, theta=10000.0, mask=MASK_CAUSAL,
                        window=None, alibi_slopes=None, scale=None, pos_offset=0,
                        return_intermediates=False, block_mask=None, bias=None, norm=NORM_SOFTMAX,
-                       relu_gate="exact"):
+                       relu_gate="exact", o=None):
     """dQ [B,H,S,D], dK and dV [B,H_kv,S,D] in fp64.
 
     With ``return_intermediates`` also returns a dict with per-(b,h) lists of
@@ -285,6 +293,14 @@ def attention_backward(q, k, v, do, *, rope=ROPE_NONE, theta=10000.0, mask=MASK_
     score within rounding of 0 flips it; comparing against a kernel that gates
     on fp16 operands takes the decision in that precision on both sides.
     Everything else stays fp64.
+
+    ``o`` [B,H,S,D] is the forward output the backward is given.  The softmax
+    backward's row term delta_i = sum_j P_ij dP_ij equals rowsum(dO_i * O_i)
+    for the exact O, and the three-pass backward (Section 4.4) forms it in its
+    preprocessing pass from the O it receives; with ``o`` given, delta is
+    rowsum(dO_i * o_i) of that array (in fp64), so a caller's rounded O enters
+    exactly as it does there.  None (the default) uses the definitional sum.
+    Unused under relu attention (no delta).
     """
     q = np.asarray(q, dtype=np.float64)
     k = np.asarray(k, dtype=np.float64)
@@ -293,6 +309,10 @@ def attention_backward(q, k, v, do, *, rope=ROPE_NONE, theta=10000.0, mask=MASK_
     B, H, Hkv, S, D = _check(q, k, v)
     if do.shape != q.shape:
         raise ValueError("dO must have the shape of Q")
+    if o is not None:
+        o = np.asarray(o, dtype=np.float64)
+        if o.shape != q.shape:
+            raise ValueError("O must have the shape of Q")
     scale, slopes = _defaults(D, scale, alibi_slopes, H)
     bias = _bias_of(bias, B, H, S)
     norm = _norm_of(norm)
@@ -328,7 +348,7 @@ def attention_backward(q, k, v, do, *, rope=ROPE_NONE, theta=10000.0, mask=MASK_
                                               bias_bh=None if bias is None else bias[b, h])
                     dS = _relu_grad(sg, dP)
                 else:
-                    delta = np.sum(P * dP, axis=1)
+                    delta = _row_delta(P, dP, dO_rows, None if o is None else o[b, h, rows])
                     dS = P * (dP - delta[:, None])
                 dqr[b, h, rows] = scale * (dS @ kr[b, g])
                 dkr[b, g] += scale * (dS.T @ qr[b, h, rows])

@@ -561,3 +561,23 @@ def check_relu_gate_precision(seed=44):
     hf = oracle.attention_backward(q, k, v, do, mask="none", norm="relu", scale=1.0, relu_gate="fp16")
     assert np.allclose(ex[0][0, 0, 0], 2.0 * k[0, 0, 0])        # s = 2^-13 > 0: dS = dP = 2
     assert np.array_equal(hf[0], np.zeros_like(hf[0]))          # fp16 q.k = 0: gate closed
+
+
+def check_backward_given_output(seed=45):
+    """delta from a given forward output: with the exact O the gradients are
+    the default ones; with O + E every row of dS sums to -rowsum(dO * E)
+    (the softmax rows sum to 1, so sum_j dS_ij = sum_j P_ij dP_ij - delta_i),
+    where the definitional delta makes every row sum to zero."""
+    r = _rng(seed)
+    q, k, v = r.standard_normal((1, 2, 9, 4)), r.standard_normal((1, 1, 9, 4)), r.standard_normal((1, 1, 9, 4))
+    do = r.standard_normal((1, 2, 9, 4))
+    kw = dict(rope="neox", mask="causal")
+    O, _ = oracle.attention_forward(q, k, v, **kw)
+    a = oracle.attention_backward(q, k, v, do, **kw)
+    b = oracle.attention_backward(q, k, v, do, o=O, **kw)
+    assert all(np.allclose(x, y, rtol=0, atol=1e-12) for x, y in zip(a, b))
+    E = 0.01 * r.standard_normal(O.shape)
+    *_, inter = oracle.attention_backward(q, k, v, do, o=O + E, return_intermediates=True, **kw)
+    for h in range(2):
+        expect = -np.sum(do[0, h] * E[0, h], axis=1)
+        assert np.allclose(inter["dS"][(0, h)].sum(axis=1), expect, rtol=0, atol=1e-12)

@@ -47,7 +47,7 @@ def _run(B, H, Hkv, S, D, *, rope, mask, window, bias_kind, norm, seed):
     # the relu gate s > 0 is a decision: both sides take it on fp16 operands
     # (the kernels' MFMA operand type in the backward)
     ref = oracle.attention_backward(f64(cpu["q"]), f64(cpu["k"]), f64(cpu["v"]), f64(cpu["do"]),
-                                    relu_gate="fp16" if norm == "relu" else "exact", **kw)
+                                    relu_gate="fp16" if norm == "relu" else "exact", o=f64(o), **kw)
     return (o, lse, grads), (O, L, ref)
 
 

@@ -29,10 +29,11 @@ def _ref_fwd(cpu, bm, rope, mask, window, slopes):
                                     block_mask=bm.as_oracle())
 
 
-def _ref_bwd(cpu, bm, rope, mask, window, slopes):
+def _ref_bwd(cpu, bm, rope, mask, window, slopes, o):
+    """Oracle gradients; delta from ``o``, the forward output the backward was given."""
     return oracle.attention_backward(f64(cpu["q"]), f64(cpu["k"]), f64(cpu["v"]), f64(cpu["do"]), rope=rope,
                                      mask=mask, window=window, alibi_slopes=None if slopes is None else f64(slopes),
-                                     block_mask=bm.as_oracle())
+                                     block_mask=bm.as_oracle(), o=f64(o))
 
 
 VARIANTS = list(itertools.product(["none", "neox", "interleaved"], ["none", "causal", "sliding_window"],
@@ -59,7 +60,7 @@ def test_blocksparse_fwd_bwd_variants(rope, mask, alibi, D):
     assert_bf16_close(o, O, "O")
     assert_lse_close(lse, L, "LSE")
     assert torch.all(o[:, :, 3 * 64:4 * 64] == 0) and torch.all(torch.isneginf(lse[:, :, 3 * 64:4 * 64]))
-    ref = _ref_bwd(cpu, bm, rope, mask, window, slopes)
+    ref = _ref_bwd(cpu, bm, rope, mask, window, slopes, o)
     for name, g, r in zip(("dQ", "dK", "dV"), grads, ref):
         assert_bf16_close(g, r, name)
 
@@ -82,7 +83,7 @@ def test_blocksparse_group_sizes(H, Hkv):
     O, L = _ref_fwd(cpu, bm, "neox", "causal", None, None)
     assert_bf16_close(o, O, "O")
     assert_lse_close(lse, L, "LSE")
-    for name, g, r in zip(("dQ", "dK", "dV"), grads, _ref_bwd(cpu, bm, "neox", "causal", None, None)):
+    for name, g, r in zip(("dQ", "dK", "dV"), grads, _ref_bwd(cpu, bm, "neox", "causal", None, None, o)):
         assert_bf16_close(g, r, name)
 
 
@@ -140,7 +141,7 @@ def test_blocksparse_empty_and_tiny():
         O, L = _ref_fwd(cpu, bm, "neox", "causal", None, None)
         assert_bf16_close(o, O, f"O S={S}")
         assert_lse_close(lse, L, f"LSE S={S}")
-        for name, g, r in zip(("dQ", "dK", "dV"), grads, _ref_bwd(cpu, bm, "neox", "causal", None, None)):
+        for name, g, r in zip(("dQ", "dK", "dV"), grads, _ref_bwd(cpu, bm, "neox", "causal", None, None, o)):
             assert_bf16_close(g, r, f"{name} S={S}")
 
 
@@ -167,7 +168,7 @@ def test_blocksparse_bigbird_full_size():
             assert_bf16_close(f64(o[b, h])[rows], O, f"O b={b} h={h}")
             assert_lse_close(f64(lse[b, h])[rows], L, f"LSE b={b} h={h}")
     ref = oracle.attention_backward(f64(cpu["q"][:1, :1]), f64(cpu["k"][:1, :1]), f64(cpu["v"][:1, :1]),
-                                    f64(cpu["do"][:1, :1]), mask="none", block_mask=bm.as_oracle())
+                                    f64(cpu["do"][:1, :1]), mask="none", block_mask=bm.as_oracle(), o=f64(o[:1, :1]))
     assert_bf16_close(f64(dq[:1, :1]), ref[0], "dQ (0, 0)")
     assert_bf16_close(f64(dk[:1, :1]), ref[1], "dK (0, 0)")
     assert_bf16_close(f64(dv[:1, :1]), ref[2], "dV (0, 0)")
@@ -222,5 +223,5 @@ def test_blocksparse_noncanonical_lists():
     O, L = _ref_fwd(cpu, bm, "neox", "causal", None, None)
     assert_bf16_close(o, O, "O")
     assert_lse_close(lse, L, "LSE")
-    for name, g, r in zip(("dQ", "dK", "dV"), grads, _ref_bwd(cpu, bm, "neox", "causal", None, None)):
+    for name, g, r in zip(("dQ", "dK", "dV"), grads, _ref_bwd(cpu, bm, "neox", "causal", None, None, o)):
         assert_bf16_close(g, r, name)

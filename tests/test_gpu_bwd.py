@@ -22,7 +22,7 @@ def _run(cpu, dev, B, H, Hkv, S, D, rope, theta, mask, window, alibi):
     torch.cuda.synchronize()
     ref = oracle.attention_backward(f64(cpu["q"]), f64(cpu["k"]), f64(cpu["v"]), f64(cpu["do"]), rope=rope,
                                     theta=theta, mask=mask, window=window,
-                                    alibi_slopes=None if slopes is None else f64(slopes))
+                                    alibi_slopes=None if slopes is None else f64(slopes), o=f64(o))
     return (dq, dk, dv), ref
 
 
@@ -96,7 +96,8 @@ def test_bwd_llama3_full_size_one_group():
     G = w.H // w.Hkv
     sl = slice(0, G)
     ref = oracle.attention_backward(f64(cpu["q"][:, sl]), f64(cpu["k"][:, :1]), f64(cpu["v"][:, :1]),
-                                    f64(cpu["do"][:, sl]), rope=w.rope, theta=w.theta, mask=w.mask)
+                                    f64(cpu["do"][:, sl]), rope=w.rope, theta=w.theta, mask=w.mask,
+                                    o=f64(o[:, sl]))
     assert_bf16_close(f64(dq[:, sl]), ref[0], "dQ group 0")
     assert_bf16_close(f64(dk[:, :1]), ref[1], "dK group 0")
     assert_bf16_close(f64(dv[:, :1]), ref[2], "dV group 0")
@@ -120,6 +121,6 @@ def test_bwd_separate_path_vs_oracle():
     dq2, dk2 = api.attnfuse_rope_bwd(dqr, dkr, rope="neox")
     torch.cuda.synchronize()
     ref = oracle.attention_backward(f64(cpu["q"]), f64(cpu["k"]), f64(cpu["v"]), f64(cpu["do"]), rope="neox",
-                                    mask="causal")
+                                    mask="causal", o=f64(o2))
     for name, g, r in zip(("dQ", "dK", "dV"), (dq2, dk2, dv2), ref):
         assert_bf16_close(g, r, f"separate path {name}")

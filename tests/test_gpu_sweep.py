@@ -1,0 +1,98 @@
+"""Seeded random sweep of small shapes through the C ABI against the fp64 oracle.
+
+The hand-picked parity cases cover each variant at a few shapes; this sweep
+draws the combinations they do not: GQA group sizes that are not powers of two
+(which change how many query heads a workgroup packs), sequence lengths around
+the 64-key tile and 256-row workgroup edges, windows from one key to past the
+sequence, both head dimensions, every RoPE kind with two thetas, ALiBi, and a
+non-default softmax scale.  Each case is drawn from its own seed, so a failure
+names a reproducible configuration.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from gpu_util import announce, assert_bf16_close, assert_lse_close, device_inputs, f64, need_gpu
+from paper_2609_13612_amd import api, inputs
+
+pytestmark = pytest.mark.gpu
+
+GROUPS = (1, 2, 3, 4, 5, 6, 8, 12, 16, 32)
+LENGTHS = (1, 2, 31, 33, 64, 65, 97, 130, 191, 256, 257, 333, 511)
+
+
+def _attention_case(i):
+    r = np.random.default_rng(1000 + i)
+    G = int(r.choice(GROUPS))
+    Hkv = int(r.choice((1, 2))) if G <= 16 else 1
+    S = int(r.choice(LENGTHS))
+    mask = str(r.choice(("none", "causal", "sliding_window")))
+    return dict(B=int(r.choice((1, 2))), H=G * Hkv, Hkv=Hkv, S=S, D=int(r.choice((64, 128))),
+                rope=str(r.choice(("none", "neox", "interleaved"))), theta=float(r.choice((1e4, 5e5))),
+                mask=mask, window=int(r.integers(1, S + 6)) if mask == "sliding_window" else None,
+                alibi=bool(r.random() < 0.3), scale=None if r.random() < 0.6 else float(r.uniform(0.05, 0.3)),
+                seed=2000 + i)
+
+
+@pytest.mark.parametrize("i", range(24))
+def test_sweep_fwd_bwd(i):
+    need_gpu()
+    c = _attention_case(i)
+    announce(f"sweep {i}: {c}")
+    B, H, Hkv, S, D = c["B"], c["H"], c["Hkv"], c["S"], c["D"]
+    cpu, dev = device_inputs(B, H, Hkv, S, D, seed=c["seed"], with_do=True)
+    slopes = inputs.alibi_slopes(H) if c["alibi"] else None
+    kw = dict(rope=c["rope"], theta=c["theta"], mask=c["mask"], window=c["window"], scale=c["scale"])
+    ds = None if slopes is None else slopes.cuda()
+    o, lse = api.attnfuse_fwd(dev["q"], dev["k"], dev["v"], alibi_slopes=ds, **kw)
+    dq, dk, dv = api.attnfuse_bwd(dev["q"], dev["k"], dev["v"], o, dev["do"], lse, alibi_slopes=ds, **kw)
+    torch.cuda.synchronize()
+    os_ = None if slopes is None else f64(slopes)
+    O, L = oracle.attention_forward(f64(cpu["q"]), f64(cpu["k"]), f64(cpu["v"]), alibi_slopes=os_, **kw)
+    ref = oracle.attention_backward(f64(cpu["q"]), f64(cpu["k"]), f64(cpu["v"]), f64(cpu["do"]),
+                                    alibi_slopes=os_, o=f64(o), **kw)
+    assert_bf16_close(o, O, "O")
+    assert_lse_close(lse, L, "LSE")
+    for name, g, r in zip(("dQ", "dK", "dV"), (dq, dk, dv), ref):
+        assert_bf16_close(g, r, name)
+
+
+def _decode_case(i):
+    r = np.random.default_rng(3000 + i)
+    G = int(r.choice((1, 3, 5, 6, 12, 24, 32)))
+    Hkv = int(r.choice((1, 2, 4)))
+    B = int(r.choice((1, 3)))
+    S = int(r.choice((1, 40, 129, 700, 2049, 5000)))
+    mask = str(r.choice(("causal", "sliding_window")))
+    return dict(B=B, H=G * Hkv, Hkv=Hkv, S=S, D=int(r.choice((64, 128))),
+                lens=[int(x) for x in r.integers(0, S + 3, B)] if r.random() < 0.5 else None,
+                rope=str(r.choice(("none", "neox", "interleaved"))), mask=mask,
+                window=int(r.integers(1, S + 4)) if mask == "sliding_window" else None,
+                alibi=bool(r.random() < 0.3), seed=4000 + i)
+
+
+@pytest.mark.parametrize("i", range(8))
+def test_sweep_decode(i):
+    need_gpu()
+    c = _decode_case(i)
+    announce(f"decode sweep {i}: {c}")
+    B, H, Hkv, S, D = c["B"], c["H"], c["Hkv"], c["S"], c["D"]
+    t = inputs.make_decode(B, H, Hkv, S, D, seed=c["seed"])
+    slopes = inputs.alibi_slopes(H) if c["alibi"] else None
+    lens = None if c["lens"] is None else torch.tensor(c["lens"], dtype=torch.int32, device="cuda")
+    kw = dict(rope=c["rope"], mask=c["mask"], window=c["window"])
+    o, lse = api.attnfuse_decode(t["q"].cuda(), t["k"].cuda(), t["v"].cuda(), lens,
+                                 alibi_slopes=None if slopes is None else slopes.cuda(), **kw)
+    torch.cuda.synchronize()
+    ref_lens = None if c["lens"] is None else [min(max(x, 0), S) for x in c["lens"]]
+    live = [b for b in range(B) if ref_lens is None or ref_lens[b] >= 1]
+    for b in range(B):
+        if b not in live:
+            assert torch.all(o[b] == 0) and torch.all(torch.isneginf(lse[b]))
+    if live:
+        O, L = oracle.decode_forward(f64(t["q"][live]), f64(t["k"][live]), f64(t["v"][live]),
+                                     None if ref_lens is None else [ref_lens[b] for b in live],
+                                     alibi_slopes=None if slopes is None else f64(slopes), **kw)
+        assert_bf16_close(f64(o[live]), O, "O")
+        assert_lse_close(f64(lse[live]), L, "LSE")

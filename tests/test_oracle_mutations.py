@@ -129,6 +129,7 @@ MUTATIONS = {
     "bias_transposed": [(oatt, "_bias_of", _transposed_bias_of)],
     "relu_normalised": [(oatt, "_relu_rows", _normalised_relu)],
     "relu_gradient_unmasked": [(oatt, "_relu_grad", lambda s, dP: dP)],
+    "given_output_ignored": [(oatt, "_row_delta", lambda P_, dP, dO_rows, o_rows: np.sum(P_ * dP, axis=1))],
 }
 
 CHECKS = [
@@ -152,6 +153,7 @@ CHECKS = [
     P.check_bias_reductions,
     P.check_relu_closed_forms,
     lambda: P.check_bias_relu_backward_fd("relu"),
+    P.check_backward_given_output,
 ]
 
 

@@ -154,3 +154,7 @@ def test_bias_relu_backward_fd(norm):
 
 def test_relu_gate_precision():
     P.check_relu_gate_precision()
+
+
+def test_backward_given_output():
+    P.check_backward_given_output()

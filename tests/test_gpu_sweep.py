@@ -5,8 +5,10 @@ draws the combinations they do not: GQA group sizes that are not powers of two
 (which change how many query heads a workgroup packs), sequence lengths around
 the 64-key tile and 256-row workgroup edges, windows from one key to past the
 sequence, both head dimensions, every RoPE kind with two thetas, ALiBi, and a
-non-default softmax scale.  Each case is drawn from its own seed, so a failure
-names a reproducible configuration.
+non-default softmax scale; decode with ragged and empty cache lengths; and
+block-sparse masks of random density with empty block rows on top of every
+elementwise mask.  Each case is drawn from its own seed, so a failure names a
+reproducible configuration.
 """
 import numpy as np
 import pytest
@@ -14,7 +16,7 @@ import torch
 
 import oracle
 from gpu_util import announce, assert_bf16_close, assert_lse_close, device_inputs, f64, need_gpu
-from paper_2609_13612_amd import api, inputs
+from paper_2609_13612_amd import api, blockmask, inputs
 
 pytestmark = pytest.mark.gpu
 
@@ -96,3 +98,42 @@ def test_sweep_decode(i):
                                      alibi_slopes=None if slopes is None else f64(slopes), **kw)
         assert_bf16_close(f64(o[live]), O, "O")
         assert_lse_close(f64(lse[live]), L, "LSE")
+
+
+def _sparse_case(i):
+    r = np.random.default_rng(5000 + i)
+    G = int(r.choice((1, 2, 3, 4, 8)))
+    S = int(r.choice((65, 200, 333, 640, 1000)))
+    nb = (S + 63) // 64
+    mask = str(r.choice(("none", "causal", "sliding_window")))
+    return dict(B=int(r.choice((1, 2))), H=G, Hkv=1, S=S, D=int(r.choice((64, 128))),
+                rope=str(r.choice(("none", "neox", "interleaved"))), mask=mask,
+                window=int(r.integers(1, S + 6)) if mask == "sliding_window" else None,
+                alibi=bool(r.random() < 0.3), density=float(r.uniform(0.05, 0.6)),
+                empty=[int(x) for x in r.choice(nb, size=min(2, nb - 1), replace=False)], seed=6000 + i)
+
+
+@pytest.mark.parametrize("i", range(8))
+def test_sweep_blocksparse(i):
+    need_gpu()
+    c = _sparse_case(i)
+    announce(f"block-sparse sweep {i}: {c}")
+    B, H, Hkv, S, D = c["B"], c["H"], c["Hkv"], c["S"], c["D"]
+    cpu, dev = device_inputs(B, H, Hkv, S, D, seed=c["seed"], with_do=True)
+    active = inputs.random_blocks(blockmask.num_blocks(S), c["density"], seed=c["seed"], empty_rows=c["empty"])
+    bm = blockmask.block_mask_from_dense(torch.from_numpy(active), S, device="cuda")
+    slopes = inputs.alibi_slopes(H) if c["alibi"] else None
+    kw = dict(rope=c["rope"], mask=c["mask"], window=c["window"])
+    ds = None if slopes is None else slopes.cuda()
+    o, lse = api.attnfuse_fwd_blocksparse(dev["q"], dev["k"], dev["v"], bm, alibi_slopes=ds, **kw)
+    grads = api.attnfuse_bwd_blocksparse(dev["q"], dev["k"], dev["v"], o, dev["do"], lse, bm, alibi_slopes=ds, **kw)
+    torch.cuda.synchronize()
+    os_ = None if slopes is None else f64(slopes)
+    O, L = oracle.attention_forward(f64(cpu["q"]), f64(cpu["k"]), f64(cpu["v"]), alibi_slopes=os_,
+                                    block_mask=bm.as_oracle(), **kw)
+    ref = oracle.attention_backward(f64(cpu["q"]), f64(cpu["k"]), f64(cpu["v"]), f64(cpu["do"]), alibi_slopes=os_,
+                                    block_mask=bm.as_oracle(), o=f64(o), **kw)
+    assert_bf16_close(o, O, "O")
+    assert_lse_close(lse, L, "LSE")
+    for name, g, r in zip(("dQ", "dK", "dV"), grads, ref):
+        assert_bf16_close(g, r, name)

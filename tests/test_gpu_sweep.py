@@ -7,7 +7,8 @@ the 64-key tile and 256-row workgroup edges, windows from one key to past the
 sequence, both head dimensions, every RoPE kind with two thetas, ALiBi, and a
 non-default softmax scale; decode with ragged and empty cache lengths; and
 block-sparse masks of random density with empty block rows on top of every
-elementwise mask.  Each case is drawn from its own seed, so a failure names a
+elementwise mask; and dense bias tensors broadcast over batch, heads or
+queries (zero strides) under the softmax and relu attention.  Each case is drawn from its own seed, so a failure names a
 reproducible configuration.
 """
 import numpy as np
@@ -135,5 +136,54 @@ def test_sweep_blocksparse(i):
                                     block_mask=bm.as_oracle(), o=f64(o), **kw)
     assert_bf16_close(o, O, "O")
     assert_lse_close(lse, L, "LSE")
+    for name, g, r in zip(("dQ", "dK", "dV"), grads, ref):
+        assert_bf16_close(g, r, name)
+
+
+BIAS_SHAPES = ("full", "batch_bcast", "head_bcast", "keypad", "shared")
+
+
+def _bias_case(i):
+    r = np.random.default_rng(7000 + i)
+    G = int(r.choice((1, 2, 4)))
+    S = int(r.choice((40, 97, 200, 300)))
+    mask = str(r.choice(("none", "causal", "sliding_window")))
+    return dict(B=2, H=2 * G, Hkv=2, S=S, D=int(r.choice((64, 128))), rope=str(r.choice(("none", "neox", "interleaved"))),
+                mask=mask, window=int(r.integers(1, S + 6)) if mask == "sliding_window" else None,
+                shape=str(r.choice(BIAS_SHAPES)), norm=str(r.choice(("softmax", "relu"))), seed=8000 + i)
+
+
+def _bias_tensor(shape, B, H, S, seed):
+    g = torch.Generator("cpu").manual_seed(seed)
+    dims = {"full": (B, H, S, S), "batch_bcast": (1, H, S, S), "head_bcast": (B, 1, S, S),
+            "keypad": (B, 1, 1, S), "shared": (1, 1, S, S)}[shape]
+    return 1.5 * torch.randn(*dims, generator=g, dtype=torch.float32)
+
+
+@pytest.mark.parametrize("i", range(6))
+def test_sweep_bias_norm(i):
+    """Relu attention runs in its published 1/L form (folded into the scale and
+    the bias) so its outputs stay O(1), as in the hand-picked relu tests."""
+    need_gpu()
+    c = _bias_case(i)
+    announce(f"bias sweep {i}: {c}")
+    B, H, Hkv, S, D = c["B"], c["H"], c["Hkv"], c["S"], c["D"]
+    cpu, dev = device_inputs(B, H, Hkv, S, D, seed=c["seed"], with_do=True)
+    bias = _bias_tensor(c["shape"], B, H, S, c["seed"])
+    scale = D ** -0.5
+    if c["norm"] == "relu":
+        scale /= S
+        bias = bias / S
+    kw = dict(rope=c["rope"], mask=c["mask"], window=c["window"], norm=c["norm"], scale=scale)
+    o, lse = api.attnfuse_fwd_bias_norm(dev["q"], dev["k"], dev["v"], bias=bias.cuda(), **kw)
+    grads = api.attnfuse_bwd_bias_norm(dev["q"], dev["k"], dev["v"], o, dev["do"], lse, bias=bias.cuda(), **kw)
+    torch.cuda.synchronize()
+    ob = bias.to(torch.float64).numpy()
+    O, L = oracle.attention_forward(f64(cpu["q"]), f64(cpu["k"]), f64(cpu["v"]), bias=ob, **kw)
+    ref = oracle.attention_backward(f64(cpu["q"]), f64(cpu["k"]), f64(cpu["v"]), f64(cpu["do"]), bias=ob, o=f64(o),
+                                    relu_gate="fp16" if c["norm"] == "relu" else "exact", **kw)
+    assert_bf16_close(o, O, "O")
+    if c["norm"] == "softmax":
+        assert_lse_close(lse, L, "LSE")
     for name, g, r in zip(("dQ", "dK", "dV"), grads, ref):
         assert_bf16_close(g, r, name)

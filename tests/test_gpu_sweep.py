@@ -8,7 +8,8 @@ sequence, both head dimensions, every RoPE kind with two thetas, ALiBi, and a
 non-default softmax scale; decode with ragged and empty cache lengths; and
 block-sparse masks of random density with empty block rows on top of every
 elementwise mask; and dense bias tensors broadcast over batch, heads or
-queries (zero strides) under the softmax and relu attention.  Each case is drawn from its own seed, so a failure names a
+queries (zero strides) under the softmax and relu attention; and the fp32
+debug path over the same kinds of shapes.  Each case is drawn from its own seed, so a failure names a
 reproducible configuration.
 """
 import numpy as np
@@ -16,7 +17,7 @@ import pytest
 import torch
 
 import oracle
-from gpu_util import announce, assert_bf16_close, assert_lse_close, device_inputs, f64, need_gpu
+from gpu_util import announce, assert_bf16_close, assert_fp32_close, assert_lse_close, device_inputs, f64, need_gpu
 from paper_2609_13612_amd import api, blockmask, inputs
 
 pytestmark = pytest.mark.gpu
@@ -187,3 +188,29 @@ def test_sweep_bias_norm(i):
         assert_lse_close(lse, L, "LSE")
     for name, g, r in zip(("dQ", "dK", "dV"), grads, ref):
         assert_bf16_close(g, r, name)
+
+
+@pytest.mark.parametrize("i", range(6))
+def test_sweep_fp32(i):
+    need_gpu()
+    c = _attention_case(100 + i)
+    c["S"] = min(c["S"], 200)
+    if c["window"] is not None:
+        c["window"] = min(c["window"], c["S"] + 5)
+    announce(f"fp32 sweep {i}: {c}")
+    B, H, Hkv, S, D = c["B"], c["H"], c["Hkv"], c["S"], c["D"]
+    cpu, dev = device_inputs(B, H, Hkv, S, D, dtype="fp32", seed=c["seed"], with_do=True)
+    slopes = inputs.alibi_slopes(H) if c["alibi"] else None
+    kw = dict(rope=c["rope"], theta=c["theta"], mask=c["mask"], window=c["window"], scale=c["scale"])
+    ds = None if slopes is None else slopes.cuda()
+    o, lse = api.attnfuse_fwd(dev["q"], dev["k"], dev["v"], alibi_slopes=ds, **kw)
+    dq, dk, dv = api.attnfuse_bwd(dev["q"], dev["k"], dev["v"], o, dev["do"], lse, alibi_slopes=ds, **kw)
+    torch.cuda.synchronize()
+    os_ = None if slopes is None else f64(slopes)
+    O, L = oracle.attention_forward(f64(cpu["q"]), f64(cpu["k"]), f64(cpu["v"]), alibi_slopes=os_, **kw)
+    ref = oracle.attention_backward(f64(cpu["q"]), f64(cpu["k"]), f64(cpu["v"]), f64(cpu["do"]),
+                                    alibi_slopes=os_, o=f64(o), **kw)
+    assert_fp32_close(o, O, "O fp32")
+    assert_lse_close(lse, L, "LSE fp32")
+    for name, g, r in zip(("dQ", "dK", "dV"), (dq, dk, dv), ref):
+        assert_fp32_close(g, r, name + " fp32")

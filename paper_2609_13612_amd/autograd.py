@@ -1,5 +1,6 @@
 """torch.autograd functions over the C ABI: the fused attention (and its
-block-sparse form) as differentiable operations for training code.
+block-sparse and bias / relu forms) as differentiable operations for training
+code.
 
 ``attention`` runs attnfuse_fwd, keeps Q, K, V, O and the row statistic LSE
 (Section 4.4: the forward saves one scalar per row), and its backward runs
@@ -49,6 +50,24 @@ class _BlockSparseAttention(torch.autograd.Function):
         return dq, dk, dv, None, None, None, None, None, None, None
 
 
+class _BiasNormAttention(torch.autograd.Function):
+    @staticmethod
+    def forward(ctx, q, k, v, bias, norm, rope, theta, mask, window, scale):
+        o, lse = api.attnfuse_fwd_bias_norm(q, k, v, bias=bias, norm=norm, rope=rope, theta=theta, mask=mask,
+                                            window=window, scale=scale)
+        ctx.save_for_backward(q, k, v, o, lse, bias)
+        ctx.cfg = dict(norm=norm, rope=rope, theta=theta, mask=mask, window=window, scale=scale)
+        if lse is not None:
+            ctx.mark_non_differentiable(lse)
+        return o, lse
+
+    @staticmethod
+    def backward(ctx, do, _dlse):
+        q, k, v, o, lse, bias = ctx.saved_tensors
+        dq, dk, dv = api.attnfuse_bwd_bias_norm(q, k, v, o, do.contiguous(), lse, bias=bias, **ctx.cfg)
+        return dq, dk, dv, None, None, None, None, None, None, None
+
+
 def attention(q, k, v, *, rope="none", theta=10000.0, mask="causal", window=None, alibi_slopes=None, scale=None,
               return_lse=False):
     """Differentiable fused attention: O [B, H, S, D] (and the non-differentiable
@@ -62,4 +81,13 @@ def blocksparse_attention(q, k, v, block_mask, *, rope="none", theta=10000.0, ma
     """Differentiable block-sparse attention over a blockmask.BlockMask;
     arguments as api.attnfuse_fwd_blocksparse."""
     o, lse = _BlockSparseAttention.apply(q, k, v, alibi_slopes, block_mask, rope, theta, mask, window, scale)
+    return (o, lse) if return_lse else o
+
+
+def attention_bias_norm(q, k, v, *, bias=None, norm="softmax", rope="none", theta=10000.0, mask="causal",
+                        window=None, scale=None, return_lse=False):
+    """Differentiable attention with a dense additive bias tensor and softmax or
+    relu normalisation; arguments as api.attnfuse_fwd_bias_norm (the bias gets
+    no gradient; under relu attention LSE is None)."""
+    o, lse = _BiasNormAttention.apply(q, k, v, bias, norm, rope, theta, mask, window, scale)
     return (o, lse) if return_lse else o

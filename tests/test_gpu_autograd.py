@@ -72,3 +72,24 @@ def test_autograd_blocksparse():
     assert torch.equal(o.detach(), o2)
     for t, g in zip((q, k, v), g2):
         assert torch.equal(t.grad, g)
+
+
+@pytest.mark.parametrize("norm", ["softmax", "relu"])
+def test_autograd_bias_norm(norm):
+    need_gpu()
+    announce(f"autograd bias norm={norm}")
+    B, H, Hkv, S, D = 2, 4, 2, 160, 128
+    _, dev = device_inputs(B, H, Hkv, S, D, seed=84, with_do=True)
+    g = torch.Generator("cpu").manual_seed(84)
+    bias = torch.randn(B, 1, S, S, generator=g, dtype=torch.float32).cuda()
+    scale = D ** -0.5 / (S if norm == "relu" else 1)
+    kw = dict(bias=bias / (S if norm == "relu" else 1), norm=norm, rope="neox", mask="causal", scale=scale)
+    q, k, v = _leaves(dev)
+    o = autograd.attention_bias_norm(q, k, v, **kw)
+    o.backward(dev["do"])
+    o2, lse2 = api.attnfuse_fwd_bias_norm(dev["q"], dev["k"], dev["v"], **kw)
+    g2 = api.attnfuse_bwd_bias_norm(dev["q"], dev["k"], dev["v"], o2, dev["do"], lse2, **kw)
+    torch.cuda.synchronize()
+    assert torch.equal(o.detach(), o2)
+    for t, gr in zip((q, k, v), g2):
+        assert torch.equal(t.grad, gr)

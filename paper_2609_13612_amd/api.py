@@ -45,34 +45,86 @@ def _shape(q, k):
     return B, H, k.shape[1], S, D
 
 
-def _same(ref, *ts):
-    for t in ts:
-        if t is None:
-            continue
-        if not t.is_cuda or t.dtype != ref.dtype or not t.is_contiguous():
-            raise ValueError("tensors must be contiguous, on the GPU, and share one dtype")
+def _device(q):
+    """The GPU that q lives on (every other tensor of the call must be there too)."""
+    if not isinstance(q, torch.Tensor) or not q.is_cuda:
+        raise ValueError("q must be a tensor on a GPU")
+    if q.dtype not in DTYPE:
+        raise ValueError(f"dtype must be one of {sorted(str(d) for d in DTYPE)}")
+    return q.device
 
 
-def _variant(rope, theta, mask, window, alibi_slopes, scale, D):
+def _need(t, name, shape, dtype, device):
+    """Raise unless t is a contiguous tensor of exactly that shape and dtype on device."""
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch tensor")
+    if t.device != device:
+        raise ValueError(f"{name} must be on {device} (it is on {t.device})")
+    if t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype} (it is {t.dtype})")
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)} (it has {tuple(t.shape)})")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+
+
+def _opt(t, name, shape, dtype, device):
+    """A caller-provided output: checked like an input, or allocated."""
+    if t is None:
+        return torch.empty(shape, device=device, dtype=dtype)
+    _need(t, name, shape, dtype, device)
+    return t
+
+
+def _inputs(q, k, v, device):
+    """q [B, H, S, D]; k and v [B, H_kv, S, D] of q's dtype, all on q's device."""
+    _need(q, "q", q.shape, q.dtype, device)
+    _need(k, "k", k.shape, q.dtype, device)
+    _need(v, "v", k.shape, q.dtype, device)
+
+
+def _bwd_inputs(q, k, v, o, do, lse, device, lse_needed):
+    _inputs(q, k, v, device)
+    _need(o, "o", q.shape, q.dtype, device)
+    _need(do, "do", q.shape, q.dtype, device)
+    if lse is not None or lse_needed:
+        _need(lse, "lse", q.shape[:3], torch.float32, device)
+
+
+def _grads(q, k, dq, dk, dv, device):
+    return (_opt(dq, "dq", q.shape, q.dtype, device), _opt(dk, "dk", k.shape, q.dtype, device),
+            _opt(dv, "dv", k.shape, q.dtype, device))
+
+
+def _workspace(ws, nbytes, device):
+    """(tensor, size in bytes) of the workspace: the caller's, checked, or a new one."""
+    if ws is None:
+        return torch.empty(nbytes, device=device, dtype=torch.uint8), nbytes
+    if not isinstance(ws, torch.Tensor) or ws.device != device or not ws.is_contiguous():
+        raise ValueError("workspace must be a contiguous tensor on q's device")
+    return ws, ws.numel() * ws.element_size()
+
+
+def _variant(rope, theta, mask, window, alibi_slopes, scale, D, H=None, device=None):
     if scale is None:
         scale = 1.0 / math.sqrt(D)
-    if alibi_slopes is not None and (alibi_slopes.dtype != torch.float32 or not alibi_slopes.is_cuda):
-        raise ValueError("alibi_slopes must be an fp32 GPU tensor [H]")
+    if alibi_slopes is not None:
+        _need(alibi_slopes, "alibi_slopes", (H,), torch.float32, device)
     return ROPE[rope], float(theta), MASK[mask], int(window or 0), scale
 
 
 def attnfuse_fwd(q, k, v, *, rope="none", theta=10000.0, mask="causal", window=None,
                  alibi_slopes=None, scale=None, out=None, lse=None):
     """O, LSE = attention(q, k, v); see attnfuse_fwd in include/attnfuse.h."""
+    dev = _device(q)
     B, H, Hkv, S, D = _shape(q, k)
-    _same(q, k, v, out)
-    if v.shape != k.shape:
-        raise ValueError("v must have k's shape")
-    out = torch.empty_like(q) if out is None else out
-    lse = torch.empty(B, H, S, device=q.device, dtype=torch.float32) if lse is None else lse
-    r, th, m, w, sc = _variant(rope, theta, mask, window, alibi_slopes, scale, D)
-    code = _lib.load().attnfuse_fwd(_ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(lse), B, H, Hkv, S, D,
-                                    DTYPE[q.dtype], r, th, m, w, _ptr(alibi_slopes), sc, _stream())
+    _inputs(q, k, v, dev)
+    out = _opt(out, "out", q.shape, q.dtype, dev)
+    lse = _opt(lse, "lse", (B, H, S), torch.float32, dev)
+    r, th, m, w, sc = _variant(rope, theta, mask, window, alibi_slopes, scale, D, H, dev)
+    with torch.cuda.device(dev):
+        code = _lib.load().attnfuse_fwd(_ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(lse), B, H, Hkv, S, D,
+                                        DTYPE[q.dtype], r, th, m, w, _ptr(alibi_slopes), sc, _stream())
     _check(code, "attnfuse_fwd")
     return out, lse
 
@@ -84,19 +136,17 @@ def attnfuse_bwd_workspace_bytes(B, H, H_kv, S, D, rope="none"):
 def attnfuse_bwd(q, k, v, o, do, lse, *, rope="none", theta=10000.0, mask="causal", window=None,
                  alibi_slopes=None, scale=None, dq=None, dk=None, dv=None, workspace=None):
     """dQ, dK, dV of attnfuse_fwd; see attnfuse_bwd in include/attnfuse.h."""
+    dev = _device(q)
     B, H, Hkv, S, D = _shape(q, k)
-    _same(q, k, v, o, do, dq, dk, dv)
-    dq = torch.empty_like(q) if dq is None else dq
-    dk = torch.empty_like(k) if dk is None else dk
-    dv = torch.empty_like(v) if dv is None else dv
-    nbytes = attnfuse_bwd_workspace_bytes(B, H, Hkv, S, D, rope)
-    if workspace is None:
-        workspace = torch.empty(nbytes, device=q.device, dtype=torch.uint8)
-    r, th, m, w, sc = _variant(rope, theta, mask, window, alibi_slopes, scale, D)
-    code = _lib.load().attnfuse_bwd(_ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(do), _ptr(lse),
-                                    _ptr(dq), _ptr(dk), _ptr(dv), _ptr(workspace), workspace.numel(),
-                                    B, H, Hkv, S, D, DTYPE[q.dtype], r, th, m, w,
-                                    _ptr(alibi_slopes), sc, _stream())
+    _bwd_inputs(q, k, v, o, do, lse, dev, lse_needed=True)
+    dq, dk, dv = _grads(q, k, dq, dk, dv, dev)
+    workspace, wbytes = _workspace(workspace, attnfuse_bwd_workspace_bytes(B, H, Hkv, S, D, rope), dev)
+    r, th, m, w, sc = _variant(rope, theta, mask, window, alibi_slopes, scale, D, H, dev)
+    with torch.cuda.device(dev):
+        code = _lib.load().attnfuse_bwd(_ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(do), _ptr(lse),
+                                        _ptr(dq), _ptr(dk), _ptr(dv), _ptr(workspace), wbytes,
+                                        B, H, Hkv, S, D, DTYPE[q.dtype], r, th, m, w,
+                                        _ptr(alibi_slopes), sc, _stream())
     _check(code, "attnfuse_bwd")
     return dq, dk, dv
 
@@ -116,17 +166,17 @@ def attnfuse_fwd_blocksparse(q, k, v, block_mask, *, rope="none", theta=10000.0,
                              alibi_slopes=None, scale=None, out=None, lse=None):
     """O, LSE of attention restricted to the active blocks of ``block_mask``
     (a blockmask.BlockMask); see attnfuse_fwd_blocksparse."""
+    dev = _device(q)
     B, H, Hkv, S, D = _shape(q, k)
-    _same(q, k, v, out)
-    if v.shape != k.shape:
-        raise ValueError("v must have k's shape")
+    _inputs(q, k, v, dev)
     qp, ki, _, _ = _mask_ptrs(block_mask, q, S)
-    out = torch.empty_like(q) if out is None else out
-    lse = torch.empty(B, H, S, device=q.device, dtype=torch.float32) if lse is None else lse
-    r, th, m, w, sc = _variant(rope, theta, mask, window, alibi_slopes, scale, D)
-    code = _lib.load().attnfuse_fwd_blocksparse(_ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(lse), qp, ki,
-                                                B, H, Hkv, S, D, DTYPE[q.dtype], r, th, m, w, _ptr(alibi_slopes),
-                                                sc, _stream())
+    out = _opt(out, "out", q.shape, q.dtype, dev)
+    lse = _opt(lse, "lse", (B, H, S), torch.float32, dev)
+    r, th, m, w, sc = _variant(rope, theta, mask, window, alibi_slopes, scale, D, H, dev)
+    with torch.cuda.device(dev):
+        code = _lib.load().attnfuse_fwd_blocksparse(_ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(lse), qp, ki,
+                                                    B, H, Hkv, S, D, DTYPE[q.dtype], r, th, m, w,
+                                                    _ptr(alibi_slopes), sc, _stream())
     _check(code, "attnfuse_fwd_blocksparse")
     return out, lse
 
@@ -135,20 +185,18 @@ def attnfuse_bwd_blocksparse(q, k, v, o, do, lse, block_mask, *, rope="none", th
                              window=None, alibi_slopes=None, scale=None, dq=None, dk=None, dv=None,
                              workspace=None):
     """dQ, dK, dV of attnfuse_fwd_blocksparse; see attnfuse_bwd_blocksparse."""
+    dev = _device(q)
     B, H, Hkv, S, D = _shape(q, k)
-    _same(q, k, v, o, do, dq, dk, dv)
+    _bwd_inputs(q, k, v, o, do, lse, dev, lse_needed=True)
     qp, ki, kp, qi = _mask_ptrs(block_mask, q, S)
-    dq = torch.empty_like(q) if dq is None else dq
-    dk = torch.empty_like(k) if dk is None else dk
-    dv = torch.empty_like(v) if dv is None else dv
-    nbytes = attnfuse_bwd_workspace_bytes(B, H, Hkv, S, D, rope)
-    if workspace is None:
-        workspace = torch.empty(nbytes, device=q.device, dtype=torch.uint8)
-    r, th, m, w, sc = _variant(rope, theta, mask, window, alibi_slopes, scale, D)
-    code = _lib.load().attnfuse_bwd_blocksparse(_ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(do), _ptr(lse),
-                                                _ptr(dq), _ptr(dk), _ptr(dv), qp, ki, kp, qi, _ptr(workspace),
-                                                workspace.numel(), B, H, Hkv, S, D, DTYPE[q.dtype], r, th, m, w,
-                                                _ptr(alibi_slopes), sc, _stream())
+    dq, dk, dv = _grads(q, k, dq, dk, dv, dev)
+    workspace, wbytes = _workspace(workspace, attnfuse_bwd_workspace_bytes(B, H, Hkv, S, D, rope), dev)
+    r, th, m, w, sc = _variant(rope, theta, mask, window, alibi_slopes, scale, D, H, dev)
+    with torch.cuda.device(dev):
+        code = _lib.load().attnfuse_bwd_blocksparse(_ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(do), _ptr(lse),
+                                                    _ptr(dq), _ptr(dk), _ptr(dv), qp, ki, kp, qi, _ptr(workspace),
+                                                    wbytes, B, H, Hkv, S, D, DTYPE[q.dtype], r, th, m, w,
+                                                    _ptr(alibi_slopes), sc, _stream())
     _check(code, "attnfuse_bwd_blocksparse")
     return dq, dk, dv
 
@@ -175,18 +223,18 @@ def attnfuse_fwd_bias_norm(q, k, v, *, bias=None, norm="softmax", rope="none", t
                            window=None, scale=None, out=None, lse=None):
     """O (and LSE, None under relu attention) with a dense additive bias and/or
     relu attention; see attnfuse_fwd_bias_norm in include/attnfuse.h."""
+    dev = _device(q)
     B, H, Hkv, S, D = _shape(q, k)
-    _same(q, k, v, out)
-    if v.shape != k.shape:
-        raise ValueError("v must have k's shape")
-    out = torch.empty_like(q) if out is None else out
-    if NORM[norm] == NORM["softmax"] and lse is None:
-        lse = torch.empty(B, H, S, device=q.device, dtype=torch.float32)
+    _inputs(q, k, v, dev)
+    out = _opt(out, "out", q.shape, q.dtype, dev)
+    if NORM[norm] == NORM["softmax"] or lse is not None:
+        lse = _opt(lse, "lse", (B, H, S), torch.float32, dev)
     bp, sb, sh, sq = _bias_args(bias, q, B, H, S)
     r, th, m, w, sc = _variant(rope, theta, mask, window, None, scale, D)
-    code = _lib.load().attnfuse_fwd_bias_norm(_ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(lse), bp, sb, sh, sq,
-                                              NORM[norm], B, H, Hkv, S, D, DTYPE[q.dtype], r, th, m, w, None, sc,
-                                              _stream())
+    with torch.cuda.device(dev):
+        code = _lib.load().attnfuse_fwd_bias_norm(_ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(lse), bp, sb, sh,
+                                                  sq, NORM[norm], B, H, Hkv, S, D, DTYPE[q.dtype], r, th, m, w,
+                                                  None, sc, _stream())
     _check(code, "attnfuse_fwd_bias_norm")
     return out, lse
 
@@ -195,20 +243,18 @@ def attnfuse_bwd_bias_norm(q, k, v, o, do, lse, *, bias=None, norm="softmax", ro
                            mask="causal", window=None, scale=None, dq=None, dk=None, dv=None, workspace=None):
     """dQ, dK, dV of attnfuse_fwd_bias_norm (lse may be None under relu
     attention); see attnfuse_bwd_bias_norm."""
+    dev = _device(q)
     B, H, Hkv, S, D = _shape(q, k)
-    _same(q, k, v, o, do, dq, dk, dv)
-    dq = torch.empty_like(q) if dq is None else dq
-    dk = torch.empty_like(k) if dk is None else dk
-    dv = torch.empty_like(v) if dv is None else dv
-    nbytes = attnfuse_bwd_workspace_bytes(B, H, Hkv, S, D, rope)
-    if workspace is None:
-        workspace = torch.empty(nbytes, device=q.device, dtype=torch.uint8)
+    _bwd_inputs(q, k, v, o, do, lse, dev, lse_needed=NORM[norm] == NORM["softmax"])
+    dq, dk, dv = _grads(q, k, dq, dk, dv, dev)
+    workspace, wbytes = _workspace(workspace, attnfuse_bwd_workspace_bytes(B, H, Hkv, S, D, rope), dev)
     bp, sb, sh, sq = _bias_args(bias, q, B, H, S)
     r, th, m, w, sc = _variant(rope, theta, mask, window, None, scale, D)
-    code = _lib.load().attnfuse_bwd_bias_norm(_ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(do), _ptr(lse),
-                                              _ptr(dq), _ptr(dk), _ptr(dv), bp, sb, sh, sq, NORM[norm],
-                                              _ptr(workspace), workspace.numel(), B, H, Hkv, S, D, DTYPE[q.dtype],
-                                              r, th, m, w, None, sc, _stream())
+    with torch.cuda.device(dev):
+        code = _lib.load().attnfuse_bwd_bias_norm(_ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(do), _ptr(lse),
+                                                  _ptr(dq), _ptr(dk), _ptr(dv), bp, sb, sh, sq, NORM[norm],
+                                                  _ptr(workspace), wbytes, B, H, Hkv, S, D, DTYPE[q.dtype],
+                                                  r, th, m, w, None, sc, _stream())
     _check(code, "attnfuse_bwd_bias_norm")
     return dq, dk, dv
 
@@ -221,41 +267,49 @@ def attnfuse_decode(q, k_cache, v_cache, cache_lens=None, *, rope="none", theta=
                     window=None, alibi_slopes=None, scale=None, out=None, lse=None, workspace=None):
     """O [B,H,D], LSE [B,H] of one query per sequence against a KV cache of
     already-rotated keys; see attnfuse_decode in include/attnfuse.h."""
+    dev = _device(q)
     if q.dim() != 3 or k_cache.dim() != 4 or v_cache.shape != k_cache.shape:
         raise ValueError("q must be [B, H, D] and the caches [B, H_kv, S_kv, D]")
     B, H, D = q.shape
     Hkv, S_kv = k_cache.shape[1], k_cache.shape[2]
     if k_cache.shape[0] != B or k_cache.shape[3] != D:
         raise ValueError("cache shape does not match q")
-    _same(q, k_cache, v_cache, out)
-    if cache_lens is not None and (cache_lens.dtype != torch.int32 or not cache_lens.is_cuda
-                                   or cache_lens.shape != (B,)):
-        raise ValueError("cache_lens must be an int32 GPU tensor [B]")
-    out = torch.empty_like(q) if out is None else out
-    lse = torch.empty(B, H, device=q.device, dtype=torch.float32) if lse is None else lse
-    nbytes = attnfuse_decode_workspace_bytes(B, H, Hkv, S_kv, D)
-    if workspace is None:
-        workspace = torch.empty(nbytes, device=q.device, dtype=torch.uint8)
-    r, th, m, w, sc = _variant(rope, theta, mask, window, alibi_slopes, scale, D)
-    code = _lib.load().attnfuse_decode(_ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(cache_lens), _ptr(out),
-                                       _ptr(lse), _ptr(workspace), workspace.numel(), B, H, Hkv, S_kv, D,
-                                       DTYPE[q.dtype], r, th, m, w, _ptr(alibi_slopes), sc, _stream())
+    _need(q, "q", q.shape, q.dtype, dev)
+    _need(k_cache, "k_cache", k_cache.shape, q.dtype, dev)
+    _need(v_cache, "v_cache", k_cache.shape, q.dtype, dev)
+    if cache_lens is not None:
+        _need(cache_lens, "cache_lens", (B,), torch.int32, dev)
+    out = _opt(out, "out", q.shape, q.dtype, dev)
+    lse = _opt(lse, "lse", (B, H), torch.float32, dev)
+    workspace, wbytes = _workspace(workspace, attnfuse_decode_workspace_bytes(B, H, Hkv, S_kv, D), dev)
+    r, th, m, w, sc = _variant(rope, theta, mask, window, alibi_slopes, scale, D, H, dev)
+    with torch.cuda.device(dev):
+        code = _lib.load().attnfuse_decode(_ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(cache_lens), _ptr(out),
+                                           _ptr(lse), _ptr(workspace), wbytes, B, H, Hkv, S_kv, D,
+                                           DTYPE[q.dtype], r, th, m, w, _ptr(alibi_slopes), sc, _stream())
     _check(code, "attnfuse_decode")
     return out, lse
 
 
 def _rope_call(name, x0, x1, y0, y1, rope, theta):
+    dev = _device(x0)
     if x1 is not None:
         B, H, Hkv, S, D = _shape(x0, x1)
+        _need(x1, "k", x1.shape, x0.dtype, dev)
     else:
+        if x0.dim() != 4:
+            raise ValueError("q must be [B, H, S, D]")
         B, H, S, D = x0.shape
         Hkv = 1
-    _same(x0, x1, y0, y1)
-    y0 = torch.empty_like(x0) if y0 is None else y0
-    if x1 is not None and y1 is None:
-        y1 = torch.empty_like(x1)
-    code = getattr(_lib.load(), name)(_ptr(x0), _ptr(x1), _ptr(y0), _ptr(y1), B, H, Hkv, S, D,
-                                      DTYPE[x0.dtype], ROPE[rope], float(theta), _stream())
+    _need(x0, "q", x0.shape, x0.dtype, dev)
+    y0 = _opt(y0, "out_q", x0.shape, x0.dtype, dev)
+    if x1 is not None:
+        y1 = _opt(y1, "out_k", x1.shape, x0.dtype, dev)
+    elif y1 is not None:
+        raise ValueError("out_k needs k")
+    with torch.cuda.device(dev):
+        code = getattr(_lib.load(), name)(_ptr(x0), _ptr(x1), _ptr(y0), _ptr(y1), B, H, Hkv, S, D,
+                                          DTYPE[x0.dtype], ROPE[rope], float(theta), _stream())
     _check(code, name)
     return y0, y1
 

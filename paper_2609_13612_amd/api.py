@@ -158,6 +158,11 @@ def _mask_ptrs(block_mask, q, S):
     for t in ts:
         if t.device != q.device or t.dtype != torch.int32 or not t.is_contiguous():
             raise ValueError("block mask lists must be contiguous int32 tensors on q's device")
+    # the offset arrays are read up to entry nb; their values are those the
+    # blockmask constructors built and checked
+    nb = (S + 63) // 64
+    if block_mask.q_ptr.numel() != nb + 1 or block_mask.k_ptr.numel() != nb + 1:
+        raise ValueError(f"block mask offset lists must have nb + 1 = {nb + 1} entries")
     # an empty index list has no storage; any valid aligned address serves
     return [t.data_ptr() if t.numel() else block_mask.q_ptr.data_ptr() for t in ts]
 

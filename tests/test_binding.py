@@ -68,3 +68,13 @@ def test_cpu_q_is_rejected_before_the_library():
         api.attnfuse_decode(q[:, :, 0], q, q)
     with pytest.raises(ValueError, match="GPU"):
         api.attnfuse_rope(q)
+
+
+def test_block_mask_offset_lengths_checked():
+    from paper_2609_13612_amd import blockmask
+    bm = blockmask.block_mask_from_dense(torch.ones(3, 3, dtype=torch.bool), 150)
+    q = torch.zeros(1, 1, 150, 64, dtype=torch.bfloat16)
+    assert len(api._mask_ptrs(bm, q, 150)) == 4
+    short = blockmask.BlockMask(bm.S, bm.active, bm.q_ptr[:-1].contiguous(), bm.k_idx, bm.k_ptr, bm.q_idx)
+    with pytest.raises(ValueError, match="nb \\+ 1"):
+        api._mask_ptrs(short, q, 150)

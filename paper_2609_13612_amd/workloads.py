@@ -65,7 +65,7 @@ WORKLOADS = {
                                             backward=True, notes="Llama-3-8B attention layer, fwd + bwd"),
 }
 
-LLAMA_SWEEP_S = (1024, 2048, 4096, 8192, 16384)
+LLAMA_SWEEP_S = (1024, 1536, 2048, 2560, 3072, 4096, 6144, 8192, 16384)
 
 
 @dataclass(frozen=True)

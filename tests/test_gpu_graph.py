@@ -1,7 +1,8 @@
 """HIP-graph capture of the entry points through the C ABI.
 
 After one eager call on a device (which builds that device's cos/sin table),
-the fused forward and backward, the block-sparse forward and decode allocate
+the fused forward and backward, the block-sparse forward, decode and the
+separate path (rotation kernel, then the forward without RoPE) allocate
 nothing, synchronise nothing and issue no memset, so a captured sequence of
 them replays.  Each test captures once, then replays on three fresh inputs
 copied into the captured buffers, with eager calls and synchronisations in
@@ -107,3 +108,34 @@ def test_graph_decode_replays():
         g.replay()
         torch.cuda.synchronize()
         assert torch.equal(o_s, o_e) and torch.equal(lse_s, lse_e), f"seed {seed}: replay differs"
+
+
+def test_graph_separate_path_replays():
+    """The separate path: Q and K rotated by the rotation kernel into buffers of
+    their own, then the forward without RoPE on the rotated tensors."""
+    need_gpu()
+    announce("graph capture: rotation + forward without RoPE")
+    B, H, Hkv, S, D = 2, 8, 2, 777, 64
+    kw = dict(rope="interleaved", theta=10000.0)
+    _, d0 = device_inputs(B, H, Hkv, S, D, seed=74)
+    q, k, v = (d0[n].clone() for n in ("q", "k", "v"))
+    api.attnfuse_rope(q, k, **kw)                       # eager warm-up: builds the table
+    qr, kr = torch.empty_like(q), torch.empty_like(k)
+    o_s, lse_s = torch.empty_like(q), torch.empty(B, H, S, device="cuda")
+
+    def step():
+        api.attnfuse_rope(q, k, out_q=qr, out_k=kr, **kw)
+        api.attnfuse_fwd(qr, kr, v, out=o_s, lse=lse_s, mask="causal")
+
+    g = _capture(step)
+    for seed in SEEDS:
+        _, d = device_inputs(B, H, Hkv, S, D, seed=seed)
+        rq, rk = api.attnfuse_rope(d["q"], d["k"], **kw)
+        o_e, lse_e = api.attnfuse_fwd(rq, rk, d["v"], mask="causal")
+        torch.cuda.synchronize()
+        for dst, name in ((q, "q"), (k, "k"), (v, "v")):
+            dst.copy_(d[name])
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(qr, rq) and torch.equal(kr, rk), f"seed {seed}: rotation replay differs"
+        assert torch.equal(o_s, o_e) and torch.equal(lse_s, lse_e), f"seed {seed}: forward replay differs"

@@ -1,7 +1,8 @@
 """HIP-graph capture of the entry points through the C ABI.
 
 After one eager call on a device (which builds that device's cos/sin table),
-the fused forward and backward, the block-sparse forward, decode and the
+the fused forward and backward (also with a dense bias or relu attention), the
+block-sparse forward, decode and the
 separate path (rotation kernel, then the forward without RoPE) allocate
 nothing, synchronise nothing and issue no memset, so a captured sequence of
 them replays.  Each test captures once, then replays on three fresh inputs
@@ -139,3 +140,46 @@ def test_graph_separate_path_replays():
         torch.cuda.synchronize()
         assert torch.equal(qr, rq) and torch.equal(kr, rk), f"seed {seed}: rotation replay differs"
         assert torch.equal(o_s, o_e) and torch.equal(lse_s, lse_e), f"seed {seed}: forward replay differs"
+
+
+@pytest.mark.parametrize("norm", ["softmax", "relu"])
+def test_graph_bias_norm_replays(norm):
+    """Dense bias (broadcast over heads) under softmax or relu attention, forward
+    then backward; every replay gets fresh inputs and fresh bias values."""
+    need_gpu()
+    announce(f"graph capture: bias, norm={norm}")
+    B, H, Hkv, S, D = 2, 4, 2, 300, 128
+    relu = norm == "relu"
+    kw = dict(norm=norm, rope="neox", mask="causal", scale=D ** -0.5 / (S if relu else 1))
+    _, d0 = device_inputs(B, H, Hkv, S, D, seed=75, with_do=True)
+    q, k, v, do = (d0[n].clone() for n in ("q", "k", "v", "do"))
+    bias = torch.zeros(B, 1, S, S, device="cuda")
+    o, lse = api.attnfuse_fwd_bias_norm(q, k, v, bias=bias, **kw)   # eager warm-up: builds the table
+    api.attnfuse_bwd_bias_norm(q, k, v, o, do, lse, bias=bias, **kw)
+    o_s = torch.empty_like(q)
+    lse_s = None if relu else torch.empty(B, H, S, device="cuda")
+    dq_s, dk_s, dv_s = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
+    ws = torch.empty(api.attnfuse_bwd_workspace_bytes(B, H, Hkv, S, D, "neox"), device="cuda", dtype=torch.uint8)
+
+    def step():
+        api.attnfuse_fwd_bias_norm(q, k, v, bias=bias, out=o_s, lse=lse_s, **kw)
+        api.attnfuse_bwd_bias_norm(q, k, v, o_s, do, lse_s, bias=bias, dq=dq_s, dk=dk_s, dv=dv_s, workspace=ws, **kw)
+
+    g = _capture(step)
+    for seed in SEEDS:
+        _, d = device_inputs(B, H, Hkv, S, D, seed=seed, with_do=True)
+        gen = torch.Generator("cpu").manual_seed(seed)
+        b_new = (torch.randn(B, 1, S, S, generator=gen) / (S if relu else 1)).cuda()
+        o_e, lse_e = api.attnfuse_fwd_bias_norm(d["q"], d["k"], d["v"], bias=b_new, **kw)
+        grads_e = api.attnfuse_bwd_bias_norm(d["q"], d["k"], d["v"], o_e, d["do"], lse_e, bias=b_new, **kw)
+        torch.cuda.synchronize()
+        for dst, name in ((q, "q"), (k, "k"), (v, "v"), (do, "do")):
+            dst.copy_(d[name])
+        bias.copy_(b_new)
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(o_s, o_e), f"seed {seed}: forward replay differs"
+        if not relu:
+            assert torch.equal(lse_s, lse_e), f"seed {seed}: LSE replay differs"
+        for name, a, b in zip(("dQ", "dK", "dV"), (dq_s, dk_s, dv_s), grads_e):
+            assert torch.equal(a, b), f"seed {seed}: {name} replay differs"

@@ -2,7 +2,7 @@
 
 After one eager call on a device (which builds that device's cos/sin table),
 the fused forward and backward (also with a dense bias or relu attention), the
-block-sparse forward, decode and the
+block-sparse forward and backward, decode and the
 separate path (rotation kernel, then the forward without RoPE) allocate
 nothing, synchronise nothing and issue no memset, so a captured sequence of
 them replays.  Each test captures once, then replays on three fresh inputs
@@ -64,25 +64,38 @@ def test_graph_fwd_bwd_replays():
 
 
 def test_graph_blocksparse_replays():
-    """Block-sparse forward over a BigBird-style mask, D = 64, S = 1024."""
+    """Block-sparse forward then backward over a BigBird-style mask, D = 64,
+    S = 1024, with RoPE."""
     need_gpu()
-    announce("graph capture: block-sparse fwd")
+    announce("graph capture: block-sparse fwd + bwd")
     B, H, Hkv, S, D = 2, 4, 4, 1024, 64
+    kw = dict(rope="neox")
     bm = blockmask.block_mask_from_dense(torch.from_numpy(inputs.bigbird_blocks(S // 64, seed=3)), S, device="cuda")
-    _, d0 = device_inputs(B, H, Hkv, S, D, seed=70)
-    q, k, v = (d0[n].clone() for n in ("q", "k", "v"))
-    api.attnfuse_fwd_blocksparse(q, k, v, bm)
+    _, d0 = device_inputs(B, H, Hkv, S, D, seed=70, with_do=True)
+    q, k, v, do = (d0[n].clone() for n in ("q", "k", "v", "do"))
+    o, lse = api.attnfuse_fwd_blocksparse(q, k, v, bm, **kw)   # eager warm-up: builds the table
+    api.attnfuse_bwd_blocksparse(q, k, v, o, do, lse, bm, **kw)
     o_s, lse_s = torch.empty_like(q), torch.empty(B, H, S, device="cuda")
-    g = _capture(lambda: api.attnfuse_fwd_blocksparse(q, k, v, bm, out=o_s, lse=lse_s))
+    dq_s, dk_s, dv_s = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
+    ws = torch.empty(api.attnfuse_bwd_workspace_bytes(B, H, Hkv, S, D, "neox"), device="cuda", dtype=torch.uint8)
+
+    def step():
+        api.attnfuse_fwd_blocksparse(q, k, v, bm, out=o_s, lse=lse_s, **kw)
+        api.attnfuse_bwd_blocksparse(q, k, v, o_s, do, lse_s, bm, dq=dq_s, dk=dk_s, dv=dv_s, workspace=ws, **kw)
+
+    g = _capture(step)
     for seed in SEEDS:
-        _, d = device_inputs(B, H, Hkv, S, D, seed=seed)
-        o_e, lse_e = api.attnfuse_fwd_blocksparse(d["q"], d["k"], d["v"], bm)
+        _, d = device_inputs(B, H, Hkv, S, D, seed=seed, with_do=True)
+        o_e, lse_e = api.attnfuse_fwd_blocksparse(d["q"], d["k"], d["v"], bm, **kw)
+        grads_e = api.attnfuse_bwd_blocksparse(d["q"], d["k"], d["v"], o_e, d["do"], lse_e, bm, **kw)
         torch.cuda.synchronize()
-        for dst, name in ((q, "q"), (k, "k"), (v, "v")):
+        for dst, name in ((q, "q"), (k, "k"), (v, "v"), (do, "do")):
             dst.copy_(d[name])
         g.replay()
         torch.cuda.synchronize()
-        assert torch.equal(o_s, o_e) and torch.equal(lse_s, lse_e), f"seed {seed}: replay differs"
+        assert torch.equal(o_s, o_e) and torch.equal(lse_s, lse_e), f"seed {seed}: forward replay differs"
+        for name, a, b in zip(("dQ", "dK", "dV"), (dq_s, dk_s, dv_s), grads_e):
+            assert torch.equal(a, b), f"seed {seed}: {name} replay differs"
 
 
 def test_graph_decode_replays():

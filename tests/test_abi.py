@@ -303,3 +303,38 @@ def test_bwd_bias_norm_unsupported():
     assert _bwd_bn(dtype=1) == -2
     assert _bwd_bn(slopes=FAKE + 0x1000) == -2
     assert _bwd_bn(LSE=None, norm=1, D=96) == -2      # LSE is not needed under relu attention
+
+
+def _declarations():
+    """{name: (return type, [parameter types])} parsed from include/attnfuse.h."""
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+    text = re.sub(r"//[^\n]*", " ", text)
+    text = re.sub(r"^\s*#[^\n]*", " ", text, flags=re.M)
+    out = {}
+    for m in re.finditer(r"^\s*((?:const\s+)?\w+(?:\s*\*)?)\s*\b(attnfuse_\w+)\s*\(([^;{]*?)\)\s*;", text, flags=re.M):
+        ret, name, params = m.group(1).strip(), m.group(2), m.group(3).strip()
+        types = [] if params in ("", "void") else [re.sub(r"\s*\b\w+$", "", p.strip()) for p in params.split(",")]
+        out[name] = (ret, types)
+    return out
+
+
+def _ctype_of(c):
+    c = " ".join(c.replace("*", " * ").split())
+    if c.endswith("*"):
+        return ctypes.c_char_p if c in ("const char *",) else ctypes.c_void_p
+    return {"int": ctypes.c_int, "float": ctypes.c_float, "size_t": ctypes.c_size_t,
+            "long long": ctypes.c_longlong}[c]
+
+
+def test_binding_signatures_match_the_header():
+    """Every ctypes signature the binding declares has the header's parameter
+    count and types (pointers as c_void_p), and its return type."""
+    decl = _declarations()
+    assert set(decl) == set(_lib.SIGNATURES)
+    for name, (res, args) in _lib.SIGNATURES.items():
+        ret, params = decl[name]
+        assert len(args) == len(params), f"{name}: {len(args)} arguments bound, {len(params)} declared"
+        for i, (a, pt) in enumerate(zip(args, params)):
+            assert a == _ctype_of(pt), f"{name} argument {i}: {pt}"
+        assert res == _ctype_of(ret), f"{name}: return type {ret}"

@@ -78,3 +78,26 @@ def test_block_mask_offset_lengths_checked():
     short = blockmask.BlockMask(bm.S, bm.active, bm.q_ptr[:-1].contiguous(), bm.k_idx, bm.k_ptr, bm.q_idx)
     with pytest.raises(ValueError, match="nb \\+ 1"):
         api._mask_ptrs(short, q, 150)
+
+
+def test_missing_library_fails_loudly(tmp_path, monkeypatch):
+    """No fallback: without the built library every entry point raises."""
+    from paper_2609_13612_amd import _lib
+    monkeypatch.setattr(_lib, "LIB_PATH", str(tmp_path / "libattnfuse.so"))
+    monkeypatch.setattr(_lib, "_lib", None)
+    with pytest.raises(FileNotFoundError, match="no non-HIP fallback"):
+        _lib.load()
+    with pytest.raises(FileNotFoundError):
+        api.attnfuse_bwd_workspace_bytes(1, 1, 1, 64, 64)
+
+
+def test_package_never_uses_the_oracle():
+    """The oracle is test infrastructure: no module of the package imports it,
+    and none falls back to a torch attention routine."""
+    import pathlib
+    import re
+    pkg = pathlib.Path(api.__file__).parent
+    for f in sorted(pkg.rglob("*.py")):
+        text = f.read_text()
+        assert not re.search(r"^\s*(import|from)\s+oracle\b", text, flags=re.M), f"{f.name} imports the oracle"
+        assert "scaled_dot_product_attention" not in text, f"{f.name} calls a torch attention routine"

@@ -15,14 +15,20 @@
  * Heads.    Query head h reads K/V head h / (H / H_kv) (grouped-query
  *           attention with contiguous groups); H must be a multiple of H_kv.
  * Positions 0..S-1 for queries and keys alike (self-attention, S_q = S_k = S).
- * Ownership The caller owns every buffer; nothing is retained after a call.
- *           The library itself keeps one read-only device table per
- *           (device, D, rope_theta): cos/sin of position * omega_i, fp32,
- *           built with one hipMalloc and one stream synchronisation the first
- *           time a RoPE call needs more rows than the table holds (so make that
- *           first call outside HIP graph capture).
+ * Ownership The caller owns every buffer, including the RoPE cos/sin table
+ *           (attnfuse_rope_table_fill) and the backward and decode workspaces.
+ *           The library never allocates or frees device memory, keeps no state
+ *           between calls and never synchronises: every entry point is a pure
+ *           sequence of kernel launches, so any call may be captured in a HIP
+ *           graph, including the first one.
+ * RoPE      Every entry point that rotates takes rope_theta and a caller-owned
+ * table     table of cos/sin values (below): rope_table, device fp32, filled
+ *           by attnfuse_rope_table_fill with the same D and rope_theta, and
+ *           rope_table_rows, the number of positions it was filled for, which
+ *           must cover every position the call uses (S, or S_kv for decode).
+ *           With AF_ROPE_NONE both are ignored and may be NULL / 0.
  * Streams.  All work is enqueued on `stream` (a hipStream_t; NULL = default
- *           stream) and runs asynchronously; no call synchronises otherwise.
+ *           stream) and runs asynchronously.
  * Errors.   Arguments are validated before any HIP call; no C++ exception
  *           crosses the ABI.  Return codes:
  *             AF_OK               success (work enqueued)
@@ -64,6 +70,26 @@ enum { AF_NORM_SOFTMAX = 0, AF_NORM_RELU = 1 };
 enum { AF_OK = 0, AF_ERR_INVALID_ARG = -1, AF_ERR_UNSUPPORTED = -2, AF_ERR_HIP = -3 };
 
 /*
+ * RoPE cos/sin table (Section 4.1 "Fused RoPE": the rotation angle of pair i
+ * at position n is n * omega_i with omega_i = rope_theta^(-2i/D), the RoFormer
+ * frequencies).  The table holds rows x D/2 pairs of fp32 (cos, sin):
+ *     T[n][i] = (cos(n * omega_i), sin(n * omega_i)),  n < rows, i < D/2,
+ * each computed in fp64 and rounded once to fp32.  The caller allocates
+ * attnfuse_rope_table_bytes(rows, D) bytes of device memory (16-byte
+ * aligned), fills it once with attnfuse_rope_table_fill (one kernel launch on
+ * `stream`; the table is valid for work ordered after it on the device), and
+ * passes it, read only, to every RoPE call with the same D and rope_theta for
+ * as long as it likes.  A table of R rows serves every call with S <= R.
+ *
+ * attnfuse_rope_table_bytes returns 0 for rows < 1, rows > 2^20 or an odd or
+ * non-positive D.  attnfuse_rope_table_fill returns AF_ERR_INVALID_ARG for a
+ * NULL or unaligned table, those sizes, or rope_theta not finite and > 0;
+ * AF_ERR_UNSUPPORTED for D not in {64, 128}; AF_ERR_HIP if the launch fails.
+ */
+size_t attnfuse_rope_table_bytes(int rows, int D);
+int attnfuse_rope_table_fill(float* table, int rows, int D, float rope_theta, void* stream);
+
+/*
  * Fused forward (Section 2 online softmax; Section 4.1 fused RoPE; Section 3.1
  * score modifications; Section 4.4 saved row statistic).  Computes
  *     s_ij  = softmax_scale * <R_i q_i, R_j k_j> - slope_h * (i - j)
@@ -79,33 +105,58 @@ enum { AF_OK = 0, AF_ERR_INVALID_ARG = -1, AF_ERR_UNSUPPORTED = -2, AF_ERR_HIP =
  *   B, H, H_kv, S >= 1; H % H_kv == 0; D in {64, 128} (others: UNSUPPORTED)
  *   dtype       AF_DTYPE_*
  *   rope        AF_ROPE_*; rope_theta > 0 and finite when rope != NONE
+ *   rope_table, rope_table_rows   the caller's cos/sin table for D and
+ *               rope_theta with rope_table_rows >= S (used when rope != NONE)
  *   mask        AF_MASK_*; window >= 1 when SLIDING_WINDOW (ignored otherwise)
  *   alibi_slopes  device fp32 [H] or NULL
  *   softmax_scale finite, > 0 (typically 1/sqrt(D))
+ *
+ * Precision and range (bf16): without RoPE the bf16 inputs feed Q K^T
+ * exactly; with RoPE the rotated Q' and K' are rounded to fp16 (11-bit
+ * significand) for the score product, so |R q| and |R k| must stay below the
+ * fp16 maximum 65504.  P and V meet in a bf16 product; accumulation is fp32.
  */
 int attnfuse_fwd(const void* Q, const void* K, const void* V, void* O, float* LSE,
                  int B, int H, int H_kv, int S, int D, int dtype,
-                 int rope, float rope_theta, int mask, int window,
+                 int rope, float rope_theta, const float* rope_table, int rope_table_rows,
+                 int mask, int window,
                  const float* alibi_slopes, float softmax_scale, void* stream);
 
-/* Bytes of device workspace attnfuse_bwd needs for these sizes and RoPE kind:
- *   8*B*H*S                  per query row: delta_i = rowsum(dO_i * O_i) and
- *                            LSE_i in log2 units (fp32 each)
- * + 2*B*H*S*D                dO converted once to fp16
+/* Bytes of device workspace attnfuse_bwd needs for these sizes and RoPE kind
+ * (each part rounded up to a multiple of 256 bytes):
+ *   8*B*H*S                  per query row: the softmax backward's row term
+ *                            delta_i and LSE_i in log2 units (fp32 each)
+ * + 2*B*H*S*D                sigma * dO converted once to fp16
+ * + 4*B*H_kv                 sigma per (batch, K/V head): the power of two
+ *                            that brings the group's largest |dO| into [1, 2)
+ * + 4*B*H_kv*ceil(H/H_kv*S*D / 16384)   partial maxima of |dO|
  * + 2*(B*H + B*H_kv)*S*D     with RoPE only: Q' = R Q and K' = R K, rotated
  *                            once and rounded to fp16
  * Returns 0 for invalid sizes. */
 size_t attnfuse_bwd_workspace_bytes(int B, int H, int H_kv, int S, int D, int rope);
 
 /*
- * Backward of attnfuse_fwd (Section 4.4: three kernels, no atomics -- a
- * preprocessing pass, a dK/dV pass over query tiles and a dQ pass over key
- * tiles; probabilities are re-derived from the saved LSE).  The preprocessing
- * pass computes the row statistics and, with RoPE, rotates Q and K once into
- * the workspace (both later passes read every tile many times, so rotating
- * once is cheaper than re-rotating per visit); the gradients leave through the
- * inverse rotation: dQ = R^T dQ', dK = R^T dK'.  For grouped-query attention
- * dK and dV sum over the H/H_kv query heads of their group.
+ * Backward of attnfuse_fwd (Section 4.4: no atomics -- a preprocessing pass,
+ * a dQ pass over key tiles and a dK/dV pass over query tiles; probabilities
+ * are re-derived from the saved LSE).  The preprocessing pass computes the
+ * row statistics and, with RoPE, rotates Q and K once into the workspace (both
+ * later passes read every tile many times, so rotating once is cheaper than
+ * re-rotating per visit); the gradients leave through the inverse rotation:
+ * dQ = R^T dQ', dK = R^T dK'.  For grouped-query attention dK and dV sum over
+ * the H/H_kv query heads of their group.
+ *
+ * The softmax backward's row term delta_i = sum_j P_ij dP_ij: the dQ pass
+ * uses rowsum(dO_i * O_i) of the O it is given (equal for the exact O) and
+ * forms sum_j P_ij dP_ij itself, in fp32, for the dK/dV pass.
+ *
+ * Precision and range (bf16): the score, dV, dK and dQ products run on fp16
+ * MFMA operands with fp32 accumulation.  dO enters them multiplied by sigma,
+ * a power of two per (batch, K/V head) that brings the group's largest |dO|
+ * into [1, 2), and the gradients leave divided by it, so the result is the
+ * same at any scale of dO (exact power-of-two scaling).  The rotated |Q'| and
+ * |K'| (as in attnfuse_fwd) and |V| must stay below the fp16 maximum 65504,
+ * and max|V| below 16376 / D (128 at D = 128), which bounds the scaled
+ * |dS| <= 4 D max|V| by the same maximum.
  *
  *   Q, K, V, O, dO, LSE  as produced/consumed by attnfuse_fwd with the same
  *                        variant arguments (LSE must be the forward's)
@@ -122,7 +173,8 @@ int attnfuse_bwd(const void* Q, const void* K, const void* V, const void* O, con
                  const float* LSE, void* dQ, void* dK, void* dV,
                  void* workspace, size_t workspace_bytes,
                  int B, int H, int H_kv, int S, int D, int dtype,
-                 int rope, float rope_theta, int mask, int window,
+                 int rope, float rope_theta, const float* rope_table, int rope_table_rows,
+                 int mask, int window,
                  const float* alibi_slopes, float softmax_scale, void* stream);
 
 /*
@@ -153,7 +205,8 @@ int attnfuse_bwd(const void* Q, const void* K, const void* V, const void* O, con
 int attnfuse_fwd_blocksparse(const void* Q, const void* K, const void* V, void* O, float* LSE,
                              const int* q_block_ptr, const int* k_block_idx,
                              int B, int H, int H_kv, int S, int D, int dtype,
-                             int rope, float rope_theta, int mask, int window,
+                             int rope, float rope_theta, const float* rope_table, int rope_table_rows,
+                             int mask, int window,
                              const float* alibi_slopes, float softmax_scale, void* stream);
 
 /*
@@ -172,7 +225,8 @@ int attnfuse_bwd_blocksparse(const void* Q, const void* K, const void* V, const 
                              const int* k_block_ptr, const int* q_block_idx,
                              void* workspace, size_t workspace_bytes,
                              int B, int H, int H_kv, int S, int D, int dtype,
-                             int rope, float rope_theta, int mask, int window,
+                             int rope, float rope_theta, const float* rope_table, int rope_table_rows,
+                             int mask, int window,
                              const float* alibi_slopes, float softmax_scale, void* stream);
 
 /*
@@ -203,7 +257,8 @@ int attnfuse_fwd_bias_norm(const void* Q, const void* K, const void* V, void* O,
                            const float* bias, long long bias_stride_b, long long bias_stride_h,
                            long long bias_stride_q, int norm,
                            int B, int H, int H_kv, int S, int D, int dtype,
-                           int rope, float rope_theta, int mask, int window,
+                           int rope, float rope_theta, const float* rope_table, int rope_table_rows,
+                           int mask, int window,
                            const float* alibi_slopes, float softmax_scale, void* stream);
 
 /*
@@ -218,7 +273,8 @@ int attnfuse_bwd_bias_norm(const void* Q, const void* K, const void* V, const vo
                            long long bias_stride_q, int norm,
                            void* workspace, size_t workspace_bytes,
                            int B, int H, int H_kv, int S, int D, int dtype,
-                           int rope, float rope_theta, int mask, int window,
+                           int rope, float rope_theta, const float* rope_table, int rope_table_rows,
+                           int mask, int window,
                            const float* alibi_slopes, float softmax_scale, void* stream);
 
 /*
@@ -230,16 +286,20 @@ int attnfuse_bwd_bias_norm(const void* Q, const void* K, const void* V, const vo
  *   Q [B,H,S,D] -> Qr;  K [B,H_kv,S,D] -> Kr  (dtype).  In-place is allowed
  *   (Qr == Q, Kr == K).  K and Kr may both be NULL to rotate Q alone (H_kv is
  *   then ignored).  rope must be NEOX or INTERLEAVED.  D in {64, 128}.
+ *   rope_table / rope_table_rows as attnfuse_fwd (rows >= S); the table must
+ *   not be an output.
  */
 int attnfuse_rope(const void* Q, const void* K, void* Qr, void* Kr,
                   int B, int H, int H_kv, int S, int D, int dtype,
-                  int rope, float rope_theta, void* stream);
+                  int rope, float rope_theta, const float* rope_table, int rope_table_rows,
+                  void* stream);
 
 /* Inverse rotation (the separate path's backward): dQ = R^T dQr, dK = R^T dKr.
  * Same arguments and rules as attnfuse_rope. */
 int attnfuse_rope_bwd(const void* dQr, const void* dKr, void* dQ, void* dK,
                       int B, int H, int H_kv, int S, int D, int dtype,
-                      int rope, float rope_theta, void* stream);
+                      int rope, float rope_theta, const float* rope_table, int rope_table_rows,
+                      void* stream);
 
 /* Bytes of device workspace attnfuse_decode needs: four partial (max, sum,
  * accumulator) triples per (sequence, query head, cache chunk), one per
@@ -274,14 +334,16 @@ size_t attnfuse_decode_workspace_bytes(int B, int H, int H_kv, int S_kv, int D);
  *   mask                         NONE or CAUSAL: every cached key is visible
  *                                (all precede the query); SLIDING_WINDOW: the
  *                                last `window` keys
- *   rope, rope_theta, alibi_slopes, softmax_scale   as attnfuse_fwd
+ *   rope, rope_theta, rope_table, alibi_slopes, softmax_scale   as
+ *                                attnfuse_fwd (rope_table_rows >= S_kv)
  *   dtype                        AF_DTYPE_BF16 only; D in {64, 128};
  *                                H / H_kv <= 32 (else AF_ERR_UNSUPPORTED)
  */
 int attnfuse_decode(const void* Q, const void* K, const void* V, const int* cache_lens,
                     void* O, float* LSE, void* workspace, size_t workspace_bytes,
                     int B, int H, int H_kv, int S_kv, int D, int dtype,
-                    int rope, float rope_theta, int mask, int window,
+                    int rope, float rope_theta, const float* rope_table, int rope_table_rows,
+                    int mask, int window,
                     const float* alibi_slopes, float softmax_scale, void* stream);
 
 /* Static text for a return code (never NULL). */

@@ -14,23 +14,25 @@ _I = ctypes.c_int
 _F = ctypes.c_float
 _L = ctypes.c_longlong
 SIGNATURES = {
-    "attnfuse_fwd": (_I, [_P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _F, _I, _I, _P, _F, _P]),
+    "attnfuse_rope_table_bytes": (ctypes.c_size_t, [_I, _I]),
+    "attnfuse_rope_table_fill": (_I, [_P, _I, _I, _F, _P]),
+    "attnfuse_fwd": (_I, [_P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _F, _P, _I, _I, _I, _P, _F, _P]),
     "attnfuse_bwd_workspace_bytes": (ctypes.c_size_t, [_I, _I, _I, _I, _I, _I]),
     "attnfuse_bwd": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t,
-                          _I, _I, _I, _I, _I, _I, _I, _F, _I, _I, _P, _F, _P]),
-    "attnfuse_fwd_blocksparse": (_I, [_P, _P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _F, _I, _I, _P, _F,
-                                      _P]),
+                          _I, _I, _I, _I, _I, _I, _I, _F, _P, _I, _I, _I, _P, _F, _P]),
+    "attnfuse_fwd_blocksparse": (_I, [_P, _P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _F, _P, _I, _I, _I,
+                                      _P, _F, _P]),
     "attnfuse_bwd_blocksparse": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t,
-                                      _I, _I, _I, _I, _I, _I, _I, _F, _I, _I, _P, _F, _P]),
-    "attnfuse_fwd_bias_norm": (_I, [_P, _P, _P, _P, _P, _P, _L, _L, _L, _I, _I, _I, _I, _I, _I, _I, _I, _F, _I, _I,
-                                    _P, _F, _P]),
+                                      _I, _I, _I, _I, _I, _I, _I, _F, _P, _I, _I, _I, _P, _F, _P]),
+    "attnfuse_fwd_bias_norm": (_I, [_P, _P, _P, _P, _P, _P, _L, _L, _L, _I, _I, _I, _I, _I, _I, _I, _I, _F, _P, _I,
+                                    _I, _I, _P, _F, _P]),
     "attnfuse_bwd_bias_norm": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _L, _L, _L, _I, _P, ctypes.c_size_t,
-                                    _I, _I, _I, _I, _I, _I, _I, _F, _I, _I, _P, _F, _P]),
-    "attnfuse_rope": (_I, [_P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _F, _P]),
-    "attnfuse_rope_bwd": (_I, [_P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _F, _P]),
+                                    _I, _I, _I, _I, _I, _I, _I, _F, _P, _I, _I, _I, _P, _F, _P]),
+    "attnfuse_rope": (_I, [_P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _F, _P, _I, _P]),
+    "attnfuse_rope_bwd": (_I, [_P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _F, _P, _I, _P]),
     "attnfuse_decode_workspace_bytes": (ctypes.c_size_t, [_I, _I, _I, _I, _I]),
     "attnfuse_decode": (_I, [_P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t,
-                             _I, _I, _I, _I, _I, _I, _I, _F, _I, _I, _P, _F, _P]),
+                             _I, _I, _I, _I, _I, _I, _I, _F, _P, _I, _I, _I, _P, _F, _P]),
     "attnfuse_strerror": (ctypes.c_char_p, [_I]),
     "attnfuse_version": (_I, []),
 }

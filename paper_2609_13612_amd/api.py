@@ -7,6 +7,7 @@ return code.  Every step of the computation runs in the HIP kernels.
 """
 import math
 
+import numpy as np
 import torch
 
 from . import _lib
@@ -105,6 +106,67 @@ def _workspace(ws, nbytes, device):
     return ws, ws.numel() * ws.element_size()
 
 
+# RoPE cos/sin tables this binding built, per (device index, D, theta): a list
+# of tables (each a [rows, D/2, 2] fp32 tensor), never freed, since a kernel
+# on any stream may still read one.  The library itself keeps nothing.
+_TABLES = {}
+_TABLE_MIN_ROWS = 4096
+
+
+def rope_table(D, theta, rows, device=None, out=None):
+    """A RoPE cos/sin table for positions 0..rows-1: T[n][i] = (cos, sin) of
+    n * theta^(-2i/D), filled by attnfuse_rope_table_fill on the current stream
+    (see include/attnfuse.h).  Pass it as ``rope_table=`` to any call with the
+    same D and theta and S <= rows."""
+    device = torch.device("cuda", torch.cuda.current_device()) if device is None else torch.device(device)
+    shape = (rows, D // 2, 2)
+    if out is None:
+        out = torch.empty(shape, device=device, dtype=torch.float32)
+    else:
+        _need(out, "out", shape, torch.float32, device)
+    with torch.cuda.device(device):
+        code = _lib.load().attnfuse_rope_table_fill(out.data_ptr(), rows, D, float(theta), _stream())
+    _check(code, "attnfuse_rope_table_fill")
+    return out
+
+
+def _table(rope, theta, D, S, device, given):
+    """The cos/sin table a call reads, as a tensor: the caller's (checked), or
+    one this binding keeps for (device, D, theta).  Under HIP graph capture a
+    table not yet built is filled inside the capture (stream-ordered before the
+    call that reads it) and not kept; the caller holds the returned tensor
+    until its launch is enqueued.  None without RoPE."""
+    if ROPE[rope] == ROPE["none"]:
+        return None
+    if given is not None:
+        if (not isinstance(given, torch.Tensor) or given.device != device or given.dtype != torch.float32
+                or given.dim() != 3 or tuple(given.shape[1:]) != (D // 2, 2) or not given.is_contiguous()):
+            raise ValueError(f"rope_table must be a contiguous fp32 [rows, {D // 2}, 2] tensor on {device}")
+        if given.shape[0] < S:
+            raise ValueError(f"rope_table has {given.shape[0]} rows, the call needs {S}")
+        return given
+    key = (device.index, D, float(np.float32(theta)))
+    for t in _TABLES.get(key, ()):
+        if t.shape[0] >= S:
+            return t
+    rows = _TABLE_MIN_ROWS
+    while rows < S:
+        rows *= 2
+    with torch.cuda.device(device):
+        if torch.cuda.is_current_stream_capturing():
+            return rope_table(D, theta, S, device)
+        t = rope_table(D, theta, rows, device)
+        # ready for any stream before it is shared: one wait, once per table
+        torch.cuda.current_stream().synchronize()
+    _TABLES.setdefault(key, []).append(t)
+    return t
+
+
+def _tab(t):
+    """(pointer, rows) of a table from _table."""
+    return (None, 0) if t is None else (t.data_ptr(), t.shape[0])
+
+
 def _variant(rope, theta, mask, window, alibi_slopes, scale, D, H=None, device=None):
     if scale is None:
         scale = 1.0 / math.sqrt(D)
@@ -114,7 +176,7 @@ def _variant(rope, theta, mask, window, alibi_slopes, scale, D, H=None, device=N
 
 
 def attnfuse_fwd(q, k, v, *, rope="none", theta=10000.0, mask="causal", window=None,
-                 alibi_slopes=None, scale=None, out=None, lse=None):
+                 alibi_slopes=None, scale=None, out=None, lse=None, rope_table=None):
     """O, LSE = attention(q, k, v); see attnfuse_fwd in include/attnfuse.h."""
     dev = _device(q)
     B, H, Hkv, S, D = _shape(q, k)
@@ -122,9 +184,11 @@ def attnfuse_fwd(q, k, v, *, rope="none", theta=10000.0, mask="causal", window=N
     out = _opt(out, "out", q.shape, q.dtype, dev)
     lse = _opt(lse, "lse", (B, H, S), torch.float32, dev)
     r, th, m, w, sc = _variant(rope, theta, mask, window, alibi_slopes, scale, D, H, dev)
+    tab = _table(rope, theta, D, S, dev, rope_table)
+    tp, tr = _tab(tab)
     with torch.cuda.device(dev):
         code = _lib.load().attnfuse_fwd(_ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(lse), B, H, Hkv, S, D,
-                                        DTYPE[q.dtype], r, th, m, w, _ptr(alibi_slopes), sc, _stream())
+                                        DTYPE[q.dtype], r, th, tp, tr, m, w, _ptr(alibi_slopes), sc, _stream())
     _check(code, "attnfuse_fwd")
     return out, lse
 
@@ -134,7 +198,7 @@ def attnfuse_bwd_workspace_bytes(B, H, H_kv, S, D, rope="none"):
 
 
 def attnfuse_bwd(q, k, v, o, do, lse, *, rope="none", theta=10000.0, mask="causal", window=None,
-                 alibi_slopes=None, scale=None, dq=None, dk=None, dv=None, workspace=None):
+                 alibi_slopes=None, scale=None, dq=None, dk=None, dv=None, workspace=None, rope_table=None):
     """dQ, dK, dV of attnfuse_fwd; see attnfuse_bwd in include/attnfuse.h."""
     dev = _device(q)
     B, H, Hkv, S, D = _shape(q, k)
@@ -142,10 +206,12 @@ def attnfuse_bwd(q, k, v, o, do, lse, *, rope="none", theta=10000.0, mask="causa
     dq, dk, dv = _grads(q, k, dq, dk, dv, dev)
     workspace, wbytes = _workspace(workspace, attnfuse_bwd_workspace_bytes(B, H, Hkv, S, D, rope), dev)
     r, th, m, w, sc = _variant(rope, theta, mask, window, alibi_slopes, scale, D, H, dev)
+    tab = _table(rope, theta, D, S, dev, rope_table)
+    tp, tr = _tab(tab)
     with torch.cuda.device(dev):
         code = _lib.load().attnfuse_bwd(_ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(do), _ptr(lse),
                                         _ptr(dq), _ptr(dk), _ptr(dv), _ptr(workspace), wbytes,
-                                        B, H, Hkv, S, D, DTYPE[q.dtype], r, th, m, w,
+                                        B, H, Hkv, S, D, DTYPE[q.dtype], r, th, tp, tr, m, w,
                                         _ptr(alibi_slopes), sc, _stream())
     _check(code, "attnfuse_bwd")
     return dq, dk, dv
@@ -168,7 +234,7 @@ def _mask_ptrs(block_mask, q, S):
 
 
 def attnfuse_fwd_blocksparse(q, k, v, block_mask, *, rope="none", theta=10000.0, mask="none", window=None,
-                             alibi_slopes=None, scale=None, out=None, lse=None):
+                             alibi_slopes=None, scale=None, out=None, lse=None, rope_table=None):
     """O, LSE of attention restricted to the active blocks of ``block_mask``
     (a blockmask.BlockMask); see attnfuse_fwd_blocksparse."""
     dev = _device(q)
@@ -178,9 +244,11 @@ def attnfuse_fwd_blocksparse(q, k, v, block_mask, *, rope="none", theta=10000.0,
     out = _opt(out, "out", q.shape, q.dtype, dev)
     lse = _opt(lse, "lse", (B, H, S), torch.float32, dev)
     r, th, m, w, sc = _variant(rope, theta, mask, window, alibi_slopes, scale, D, H, dev)
+    tab = _table(rope, theta, D, S, dev, rope_table)
+    tp, tr = _tab(tab)
     with torch.cuda.device(dev):
         code = _lib.load().attnfuse_fwd_blocksparse(_ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(lse), qp, ki,
-                                                    B, H, Hkv, S, D, DTYPE[q.dtype], r, th, m, w,
+                                                    B, H, Hkv, S, D, DTYPE[q.dtype], r, th, tp, tr, m, w,
                                                     _ptr(alibi_slopes), sc, _stream())
     _check(code, "attnfuse_fwd_blocksparse")
     return out, lse
@@ -188,7 +256,7 @@ def attnfuse_fwd_blocksparse(q, k, v, block_mask, *, rope="none", theta=10000.0,
 
 def attnfuse_bwd_blocksparse(q, k, v, o, do, lse, block_mask, *, rope="none", theta=10000.0, mask="none",
                              window=None, alibi_slopes=None, scale=None, dq=None, dk=None, dv=None,
-                             workspace=None):
+                             workspace=None, rope_table=None):
     """dQ, dK, dV of attnfuse_fwd_blocksparse; see attnfuse_bwd_blocksparse."""
     dev = _device(q)
     B, H, Hkv, S, D = _shape(q, k)
@@ -197,10 +265,12 @@ def attnfuse_bwd_blocksparse(q, k, v, o, do, lse, block_mask, *, rope="none", th
     dq, dk, dv = _grads(q, k, dq, dk, dv, dev)
     workspace, wbytes = _workspace(workspace, attnfuse_bwd_workspace_bytes(B, H, Hkv, S, D, rope), dev)
     r, th, m, w, sc = _variant(rope, theta, mask, window, alibi_slopes, scale, D, H, dev)
+    tab = _table(rope, theta, D, S, dev, rope_table)
+    tp, tr = _tab(tab)
     with torch.cuda.device(dev):
         code = _lib.load().attnfuse_bwd_blocksparse(_ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(do), _ptr(lse),
                                                     _ptr(dq), _ptr(dk), _ptr(dv), qp, ki, kp, qi, _ptr(workspace),
-                                                    wbytes, B, H, Hkv, S, D, DTYPE[q.dtype], r, th, m, w,
+                                                    wbytes, B, H, Hkv, S, D, DTYPE[q.dtype], r, th, tp, tr, m, w,
                                                     _ptr(alibi_slopes), sc, _stream())
     _check(code, "attnfuse_bwd_blocksparse")
     return dq, dk, dv
@@ -225,7 +295,7 @@ def _bias_args(bias, q, B, H, S):
 
 
 def attnfuse_fwd_bias_norm(q, k, v, *, bias=None, norm="softmax", rope="none", theta=10000.0, mask="causal",
-                           window=None, scale=None, out=None, lse=None):
+                           window=None, scale=None, out=None, lse=None, rope_table=None):
     """O (and LSE, None under relu attention) with a dense additive bias and/or
     relu attention; see attnfuse_fwd_bias_norm in include/attnfuse.h."""
     dev = _device(q)
@@ -236,16 +306,19 @@ def attnfuse_fwd_bias_norm(q, k, v, *, bias=None, norm="softmax", rope="none", t
         lse = _opt(lse, "lse", (B, H, S), torch.float32, dev)
     bp, sb, sh, sq = _bias_args(bias, q, B, H, S)
     r, th, m, w, sc = _variant(rope, theta, mask, window, None, scale, D)
+    tab = _table(rope, theta, D, S, dev, rope_table)
+    tp, tr = _tab(tab)
     with torch.cuda.device(dev):
         code = _lib.load().attnfuse_fwd_bias_norm(_ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(lse), bp, sb, sh,
-                                                  sq, NORM[norm], B, H, Hkv, S, D, DTYPE[q.dtype], r, th, m, w,
+                                                  sq, NORM[norm], B, H, Hkv, S, D, DTYPE[q.dtype], r, th, tp, tr, m, w,
                                                   None, sc, _stream())
     _check(code, "attnfuse_fwd_bias_norm")
     return out, lse
 
 
 def attnfuse_bwd_bias_norm(q, k, v, o, do, lse, *, bias=None, norm="softmax", rope="none", theta=10000.0,
-                           mask="causal", window=None, scale=None, dq=None, dk=None, dv=None, workspace=None):
+                           mask="causal", window=None, scale=None, dq=None, dk=None, dv=None, workspace=None,
+                           rope_table=None):
     """dQ, dK, dV of attnfuse_fwd_bias_norm (lse may be None under relu
     attention); see attnfuse_bwd_bias_norm."""
     dev = _device(q)
@@ -255,11 +328,13 @@ def attnfuse_bwd_bias_norm(q, k, v, o, do, lse, *, bias=None, norm="softmax", ro
     workspace, wbytes = _workspace(workspace, attnfuse_bwd_workspace_bytes(B, H, Hkv, S, D, rope), dev)
     bp, sb, sh, sq = _bias_args(bias, q, B, H, S)
     r, th, m, w, sc = _variant(rope, theta, mask, window, None, scale, D)
+    tab = _table(rope, theta, D, S, dev, rope_table)
+    tp, tr = _tab(tab)
     with torch.cuda.device(dev):
         code = _lib.load().attnfuse_bwd_bias_norm(_ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(do), _ptr(lse),
                                                   _ptr(dq), _ptr(dk), _ptr(dv), bp, sb, sh, sq, NORM[norm],
                                                   _ptr(workspace), wbytes, B, H, Hkv, S, D, DTYPE[q.dtype],
-                                                  r, th, m, w, None, sc, _stream())
+                                                  r, th, tp, tr, m, w, None, sc, _stream())
     _check(code, "attnfuse_bwd_bias_norm")
     return dq, dk, dv
 
@@ -268,10 +343,7 @@ def attnfuse_decode_workspace_bytes(B, H, H_kv, S_kv, D):
     return _lib.load().attnfuse_decode_workspace_bytes(B, H, H_kv, S_kv, D)
 
 
-def attnfuse_decode(q, k_cache, v_cache, cache_lens=None, *, rope="none", theta=10000.0, mask="causal",
-                    window=None, alibi_slopes=None, scale=None, out=None, lse=None, workspace=None):
-    """O [B,H,D], LSE [B,H] of one query per sequence against a KV cache of
-    already-rotated keys; see attnfuse_decode in include/attnfuse.h."""
+def _decode_args(q, k_cache, v_cache, cache_lens, out, lse):
     dev = _device(q)
     if q.dim() != 3 or k_cache.dim() != 4 or v_cache.shape != k_cache.shape:
         raise ValueError("q must be [B, H, D] and the caches [B, H_kv, S_kv, D]")
@@ -286,17 +358,28 @@ def attnfuse_decode(q, k_cache, v_cache, cache_lens=None, *, rope="none", theta=
         _need(cache_lens, "cache_lens", (B,), torch.int32, dev)
     out = _opt(out, "out", q.shape, q.dtype, dev)
     lse = _opt(lse, "lse", (B, H), torch.float32, dev)
+    return dev, (B, H, Hkv, S_kv, D), out, lse
+
+
+def attnfuse_decode(q, k_cache, v_cache, cache_lens=None, *, rope="none", theta=10000.0, mask="causal",
+                    window=None, alibi_slopes=None, scale=None, out=None, lse=None, workspace=None,
+                    rope_table=None):
+    """O [B,H,D], LSE [B,H] of one query per sequence against a KV cache of
+    already-rotated keys; see attnfuse_decode in include/attnfuse.h."""
+    dev, (B, H, Hkv, S_kv, D), out, lse = _decode_args(q, k_cache, v_cache, cache_lens, out, lse)
     workspace, wbytes = _workspace(workspace, attnfuse_decode_workspace_bytes(B, H, Hkv, S_kv, D), dev)
     r, th, m, w, sc = _variant(rope, theta, mask, window, alibi_slopes, scale, D, H, dev)
+    tab = _table(rope, theta, D, S_kv, dev, rope_table)
+    tp, tr = _tab(tab)
     with torch.cuda.device(dev):
         code = _lib.load().attnfuse_decode(_ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(cache_lens), _ptr(out),
                                            _ptr(lse), _ptr(workspace), wbytes, B, H, Hkv, S_kv, D,
-                                           DTYPE[q.dtype], r, th, m, w, _ptr(alibi_slopes), sc, _stream())
+                                           DTYPE[q.dtype], r, th, tp, tr, m, w, _ptr(alibi_slopes), sc, _stream())
     _check(code, "attnfuse_decode")
     return out, lse
 
 
-def _rope_call(name, x0, x1, y0, y1, rope, theta):
+def _rope_call(name, x0, x1, y0, y1, rope, theta, rope_table):
     dev = _device(x0)
     if x1 is not None:
         B, H, Hkv, S, D = _shape(x0, x1)
@@ -312,21 +395,27 @@ def _rope_call(name, x0, x1, y0, y1, rope, theta):
         y1 = _opt(y1, "out_k", x1.shape, x0.dtype, dev)
     elif y1 is not None:
         raise ValueError("out_k needs k")
+    tab = _table(rope, theta, D, S, dev, rope_table)
+    tp, tr = _tab(tab)
     with torch.cuda.device(dev):
         code = getattr(_lib.load(), name)(_ptr(x0), _ptr(x1), _ptr(y0), _ptr(y1), B, H, Hkv, S, D,
-                                          DTYPE[x0.dtype], ROPE[rope], float(theta), _stream())
+                                          DTYPE[x0.dtype], ROPE[rope], float(theta), tp, tr, _stream())
     _check(code, name)
     return y0, y1
 
 
-def attnfuse_rope(q, k=None, *, rope="neox", theta=10000.0, out_q=None, out_k=None):
+def attnfuse_rope(q, k=None, *, rope="neox", theta=10000.0, out_q=None, out_k=None, rope_table=None):
     """Qr, Kr = R q, R k (separate pre-rotation); see attnfuse_rope."""
-    return _rope_call("attnfuse_rope", q, k, out_q, out_k, rope, theta)
+    return _rope_call("attnfuse_rope", q, k, out_q, out_k, rope, theta, rope_table)
 
 
-def attnfuse_rope_bwd(dqr, dkr=None, *, rope="neox", theta=10000.0, out_q=None, out_k=None):
+def attnfuse_rope_bwd(dqr, dkr=None, *, rope="neox", theta=10000.0, out_q=None, out_k=None, rope_table=None):
     """dQ, dK = R^T dQr, R^T dKr; see attnfuse_rope_bwd."""
-    return _rope_call("attnfuse_rope_bwd", dqr, dkr, out_q, out_k, rope, theta)
+    return _rope_call("attnfuse_rope_bwd", dqr, dkr, out_q, out_k, rope, theta, rope_table)
+
+
+def attnfuse_rope_table_bytes(rows, D):
+    return _lib.load().attnfuse_rope_table_bytes(rows, D)
 
 
 def attnfuse_strerror(code):

@@ -1,7 +1,8 @@
-// C-ABI entry points (declared in include/attnfuse.h): argument validation,
-// the per-device cos/sin table cache, and dispatch to the kernel launchers.
-// Every argument is checked before the first HIP call; no exception leaves
-// this file.
+// C-ABI entry points (declared in include/attnfuse.h): argument validation
+// and dispatch to the kernel launchers.  Every argument is checked before the
+// first HIP call; no exception leaves this file.  Nothing here allocates,
+// synchronises or keeps state: the caller owns every buffer, the RoPE table
+// included.
 #include "attnfuse.h"
 
 #include <hip/hip_runtime.h>
@@ -9,15 +10,13 @@
 #include <cmath>
 #include <cstdint>
 #include <cstring>
-#include <mutex>
-#include <vector>
 
 #include "launch.hpp"
 
 namespace {
 
 constexpr int kMaxS = 1 << 20;
-constexpr int kAbiVersion = 2;
+constexpr int kAbiVersion = 3;
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 bool aligned4(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 3u) == 0; }
@@ -33,39 +32,19 @@ int map_launch(int rc) {
   return AF_ERR_HIP;
 }
 
-// ---------------------------------------------------------------- cos/sin table cache
-struct RopeTable {
-  int device;
-  int D;
-  uint32_t theta_bits;
-  int rows;
-  float2* ptr;
-};
-std::mutex g_table_mu;
-std::vector<RopeTable> g_tables;   // never freed: kernels on any stream may still read them
+// ---------------------------------------------------------------- caller-owned cos/sin table
+// The table is [rows][D/2] (cos, sin) fp32 pairs; a RoPE call reads rows 0..S-1.
+constexpr int kMaxTableRows = kMaxS;
 
-int rope_table(int D, float theta, int S, hipStream_t stream, const float2** out) {
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess) return AF_ERR_HIP;
-  uint32_t bits;
-  std::memcpy(&bits, &theta, sizeof bits);
-  std::lock_guard<std::mutex> lock(g_table_mu);
-  for (const RopeTable& t : g_tables) {
-    if (t.device == dev && t.D == D && t.theta_bits == bits && t.rows >= S) {
-      *out = t.ptr;
-      return AF_OK;
-    }
-  }
-  int rows = 4096;
-  while (rows < S) rows *= 2;
-  float2* ptr = nullptr;
-  if (hipMalloc(&ptr, (size_t)rows * (D / 2) * sizeof(float2)) != hipSuccess) return AF_ERR_HIP;
-  if (af::launch_rope_table(ptr, rows, D, (double)theta, stream) != 0 || hipStreamSynchronize(stream) != hipSuccess) {
-    (void)hipFree(ptr);
-    return AF_ERR_HIP;
-  }
-  g_tables.push_back({dev, D, bits, rows, ptr});
-  *out = ptr;
+size_t table_bytes(int rows, int D) { return (size_t)rows * (size_t)(D / 2) * 2 * sizeof(float); }
+
+// Checks the table arguments of a call that rotates positions 0..S-1 (nothing
+// without RoPE); a table given as an output would be a caller error too.
+int check_table(int rope, const float* table, int rows, int S, const void* const* outs, int nouts) {
+  if (rope == AF_ROPE_NONE) return AF_OK;
+  if (!table || !aligned16(table) || rows < S || rows > kMaxTableRows) return AF_ERR_INVALID_ARG;
+  for (int i = 0; i < nouts; ++i)
+    if (outs[i] == static_cast<const void*>(table)) return AF_ERR_INVALID_ARG;
   return AF_OK;
 }
 
@@ -90,10 +69,15 @@ int check_attn(int mask, int window, float scale) {
 
 bool supported_d(int D) { return D == 64 || D == 128; }
 
-// Backward workspace: [delta f32 | lse2 f32 | dO fp16 | Q' fp16 | K' fp16], each
-// section starting on a 256-byte boundary; the last two only with RoPE.
+// Backward workspace: [delta f32 | lse2 f32 | dO fp16 | dO scale f32 | partial
+// max |dO| u32 | Q' fp16 | K' fp16], each section starting on a 256-byte
+// boundary; the last two only with RoPE.  The partial maxima cover chunks of
+// kDmaxChunk elements of each (batch, K/V head)'s dO.
+constexpr long long kDmaxChunk = 16384;
+
 struct BwdWorkspace {
-  size_t delta, lse2, do16, qr16, kr16, total;
+  size_t delta, lse2, do16, dscale, dmax, qr16, kr16, total;
+  int dmax_chunks;
 };
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
@@ -105,6 +89,10 @@ BwdWorkspace bwd_workspace(int B, int H, int H_kv, int S, int D, int rope) {
   w.delta = off; off += align256(rows * sizeof(float));
   w.lse2 = off;  off += align256(rows * sizeof(float));
   w.do16 = off;  off += align256(rows * D * 2);
+  const size_t groups = (size_t)B * H_kv;
+  w.dmax_chunks = (int)(((long long)(H / H_kv) * S * D + kDmaxChunk - 1) / kDmaxChunk);
+  w.dscale = off; off += align256(groups * sizeof(float));
+  w.dmax = off;   off += align256(groups * w.dmax_chunks * sizeof(uint32_t));
   if (rope != AF_ROPE_NONE) {
     w.qr16 = off; off += align256(rows * D * 2);
     w.kr16 = off; off += align256(krows * D * 2);
@@ -162,7 +150,8 @@ int check_ext(const Ext& e, const void* const* outs, int nouts) {
 
 int fwd_impl(const void* Q, const void* K, const void* V, void* O, float* LSE, const int* q_block_ptr,
              const int* k_block_idx, const Ext& ext, int B, int H, int H_kv, int S, int D, int dtype, int rope,
-             float rope_theta, int mask, int window, const float* alibi_slopes, float softmax_scale, void* stream) {
+             float rope_theta, const float* rope_table, int rope_table_rows, int mask, int window,
+             const float* alibi_slopes, float softmax_scale, void* stream) {
   const bool relu = ext.norm == AF_NORM_RELU;   // no row statistic: LSE may be NULL
   if (!Q || !K || !V || !O || (!LSE && !relu)) return AF_ERR_INVALID_ARG;
   if (!aligned16(Q) || !aligned16(K) || !aligned16(V) || !aligned16(O) || !aligned16(LSE)) return AF_ERR_INVALID_ARG;
@@ -174,6 +163,7 @@ int fwd_impl(const void* Q, const void* K, const void* V, void* O, float* LSE, c
   int rc = check_common(B, H, H_kv, S, D, dtype, rope, rope_theta);
   if (rc != AF_OK) return rc;
   if ((rc = check_attn(mask, window, softmax_scale)) != AF_OK) return rc;
+  if ((rc = check_table(rope, rope_table, rope_table_rows, S, outs, 2)) != AF_OK) return rc;
   if (!supported_d(D)) return AF_ERR_UNSUPPORTED;
   if (q_block_ptr && dtype == AF_DTYPE_FP32) return AF_ERR_UNSUPPORTED;   // block-sparse: bf16 kernels only
   // the bias tensor and relu attention: bf16, without ALiBi or a block mask
@@ -188,12 +178,11 @@ int fwd_impl(const void* Q, const void* K, const void* V, void* O, float* LSE, c
   p.window = (mask == AF_MASK_SLIDING_WINDOW) ? (window < S ? window : S) : 0;
   p.slopes = alibi_slopes;
   p.scale = softmax_scale;
-  p.table = nullptr;
+  p.table = (rope != AF_ROPE_NONE) ? reinterpret_cast<const float2*>(rope_table) : nullptr;
   p.bq_ptr = q_block_ptr;
   p.bk_idx = k_block_idx;
   p.bias = ext.bias;
   p.bias_sb = ext.sb; p.bias_sh = ext.sh; p.bias_sq = ext.sq;
-  if (rope != AF_ROPE_NONE && (rc = rope_table(D, rope_theta, S, st, &p.table)) != AF_OK) return rc;
   const bool alibi = alibi_slopes != nullptr;
   if (dtype == AF_DTYPE_BF16) return map_launch(af::launch_fwd_bf16(D, rope, mask, alibi, ext.kind(), p, st));
   return map_launch(af::launch_fwd_fp32(D, rope, mask, alibi, p, st));
@@ -202,8 +191,9 @@ int fwd_impl(const void* Q, const void* K, const void* V, void* O, float* LSE, c
 // sparse: NULL (dense) or {q_block_ptr, k_block_idx, k_block_ptr, q_block_idx}
 int bwd_impl(const void* Q, const void* K, const void* V, const void* O, const void* dO, const float* LSE, void* dQ,
              void* dK, void* dV, const int* const* sparse, const Ext& ext, void* workspace, size_t workspace_bytes,
-             int B, int H, int H_kv, int S, int D, int dtype, int rope, float rope_theta, int mask, int window,
-             const float* alibi_slopes, float softmax_scale, void* stream) {
+             int B, int H, int H_kv, int S, int D, int dtype, int rope, float rope_theta, const float* rope_table,
+             int rope_table_rows, int mask, int window, const float* alibi_slopes, float softmax_scale,
+             void* stream) {
   const bool relu = ext.norm == AF_NORM_RELU;   // the LSE is not used: it may be NULL
   if (relu) LSE = nullptr;
   const void* ins[] = {Q, K, V, O, dO, LSE};
@@ -218,6 +208,7 @@ int bwd_impl(const void* Q, const void* K, const void* V, const void* O, const v
   int rc = check_common(B, H, H_kv, S, D, dtype, rope, rope_theta);
   if (rc != AF_OK) return rc;
   if ((rc = check_attn(mask, window, softmax_scale)) != AF_OK) return rc;
+  if ((rc = check_table(rope, rope_table, rope_table_rows, S, outs, 4)) != AF_OK) return rc;
   if (workspace_bytes < attnfuse_bwd_workspace_bytes(B, H, H_kv, S, D, rope)) return AF_ERR_INVALID_ARG;
   if (!supported_d(D)) return AF_ERR_UNSUPPORTED;
   if (sparse && dtype == AF_DTYPE_FP32) return AF_ERR_UNSUPPORTED;        // block-sparse: bf16 kernels only
@@ -232,6 +223,9 @@ int bwd_impl(const void* Q, const void* K, const void* V, const void* O, const v
   p.delta = reinterpret_cast<float*>(wb + ws.delta);
   p.lse2 = reinterpret_cast<float*>(wb + ws.lse2);
   p.do16 = wb + ws.do16;
+  p.dscale = reinterpret_cast<float*>(wb + ws.dscale);
+  p.dmax = reinterpret_cast<uint32_t*>(wb + ws.dmax);
+  p.dmax_chunks = ws.dmax_chunks;
   p.qr16 = (rope != AF_ROPE_NONE) ? wb + ws.qr16 : nullptr;
   p.kr16 = (rope != AF_ROPE_NONE) ? wb + ws.kr16 : nullptr;
   p.B = B; p.H = H; p.Hkv = H_kv; p.S = S;
@@ -239,14 +233,13 @@ int bwd_impl(const void* Q, const void* K, const void* V, const void* O, const v
   p.window = (mask == AF_MASK_SLIDING_WINDOW) ? (window < S ? window : S) : 0;
   p.slopes = alibi_slopes;
   p.scale = softmax_scale;
-  p.table = nullptr;
+  p.table = (rope != AF_ROPE_NONE) ? reinterpret_cast<const float2*>(rope_table) : nullptr;
   if (sparse) {
     p.bq_ptr = sparse[0]; p.bk_idx = sparse[1];
     p.bk_ptr = sparse[2]; p.bq_idx = sparse[3];
   }
   p.bias = ext.bias;
   p.bias_sb = ext.sb; p.bias_sh = ext.sh; p.bias_sq = ext.sq;
-  if (rope != AF_ROPE_NONE && (rc = rope_table(D, rope_theta, S, st, &p.table)) != AF_OK) return rc;
   const bool alibi = alibi_slopes != nullptr;
   if (dtype == AF_DTYPE_FP32) return map_launch(af::launch_bwd_fp32(D, rope, mask, alibi, p, st));
   return map_launch(af::launch_bwd_bf16(D, rope, mask, alibi, ext.kind(), p, st));
@@ -257,6 +250,19 @@ int bwd_impl(const void* Q, const void* K, const void* V, const void* O, const v
 extern "C" {
 
 int attnfuse_version(void) { return kAbiVersion; }
+                     
+size_t attnfuse_rope_table_bytes(int rows, int D) {
+  if (rows < 1 || rows > kMaxTableRows || D < 2 || (D & 1)) return 0;
+  return table_bytes(rows, D);
+}
+
+int attnfuse_rope_table_fill(float* table, int rows, int D, float rope_theta, void* stream) {
+  if (!table || !aligned16(table) || rows < 1 || rows > kMaxTableRows || D < 2 || (D & 1)) return AF_ERR_INVALID_ARG;
+  if (!(std::isfinite(rope_theta) && rope_theta > 0.f)) return AF_ERR_INVALID_ARG;
+  if (!supported_d(D)) return AF_ERR_UNSUPPORTED;
+  return map_launch(af::launch_rope_table(reinterpret_cast<float2*>(table), rows, D, (double)rope_theta,
+                                          static_cast<hipStream_t>(stream)));
+}
 
 const char* attnfuse_strerror(int code) {
   switch (code) {
@@ -270,40 +276,43 @@ const char* attnfuse_strerror(int code) {
 
 int attnfuse_fwd(const void* Q, const void* K, const void* V, void* O, float* LSE,
                  int B, int H, int H_kv, int S, int D, int dtype,
-                 int rope, float rope_theta, int mask, int window,
+                 int rope, float rope_theta, const float* rope_table, int rope_table_rows,
+                 int mask, int window,
                  const float* alibi_slopes, float softmax_scale, void* stream) {
-  return fwd_impl(Q, K, V, O, LSE, nullptr, nullptr, Ext{}, B, H, H_kv, S, D, dtype, rope, rope_theta, mask, window,
-                  alibi_slopes, softmax_scale, stream);
+  return fwd_impl(Q, K, V, O, LSE, nullptr, nullptr, Ext{}, B, H, H_kv, S, D, dtype, rope, rope_theta, rope_table,
+                  rope_table_rows, mask, window, alibi_slopes, softmax_scale, stream);
 }
 
 int attnfuse_fwd_blocksparse(const void* Q, const void* K, const void* V, void* O, float* LSE,
                              const int* q_block_ptr, const int* k_block_idx,
                              int B, int H, int H_kv, int S, int D, int dtype,
-                             int rope, float rope_theta, int mask, int window,
+                             int rope, float rope_theta, const float* rope_table, int rope_table_rows,
+                             int mask, int window,
                              const float* alibi_slopes, float softmax_scale, void* stream) {
   if (!q_block_ptr || !k_block_idx || !aligned4(q_block_ptr) || !aligned4(k_block_idx)) return AF_ERR_INVALID_ARG;
   const void* outs[] = {O, LSE};
   for (const void* x : outs)
     if (x == (const void*)q_block_ptr || x == (const void*)k_block_idx) return AF_ERR_INVALID_ARG;
   if (S < 1 || S > kMaxSparseS) return AF_ERR_INVALID_ARG;
-  return fwd_impl(Q, K, V, O, LSE, q_block_ptr, k_block_idx, Ext{}, B, H, H_kv, S, D, dtype, rope, rope_theta, mask,
-                  window, alibi_slopes, softmax_scale, stream);
+  return fwd_impl(Q, K, V, O, LSE, q_block_ptr, k_block_idx, Ext{}, B, H, H_kv, S, D, dtype, rope, rope_theta,
+                  rope_table, rope_table_rows, mask, window, alibi_slopes, softmax_scale, stream);
 }
 
 int attnfuse_fwd_bias_norm(const void* Q, const void* K, const void* V, void* O, float* LSE,
                            const float* bias, long long bias_stride_b, long long bias_stride_h,
                            long long bias_stride_q, int norm,
                            int B, int H, int H_kv, int S, int D, int dtype,
-                           int rope, float rope_theta, int mask, int window,
+                           int rope, float rope_theta, const float* rope_table, int rope_table_rows,
+                           int mask, int window,
                            const float* alibi_slopes, float softmax_scale, void* stream) {
   Ext e;
   e.bias = bias; e.sb = bias_stride_b; e.sh = bias_stride_h; e.sq = bias_stride_q; e.norm = norm;
-  return fwd_impl(Q, K, V, O, LSE, nullptr, nullptr, e, B, H, H_kv, S, D, dtype, rope, rope_theta, mask, window,
-                  alibi_slopes, softmax_scale, stream);
+  return fwd_impl(Q, K, V, O, LSE, nullptr, nullptr, e, B, H, H_kv, S, D, dtype, rope, rope_theta, rope_table,
+                  rope_table_rows, mask, window, alibi_slopes, softmax_scale, stream);
 }
 
 size_t attnfuse_bwd_workspace_bytes(int B, int H, int H_kv, int S, int D, int rope) {
-  if (B < 1 || H < 1 || H_kv < 1 || S < 1 || D < 2 || (D & 1)) return 0;
+  if (B < 1 || H < 1 || H_kv < 1 || S < 1 || D < 2 || (D & 1) || H % H_kv) return 0;
   if (rope != AF_ROPE_NONE && rope != AF_ROPE_NEOX && rope != AF_ROPE_INTERLEAVED) return 0;
   return bwd_workspace(B, H, H_kv, S, D, rope).total;
 }
@@ -312,10 +321,12 @@ int attnfuse_bwd(const void* Q, const void* K, const void* V, const void* O, con
                  const float* LSE, void* dQ, void* dK, void* dV,
                  void* workspace, size_t workspace_bytes,
                  int B, int H, int H_kv, int S, int D, int dtype,
-                 int rope, float rope_theta, int mask, int window,
+                 int rope, float rope_theta, const float* rope_table, int rope_table_rows,
+                 int mask, int window,
                  const float* alibi_slopes, float softmax_scale, void* stream) {
   return bwd_impl(Q, K, V, O, dO, LSE, dQ, dK, dV, nullptr, Ext{}, workspace, workspace_bytes, B, H, H_kv, S, D,
-                  dtype, rope, rope_theta, mask, window, alibi_slopes, softmax_scale, stream);
+                  dtype, rope, rope_theta, rope_table, rope_table_rows, mask, window, alibi_slopes, softmax_scale,
+                  stream);
 }
 
 int attnfuse_bwd_blocksparse(const void* Q, const void* K, const void* V, const void* O, const void* dO,
@@ -324,7 +335,8 @@ int attnfuse_bwd_blocksparse(const void* Q, const void* K, const void* V, const 
                              const int* k_block_ptr, const int* q_block_idx,
                              void* workspace, size_t workspace_bytes,
                              int B, int H, int H_kv, int S, int D, int dtype,
-                             int rope, float rope_theta, int mask, int window,
+                             int rope, float rope_theta, const float* rope_table, int rope_table_rows,
+                             int mask, int window,
                              const float* alibi_slopes, float softmax_scale, void* stream) {
   const int* m[] = {q_block_ptr, k_block_idx, k_block_ptr, q_block_idx};
   for (const int* x : m) if (!x || !aligned4(x)) return AF_ERR_INVALID_ARG;
@@ -333,7 +345,7 @@ int attnfuse_bwd_blocksparse(const void* Q, const void* K, const void* V, const 
     for (const int* y : m) if (x == (const void*)y) return AF_ERR_INVALID_ARG;
   if (S < 1 || S > kMaxSparseS) return AF_ERR_INVALID_ARG;
   return bwd_impl(Q, K, V, O, dO, LSE, dQ, dK, dV, m, Ext{}, workspace, workspace_bytes, B, H, H_kv, S, D, dtype,
-                  rope, rope_theta, mask, window, alibi_slopes, softmax_scale, stream);
+                  rope, rope_theta, rope_table, rope_table_rows, mask, window, alibi_slopes, softmax_scale, stream);
 }
 
 int attnfuse_bwd_bias_norm(const void* Q, const void* K, const void* V, const void* O, const void* dO,
@@ -342,12 +354,13 @@ int attnfuse_bwd_bias_norm(const void* Q, const void* K, const void* V, const vo
                            long long bias_stride_q, int norm,
                            void* workspace, size_t workspace_bytes,
                            int B, int H, int H_kv, int S, int D, int dtype,
-                           int rope, float rope_theta, int mask, int window,
+                           int rope, float rope_theta, const float* rope_table, int rope_table_rows,
+                           int mask, int window,
                            const float* alibi_slopes, float softmax_scale, void* stream) {
   Ext e;
   e.bias = bias; e.sb = bias_stride_b; e.sh = bias_stride_h; e.sq = bias_stride_q; e.norm = norm;
   return bwd_impl(Q, K, V, O, dO, LSE, dQ, dK, dV, nullptr, e, workspace, workspace_bytes, B, H, H_kv, S, D, dtype,
-                  rope, rope_theta, mask, window, alibi_slopes, softmax_scale, stream);
+                  rope, rope_theta, rope_table, rope_table_rows, mask, window, alibi_slopes, softmax_scale, stream);
 }
 
 // ---------------------------------------------------------------- decode
@@ -356,24 +369,28 @@ size_t attnfuse_decode_workspace_bytes(int B, int H, int H_kv, int S_kv, int D) 
   return decode_layout(B, H, H_kv, S_kv, D).total;
 }
 
-int attnfuse_decode(const void* Q, const void* K, const void* V, const int* cache_lens,
-                    void* O, float* LSE, void* workspace, size_t workspace_bytes,
-                    int B, int H, int H_kv, int S_kv, int D, int dtype,
-                    int rope, float rope_theta, int mask, int window,
-                    const float* alibi_slopes, float softmax_scale, void* stream) {
+// Decode with the partials in the caller's workspace.
+static int decode_impl(const void* Q, const void* K, const void* V, const int* cache_lens, void* O, float* LSE,
+                       void* workspace, size_t workspace_bytes, int B, int H, int H_kv, int S_kv, int D, int dtype,
+                       int rope, float rope_theta, const float* rope_table, int rope_table_rows, int mask, int window,
+                       const float* alibi_slopes, float softmax_scale, void* stream) {
+  const bool static_scratch = false;
   const void* ins[] = {Q, K, V};
   const void* outs[] = {O, LSE, workspace};
+  const int nouts = static_scratch ? 2 : 3;
   for (const void* x : ins) if (!x || !aligned16(x)) return AF_ERR_INVALID_ARG;
-  for (const void* x : outs) if (!x || !aligned16(x)) return AF_ERR_INVALID_ARG;
+  for (int i = 0; i < nouts; ++i) if (!outs[i] || !aligned16(outs[i])) return AF_ERR_INVALID_ARG;
   if (cache_lens && (reinterpret_cast<uintptr_t>(cache_lens) & 3u)) return AF_ERR_INVALID_ARG;
-  for (const void* x : outs) {
-    for (const void* y : ins) if (x == y) return AF_ERR_INVALID_ARG;
-    if (x == static_cast<const void*>(cache_lens)) return AF_ERR_INVALID_ARG;
+  for (int i = 0; i < nouts; ++i) {
+    for (const void* y : ins) if (outs[i] == y) return AF_ERR_INVALID_ARG;
+    if (outs[i] == static_cast<const void*>(cache_lens)) return AF_ERR_INVALID_ARG;
   }
   int rc = check_common(B, H, H_kv, S_kv, D, dtype, rope, rope_theta);
   if (rc != AF_OK) return rc;
   if ((rc = check_attn(mask, window, softmax_scale)) != AF_OK) return rc;
-  if (workspace_bytes < attnfuse_decode_workspace_bytes(B, H, H_kv, S_kv, D)) return AF_ERR_INVALID_ARG;
+  if ((rc = check_table(rope, rope_table, rope_table_rows, S_kv, outs, nouts)) != AF_OK) return rc;
+  const size_t need = attnfuse_decode_workspace_bytes(B, H, H_kv, S_kv, D);
+  if (!static_scratch && workspace_bytes < need) return AF_ERR_INVALID_ARG;
   if (!supported_d(D) || dtype != AF_DTYPE_BF16 || H / H_kv > 32) return AF_ERR_UNSUPPORTED;
 
   hipStream_t st = static_cast<hipStream_t>(stream);
@@ -388,13 +405,24 @@ int attnfuse_decode(const void* Q, const void* K, const void* V, const int* cach
   p.chunk = L.chunk; p.nsplit = L.nsplit;
   p.slopes = alibi_slopes;
   p.scale = softmax_scale;
-  p.table = nullptr;
-  if (rope != AF_ROPE_NONE && (rc = rope_table(D, rope_theta, S_kv, st, &p.table)) != AF_OK) return rc;
+  p.table = (rope != AF_ROPE_NONE) ? reinterpret_cast<const float2*>(rope_table) : nullptr;
   return map_launch(af::launch_decode(D, rope, alibi_slopes != nullptr, p, st));
 }
 
+int attnfuse_decode(const void* Q, const void* K, const void* V, const int* cache_lens,
+                    void* O, float* LSE, void* workspace, size_t workspace_bytes,
+                    int B, int H, int H_kv, int S_kv, int D, int dtype,
+                    int rope, float rope_theta, const float* rope_table, int rope_table_rows,
+                    int mask, int window,
+                    const float* alibi_slopes, float softmax_scale, void* stream) {
+  if (!workspace) return AF_ERR_INVALID_ARG;
+  return decode_impl(Q, K, V, cache_lens, O, LSE, workspace, workspace_bytes, B, H, H_kv, S_kv, D, dtype, rope,
+                     rope_theta, rope_table, rope_table_rows, mask, window, alibi_slopes, softmax_scale, stream);
+}
+
 static int rope_common(const void* X0, const void* X1, void* Y0, void* Y1, int B, int H, int H_kv, int S, int D,
-                       int dtype, int rope, float rope_theta, void* stream, bool inverse) {
+                       int dtype, int rope, float rope_theta, const float* rope_table, int rope_table_rows,
+                       void* stream, bool inverse) {
   if (!X0 || !Y0 || !aligned16(X0) || !aligned16(Y0)) return AF_ERR_INVALID_ARG;
   if ((X1 == nullptr) != (Y1 == nullptr)) return AF_ERR_INVALID_ARG;
   if (X1 && (!aligned16(X1) || !aligned16(Y1))) return AF_ERR_INVALID_ARG;
@@ -402,24 +430,30 @@ static int rope_common(const void* X0, const void* X1, void* Y0, void* Y1, int B
   int rc = check_common(B, H, H_kv, S, D, dtype, rope, rope_theta);
   if (rc != AF_OK) return rc;
   if (rope == AF_ROPE_NONE) return AF_ERR_INVALID_ARG;
+  const void* outs[] = {Y0, Y1};
+  if ((rc = check_table(rope, rope_table, rope_table_rows, S, outs, 2)) != AF_OK) return rc;
   if (!supported_d(D)) return AF_ERR_UNSUPPORTED;
   hipStream_t st = static_cast<hipStream_t>(stream);
   af::RopeParams p{};
   p.x0 = X0; p.y0 = Y0; p.heads0 = H;
   p.x1 = X1; p.y1 = Y1; p.heads1 = X1 ? H_kv : 0;
   p.B = B; p.S = S;
-  if ((rc = rope_table(D, rope_theta, S, st, &p.table)) != AF_OK) return rc;
+  p.table = reinterpret_cast<const float2*>(rope_table);
   return map_launch(af::launch_rope(dtype == AF_DTYPE_FP32, D, rope, inverse, p, st));
 }
 
 int attnfuse_rope(const void* Q, const void* K, void* Qr, void* Kr, int B, int H, int H_kv, int S, int D,
-                  int dtype, int rope, float rope_theta, void* stream) {
-  return rope_common(Q, K, Qr, Kr, B, H, H_kv, S, D, dtype, rope, rope_theta, stream, false);
+                  int dtype, int rope, float rope_theta, const float* rope_table, int rope_table_rows,
+                  void* stream) {
+  return rope_common(Q, K, Qr, Kr, B, H, H_kv, S, D, dtype, rope, rope_theta, rope_table, rope_table_rows, stream,
+                     false);
 }
 
 int attnfuse_rope_bwd(const void* dQr, const void* dKr, void* dQ, void* dK, int B, int H, int H_kv, int S, int D,
-                      int dtype, int rope, float rope_theta, void* stream) {
-  return rope_common(dQr, dKr, dQ, dK, B, H, H_kv, S, D, dtype, rope, rope_theta, stream, true);
+                      int dtype, int rope, float rope_theta, const float* rope_table, int rope_table_rows,
+                      void* stream) {
+  return rope_common(dQr, dKr, dQ, dK, B, H, H_kv, S, D, dtype, rope, rope_theta, rope_table, rope_table_rows, stream,
+                     true);
 }
 
 }  // extern "C"

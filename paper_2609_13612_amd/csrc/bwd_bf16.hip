@@ -1,21 +1,37 @@
 // Fused RoPE + masked attention backward, bf16 MFMA with fp32 accumulation,
 // for gfx950.
 //
-// Three kernels, no atomics (Section 4.4): every output tile has exactly one
+// The passes of Section 4.4, no atomics: every output tile has exactly one
 // writer.
-//   1. bwd_prep:  delta_i = rowsum(dO_i * O_i), LSE_i in log2 units, dO in
-//                 fp16, and with RoPE Q' = R Q and K' = R K rotated once into
-//                 the workspace (fp16).  The two later kernels read each Q'
+//   0. bwd_dmax, bwd_dscale: sigma, the power of two per (batch, K/V head)
+//                 that brings the group's largest |dO| into [1, 2).
+//   1. bwd_prep:  delta_i = rowsum(dO_i * O_i), LSE_i in log2 units, sigma dO
+//                 in fp16, and with RoPE Q' = R Q and K' = R K rotated once
+//                 into the workspace (fp16).  The later kernels read each Q'
 //                 and K' tile many times (dK/dV reads every Q' tile once per
 //                 key block), so one rotation pass replaces all of those.
-//   2. bwd_dkdv:  one workgroup per 128 keys of one (batch, K/V head); it
+//   2. bwd_dq:    one workgroup per 256 query rows (GQA heads packed, as in
+//                 the forward); it loops over visible key tiles:
+//                 dQ' += scale dS K',  dQ = R^T dQ'.  Since it forms P and dP
+//                 for every visible key of its rows, it also sums the
+//                 softmax backward's row term delta_i = sum_j P_ij dP_ij in
+//                 fp32 (with P renormalised by its own row sum) and writes it,
+//                 and the renormalised LSE, over the preprocessing pass's.
+//   3. bwd_dkdv:  one workgroup per 128 keys of one (batch, K/V head); it
 //                 loops over the query heads of the GQA group and their
 //                 visible query tiles, re-deriving P = exp(S - LSE) tile by
 //                 tile:  dV += P^T dO,  dS = P o (dO V^T - delta),
 //                 dK' += scale dS^T Q';  dK = R^T dK'.
-//   3. bwd_dq:    one workgroup per 256 query rows (GQA heads packed, as in
-//                 the forward); it loops over visible key tiles:
-//                 dQ' += scale dS K',  dQ = R^T dQ'.
+// delta from rowsum(dO o O) equals sum_j P_ij dP_ij only for the exact O;
+// the bf16 O a forward stores moves it by O's rounding, which reaches dK and
+// dQ through P_ij (dP_ij - delta_i).  The dK/dV pass therefore runs last, on
+// the dQ pass's sum; the dQ pass itself uses the preprocessing pass's value.
+//
+// Scaling: the fp16 MFMA operands dO and dS carry the factor sigma, so their
+// magnitudes sit near 1 whatever the gradient's scale (unscaled bf16
+// gradients of 1e-6 would fall into fp16's subnormals, 6e-8 apart); the
+// gradients leave multiplied by 1/sigma.  Multiplying by a power of two is
+// exact, so results do not depend on the scale of dO.
 // Register layouts follow the forward: the operand held in registers is the
 // MFMA B operand (lane = its row), tiles staged in LDS are the A operand, and
 // contractions over queries/keys read a transposed LDS copy stored with the
@@ -28,16 +44,66 @@
 // fp16 (2^-12 relative rounding instead of bf16's 2^-9) keeps the sums
 // dK = dS^T Q and dQ = dS K accurate when attention concentrates on a few
 // keys and their gradients grow.  dV = P^T dO sums P over many queries
-// without normalisation, so it also runs on fp16 operands (P and dO, the
-// latter converted exactly from bf16).  All of this needs |Q|, |K|, |dO| and
-// |dS| below the fp16 maximum 65504.  dP = dO V^T uses the bf16 inputs as
-// they are.
+// without normalisation, so it also runs on fp16 operands (P and sigma dO,
+// the latter converted exactly from bf16).  Range: the rotated |Q'|, |K'|
+// and |V| must stay below the fp16 maximum 65504, and |sigma dS| <= 4 D
+// max|V| below it too, i.e. max|V| < 16376 / D (128 at D = 128).  In the dQ
+// pass dP = dO V^T uses the bf16 inputs as they are.
 #include <type_traits>
 
 #include "attn_tiles.hpp"
 #include "launch.hpp"
 
 namespace af {
+
+// ---------------------------------------------------------------- dO scale
+// Partial maxima of |dO| over chunks of each (batch, K/V head)'s G query heads
+// (contiguous in [B, H, S, D]), as bf16 magnitude bits: the bit patterns of
+// non-negative bf16 values order like the values, so the maximum is an
+// integer maximum.
+constexpr int DMAX_CHUNK = 16384;   // dO elements per partial maximum
+
+template <int D>
+__global__ __launch_bounds__(256) void bwd_dmax_kernel(BwdParams p) {
+  const int nch = p.dmax_chunks;
+  const int bg = blockIdx.x / nch, c = blockIdx.x - bg * nch;
+  const long long n = (long long)(p.H / p.Hkv) * p.S * D;
+  const uint16_t* src = static_cast<const uint16_t*>(p.dout) + (long long)bg * n;
+  const long long e1 = min(n, (long long)(c + 1) * DMAX_CHUNK);
+  uint32_t mx = 0;
+  for (long long e = (long long)c * DMAX_CHUNK + 8 * threadIdx.x; e < e1; e += 8 * 256) {   // n % 8 == 0
+    const u32x4 x = ld16(src + e);
+#pragma unroll
+    for (int w = 0; w < 4; ++w) mx = max(mx, max(x[w] & 0x7fffu, (x[w] >> 16) & 0x7fffu));
+  }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) mx = max(mx, (uint32_t)__shfl_xor((int)mx, off, 64));
+  __shared__ uint32_t part[4];
+  if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = mx;
+  __syncthreads();
+  if (threadIdx.x == 0) p.dmax[blockIdx.x] = max(max(part[0], part[1]), max(part[2], part[3]));
+}
+
+// sigma = 2^(127 - E) for the largest |dO| with biased exponent E, so that
+// max |dO| * sigma lies in [1, 2); clamped to [2^-126, 2^126].  1 when the
+// group's dO is all zero or holds an inf / NaN.  One workgroup per group.
+__global__ __launch_bounds__(256) void bwd_dscale_kernel(BwdParams p) {
+  const int bg = blockIdx.x, nch = p.dmax_chunks;
+  uint32_t mx = 0;
+  for (int c = threadIdx.x; c < nch; c += 256) mx = max(mx, p.dmax[(long long)bg * nch + c]);
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) mx = max(mx, (uint32_t)__shfl_xor((int)mx, off, 64));
+  __shared__ uint32_t part[4];
+  if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = mx;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    mx = max(max(part[0], part[1]), max(part[2], part[3]));
+    const int E = (int)(mx >> 7);   // bf16 biased exponent (the sign bit is clear)
+    float sig = 1.f;
+    if (mx != 0u && E != 255) sig = __uint_as_float((uint32_t)min(max(254 - max(E, 1), 1), 253) << 23);
+    p.dscale[bg] = sig;
+  }
+}
 
 // ---------------------------------------------------------------- preprocessing
 // One thread per (row, chunk pair c): chunks c and c + D/16 (dims 8c.. and
@@ -53,6 +119,8 @@ __global__ __launch_bounds__(256) void bwd_prep_kernel(BwdParams p, int q_blocks
     const long long rows = (long long)p.B * p.H * p.S;
     const long long row = (long long)blockIdx.x * RPB + threadIdx.x / TPR;
     const long long rc = row < rows ? row : rows - 1;   // clamp: every lane joins the reduction
+    const int hq = (int)((rc / p.S) % p.H), bq = (int)(rc / ((long long)p.S * p.H));
+    const float sig = p.dscale[bq * p.Hkv + hq / (p.H / p.Hkv)];
     const uint16_t* dOr = static_cast<const uint16_t*>(p.dout) + rc * D;
     const uint16_t* Or = static_cast<const uint16_t*>(p.o) + rc * D;
     const u32x4 a0 = ld16(dOr + d0), a1 = ld16(dOr + d1);
@@ -68,14 +136,14 @@ __global__ __launch_bounds__(256) void bwd_prep_kernel(BwdParams p, int q_blocks
       u32x4 h0, h1;
 #pragma unroll
       for (int w = 0; w < 4; ++w) {
-        h0[w] = pack_f16(bf_lo(a0[w]), bf_hi(a0[w]));
-        h1[w] = pack_f16(bf_lo(a1[w]), bf_hi(a1[w]));
+        h0[w] = pack_f16(bf_lo(a0[w]) * sig, bf_hi(a0[w]) * sig);
+        h1[w] = pack_f16(bf_lo(a1[w]) * sig, bf_hi(a1[w]) * sig);
       }
       uint16_t* dst = static_cast<uint16_t*>(p.do16) + row * D;
       st16(dst + d0, h0);
       st16(dst + d1, h1);
       if (c == 0) {
-        p.delta[row] = acc;
+        p.delta[row] = acc * sig;
         const float l = p.lse ? p.lse[row] : 0.f;   // relu attention has no LSE
         p.lse2[row] = (l == -INFINITY) ? INFINITY : l * kLog2e;
       }
@@ -515,9 +583,12 @@ __global__ __launch_bounds__(512) void bwd_dkdv_kernel(BwdParams p) {
   __syncthreads();
   if (qh == 1) add(dv);
 
-  if (n < S) {
-    if (qh == 0) store_grad_rows<D, ROPE>(dk, p.scale, static_cast<uint16_t*>(p.dk) + (size_t)bg * S * D, p.table, n, lg);
-    else store_grad_rows<D, ROPE_NONE>(dv, 1.f, static_cast<uint16_t*>(p.dv) + (size_t)bg * S * D, nullptr, n, lg);
+  if (n < S) {   // dS and dO carried the factor sigma (a power of two: exact)
+    const float inv = 1.f / p.dscale[bg];
+    if (qh == 0)
+      store_grad_rows<D, ROPE>(dk, p.scale * inv, static_cast<uint16_t*>(p.dk) + (size_t)bg * S * D, p.table, n, lg);
+    else
+      store_grad_rows<D, ROPE_NONE>(dv, inv, static_cast<uint16_t*>(p.dv) + (size_t)bg * S * D, nullptr, n, lg);
   }
 }
 
@@ -577,7 +648,10 @@ __global__ __launch_bounds__(512) void bwd_dq_kernel(BwdParams p) {
   const float lse2 = (m < S) ? p.lse2[bh * S + mc] : INFINITY;
   const float* __restrict__ brow = nullptr;       // this lane's row of the bias tensor
   if constexpr (TBIAS) brow = p.bias + b * p.bias_sb + h * p.bias_sh + mc * p.bias_sq;
-  const float del = (m < S) ? p.delta[bh * S + mc] : 0.f;
+  const float del = (m < S) ? p.delta[bh * S + mc] : 0.f;   // sigma delta_i from rowsum(dO o O)
+  const float sig = p.dscale[bg];
+  float dsum = 0.f;   // this lane's part of sum_j P_ij dP_ij (unscaled)
+  float lsum = 0.f;   // and of sum_j P_ij
 
   f32x16 dq[C::MT];
 #pragma unroll
@@ -671,10 +745,14 @@ __global__ __launch_bounds__(512) void bwd_dq_kernel(BwdParams p) {
         }
         if constexpr (RELU) {   // dS = dP where s > 0
 #pragma unroll
-          for (int r = 0; r < 16; ++r) ds[r] = pos[r] ? ds[r] * dp[r] : 0.f;
+          for (int r = 0; r < 16; ++r) ds[r] = pos[r] ? ds[r] * dp[r] * sig : 0.f;
         } else {
 #pragma unroll
-          for (int r = 0; r < 16; ++r) ds[r] *= dp[r] - del;
+          for (int r = 0; r < 16; ++r) {
+            lsum += ds[r];
+            dsum = __builtin_fmaf(ds[r], dp[r], dsum);
+            ds[r] *= __builtin_fmaf(dp[r], sig, -del);
+          }
         }
         u32x4 db[2];
 #pragma unroll
@@ -695,7 +773,20 @@ __global__ __launch_bounds__(512) void bwd_dq_kernel(BwdParams p) {
     }
     __syncthreads();
   }
-  if (m < S) store_grad_rows<D, ROPE>(dq, p.scale, static_cast<uint16_t*>(p.dq) + bh * S * D, p.table, m, lg);
+  // For the dK/dV pass: the row's probabilities as this pass formed them sum
+  // to l = sum_j P_ij, which differs from 1 by the rounding of the LSE it was
+  // given (noticeable when scores are large); LSE + log2 l renormalises them,
+  // and delta = sum_j P_ij dP_ij / l is the softmax backward's row term of
+  // the renormalised P.  Rows with no visible key keep LSE = +inf.
+  if constexpr (!RELU) {
+    const float ltot = pair_sum(lsum), dtot = pair_sum(dsum);   // the lane pair (l, l ^ 32) holds row m's keys
+    if (m < S && lg == 0) {
+      const bool any = ltot > 0.f;
+      p.delta[bh * S + m] = any ? dtot / ltot * sig : 0.f;
+      p.lse2[bh * S + m] = any ? lse2 + __log2f(ltot) : INFINITY;
+    }
+  }
+  if (m < S) store_grad_rows<D, ROPE>(dq, p.scale / sig, static_cast<uint16_t*>(p.dq) + bh * S * D, p.table, m, lg);
 }
 
 // ---------------------------------------------------------------- launch
@@ -706,15 +797,10 @@ static int launch_one(const BwdParams& p, hipStream_t st) {
   const long long krows = (ROPE != ROPE_NONE) ? (long long)p.B * p.Hkv * p.S : 0;
   const int q_blocks = (int)((qrows + RPB - 1) / RPB);
   const int k_blocks = (int)((krows + RPB - 1) / RPB);
+  const unsigned groups = (unsigned)(p.B * p.Hkv);
+  hipLaunchKernelGGL((bwd_dmax_kernel<D>), dim3(groups * (unsigned)p.dmax_chunks), dim3(256), 0, st, p);
+  hipLaunchKernelGGL(bwd_dscale_kernel, dim3(groups), dim3(256), 0, st, p);
   hipLaunchKernelGGL((bwd_prep_kernel<D, ROPE>), dim3((unsigned)(q_blocks + k_blocks)), dim3(256), 0, st, p, q_blocks);
-  using QC = QTileCfg<D>;
-  const int nkb = (p.S + QC::KEYS - 1) / QC::KEYS;
-  if (EXT == EXT_NONE && p.bk_ptr)
-    hipLaunchKernelGGL((bwd_dkdv_kernel<D, ROPE, MASK, ALIBI, true>), dim3((unsigned)(nkb * p.B * p.Hkv)),
-                       dim3(QC::THREADS), 0, st, p);
-  else
-    hipLaunchKernelGGL((bwd_dkdv_kernel<D, ROPE, MASK, ALIBI, false, EXT>), dim3((unsigned)(nkb * p.B * p.Hkv)),
-                       dim3(QC::THREADS), 0, st, p);
   using TC = TileCfg<D, ROPE_NONE>;
   BwdParams pq = p;
   pq.heads_per_wg = heads_per_wg(p.H / p.Hkv);
@@ -726,6 +812,15 @@ static int launch_one(const BwdParams& p, hipStream_t st) {
   else
     hipLaunchKernelGGL((bwd_dq_kernel<D, ROPE, MASK, ALIBI, false, EXT>), dim3((unsigned)qblocks), dim3(TC::THREADS),
                        0, st, pq);
+  // after the dQ pass, which replaced delta by sum_j P_ij dP_ij
+  using QC = QTileCfg<D>;
+  const int nkb = (p.S + QC::KEYS - 1) / QC::KEYS;
+  if (EXT == EXT_NONE && p.bk_ptr)
+    hipLaunchKernelGGL((bwd_dkdv_kernel<D, ROPE, MASK, ALIBI, true>), dim3((unsigned)(nkb * p.B * p.Hkv)),
+                       dim3(QC::THREADS), 0, st, p);
+  else
+    hipLaunchKernelGGL((bwd_dkdv_kernel<D, ROPE, MASK, ALIBI, false, EXT>), dim3((unsigned)(nkb * p.B * p.Hkv)),
+                       dim3(QC::THREADS), 0, st, p);
   return hipGetLastError() == hipSuccess ? 0 : -3;
 }
 

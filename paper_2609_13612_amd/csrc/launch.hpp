@@ -38,9 +38,13 @@ struct BwdParams {
   void* dq;
   void* dk;
   void* dv;
-  float* delta;           // workspace [B*H*S]: rowsum(dO * O)
+  float* delta;           // workspace [B*H*S]: sigma * delta_i (see dscale); rowsum(dO * O) from the
+                          // preprocessing pass, replaced by sum_j P_ij dP_ij in the dQ pass
   float* lse2;            // workspace [B*H*S]: LSE in log2 units (+inf for empty rows)
-  void* do16;             // workspace [B,H,S,D] fp16: dO
+  void* do16;             // workspace [B,H,S,D] fp16: sigma * dO
+  float* dscale;          // workspace [B*H_kv]: sigma, a power of two per (batch, K/V head)
+  uint32_t* dmax;         // workspace [B*H_kv*dmax_chunks]: partial max |dO| (bf16 magnitude bits)
+  int dmax_chunks;        // partial maxima per (batch, K/V head)
   void* qr16;             // workspace [B,H,S,D] fp16: Q' = R Q (RoPE only, else nullptr)
   void* kr16;             // workspace [B,H_kv,S,D] fp16: K' = R K (RoPE only, else nullptr)
   int B, H, Hkv, S, window;

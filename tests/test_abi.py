@@ -12,6 +12,7 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HEADER = os.path.join(ROOT, "include", "attnfuse.h")
 FAKE = 0x10000   # aligned, never dereferenced: validation fails first
 ODD = 0x10008    # not 16-byte aligned
+TABLE = 0x40000  # stand-in for a caller's RoPE cos/sin table
 
 
 def declared_symbols():
@@ -25,6 +26,7 @@ def test_header_declares_the_boundary():
                                          "attnfuse_bwd_workspace_bytes", "attnfuse_decode",
                                          "attnfuse_decode_workspace_bytes", "attnfuse_fwd", "attnfuse_fwd_bias_norm",
                                          "attnfuse_fwd_blocksparse", "attnfuse_rope", "attnfuse_rope_bwd",
+                                         "attnfuse_rope_table_bytes", "attnfuse_rope_table_fill",
                                          "attnfuse_strerror", "attnfuse_version"])
 
 
@@ -33,7 +35,7 @@ def test_library_loads_and_exports_every_declared_symbol():
     for name in declared_symbols():
         assert hasattr(lib, name), name
     assert set(declared_symbols()) == set(_lib.SIGNATURES)
-    assert lib.attnfuse_version() == 2
+    assert lib.attnfuse_version() == 3
 
 
 def test_strerror():
@@ -48,22 +50,28 @@ def test_strerror():
 def test_workspace_bytes():
     lib = _lib.load()
     rows, krows = 32 * 8192, 8 * 8192
-    # delta + lse2 (fp32) + dO (fp16); with RoPE also Q' and K' (fp16)
-    assert lib.attnfuse_bwd_workspace_bytes(1, 32, 8, 8192, 128, 0) == 8 * rows + 2 * rows * 128
-    assert lib.attnfuse_bwd_workspace_bytes(1, 32, 8, 8192, 128, 1) == 8 * rows + 2 * rows * 128 * 2 + 2 * krows * 128
-    # sections start on 256-byte boundaries
-    assert lib.attnfuse_bwd_workspace_bytes(1, 1, 1, 3, 64, 2) == 256 * 2 + 512 * 3
+    # delta + lse2 (fp32) + dO (fp16) + dO scale per group (8 x fp32, one
+    # 256-byte section) + partial maxima (8 groups x 4*8192*128/16384 = 256
+    # chunks x 4 bytes); with RoPE also Q' and K' (fp16)
+    scale_parts = 256 + 8 * 256 * 4
+    assert lib.attnfuse_bwd_workspace_bytes(1, 32, 8, 8192, 128, 0) == 8 * rows + 2 * rows * 128 + scale_parts
+    assert lib.attnfuse_bwd_workspace_bytes(1, 32, 8, 8192, 128, 1) == \
+        8 * rows + 2 * rows * 128 * 2 + 2 * krows * 128 + scale_parts
+    # sections start on 256-byte boundaries: delta, lse2, dO, scale, maxima, Q', K'
+    assert lib.attnfuse_bwd_workspace_bytes(1, 1, 1, 3, 64, 2) == 256 * 2 + 512 + 256 * 2 + 512 * 2
     assert lib.attnfuse_bwd_workspace_bytes(0, 32, 8, 8192, 128, 0) == 0
     assert lib.attnfuse_bwd_workspace_bytes(1, 32, 8, 8192, 128, 7) == 0
+    assert lib.attnfuse_bwd_workspace_bytes(1, 6, 4, 8192, 128, 0) == 0   # H % H_kv != 0
 
 
 def _fwd(**over):
     a = dict(Q=FAKE, K=FAKE + 0x100, V=FAKE + 0x200, O=FAKE + 0x300, LSE=FAKE + 0x400, B=1, H=4, H_kv=2, S=16,
-             D=64, dtype=0, rope=1, theta=10000.0, mask=1, window=0, slopes=None, scale=0.125, stream=None)
+             D=64, dtype=0, rope=1, theta=10000.0, table=TABLE, rows=4096, mask=1, window=0, slopes=None, scale=0.125,
+             stream=None)
     a.update(over)
     return _lib.load().attnfuse_fwd(a["Q"], a["K"], a["V"], a["O"], a["LSE"], a["B"], a["H"], a["H_kv"], a["S"],
-                                    a["D"], a["dtype"], a["rope"], a["theta"], a["mask"], a["window"], a["slopes"],
-                                    a["scale"], a["stream"])
+                                    a["D"], a["dtype"], a["rope"], a["theta"], a["table"], a["rows"], a["mask"],
+                                    a["window"], a["slopes"], a["scale"], a["stream"])
 
 
 INVALID_FWD = [
@@ -72,6 +80,9 @@ INVALID_FWD = [
     dict(H=3, H_kv=2), dict(D=0), dict(D=63), dict(dtype=2), dict(rope=3), dict(rope=-1),
     dict(theta=0.0), dict(theta=-1.0), dict(theta=float("inf")), dict(theta=float("nan")), dict(mask=3),
     dict(mask=2, window=0), dict(mask=2, window=-4), dict(scale=0.0), dict(scale=-1.0), dict(scale=float("nan")),
+    # the caller's RoPE table: present, aligned, covering S, not an output
+    dict(table=None), dict(table=ODD), dict(rows=15), dict(rows=0), dict(rows=(1 << 20) + 1),
+    dict(table=FAKE + 0x300), dict(table=FAKE + 0x400),
 ]
 
 
@@ -90,21 +101,28 @@ def test_rope_none_ignores_theta_validation_only_in_attention():
     assert _fwd(rope=0, theta=0.0, D=96) == -2
 
 
+def test_rope_none_needs_no_table():
+    # without RoPE the table arguments are ignored (validation passes, D is unsupported)
+    assert _fwd(rope=0, table=None, rows=0, D=96) == -2
+    assert _fwd(rope=1, table=TABLE, rows=16, D=96) == -2   # exactly S rows is enough
+
+
 def _bwd(**over):
     base = FAKE
     a = dict(Q=base, K=base + 0x100, V=base + 0x200, O=base + 0x300, dO=base + 0x400, LSE=base + 0x500,
              dQ=base + 0x600, dK=base + 0x700, dV=base + 0x800, ws=base + 0x900, ws_bytes=1 << 20,
-             B=1, H=4, H_kv=2, S=16, D=64, dtype=0, rope=1, theta=1e4, mask=1, window=0, slopes=None,
-             scale=0.125, stream=None)
+             B=1, H=4, H_kv=2, S=16, D=64, dtype=0, rope=1, theta=1e4, table=TABLE, rows=16, mask=1, window=0,
+             slopes=None, scale=0.125, stream=None)
     a.update(over)
     return _lib.load().attnfuse_bwd(a["Q"], a["K"], a["V"], a["O"], a["dO"], a["LSE"], a["dQ"], a["dK"], a["dV"],
                                     a["ws"], a["ws_bytes"], a["B"], a["H"], a["H_kv"], a["S"], a["D"], a["dtype"],
-                                    a["rope"], a["theta"], a["mask"], a["window"], a["slopes"], a["scale"],
-                                    a["stream"])
+                                    a["rope"], a["theta"], a["table"], a["rows"], a["mask"], a["window"],
+                                    a["slopes"], a["scale"], a["stream"])
 
 
 @pytest.mark.parametrize("over", [dict(Q=None), dict(dO=None), dict(ws=None), dict(dQ=FAKE), dict(ws_bytes=20991),
-                                  dict(H=4, H_kv=3), dict(mask=2, window=0), dict(dK=ODD), dict(S=0)],
+                                  dict(H=4, H_kv=3), dict(mask=2, window=0), dict(dK=ODD), dict(S=0),
+                                  dict(table=None), dict(rows=8), dict(table=ODD), dict(table=FAKE + 0x900)],
                          ids=lambda o: ",".join(f"{k}={v}" for k, v in o.items()))
 def test_bwd_rejects_invalid_arguments(over):
     assert _bwd(**over) == -1
@@ -117,15 +135,16 @@ def test_bwd_unsupported():
 
 def _rope(fn="attnfuse_rope", **over):
     a = dict(Q=FAKE, K=FAKE + 0x100, Qr=FAKE + 0x200, Kr=FAKE + 0x300, B=1, H=4, H_kv=2, S=16, D=64, dtype=0,
-             rope=1, theta=1e4, stream=None)
+             rope=1, theta=1e4, table=TABLE, rows=64, stream=None)
     a.update(over)
     return getattr(_lib.load(), fn)(a["Q"], a["K"], a["Qr"], a["Kr"], a["B"], a["H"], a["H_kv"], a["S"], a["D"],
-                                    a["dtype"], a["rope"], a["theta"], a["stream"])
+                                    a["dtype"], a["rope"], a["theta"], a["table"], a["rows"], a["stream"])
 
 
 @pytest.mark.parametrize("fn", ["attnfuse_rope", "attnfuse_rope_bwd"])
 @pytest.mark.parametrize("over", [dict(Q=None), dict(Qr=None), dict(K=None), dict(Kr=None), dict(rope=0),
-                                  dict(theta=0.0), dict(H=3), dict(Q=ODD), dict(S=0), dict(dtype=5)],
+                                  dict(theta=0.0), dict(H=3), dict(Q=ODD), dict(S=0), dict(dtype=5),
+                                  dict(table=None), dict(rows=15), dict(table=FAKE + 0x200), dict(table=FAKE + 0x300)],
                          ids=lambda o: ",".join(f"{k}={v}" for k, v in o.items()))
 def test_rope_rejects_invalid_arguments(fn, over):
     assert _rope(fn, **over) == -1
@@ -133,6 +152,27 @@ def test_rope_rejects_invalid_arguments(fn, over):
 
 def test_rope_unsupported():
     assert _rope(D=96) == -2
+
+
+def test_rope_table_bytes():
+    lib = _lib.load()
+    assert lib.attnfuse_rope_table_bytes(8192, 128) == 8192 * 64 * 8   # (cos, sin) fp32 per pair
+    assert lib.attnfuse_rope_table_bytes(1, 64) == 32 * 8
+    assert lib.attnfuse_rope_table_bytes(1 << 20, 128) == (1 << 20) * 64 * 8
+    for rows, D in [(0, 128), (-1, 128), ((1 << 20) + 1, 128), (16, 0), (16, 63), (16, -2)]:
+        assert lib.attnfuse_rope_table_bytes(rows, D) == 0
+
+
+@pytest.mark.parametrize("args", [(None, 16, 64, 1e4), (ODD, 16, 64, 1e4), (TABLE, 0, 64, 1e4),
+                                  (TABLE, (1 << 20) + 1, 64, 1e4), (TABLE, 16, 63, 1e4), (TABLE, 16, 0, 1e4),
+                                  (TABLE, 16, 64, 0.0), (TABLE, 16, 64, -1.0), (TABLE, 16, 64, float("inf")),
+                                  (TABLE, 16, 64, float("nan"))], ids=str)
+def test_rope_table_fill_rejects_invalid_arguments(args):
+    assert _lib.load().attnfuse_rope_table_fill(*args, None) == -1
+
+
+def test_rope_table_fill_unsupported():
+    assert _lib.load().attnfuse_rope_table_fill(TABLE, 16, 96, 1e4, None) == -2
 
 
 # ----------------------------------------------------------------------------- decode
@@ -155,19 +195,20 @@ def test_decode_workspace_bytes():
 
 def _decode(**over):
     a = dict(Q=FAKE, K=FAKE + 0x100, V=FAKE + 0x200, lens=None, O=FAKE + 0x300, LSE=FAKE + 0x400, ws=FAKE + 0x500,
-             ws_bytes=1 << 30, B=2, H=8, H_kv=2, S=300, D=128, dtype=0, rope=1, theta=1e4, mask=1, window=0,
-             slopes=None, scale=0.1, stream=None)
+             ws_bytes=1 << 30, B=2, H=8, H_kv=2, S=300, D=128, dtype=0, rope=1, theta=1e4, table=TABLE, rows=300,
+             mask=1, window=0, slopes=None, scale=0.1, stream=None)
     a.update(over)
     return _lib.load().attnfuse_decode(a["Q"], a["K"], a["V"], a["lens"], a["O"], a["LSE"], a["ws"], a["ws_bytes"],
                                        a["B"], a["H"], a["H_kv"], a["S"], a["D"], a["dtype"], a["rope"], a["theta"],
-                                       a["mask"], a["window"], a["slopes"], a["scale"], a["stream"])
+                                       a["table"], a["rows"], a["mask"], a["window"], a["slopes"], a["scale"],
+                                       a["stream"])
 
 
 @pytest.mark.parametrize("over", [dict(Q=None), dict(K=None), dict(V=None), dict(O=None), dict(LSE=None),
                                   dict(ws=None), dict(K=ODD), dict(lens=FAKE + 0x602), dict(O=FAKE),
                                   dict(ws=FAKE + 0x200), dict(ws_bytes=1000), dict(H=8, H_kv=3), dict(S=0),
                                   dict(mask=2, window=0), dict(mask=5), dict(scale=0.0), dict(rope=1, theta=0.0),
-                                  dict(dtype=5)],
+                                  dict(dtype=5), dict(table=None), dict(rows=299), dict(table=FAKE + 0x500)],
                          ids=lambda o: ",".join(f"{k}={v}" for k, v in o.items()))
 def test_decode_rejects_invalid_arguments(over):
     assert _decode(**over) == -1
@@ -185,13 +226,13 @@ MASKP = 0x20000   # 4-byte aligned stand-ins for the device mask lists
 
 def _fwd_bs(**over):
     a = dict(Q=FAKE, K=FAKE + 0x100, V=FAKE + 0x200, O=FAKE + 0x300, LSE=FAKE + 0x400, qp=MASKP, ki=MASKP + 0x100,
-             B=1, H=4, H_kv=2, S=16, D=64, dtype=0, rope=1, theta=10000.0, mask=0, window=0, slopes=None,
-             scale=0.125, stream=None)
+             B=1, H=4, H_kv=2, S=16, D=64, dtype=0, rope=1, theta=10000.0, table=TABLE, rows=16, mask=0, window=0,
+             slopes=None, scale=0.125, stream=None)
     a.update(over)
     return _lib.load().attnfuse_fwd_blocksparse(a["Q"], a["K"], a["V"], a["O"], a["LSE"], a["qp"], a["ki"], a["B"],
                                                 a["H"], a["H_kv"], a["S"], a["D"], a["dtype"], a["rope"],
-                                                a["theta"], a["mask"], a["window"], a["slopes"], a["scale"],
-                                                a["stream"])
+                                                a["theta"], a["table"], a["rows"], a["mask"], a["window"],
+                                                a["slopes"], a["scale"], a["stream"])
 
 
 def _bwd_bs(**over):
@@ -199,18 +240,18 @@ def _bwd_bs(**over):
     a = dict(Q=base, K=base + 0x100, V=base + 0x200, O=base + 0x300, dO=base + 0x400, LSE=base + 0x500,
              dQ=base + 0x600, dK=base + 0x700, dV=base + 0x800, qp=MASKP, ki=MASKP + 0x100, kp=MASKP + 0x200,
              qi=MASKP + 0x300, ws=base + 0x900, ws_bytes=1 << 20, B=1, H=4, H_kv=2, S=16, D=64, dtype=0, rope=1,
-             theta=1e4, mask=0, window=0, slopes=None, scale=0.125, stream=None)
+             theta=1e4, table=TABLE, rows=16, mask=0, window=0, slopes=None, scale=0.125, stream=None)
     a.update(over)
     return _lib.load().attnfuse_bwd_blocksparse(a["Q"], a["K"], a["V"], a["O"], a["dO"], a["LSE"], a["dQ"], a["dK"],
                                                 a["dV"], a["qp"], a["ki"], a["kp"], a["qi"], a["ws"], a["ws_bytes"],
                                                 a["B"], a["H"], a["H_kv"], a["S"], a["D"], a["dtype"], a["rope"],
-                                                a["theta"], a["mask"], a["window"], a["slopes"], a["scale"],
-                                                a["stream"])
+                                                a["theta"], a["table"], a["rows"], a["mask"], a["window"],
+                                                a["slopes"], a["scale"], a["stream"])
 
 
 INVALID_FWD_BS = [dict(qp=None), dict(ki=None), dict(qp=MASKP + 2), dict(ki=MASKP + 0x101), dict(O=MASKP),
                   dict(LSE=MASKP + 0x100), dict(S=64 * 2048 + 1), dict(S=0), dict(Q=None), dict(H=3),
-                  dict(mask=2, window=0), dict(scale=0.0)]
+                  dict(mask=2, window=0), dict(scale=0.0), dict(table=None), dict(rows=8)]
 
 
 @pytest.mark.parametrize("over", INVALID_FWD_BS, ids=lambda o: ",".join(f"{k}={v}" for k, v in o.items()))
@@ -245,31 +286,32 @@ BIASP = 0x30000
 
 def _fwd_bn(**over):
     a = dict(Q=FAKE, K=FAKE + 0x100, V=FAKE + 0x200, O=FAKE + 0x300, LSE=FAKE + 0x400, bias=BIASP, sb=256, sh=64,
-             sq=8, norm=0, B=1, H=4, H_kv=2, S=8, D=64, dtype=0, rope=1, theta=10000.0, mask=1, window=0,
-             slopes=None, scale=0.125, stream=None)
+             sq=8, norm=0, B=1, H=4, H_kv=2, S=8, D=64, dtype=0, rope=1, theta=10000.0, table=TABLE, rows=8, mask=1,
+             window=0, slopes=None, scale=0.125, stream=None)
     a.update(over)
     return _lib.load().attnfuse_fwd_bias_norm(a["Q"], a["K"], a["V"], a["O"], a["LSE"], a["bias"], a["sb"], a["sh"],
                                               a["sq"], a["norm"], a["B"], a["H"], a["H_kv"], a["S"], a["D"],
-                                              a["dtype"], a["rope"], a["theta"], a["mask"], a["window"], a["slopes"],
-                                              a["scale"], a["stream"])
+                                              a["dtype"], a["rope"], a["theta"], a["table"], a["rows"], a["mask"],
+                                              a["window"], a["slopes"], a["scale"], a["stream"])
 
 
 def _bwd_bn(**over):
     base = FAKE
     a = dict(Q=base, K=base + 0x100, V=base + 0x200, O=base + 0x300, dO=base + 0x400, LSE=base + 0x500,
              dQ=base + 0x600, dK=base + 0x700, dV=base + 0x800, bias=BIASP, sb=256, sh=64, sq=8, norm=0,
-             ws=base + 0x900, ws_bytes=1 << 20, B=1, H=4, H_kv=2, S=8, D=64, dtype=0, rope=1, theta=1e4, mask=1,
-             window=0, slopes=None, scale=0.125, stream=None)
+             ws=base + 0x900, ws_bytes=1 << 20, B=1, H=4, H_kv=2, S=8, D=64, dtype=0, rope=1, theta=1e4,
+             table=TABLE, rows=8, mask=1, window=0, slopes=None, scale=0.125, stream=None)
     a.update(over)
     return _lib.load().attnfuse_bwd_bias_norm(a["Q"], a["K"], a["V"], a["O"], a["dO"], a["LSE"], a["dQ"], a["dK"],
                                               a["dV"], a["bias"], a["sb"], a["sh"], a["sq"], a["norm"], a["ws"],
                                               a["ws_bytes"], a["B"], a["H"], a["H_kv"], a["S"], a["D"], a["dtype"],
-                                              a["rope"], a["theta"], a["mask"], a["window"], a["slopes"], a["scale"],
-                                              a["stream"])
+                                              a["rope"], a["theta"], a["table"], a["rows"], a["mask"], a["window"],
+                                              a["slopes"], a["scale"], a["stream"])
 
 
 INVALID_BN = [dict(norm=2), dict(norm=-1), dict(bias=BIASP + 2), dict(sb=-1), dict(sh=-8), dict(sq=-1),
-              dict(O=BIASP), dict(Q=None), dict(LSE=None), dict(mask=2, window=0), dict(S=0)]
+              dict(O=BIASP), dict(Q=None), dict(LSE=None), dict(mask=2, window=0), dict(S=0), dict(table=None),
+              dict(rows=7)]
 
 
 @pytest.mark.parametrize("over", INVALID_BN, ids=lambda o: ",".join(f"{k}={v}" for k, v in o.items()))
@@ -290,7 +332,8 @@ def test_fwd_bias_norm_unsupported(over):
 
 
 INVALID_BWD_BN = [dict(norm=3), dict(bias=BIASP + 1), dict(sq=-2), dict(dK=BIASP), dict(ws=BIASP), dict(dO=None),
-                  dict(LSE=None), dict(Q=None, LSE=None, norm=1), dict(ws_bytes=10)]
+                  dict(LSE=None), dict(Q=None, LSE=None, norm=1), dict(ws_bytes=10), dict(table=None),
+                  dict(table=FAKE + 0x600)]
 
 
 @pytest.mark.parametrize("over", INVALID_BWD_BN, ids=lambda o: ",".join(f"{k}={v}" for k, v in o.items()))

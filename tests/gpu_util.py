@@ -8,10 +8,22 @@ x to it can move it by up to half an ulp, 2^-8 |x| (the format's unit
 roundoff: up to 0.0039 just above |x| = 1, 0.0625 just above |x| = 16), which no
 implementation with bf16 outputs can avoid -- from |x| = 8 on even the
 correctly rounded exact value can miss a flat 2e-2.  The max-abs bound is
-therefore applied per element as 2e-2 + 2^-8 |ref|: the stated 2e-2 plus at
-most 0.0039 for the O(1) values it was written for, and the format's own
-resolution for large gradients.  The mean-abs bound is unchanged.
+therefore applied per element as 2e-2 + 2^-8 |ref|, and the mean-abs bound as
+2e-3 + 2^-9 mean|ref| (rounding to bf16 costs at most a quarter ulp on
+average).  Every check also reports its max-abs and mean-abs against the flat
+2e-2 / 2e-3 figures: printed, and appended as a JSON line to the file named by
+the environment variable ATTNFUSE_ERR_LOG when it is set.
+
+Backward parity takes no value from the GPU path into the oracle: the forward
+output O and the LSE a backward test hands the kernels come from the oracle's
+own forward (O rounded to the tensor dtype, as a forward stores it), and the
+oracle's backward is given that same O where the kernels use it (dQ; see
+``bwd_refs``).  The definitional tests instead run
+the GPU forward and backward end to end and compare with the oracle's
+gradients of the exact function (no O given).
 """
+import json
+import os
 import sys
 
 import numpy as np
@@ -47,10 +59,52 @@ BF16_HALF_ULP = 2.0 ** -8   # bf16 unit roundoff
 BF16_QUARTER_ULP = 2.0 ** -9   # mean bf16 rounding error of a value, relative, at most
 
 
+def report(what, err, ref, flat_max, flat_mean):
+    """Print (and log) one check's errors against the flat stated bounds."""
+    mx = float(err.max()) if err.size else 0.0
+    mn = float(err.mean()) if err.size else 0.0
+    rmax = float(np.abs(ref).max()) if err.size else 0.0
+    ok = lambda x, t: "ok" if x <= t else "over"
+    print(f"[err] {what}: max-abs {mx:.3e} (flat {flat_max:g} {ok(mx, flat_max)}), mean-abs {mn:.3e} "
+          f"(flat {flat_mean:g} {ok(mn, flat_mean)}), max|ref| {rmax:.3g}", flush=True)
+    path = os.environ.get("ATTNFUSE_ERR_LOG")
+    if path:
+        rec = {"test": os.environ.get("PYTEST_CURRENT_TEST", "").split(" ")[0], "what": what, "max_abs": mx,
+               "mean_abs": mn, "max_ref": rmax, "flat_max": flat_max, "flat_mean": flat_mean}
+        with open(path, "a") as f:
+            f.write(json.dumps(rec) + "\n")
+    return mx, mn
+
+
+def given_o(O, dtype="bf16"):
+    """The oracle's forward output as a forward of ``dtype`` stores it: the
+    rounded values as the fp64 array the oracle's backward takes (``o=``) and
+    as a device tensor for the kernels."""
+    t = torch.from_numpy(np.ascontiguousarray(O)).to(torch.bfloat16 if dtype == "bf16" else torch.float32)
+    return t.to(torch.float64).numpy(), t.cuda()
+
+
+def bwd_refs(backward, o_ref):
+    """The oracle gradients a bf16 backward handed the forward output o_ref is
+    held to: dQ with the row term delta from o_ref (the dQ pass forms it from
+    the O it is given), dK and dV with the definitional delta = sum_j P_ij
+    dP_ij (the dK/dV pass uses the dQ pass's own sum).  ``backward(o)`` runs
+    the oracle's backward with that ``o`` (None: the definition)."""
+    given = backward(o_ref)
+    exact = backward(None)
+    return given[0], exact[1], exact[2]
+
+
+def given_lse(L):
+    """The oracle's LSE as the fp32 device tensor a forward stores."""
+    return torch.from_numpy(np.ascontiguousarray(L)).to(torch.float32).cuda()
+
+
 def assert_bf16_close(gpu, ref, what, max_tol=BF16_MAX, mean_tol=BF16_MEAN):
     g = f64(gpu) if isinstance(gpu, torch.Tensor) else gpu
     err = np.abs(g - ref)
     assert np.isfinite(g).all(), f"{what}: non-finite values"
+    report(what, err, ref, max_tol, mean_tol)
     excess = err - (max_tol + BF16_HALF_ULP * np.abs(ref))
     i = np.unravel_index(np.argmax(excess), err.shape) if err.size else None
     assert err.size == 0 or excess.max() <= 0, \
@@ -70,6 +124,7 @@ def bf16_round(x):
 def assert_fp32_close(gpu, ref, what, tol=FP32_MAX):
     g = f64(gpu) if isinstance(gpu, torch.Tensor) else gpu
     err = np.abs(g - ref)
+    report(what, err, ref, tol, tol)
     assert err.max() <= tol, f"{what}: max-abs {err.max():.3e} > {tol}"
     return float(err.max())
 
@@ -79,4 +134,5 @@ def assert_lse_close(gpu, ref, what, tol=LSE_MAX):
     assert np.array_equal(np.isneginf(g), np.isneginf(ref)), f"{what}: -inf pattern differs"
     fin = np.isfinite(ref)
     err = np.abs(g[fin] - ref[fin])
+    report(what, err, ref[fin], tol, tol)
     assert err.size == 0 or err.max() <= tol, f"{what}: LSE max-abs {err.max():.3e} > {tol}"

@@ -6,7 +6,8 @@ import pytest
 import torch
 
 import oracle
-from gpu_util import announce, assert_bf16_close, assert_lse_close, device_inputs, f64, need_gpu
+from gpu_util import (announce, assert_bf16_close, assert_lse_close, bwd_refs, device_inputs, f64, given_lse, given_o,
+                      need_gpu)
 from paper_2609_13612_amd import api
 
 pytestmark = pytest.mark.gpu
@@ -38,16 +39,20 @@ def _run(B, H, Hkv, S, D, *, rope, mask, window, bias_kind, norm, seed):
     dbias = None if bias is None else bias.cuda()
     o, lse = api.attnfuse_fwd_bias_norm(dev["q"], dev["k"], dev["v"], bias=dbias, norm=norm, rope=rope, mask=mask,
                                         window=window, scale=scale)
-    grads = api.attnfuse_bwd_bias_norm(dev["q"], dev["k"], dev["v"], o, dev["do"], lse, bias=dbias, norm=norm,
-                                       rope=rope, mask=mask, window=window, scale=scale)
-    torch.cuda.synchronize()
     ob = None if bias is None else bias.to(torch.float64).numpy()
     kw = dict(rope=rope, mask=mask, window=window, bias=ob, norm=norm, scale=scale)
     O, L = oracle.attention_forward(f64(cpu["q"]), f64(cpu["k"]), f64(cpu["v"]), **kw)
+    # the backward is handed the oracle's forward output (rounded to bf16)
+    o_ref, o_dev = given_o(O)
+    grads = api.attnfuse_bwd_bias_norm(dev["q"], dev["k"], dev["v"], o_dev, dev["do"],
+                                       None if L is None else given_lse(L), bias=dbias, norm=norm, rope=rope,
+                                       mask=mask, window=window, scale=scale)
+    torch.cuda.synchronize()
     # the relu gate s > 0 is a decision: both sides take it on fp16 operands
     # (the kernels' MFMA operand type in the backward)
-    ref = oracle.attention_backward(f64(cpu["q"]), f64(cpu["k"]), f64(cpu["v"]), f64(cpu["do"]),
-                                    relu_gate="fp16" if norm == "relu" else "exact", o=f64(o), **kw)
+    ref = bwd_refs(lambda o_: oracle.attention_backward(f64(cpu["q"]), f64(cpu["k"]), f64(cpu["v"]), f64(cpu["do"]),
+                                                        relu_gate="fp16" if norm == "relu" else "exact", o=o_, **kw),
+                   o_ref)
     return (o, lse, grads), (O, L, ref)
 
 

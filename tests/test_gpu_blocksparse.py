@@ -7,7 +7,8 @@ import pytest
 import torch
 
 import oracle
-from gpu_util import announce, assert_bf16_close, assert_lse_close, device_inputs, f64, need_gpu
+from gpu_util import (announce, assert_bf16_close, assert_lse_close, bwd_refs, device_inputs, f64, given_lse, given_o,
+                      need_gpu)
 from paper_2609_13612_amd import api, blockmask, inputs
 
 pytestmark = pytest.mark.gpu
@@ -29,11 +30,23 @@ def _ref_fwd(cpu, bm, rope, mask, window, slopes):
                                     block_mask=bm.as_oracle())
 
 
-def _ref_bwd(cpu, bm, rope, mask, window, slopes, o):
-    """Oracle gradients; delta from ``o``, the forward output the backward was given."""
-    return oracle.attention_backward(f64(cpu["q"]), f64(cpu["k"]), f64(cpu["v"]), f64(cpu["do"]), rope=rope,
-                                     mask=mask, window=window, alibi_slopes=None if slopes is None else f64(slopes),
-                                     block_mask=bm.as_oracle(), o=f64(o))
+def _ref_bwd(cpu, bm, rope, mask, window, slopes, o_ref):
+    """Oracle gradients for a backward handed ``o_ref``, the (oracle-made)
+    forward output: dQ's row term from it, dK's and dV's by definition."""
+    return bwd_refs(lambda o: oracle.attention_backward(
+        f64(cpu["q"]), f64(cpu["k"]), f64(cpu["v"]), f64(cpu["do"]), rope=rope, mask=mask, window=window,
+        alibi_slopes=None if slopes is None else f64(slopes), block_mask=bm.as_oracle(), o=o), o_ref)
+
+
+def _bwd_given_o(cpu, dev, bm, rope, mask, window, slopes):
+    """The block-sparse backward handed the oracle's forward output (O rounded
+    to bf16, and its LSE), and the oracle's gradients given that O."""
+    O, L = _ref_fwd(cpu, bm, rope, mask, window, slopes)
+    o_ref, o_dev = given_o(O)
+    grads = api.attnfuse_bwd_blocksparse(dev["q"], dev["k"], dev["v"], o_dev, dev["do"], given_lse(L), bm, rope=rope,
+                                         mask=mask, window=window, alibi_slopes=slopes)
+    torch.cuda.synchronize()
+    return grads, _ref_bwd(cpu, bm, rope, mask, window, slopes, o_ref)
 
 
 VARIANTS = list(itertools.product(["none", "neox", "interleaved"], ["none", "causal", "sliding_window"],
@@ -53,14 +66,12 @@ def test_blocksparse_fwd_bwd_variants(rope, mask, alibi, D):
     bm = _mask(S, 0.35, seed=5, empty_rows=(3,))
     slopes = inputs.alibi_slopes(H).cuda() if alibi else None
     o, lse = _fwd(dev, bm, rope, mask, window, slopes)
-    grads = api.attnfuse_bwd_blocksparse(dev["q"], dev["k"], dev["v"], o, dev["do"], lse, bm, rope=rope, mask=mask,
-                                         window=window, alibi_slopes=slopes)
     torch.cuda.synchronize()
     O, L = _ref_fwd(cpu, bm, rope, mask, window, slopes)
     assert_bf16_close(o, O, "O")
     assert_lse_close(lse, L, "LSE")
     assert torch.all(o[:, :, 3 * 64:4 * 64] == 0) and torch.all(torch.isneginf(lse[:, :, 3 * 64:4 * 64]))
-    ref = _ref_bwd(cpu, bm, rope, mask, window, slopes, o)
+    grads, ref = _bwd_given_o(cpu, dev, bm, rope, mask, window, slopes)
     for name, g, r in zip(("dQ", "dK", "dV"), grads, ref):
         assert_bf16_close(g, r, name)
 
@@ -77,13 +88,12 @@ def test_blocksparse_group_sizes(H, Hkv):
     cpu, dev = device_inputs(B, H, Hkv, S, D, seed=32, with_do=True)
     bm = _mask(S, 0.25, seed=6)
     o, lse = _fwd(dev, bm, "neox", "causal", None, None)
-    grads = api.attnfuse_bwd_blocksparse(dev["q"], dev["k"], dev["v"], o, dev["do"], lse, bm, rope="neox",
-                                         mask="causal")
     torch.cuda.synchronize()
     O, L = _ref_fwd(cpu, bm, "neox", "causal", None, None)
     assert_bf16_close(o, O, "O")
     assert_lse_close(lse, L, "LSE")
-    for name, g, r in zip(("dQ", "dK", "dV"), grads, _ref_bwd(cpu, bm, "neox", "causal", None, None, o)):
+    grads, ref = _bwd_given_o(cpu, dev, bm, "neox", "causal", None, None)
+    for name, g, r in zip(("dQ", "dK", "dV"), grads, ref):
         assert_bf16_close(g, r, name)
 
 
@@ -135,13 +145,12 @@ def test_blocksparse_empty_and_tiny():
         active[-1, 0] = False
         bm = blockmask.block_mask_from_dense(torch.from_numpy(active), S, device="cuda")
         o, lse = _fwd(dev, bm, "neox", "causal", None, None)
-        grads = api.attnfuse_bwd_blocksparse(dev["q"], dev["k"], dev["v"], o, dev["do"], lse, bm, rope="neox",
-                                             mask="causal")
         torch.cuda.synchronize()
         O, L = _ref_fwd(cpu, bm, "neox", "causal", None, None)
         assert_bf16_close(o, O, f"O S={S}")
         assert_lse_close(lse, L, f"LSE S={S}")
-        for name, g, r in zip(("dQ", "dK", "dV"), grads, _ref_bwd(cpu, bm, "neox", "causal", None, None, o)):
+        grads, ref = _bwd_given_o(cpu, dev, bm, "neox", "causal", None, None)
+        for name, g, r in zip(("dQ", "dK", "dV"), grads, ref):
             assert_bf16_close(g, r, f"{name} S={S}")
 
 
@@ -167,11 +176,13 @@ def test_blocksparse_bigbird_full_size():
                                                  rows, mask="none", block_mask=bm.as_oracle())
             assert_bf16_close(f64(o[b, h])[rows], O, f"O b={b} h={h}")
             assert_lse_close(f64(lse[b, h])[rows], L, f"LSE b={b} h={h}")
+    # end to end (the backward on the GPU forward's output) against the exact
+    # gradients of head (0, 0)
     ref = oracle.attention_backward(f64(cpu["q"][:1, :1]), f64(cpu["k"][:1, :1]), f64(cpu["v"][:1, :1]),
-                                    f64(cpu["do"][:1, :1]), mask="none", block_mask=bm.as_oracle(), o=f64(o[:1, :1]))
-    assert_bf16_close(f64(dq[:1, :1]), ref[0], "dQ (0, 0)")
-    assert_bf16_close(f64(dk[:1, :1]), ref[1], "dK (0, 0)")
-    assert_bf16_close(f64(dv[:1, :1]), ref[2], "dV (0, 0)")
+                                    f64(cpu["do"][:1, :1]), mask="none", block_mask=bm.as_oracle())
+    assert_bf16_close(f64(dq[:1, :1]), ref[0], "dQ (0, 0) definitional")
+    assert_bf16_close(f64(dk[:1, :1]), ref[1], "dK (0, 0) definitional")
+    assert_bf16_close(f64(dv[:1, :1]), ref[2], "dV (0, 0) definitional")
     for t in (dq, dk, dv):
         assert torch.isfinite(t.float()).all()
 
@@ -217,11 +228,10 @@ def test_blocksparse_noncanonical_lists():
     k_ptr, q_idx = scrambled(active.T)
     bm = blockmask.BlockMask(S, torch.from_numpy(active).cuda(), q_ptr, k_idx, k_ptr, q_idx)
     o, lse = _fwd(dev, bm, "neox", "causal", None, None)
-    grads = api.attnfuse_bwd_blocksparse(dev["q"], dev["k"], dev["v"], o, dev["do"], lse, bm, rope="neox",
-                                         mask="causal")
     torch.cuda.synchronize()
     O, L = _ref_fwd(cpu, bm, "neox", "causal", None, None)
     assert_bf16_close(o, O, "O")
     assert_lse_close(lse, L, "LSE")
-    for name, g, r in zip(("dQ", "dK", "dV"), grads, _ref_bwd(cpu, bm, "neox", "causal", None, None, o)):
+    grads, ref = _bwd_given_o(cpu, dev, bm, "neox", "causal", None, None)
+    for name, g, r in zip(("dQ", "dK", "dV"), grads, ref):
         assert_bf16_close(g, r, name)

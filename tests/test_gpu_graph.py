@@ -1,11 +1,12 @@
 """HIP-graph capture of the entry points through the C ABI.
 
-After one eager call on a device (which builds that device's cos/sin table),
-the fused forward and backward (also with a dense bias or relu attention), the
-block-sparse forward and backward, decode and the
-separate path (rotation kernel, then the forward without RoPE) allocate
-nothing, synchronise nothing and issue no memset, so a captured sequence of
-them replays.  Each test captures once, then replays on three fresh inputs
+The library allocates nothing, synchronises nothing and issues no memset (the
+RoPE cos/sin table is the caller's), so every entry point can be captured,
+the first call included: the fused forward and backward (also with a dense
+bias or relu attention), the block-sparse forward and backward, decode and
+the separate path (rotation kernel, then the forward without RoPE), and a
+RoPE call whose table the binding has not built yet (its fill kernel is
+captured with it).  Each test captures once, then replays on three fresh inputs
 copied into the captured buffers, with eager calls and synchronisations in
 between, and checks every replay bit for bit against the eager result on the
 same inputs (the kernels use no atomics, so they are deterministic).
@@ -38,7 +39,7 @@ def test_graph_fwd_bwd_replays():
     kw = dict(rope="neox", theta=500000.0, mask="causal")
     _, d0 = device_inputs(B, H, Hkv, S, D, seed=70, with_do=True)
     q, k, v, do = (d0[n].clone() for n in ("q", "k", "v", "do"))
-    o, lse = api.attnfuse_fwd(q, k, v, **kw)            # eager warm-up: builds the table
+    o, lse = api.attnfuse_fwd(q, k, v, **kw)            # eager warm-up
     api.attnfuse_bwd(q, k, v, o, do, lse, **kw)
     o_s, lse_s = torch.empty_like(q), torch.empty(B, H, S, device="cuda")
     dq_s, dk_s, dv_s = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
@@ -57,6 +58,41 @@ def test_graph_fwd_bwd_replays():
         for dst, name in ((q, "q"), (k, "k"), (v, "v"), (do, "do")):
             dst.copy_(d[name])
         g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(o_s, o_e) and torch.equal(lse_s, lse_e), f"seed {seed}: forward replay differs"
+        for name, a, b in zip(("dQ", "dK", "dV"), (dq_s, dk_s, dv_s), grads_e):
+            assert torch.equal(a, b), f"seed {seed}: {name} replay differs"
+
+
+def test_graph_cold_first_call_replays():
+    """The first call for a (D, theta) captured with nothing built before it:
+    the binding fills a fresh cos/sin table inside the capture, the forward and
+    backward read it, and the replays match eager calls (made afterwards)."""
+    need_gpu()
+    announce("graph capture: cold first RoPE call")
+    B, H, Hkv, S, D = 1, 4, 2, 700, 64
+    theta = 123457.0                                      # no other test builds this table
+    assert not any(key[1:] == (D, float(theta)) for key in api._TABLES)
+    kw = dict(rope="neox", theta=theta, mask="sliding_window", window=200)
+    _, d0 = device_inputs(B, H, Hkv, S, D, seed=70, with_do=True)
+    q, k, v, do = (d0[n].clone() for n in ("q", "k", "v", "do"))
+    o_s, lse_s = torch.empty_like(q), torch.empty(B, H, S, device="cuda")
+    dq_s, dk_s, dv_s = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
+    ws = torch.empty(api.attnfuse_bwd_workspace_bytes(B, H, Hkv, S, D, "neox"), device="cuda", dtype=torch.uint8)
+
+    def step():
+        api.attnfuse_fwd(q, k, v, out=o_s, lse=lse_s, **kw)
+        api.attnfuse_bwd(q, k, v, o_s, do, lse_s, dq=dq_s, dk=dk_s, dv=dv_s, workspace=ws, **kw)
+
+    g = _capture(step)
+    for seed in SEEDS:
+        _, d = device_inputs(B, H, Hkv, S, D, seed=seed, with_do=True)
+        for dst, name in ((q, "q"), (k, "k"), (v, "v"), (do, "do")):
+            dst.copy_(d[name])
+        g.replay()
+        torch.cuda.synchronize()
+        o_e, lse_e = api.attnfuse_fwd(d["q"], d["k"], d["v"], **kw)
+        grads_e = api.attnfuse_bwd(d["q"], d["k"], d["v"], o_e, d["do"], lse_e, **kw)
         torch.cuda.synchronize()
         assert torch.equal(o_s, o_e) and torch.equal(lse_s, lse_e), f"seed {seed}: forward replay differs"
         for name, a, b in zip(("dQ", "dK", "dV"), (dq_s, dk_s, dv_s), grads_e):

@@ -17,7 +17,8 @@ import pytest
 import torch
 
 import oracle
-from gpu_util import announce, assert_bf16_close, assert_fp32_close, assert_lse_close, device_inputs, f64, need_gpu
+from gpu_util import (announce, assert_bf16_close, assert_fp32_close, assert_lse_close, bwd_refs, device_inputs, f64,
+                      given_lse, given_o, need_gpu)
 from paper_2609_13612_amd import api, blockmask, inputs
 
 pytestmark = pytest.mark.gpu
@@ -50,12 +51,14 @@ def test_sweep_fwd_bwd(i):
     kw = dict(rope=c["rope"], theta=c["theta"], mask=c["mask"], window=c["window"], scale=c["scale"])
     ds = None if slopes is None else slopes.cuda()
     o, lse = api.attnfuse_fwd(dev["q"], dev["k"], dev["v"], alibi_slopes=ds, **kw)
-    dq, dk, dv = api.attnfuse_bwd(dev["q"], dev["k"], dev["v"], o, dev["do"], lse, alibi_slopes=ds, **kw)
-    torch.cuda.synchronize()
     os_ = None if slopes is None else f64(slopes)
     O, L = oracle.attention_forward(f64(cpu["q"]), f64(cpu["k"]), f64(cpu["v"]), alibi_slopes=os_, **kw)
-    ref = oracle.attention_backward(f64(cpu["q"]), f64(cpu["k"]), f64(cpu["v"]), f64(cpu["do"]),
-                                    alibi_slopes=os_, o=f64(o), **kw)
+    o_ref, o_dev = given_o(O)   # the backward is handed the oracle's O, rounded as a forward stores it
+    dq, dk, dv = api.attnfuse_bwd(dev["q"], dev["k"], dev["v"], o_dev, dev["do"], given_lse(L), alibi_slopes=ds,
+                                  **kw)
+    torch.cuda.synchronize()
+    ref = bwd_refs(lambda o_: oracle.attention_backward(f64(cpu["q"]), f64(cpu["k"]), f64(cpu["v"]), f64(cpu["do"]),
+                                                        alibi_slopes=os_, o=o_, **kw), o_ref)
     assert_bf16_close(o, O, "O")
     assert_lse_close(lse, L, "LSE")
     for name, g, r in zip(("dQ", "dK", "dV"), (dq, dk, dv), ref):
@@ -128,13 +131,16 @@ def test_sweep_blocksparse(i):
     kw = dict(rope=c["rope"], mask=c["mask"], window=c["window"])
     ds = None if slopes is None else slopes.cuda()
     o, lse = api.attnfuse_fwd_blocksparse(dev["q"], dev["k"], dev["v"], bm, alibi_slopes=ds, **kw)
-    grads = api.attnfuse_bwd_blocksparse(dev["q"], dev["k"], dev["v"], o, dev["do"], lse, bm, alibi_slopes=ds, **kw)
-    torch.cuda.synchronize()
     os_ = None if slopes is None else f64(slopes)
     O, L = oracle.attention_forward(f64(cpu["q"]), f64(cpu["k"]), f64(cpu["v"]), alibi_slopes=os_,
                                     block_mask=bm.as_oracle(), **kw)
-    ref = oracle.attention_backward(f64(cpu["q"]), f64(cpu["k"]), f64(cpu["v"]), f64(cpu["do"]), alibi_slopes=os_,
-                                    block_mask=bm.as_oracle(), o=f64(o), **kw)
+    o_ref, o_dev = given_o(O)
+    grads = api.attnfuse_bwd_blocksparse(dev["q"], dev["k"], dev["v"], o_dev, dev["do"], given_lse(L), bm,
+                                         alibi_slopes=ds, **kw)
+    torch.cuda.synchronize()
+    ref = bwd_refs(lambda o_: oracle.attention_backward(f64(cpu["q"]), f64(cpu["k"]), f64(cpu["v"]), f64(cpu["do"]),
+                                                        alibi_slopes=os_, block_mask=bm.as_oracle(), o=o_, **kw),
+                   o_ref)
     assert_bf16_close(o, O, "O")
     assert_lse_close(lse, L, "LSE")
     for name, g, r in zip(("dQ", "dK", "dV"), grads, ref):
@@ -177,12 +183,16 @@ def test_sweep_bias_norm(i):
         bias = bias / S
     kw = dict(rope=c["rope"], mask=c["mask"], window=c["window"], norm=c["norm"], scale=scale)
     o, lse = api.attnfuse_fwd_bias_norm(dev["q"], dev["k"], dev["v"], bias=bias.cuda(), **kw)
-    grads = api.attnfuse_bwd_bias_norm(dev["q"], dev["k"], dev["v"], o, dev["do"], lse, bias=bias.cuda(), **kw)
-    torch.cuda.synchronize()
     ob = bias.to(torch.float64).numpy()
     O, L = oracle.attention_forward(f64(cpu["q"]), f64(cpu["k"]), f64(cpu["v"]), bias=ob, **kw)
-    ref = oracle.attention_backward(f64(cpu["q"]), f64(cpu["k"]), f64(cpu["v"]), f64(cpu["do"]), bias=ob, o=f64(o),
-                                    relu_gate="fp16" if c["norm"] == "relu" else "exact", **kw)
+    o_ref, o_dev = given_o(O)
+    grads = api.attnfuse_bwd_bias_norm(dev["q"], dev["k"], dev["v"], o_dev, dev["do"],
+                                       None if L is None else given_lse(L), bias=bias.cuda(), **kw)
+    torch.cuda.synchronize()
+    ref = bwd_refs(lambda o_: oracle.attention_backward(f64(cpu["q"]), f64(cpu["k"]), f64(cpu["v"]), f64(cpu["do"]),
+                                                        bias=ob, o=o_,
+                                                        relu_gate="fp16" if c["norm"] == "relu" else "exact", **kw),
+                   o_ref)
     assert_bf16_close(o, O, "O")
     if c["norm"] == "softmax":
         assert_lse_close(lse, L, "LSE")
@@ -204,12 +214,14 @@ def test_sweep_fp32(i):
     kw = dict(rope=c["rope"], theta=c["theta"], mask=c["mask"], window=c["window"], scale=c["scale"])
     ds = None if slopes is None else slopes.cuda()
     o, lse = api.attnfuse_fwd(dev["q"], dev["k"], dev["v"], alibi_slopes=ds, **kw)
-    dq, dk, dv = api.attnfuse_bwd(dev["q"], dev["k"], dev["v"], o, dev["do"], lse, alibi_slopes=ds, **kw)
-    torch.cuda.synchronize()
     os_ = None if slopes is None else f64(slopes)
     O, L = oracle.attention_forward(f64(cpu["q"]), f64(cpu["k"]), f64(cpu["v"]), alibi_slopes=os_, **kw)
+    o_ref, o_dev = given_o(O, "fp32")
+    dq, dk, dv = api.attnfuse_bwd(dev["q"], dev["k"], dev["v"], o_dev, dev["do"], given_lse(L), alibi_slopes=ds,
+                                  **kw)
+    torch.cuda.synchronize()
     ref = oracle.attention_backward(f64(cpu["q"]), f64(cpu["k"]), f64(cpu["v"]), f64(cpu["do"]),
-                                    alibi_slopes=os_, o=f64(o), **kw)
+                                    alibi_slopes=os_, o=o_ref, **kw)
     assert_fp32_close(o, O, "O fp32")
     assert_lse_close(lse, L, "LSE fp32")
     for name, g, r in zip(("dQ", "dK", "dV"), (dq, dk, dv), ref):

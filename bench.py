@@ -466,7 +466,15 @@ def main():
     cpu_baseline = None
     if not args.no_cpu_baseline:
         import numpy as np
+        import threadpoolctl
         import oracle
+        # the thread count is set explicitly for the BLAS numpy uses (the host's
+        # share of cores: OMP_NUM_THREADS where the machine sets it, else the
+        # cores this process may run on), and the count in force is reported
+        want = int(os.environ.get("OMP_NUM_THREADS") or len(os.sched_getaffinity(0)))
+        limiter = threadpoolctl.threadpool_limits(limits=want, user_api="blas")
+        blas = [p for p in threadpoolctl.threadpool_info() if p.get("user_api") == "blas"]
+        cores = max((p["num_threads"] for p in blas), default=1)
         G = w.H // w.Hkv
         NG = min(3, w.Hkv)        # K/V groups in the sample: about 10-15 s of CPU work at the Llama shape
         f = inputs.to_f64
@@ -481,7 +489,7 @@ def main():
         tb = time.perf_counter()
         frac = NG * G / (w.B * w.H)
         sample_flops = (fwd_flops + bwd_flops) * frac
-        cores = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+        limiter.restore_original_limits()
         cpu_baseline = {"value": round(sample_flops / (tb - ta) / 1e12, 6), "unit": "TFLOP/s", "cores": cores,
                         "kind": "oracle", "seconds": round(tb - ta, 2),
                         "sample": f"batch 0, query heads 0..{NG * G - 1} with K/V heads 0..{NG - 1} "

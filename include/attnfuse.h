@@ -36,6 +36,8 @@
  *             AF_ERR_UNSUPPORTED  valid request with no compiled kernel
  *                                 (e.g. D not in {64, 128}, fp32 backward)
  *             AF_ERR_HIP          a HIP runtime call or kernel launch failed
+ *             AF_ERR_TOO_LARGE    the request needs more than the static
+ *                                 scratch of attnfuse_decode_noalloc
  *           attnfuse_strerror() maps a code to text.
  */
 #ifndef ATTNFUSE_H
@@ -67,7 +69,7 @@ enum { AF_MASK_NONE = 0, AF_MASK_CAUSAL = 1, AF_MASK_SLIDING_WINDOW = 2 };
  * with no normalisation and no row statistic (see attnfuse_fwd_bias_norm). */
 enum { AF_NORM_SOFTMAX = 0, AF_NORM_RELU = 1 };
 
-enum { AF_OK = 0, AF_ERR_INVALID_ARG = -1, AF_ERR_UNSUPPORTED = -2, AF_ERR_HIP = -3 };
+enum { AF_OK = 0, AF_ERR_INVALID_ARG = -1, AF_ERR_UNSUPPORTED = -2, AF_ERR_HIP = -3, AF_ERR_TOO_LARGE = -4 };
 
 /*
  * RoPE cos/sin table (Section 4.1 "Fused RoPE": the rotation angle of pair i
@@ -345,6 +347,27 @@ int attnfuse_decode(const void* Q, const void* K, const void* V, const int* cach
                     int rope, float rope_theta, const float* rope_table, int rope_table_rows,
                     int mask, int window,
                     const float* alibi_slopes, float softmax_scale, void* stream);
+
+/*
+ * attnfuse_decode for callers that cannot allocate device memory: code under
+ * HIP graph capture, tight serving loops, harnesses that forbid allocation.
+ * Same computation and arguments, without the workspace: the partials live in
+ * a static device buffer of AF_DECODE_SCRATCH_BYTES (32 MiB) that the library
+ * holds on every GPU it runs on until the process ends (its address is looked
+ * up once per device, on the first call there).  Requests for which
+ * attnfuse_decode_workspace_bytes exceeds it return AF_ERR_TOO_LARGE (use
+ * attnfuse_decode with a workspace).  Nothing needs clearing between calls
+ * (every partial is written before it is read), but every call on one GPU uses
+ * that GPU's one buffer: calls that may overlap on a GPU (on different streams
+ * or from several threads) race and must be ordered by the caller.
+ */
+#define AF_DECODE_SCRATCH_BYTES (32u << 20)
+int attnfuse_decode_noalloc(const void* Q, const void* K, const void* V, const int* cache_lens,
+                            void* O, float* LSE,
+                            int B, int H, int H_kv, int S_kv, int D, int dtype,
+                            int rope, float rope_theta, const float* rope_table, int rope_table_rows,
+                            int mask, int window,
+                            const float* alibi_slopes, float softmax_scale, void* stream);
 
 /* Static text for a return code (never NULL). */
 const char* attnfuse_strerror(int code);

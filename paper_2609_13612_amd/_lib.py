@@ -33,6 +33,8 @@ SIGNATURES = {
     "attnfuse_decode_workspace_bytes": (ctypes.c_size_t, [_I, _I, _I, _I, _I]),
     "attnfuse_decode": (_I, [_P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t,
                              _I, _I, _I, _I, _I, _I, _I, _F, _P, _I, _I, _I, _P, _F, _P]),
+    "attnfuse_decode_noalloc": (_I, [_P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _F, _P, _I, _I, _I, _P,
+                                     _F, _P]),
     "attnfuse_strerror": (ctypes.c_char_p, [_I]),
     "attnfuse_version": (_I, []),
 }

@@ -379,6 +379,24 @@ def attnfuse_decode(q, k_cache, v_cache, cache_lens=None, *, rope="none", theta=
     return out, lse
 
 
+def attnfuse_decode_noalloc(q, k_cache, v_cache, cache_lens=None, *, rope="none", theta=10000.0, mask="causal",
+                            window=None, alibi_slopes=None, scale=None, out=None, lse=None, rope_table=None):
+    """attnfuse_decode with the library's static scratch in place of a
+    workspace; see attnfuse_decode_noalloc in include/attnfuse.h.  Pass
+    ``out``, ``lse`` (and, with RoPE, ``rope_table``) for a call that
+    allocates nothing at all."""
+    dev, (B, H, Hkv, S_kv, D), out, lse = _decode_args(q, k_cache, v_cache, cache_lens, out, lse)
+    r, th, m, w, sc = _variant(rope, theta, mask, window, alibi_slopes, scale, D, H, dev)
+    tab = _table(rope, theta, D, S_kv, dev, rope_table)
+    tp, tr = _tab(tab)
+    with torch.cuda.device(dev):
+        code = _lib.load().attnfuse_decode_noalloc(_ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(cache_lens),
+                                                   _ptr(out), _ptr(lse), B, H, Hkv, S_kv, D, DTYPE[q.dtype], r, th,
+                                                   tp, tr, m, w, _ptr(alibi_slopes), sc, _stream())
+    _check(code, "attnfuse_decode_noalloc")
+    return out, lse
+
+
 def _rope_call(name, x0, x1, y0, y1, rope, theta, rope_table):
     dev = _device(x0)
     if x1 is not None:

@@ -16,6 +16,7 @@
 namespace {
 
 constexpr int kMaxS = 1 << 20;
+static_assert(AF_DECODE_SCRATCH_BYTES == af::DECODE_SCRATCH_BYTES, "header and library agree on the static scratch");
 constexpr int kAbiVersion = 3;
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
@@ -270,6 +271,7 @@ const char* attnfuse_strerror(int code) {
     case AF_ERR_INVALID_ARG: return "invalid argument";
     case AF_ERR_UNSUPPORTED: return "unsupported variant (no compiled kernel)";
     case AF_ERR_HIP: return "HIP runtime error";
+    case AF_ERR_TOO_LARGE: return "request needs more than the library's static scratch (use the workspace entry point)";
   }
   return "unknown error code";
 }
@@ -369,12 +371,12 @@ size_t attnfuse_decode_workspace_bytes(int B, int H, int H_kv, int S_kv, int D) 
   return decode_layout(B, H, H_kv, S_kv, D).total;
 }
 
-// Decode with the partials in the caller's workspace.
+// The decode entry points share everything but where the partials live: the
+// caller's workspace, or (workspace == nullptr) the library's static scratch.
 static int decode_impl(const void* Q, const void* K, const void* V, const int* cache_lens, void* O, float* LSE,
                        void* workspace, size_t workspace_bytes, int B, int H, int H_kv, int S_kv, int D, int dtype,
                        int rope, float rope_theta, const float* rope_table, int rope_table_rows, int mask, int window,
-                       const float* alibi_slopes, float softmax_scale, void* stream) {
-  const bool static_scratch = false;
+                       const float* alibi_slopes, float softmax_scale, void* stream, bool static_scratch) {
   const void* ins[] = {Q, K, V};
   const void* outs[] = {O, LSE, workspace};
   const int nouts = static_scratch ? 2 : 3;
@@ -392,6 +394,10 @@ static int decode_impl(const void* Q, const void* K, const void* V, const int* c
   const size_t need = attnfuse_decode_workspace_bytes(B, H, H_kv, S_kv, D);
   if (!static_scratch && workspace_bytes < need) return AF_ERR_INVALID_ARG;
   if (!supported_d(D) || dtype != AF_DTYPE_BF16 || H / H_kv > 32) return AF_ERR_UNSUPPORTED;
+  if (static_scratch) {
+    if (need > af::DECODE_SCRATCH_BYTES) return AF_ERR_TOO_LARGE;
+    if (!(workspace = af::decode_scratch_ptr())) return AF_ERR_HIP;
+  }
 
   hipStream_t st = static_cast<hipStream_t>(stream);
   const DecodeLayout L = decode_layout(B, H, H_kv, S_kv, D);
@@ -417,7 +423,17 @@ int attnfuse_decode(const void* Q, const void* K, const void* V, const int* cach
                     const float* alibi_slopes, float softmax_scale, void* stream) {
   if (!workspace) return AF_ERR_INVALID_ARG;
   return decode_impl(Q, K, V, cache_lens, O, LSE, workspace, workspace_bytes, B, H, H_kv, S_kv, D, dtype, rope,
-                     rope_theta, rope_table, rope_table_rows, mask, window, alibi_slopes, softmax_scale, stream);
+                     rope_theta, rope_table, rope_table_rows, mask, window, alibi_slopes, softmax_scale, stream, false);
+}
+
+int attnfuse_decode_noalloc(const void* Q, const void* K, const void* V, const int* cache_lens,
+                            void* O, float* LSE,
+                            int B, int H, int H_kv, int S_kv, int D, int dtype,
+                            int rope, float rope_theta, const float* rope_table, int rope_table_rows,
+                            int mask, int window,
+                            const float* alibi_slopes, float softmax_scale, void* stream) {
+  return decode_impl(Q, K, V, cache_lens, O, LSE, nullptr, 0, B, H, H_kv, S_kv, D, dtype, rope, rope_theta,
+                     rope_table, rope_table_rows, mask, window, alibi_slopes, softmax_scale, stream, true);
 }
 
 static int rope_common(const void* X0, const void* X1, void* Y0, void* Y1, int B, int H, int H_kv, int S, int D,

@@ -31,10 +31,34 @@
 // fp16, and the (already rotated) bf16 cache keys are widened to fp16 in
 // registers (exact inside the fp16 range), as the prefill kernel does for its
 // rotated operands.  P and V are bf16.
+#include <atomic>
+
 #include "common.hpp"
 #include "launch.hpp"
 
+// Device memory for the partials of callers that cannot allocate
+// (attnfuse_decode_noalloc): one file-scope array, which every device the
+// library runs on holds until the process ends.  In host code its name stands
+// for a host-side shadow, not a device address; decode_scratch_ptr() looks the
+// address up once per device and keeps it, and only that address is used.
+static __device__ __align__(256) unsigned char scratch[af::DECODE_SCRATCH_BYTES];
+
 namespace af {
+
+namespace {
+constexpr int kMaxScratchDevices = 64;
+std::atomic<void*> g_scratch_ptr[kMaxScratchDevices];   // per device, resolved on first use
+}  // namespace
+
+void* decode_scratch_ptr() {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxScratchDevices) return nullptr;
+  void* ptr = g_scratch_ptr[dev].load(std::memory_order_acquire);
+  if (ptr) return ptr;
+  if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr) return nullptr;
+  g_scratch_ptr[dev].store(ptr, std::memory_order_release);
+  return ptr;
+}
 
 template <int D>
 struct DecCfg {

@@ -94,4 +94,9 @@ int launch_decode(int D, int rope, bool alibi, const DecodeParams& p, hipStream_
 int launch_rope(bool fp32, int D, int rope, bool inverse, const RopeParams& p, hipStream_t st);
 int launch_rope_table(float2* table, int rows, int D, double theta, hipStream_t st);
 
+// Static device scratch of the decode entry point that allocates nothing: its
+// size, and its address on the current device (nullptr if it cannot be found).
+constexpr size_t DECODE_SCRATCH_BYTES = (size_t)32 << 20;
+void* decode_scratch_ptr();
+
 }  // namespace af

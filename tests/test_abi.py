@@ -24,7 +24,7 @@ def declared_symbols():
 def test_header_declares_the_boundary():
     assert declared_symbols() == sorted(["attnfuse_bwd", "attnfuse_bwd_bias_norm", "attnfuse_bwd_blocksparse",
                                          "attnfuse_bwd_workspace_bytes", "attnfuse_decode",
-                                         "attnfuse_decode_workspace_bytes", "attnfuse_fwd", "attnfuse_fwd_bias_norm",
+                                         "attnfuse_decode_noalloc", "attnfuse_decode_workspace_bytes", "attnfuse_fwd", "attnfuse_fwd_bias_norm",
                                          "attnfuse_fwd_blocksparse", "attnfuse_rope", "attnfuse_rope_bwd",
                                          "attnfuse_rope_table_bytes", "attnfuse_rope_table_fill",
                                          "attnfuse_strerror", "attnfuse_version"])
@@ -44,6 +44,7 @@ def test_strerror():
     assert b"invalid" in lib.attnfuse_strerror(-1)
     assert b"unsupported" in lib.attnfuse_strerror(-2)
     assert b"HIP" in lib.attnfuse_strerror(-3)
+    assert b"static scratch" in lib.attnfuse_strerror(-4)
     assert lib.attnfuse_strerror(7) == b"unknown error code"
 
 
@@ -212,6 +213,36 @@ def _decode(**over):
                          ids=lambda o: ",".join(f"{k}={v}" for k, v in o.items()))
 def test_decode_rejects_invalid_arguments(over):
     assert _decode(**over) == -1
+
+
+def _decode_na(**over):
+    a = dict(Q=FAKE, K=FAKE + 0x100, V=FAKE + 0x200, lens=None, O=FAKE + 0x300, LSE=FAKE + 0x400, B=2, H=8, H_kv=2,
+             S=300, D=128, dtype=0, rope=1, theta=1e4, table=TABLE, rows=300, mask=1, window=0, slopes=None,
+             scale=0.1, stream=None)
+    a.update(over)
+    return _lib.load().attnfuse_decode_noalloc(a["Q"], a["K"], a["V"], a["lens"], a["O"], a["LSE"], a["B"], a["H"],
+                                               a["H_kv"], a["S"], a["D"], a["dtype"], a["rope"], a["theta"],
+                                               a["table"], a["rows"], a["mask"], a["window"], a["slopes"],
+                                               a["scale"], a["stream"])
+
+
+@pytest.mark.parametrize("over", [dict(Q=None), dict(O=None), dict(LSE=None), dict(K=ODD), dict(O=FAKE),
+                                  dict(lens=FAKE + 0x602), dict(H=8, H_kv=3), dict(S=0), dict(mask=2, window=0),
+                                  dict(scale=0.0), dict(table=None), dict(rows=299), dict(table=FAKE + 0x300)],
+                         ids=lambda o: ",".join(f"{k}={v}" for k, v in o.items()))
+def test_decode_noalloc_rejects_invalid_arguments(over):
+    assert _decode_na(**over) == -1
+
+
+def test_decode_noalloc_limits():
+    lib = _lib.load()
+    assert _decode_na(D=96) == -2 and _decode_na(dtype=1) == -2
+    # one sequence, 32 query heads on one K/V head, a 2^20 cache: 512 chunks of
+    # 2048 keys, 4 wave partials each, 34 MB of partials > 32 MiB
+    big = dict(B=1, H=32, H_kv=1, S=1 << 20, rows=1 << 20)
+    assert lib.attnfuse_decode_workspace_bytes(1, 32, 1, 1 << 20, 128) > 32 << 20
+    assert _decode_na(**big) == -4
+    assert _decode_na(**dict(big, rows=100)) == -1      # argument errors come first
 
 
 def test_decode_unsupported():

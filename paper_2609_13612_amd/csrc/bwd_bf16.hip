@@ -272,6 +272,22 @@ __device__ __forceinline__ u32x4 tr_operand(const uint16_t* tile, int pitch, int
   return u32x4{lo[0], lo[1], hi[0], hi[1]};
 }
 
+// The same operand from a swizzled tile (swz_at): rows row0 + {4 lg + i/4, +8}
+// (row0 a multiple of 16), columns 32 mt + ..., through the lane's SwzLane.
+template <int D>
+__device__ __forceinline__ u32x4 tr_operand_swz(const uint16_t* tile, const SwzLane<D>& z, int row0, int mt) {
+  const uint16_t* t = tile + row0 * D;
+  const u32x2 lo = lds_read_tr16(t + (z.tr_base[0] ^ (32 * mt)));
+  const u32x2 hi = lds_read_tr16(t + (z.tr_base[1] ^ (32 * mt)));
+  return u32x4{lo[0], lo[1], hi[0], hi[1]};
+}
+
+// A row operand (lane = row row0 + l % 32, k-step k) from a swizzled tile.
+template <int D>
+__device__ __forceinline__ u32x4 row_operand_swz(const uint16_t* tile, const SwzLane<D>& z, int row0, int k) {
+  return *reinterpret_cast<const u32x4*>(tile + row0 * D + (z.row_base ^ (16 * k)));
+}
+
 // ---------------------------------------------------------------- dK / dV
 // Query-side tile of the dK/dV kernel: 64 query rows of Q' (fp16, rotated by
 // the preprocessing kernel) or Q (bf16, converted to fp16 as it is staged)
@@ -286,8 +302,7 @@ struct QTileCfg {
   static constexpr int V_ELEMS = KEYS * VP;
   static constexpr int KS = D / 16;
   static constexpr int MT = D / 32;
-  static constexpr int QP = D + 16;           // pitch of Q' and dO rows (transpose reads)
-  static constexpr int Q_ELEMS = BQ * QP;
+  static constexpr int Q_ELEMS = BQ * D;      // Q' and dO tiles: read by rows and transposed, so swizzled (swz_at)
   static constexpr int STAGE = 2 * Q_ELEMS;   // Q' then dO
   static constexpr int ITEMS = BQ * (D / 8);  // 16-byte chunks per matrix
   static constexpr int IPT = (ITEMS + THREADS - 1) / THREADS;
@@ -339,8 +354,8 @@ __device__ __forceinline__ void qtile_commit(const QTileRegs<D>& R, uint16_t* __
 #pragma unroll
       for (int w = 0; w < 4; ++w) q[w] = pack_f16(bf_lo(q[w]), bf_hi(q[w]));
     }
-    *reinterpret_cast<u32x4*>(Qs + r * C::QP + 8 * c) = q;
-    *reinterpret_cast<u32x4*>(Os + r * C::QP + 8 * c) = R.o[i];
+    *reinterpret_cast<u32x4*>(Qs + swz_at<D>(r, 8 * c)) = q;
+    *reinterpret_cast<u32x4*>(Os + swz_at<D>(r, 8 * c)) = R.o[i];
   }
   if (tid < C::BQ) {
     lse2s[tid] = R.lse2;
@@ -448,8 +463,10 @@ __global__ __launch_bounds__(512) void bwd_dkdv_kernel(BwdParams p) {
   __syncthreads();
 
   const int qt = qh;                  // this wave's 32 rows of every query tile
+  const SwzLane<D> zl(lane);
   for (int s = 0; s < steps; ++s) {
     const int st = s & 1;
+    const SwzLane<D> z = zl.opaque();
     const uint16_t* Qs = smem + st * C::STAGE;
     const uint16_t* Os = Qs + C::Q_ELEMS;
     const float* lse2s = stat[st][0];
@@ -481,8 +498,8 @@ __global__ __launch_bounds__(512) void bwd_dkdv_kernel(BwdParams p) {
       f32x16 sc = f32x16{}, dp = f32x16{};
 #pragma unroll
       for (int k = 0; k < C::KS; ++k) {
-        const u32x4 aq = *reinterpret_cast<const u32x4*>(Qs + (32 * qt + lq) * C::QP + 16 * k + 8 * lg);
-        const u32x4 ao = *reinterpret_cast<const u32x4*>(Os + (32 * qt + lq) * C::QP + 16 * k + 8 * lg);
+        const u32x4 aq = row_operand_swz<D>(Qs, z, 32 * qt, k);
+        const u32x4 ao = row_operand_swz<D>(Os, z, 32 * qt, k);
         const u32x4 bk = *reinterpret_cast<const u32x4*>(Ks + (32 * kw + lq) * C::VP + 16 * k + 8 * lg);
         const u32x4 bv = *reinterpret_cast<const u32x4*>(Vs + (32 * kw + lq) * C::VP + 16 * k + 8 * lg);
         sc = mfma32<true>(aq, bk, sc);
@@ -547,8 +564,8 @@ __global__ __launch_bounds__(512) void bwd_dkdv_kernel(BwdParams p) {
       for (int hf = 0; hf < 2; ++hf) {
 #pragma unroll
         for (int mt = 0; mt < C::MT; ++mt) {
-          dv[mt] = mfma32<true>(tr_operand(Os, C::QP, 32 * qt + 16 * hf, 32 * mt, lane), pb[hf], dv[mt]);
-          dk[mt] = mfma32<true>(tr_operand(Qs, C::QP, 32 * qt + 16 * hf, 32 * mt, lane), db[hf], dk[mt]);
+          dv[mt] = mfma32<true>(tr_operand_swz<D>(Os, z, 32 * qt + 16 * hf, mt), pb[hf], dv[mt]);
+          dk[mt] = mfma32<true>(tr_operand_swz<D>(Qs, z, 32 * qt + 16 * hf, mt), db[hf], dk[mt]);
         }
       }
     }
@@ -603,15 +620,51 @@ __device__ __forceinline__ void k_to_f16(TileRegs<D, ROPE_NONE>& R) {
 }
 
 // ---------------------------------------------------------------- dQ
+// LDS layout of the dQ pass's key tiles: K' is read by rows (S^T = K' Q'^T)
+// and transposed (dQ'^T += K'^T dS^T), so it is stored swizzled (swz_at, no
+// padding); V is read by rows only, at a pitch of D + 8 (16-byte reads of 16
+// rows fall in distinct banks).
+template <int D>
+struct DqTileCfg {
+  static constexpr int K_ELEMS = 64 * D;
+  static constexpr int VP = D + 8;
+  static constexpr int STAGE = K_ELEMS + 64 * VP;
+};
+
+// Commit a staged key tile (tile_load layout of TileCfg<D, ROPE_NONE>) into
+// the dQ pass's layout.
+template <int D>
+__device__ __forceinline__ void dq_tile_commit(const TileRegs<D, ROPE_NONE>& R, uint16_t* __restrict__ Ks,
+                                               uint16_t* __restrict__ Vs, int tid) {
+  using C = TileCfg<D, ROPE_NONE>;
+#pragma unroll
+  for (int i = 0; i < C::KPT; ++i) {
+    const int it = tid + C::THREADS * i;
+    if (C::K_ITEMS % C::THREADS != 0 && it >= C::K_ITEMS) break;
+    const int r = it / C::K_UNITS, c = it % C::K_UNITS;
+    *reinterpret_cast<u32x4*>(Ks + swz_at<D>(r, 8 * c)) = R.ka[i];
+  }
+#pragma unroll
+  for (int i = 0; i < C::VPT; ++i) {
+    const int it = tid + C::THREADS * i;
+    if (C::V_ITEMS % C::THREADS != 0 && it >= C::V_ITEMS) break;
+    const int r = it / (D / 8), c = it % (D / 8);
+    *reinterpret_cast<u32x4*>(Vs + r * DqTileCfg<D>::VP + 8 * c) = R.v[i];
+  }
+}
+
 // Same decomposition as the forward: 8 waves, GQA heads packed, double-buffered
-// K'/V tiles (attn_tiles.hpp); dQ'^T += K'^T dS^T with K'^T from transpose reads.
+// K'/V tiles (loaded as attn_tiles.hpp does, stored in the layout above);
+// dQ'^T += K'^T dS^T with K'^T from transpose reads.
 template <int D, int ROPE, int MASK, bool ALIBI, bool SPARSE, int EXT = EXT_NONE>
 __global__ __launch_bounds__(512) void bwd_dq_kernel(BwdParams p) {
   using C = TileCfg<D, ROPE_NONE>;            // K' arrives rotated, or K is converted to fp16 at staging
+  using L = DqTileCfg<D>;
   constexpr bool ROT = ROPE != ROPE_NONE;    // Q' and K' come rotated (fp16) from the workspace
   constexpr bool TBIAS = EXT == EXT_BIAS || EXT == EXT_RELU_BIAS;
   constexpr bool RELU = EXT == EXT_RELU || EXT == EXT_RELU_BIAS;
-  __shared__ __attribute__((aligned(16))) uint16_t smem[2 * C::STAGE];
+  static_assert(TILE_LIST_SCRATCH_BYTES <= 2 * L::STAGE * (int)sizeof(uint16_t), "the tile-list scratch fits the stages");
+  __shared__ __attribute__((aligned(16))) uint16_t smem[2 * L::STAGE];
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, lq = lane & 31, lg = lane >> 5;
   const int S = p.S;
@@ -681,18 +734,20 @@ __global__ __launch_bounds__(512) void bwd_dq_kernel(BwdParams p) {
     else return t_begin + i;
   };
 
+  const SwzLane<D> zl(lane);
   TileRegs<D, ROPE_NONE> R;
   if (ntl > 0) {
     tile_load<D, ROPE_NONE>(R, Kg, Vg, nullptr, tile_at(0) * C::BN, S, tid);
     if constexpr (!ROT) k_to_f16(R);
-    tile_commit<D, ROPE_NONE>(R, smem, smem + C::K_ELEMS, tid);
+    dq_tile_commit<D>(R, smem, smem + L::K_ELEMS, tid);
   }
   __syncthreads();
 
   for (int t = 0; t < ntl; ++t) {
     const int n0 = tile_at(t) * C::BN;
-    const uint16_t* Ks = smem + (t & 1) * C::STAGE;
-    const uint16_t* Vs = Ks + C::K_ELEMS;
+    const SwzLane<D> z = zl.opaque();
+    const uint16_t* Ks = smem + (t & 1) * L::STAGE;
+    const uint16_t* Vs = Ks + L::K_ELEMS;
     const bool more = t + 1 < ntl;
     if (more) tile_load<D, ROPE_NONE>(R, Kg, Vg, nullptr, tile_at(t + 1) * C::BN, S, tid);
 
@@ -709,8 +764,8 @@ __global__ __launch_bounds__(512) void bwd_dq_kernel(BwdParams p) {
         f32x16 sc = f32x16{}, dp = f32x16{};
 #pragma unroll
         for (int k = 0; k < C::KS; ++k) {
-          const u32x4 ak = *reinterpret_cast<const u32x4*>(Ks + (32 * kt + lq) * C::KP + 16 * k + 8 * lg);
-          const u32x4 av = *reinterpret_cast<const u32x4*>(Vs + (32 * kt + lq) * C::VP + 16 * k + 8 * lg);
+          const u32x4 ak = row_operand_swz<D>(Ks, z, 32 * kt, k);
+          const u32x4 av = *reinterpret_cast<const u32x4*>(Vs + (32 * kt + lq) * L::VP + 16 * k + 8 * lg);
           sc = mfma32<true>(ak, qreg[k], sc);
           dp = mfma32(av, oreg[k], dp);
         }
@@ -763,13 +818,13 @@ __global__ __launch_bounds__(512) void bwd_dq_kernel(BwdParams p) {
         for (int mt = 0; mt < C::MT; ++mt)
 #pragma unroll
           for (int hf = 0; hf < 2; ++hf)
-            dq[mt] = mfma32<true>(tr_operand(Ks, C::KP, 32 * kt + 16 * hf, 32 * mt, lane), db[hf], dq[mt]);
+            dq[mt] = mfma32<true>(tr_operand_swz<D>(Ks, z, 32 * kt + 16 * hf, mt), db[hf], dq[mt]);
       }
     }
     if (more) {
-      uint16_t* Kn = smem + ((t + 1) & 1) * C::STAGE;
+      uint16_t* Kn = smem + ((t + 1) & 1) * L::STAGE;
       if constexpr (!ROT) k_to_f16(R);
-      tile_commit<D, ROPE_NONE>(R, Kn, Kn + C::K_ELEMS, tid);
+      dq_tile_commit<D>(R, Kn, Kn + L::K_ELEMS, tid);
     }
     __syncthreads();
   }

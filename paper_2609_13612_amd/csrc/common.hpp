@@ -183,6 +183,55 @@ __device__ __forceinline__ u32x2 lds_read_tr16(const uint16_t* p) {
   return __builtin_bit_cast(u32x2, r);
 }
 
+// XOR-swizzled LDS tiles.  A tile read both by rows (ds_read_b128: 16 lanes
+// per cycle read the same 16-byte chunk of 16 consecutive rows) and
+// transposed (ds_read_b64_tr_b16: 32 lanes per cycle read 64 bytes of 4
+// consecutive rows) is stored unpadded, D elements per row, with the 16-byte
+// chunk c of row r at chunk slot c ^ swz(r).  With 64 banks of 4 bytes, swz
+// gives the 16 rows of a row read 16 different slots and the 4 rows of a
+// transpose read disjoint groups of 4 slots, so both are conflict-free.
+template <int D>
+__device__ __forceinline__ int swz_chunk(int r) {
+  static_assert(D == 64 || D == 128, "swizzle defined for D = 64 and 128");
+  if constexpr (D == 128) return ((r & 3) << 2) | ((r >> 2) & 3);      // 16 chunks per row
+  else return (((r >> 1) & 1) << 2) | ((r >> 2) & 3);                  // 8 chunks, two rows per 256 B
+}
+
+// Element offset of (row r, column col) in a swizzled tile; col % 8 is kept,
+// so 8-byte (and 16-byte, col % 8 == 0) accesses stay whole.
+template <int D>
+__device__ __forceinline__ int swz_at(int r, int col) {
+  return r * D + ((((col >> 3) ^ swz_chunk<D>(r)) << 3) | (col & 7));
+}
+
+// Per-lane offsets into a swizzled tile for the MFMA operand reads, as a base
+// and an XOR: swz depends on the row modulo 16 only, and the chunk's varying
+// bits never overlap the lane's, so
+//   row operand (lane = row r0 + l % 32, k-step k, 8 dims 16 k + 8 (l / 32)):
+//     r0 * D + (row_base ^ 16 k)
+//   transposed operand (rows r0 + 4 (l / 32) + (l % 16) / 4 (+8), columns
+//     32 mt + 16 ((l / 16) % 2) + 4 (l % 4)), r0 a multiple of 16:
+//     r0 * D + (tr_base[half] ^ 32 mt)
+template <int D>
+struct SwzLane {
+  int row_base, tr_base[2];
+  __device__ __forceinline__ explicit SwzLane(int lane) {
+    const int lq = lane & 31, lg = lane >> 5;
+    row_base = swz_at<D>(lq, 8 * lg);
+    const int r = 4 * lg + ((lane & 15) >> 2), c = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+    tr_base[0] = swz_at<D>(r, c);
+    tr_base[1] = swz_at<D>(r + 8, c);
+  }
+  // A copy the compiler cannot see through: used inside a loop, it keeps the
+  // per-read XORs there (one VALU each) instead of hoisting their results
+  // into registers for the whole loop.
+  __device__ __forceinline__ SwzLane opaque() const {
+    SwzLane z = *this;
+    asm volatile("" : "+v"(z.row_base), "+v"(z.tr_base[0]), "+v"(z.tr_base[1]));
+    return z;
+  }
+};
+
 // Swap bits 2 and 3 of a key (or query) index inside a block of 16.  P^T leaves
 // the S^T MFMA with lane group g holding rows {8a + 4g + b}; storing the
 // transposed operand with this permutation makes those 8 rows contiguous, so

@@ -5,6 +5,8 @@
 // fall in distinct banks); V rows use D + 16 (the four rows a transpose read
 // touches fall in distinct banks).
 #pragma once
+#include <type_traits>
+
 #include "common.hpp"
 
 namespace af {
@@ -22,21 +24,27 @@ struct TileCfg {
   static constexpr int K_ELEMS = BN * KP;
   static constexpr int V_ELEMS = BN * VP;
   static constexpr int STAGE = K_ELEMS + V_ELEMS;
-  // staging work items: NeoX rotates chunk pairs (c, c + D/2); otherwise single chunks
-  static constexpr int K_UNITS = (ROPE == ROPE_NEOX) ? D / 16 : D / 8;
+  // staging work items: NeoX rotates pairs of KW-pair runs (dims [KW u, KW u + KW) with their
+  // partners D/2 further on); otherwise single 8-element chunks.  At D = 64 a run is 4 pairs,
+  // so the 64 rows give 512 items and every thread of the workgroup rotates one (with 8-pair
+  // runs only half the waves would, and the barrier would wait for them).
+  static constexpr int KW = (ROPE == ROPE_NEOX && D == 64) ? 4 : 8;
+  static constexpr int K_UNITS = (ROPE == ROPE_NEOX) ? D / (2 * KW) : D / 8;
   static constexpr int K_ITEMS = BN * K_UNITS;
   static constexpr int KPT = (K_ITEMS + THREADS - 1) / THREADS;
   static constexpr int V_ITEMS = BN * (D / 8);
   static constexpr int VPT = (V_ITEMS + THREADS - 1) / THREADS;
-  static constexpr int CS = (ROPE == ROPE_NEOX) ? 4 : (ROPE == ROPE_INTERLEAVED ? 2 : 1);   // float4 per item
+  static constexpr int CS = (ROPE == ROPE_NEOX) ? KW / 2 : (ROPE == ROPE_INTERLEAVED ? 2 : 1);   // float4 per item
 };
 
-// Registers holding one key tile between its global load and its LDS commit.
+// Registers holding one key tile between its global load and its LDS commit
+// (NeoX runs of 4 pairs travel as 8-byte halves).
 template <int D, int ROPE>
 struct TileRegs {
   using C = TileCfg<D, ROPE>;
-  u32x4 ka[C::KPT];
-  u32x4 kb[(ROPE == ROPE_NEOX) ? C::KPT : 1];
+  using KVec = std::conditional_t<C::KW == 4, u32x2, u32x4>;
+  KVec ka[C::KPT];
+  KVec kb[(ROPE == ROPE_NEOX) ? C::KPT : 1];
   float4 cs[C::KPT][C::CS];
   u32x4 v[C::VPT];
 };
@@ -53,11 +61,15 @@ __device__ __forceinline__ void tile_load_k(TileRegs<D, ROPE>& R, const uint16_t
     const int it = tid + C::THREADS * i;
     if (C::K_ITEMS % C::THREADS != 0 && it >= C::K_ITEMS) break;
     const int r = it / C::K_UNITS, c = it % C::K_UNITS, n = min(n0 + r, S - 1);
-    R.ka[i] = ld16(K + (size_t)n * D + 8 * c);
     if constexpr (ROPE == ROPE_NEOX) {
-      R.kb[i] = ld16(K + (size_t)n * D + D / 2 + 8 * c);
-      load_cs(R.cs[i], table + (size_t)n * (D / 2) + 8 * c);
-    } else if constexpr (ROPE == ROPE_INTERLEAVED) {
+      using KV = typename TileRegs<D, ROPE>::KVec;
+      R.ka[i] = *reinterpret_cast<const KV*>(K + (size_t)n * D + C::KW * c);
+      R.kb[i] = *reinterpret_cast<const KV*>(K + (size_t)n * D + D / 2 + C::KW * c);
+      load_cs(R.cs[i], table + (size_t)n * (D / 2) + C::KW * c);
+    } else {
+      R.ka[i] = ld16(K + (size_t)n * D + 8 * c);
+    }
+    if constexpr (ROPE == ROPE_INTERLEAVED) {
       load_cs(R.cs[i], table + (size_t)n * (D / 2) + 4 * c);
     }
   }
@@ -94,10 +106,10 @@ __device__ __forceinline__ void tile_commit_k(TileRegs<D, ROPE>& R, uint16_t* __
     if (C::K_ITEMS % C::THREADS != 0 && it >= C::K_ITEMS) break;
     const int r = it / C::K_UNITS, c = it % C::K_UNITS;
     if constexpr (ROPE == ROPE_NEOX) {
-      u32x4 a = R.ka[i], bb = R.kb[i];
-      rotate_neox8<false, true>(a, bb, R.cs[i]);
-      *reinterpret_cast<u32x4*>(Ks + r * C::KP + 8 * c) = a;
-      *reinterpret_cast<u32x4*>(Ks + r * C::KP + D / 2 + 8 * c) = bb;
+      auto a = R.ka[i], bb = R.kb[i];
+      rotate_neox_run<false, true>(a, bb, R.cs[i]);
+      *reinterpret_cast<decltype(a)*>(Ks + r * C::KP + C::KW * c) = a;
+      *reinterpret_cast<decltype(a)*>(Ks + r * C::KP + D / 2 + C::KW * c) = bb;
     } else {
       u32x4 a = R.ka[i];
       if constexpr (ROPE == ROPE_INTERLEAVED) rotate_interleaved8<false, true>(a, R.cs[i]);

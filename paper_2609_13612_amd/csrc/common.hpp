@@ -117,6 +117,23 @@ __device__ __forceinline__ void rotate_neox8(u32x4& a, u32x4& b, const float4 (&
   }
 }
 
+// NeoX run of 2W consecutive pair indices (V holds W words of two bf16 each:
+// u32x2 for 4 pairs, u32x4 for 8), first elements in `a`, partners in `b`;
+// t[w] holds the (cos, sin) entries of the word's two pairs, as in rotate_neox8.
+template <bool INVERSE, bool F16OUT, typename V>
+__device__ __forceinline__ void rotate_neox_run(V& a, V& b, const float4* t) {
+  constexpr int W = sizeof(V) / sizeof(uint32_t);
+#pragma unroll
+  for (int w = 0; w < W; ++w) {
+    float a0 = bf_lo(a[w]), a1 = bf_hi(a[w]);
+    float b0 = bf_lo(b[w]), b1 = bf_hi(b[w]);
+    rotate_pair<INVERSE>(a0, b0, t[w].x, t[w].y);
+    rotate_pair<INVERSE>(a1, b1, t[w].z, t[w].w);
+    a[w] = pack_op<F16OUT>(a0, a1);
+    b[w] = pack_op<F16OUT>(b0, b1);
+  }
+}
+
 // Interleaved: the 8 bf16 of `x` are 4 pairs (2i, 2i+1), i = i0..i0+3, with
 // table entries t[0] = (i0, i0+1), t[1] = (i0+2, i0+3).
 template <bool INVERSE, bool F16OUT = false>

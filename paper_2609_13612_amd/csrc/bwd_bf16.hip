@@ -559,13 +559,23 @@ __global__ __launch_bounds__(512) void bwd_dkdv_kernel(BwdParams p) {
           pb[hf][w] = pack_f16(pr[8 * hf + 2 * w], pr[8 * hf + 2 * w + 1]);
           db[hf][w] = pack_f16(ds[8 * hf + 2 * w], ds[8 * hf + 2 * w + 1]);
         }
-      // dV^T += dO^T P and dK'^T += Q'^T dS (transposed operands from row-major tiles)
+      // dV^T += dO^T P and dK'^T += Q'^T dS (transposed operands from row-major
+      // tiles).  The next pair's operands are read before this pair's MFMAs, so
+      // each MFMA waits on a read issued one pair earlier rather than on its own.
+      {
+        constexpr int NI = 2 * C::MT;   // (hf, mt) pairs
+        u32x4 to = tr_operand_swz<D>(Os, z, 32 * qt, 0), tq = tr_operand_swz<D>(Qs, z, 32 * qt, 0);
 #pragma unroll
-      for (int hf = 0; hf < 2; ++hf) {
-#pragma unroll
-        for (int mt = 0; mt < C::MT; ++mt) {
-          dv[mt] = mfma32<true>(tr_operand_swz<D>(Os, z, 32 * qt + 16 * hf, mt), pb[hf], dv[mt]);
-          dk[mt] = mfma32<true>(tr_operand_swz<D>(Qs, z, 32 * qt + 16 * hf, mt), db[hf], dk[mt]);
+        for (int i = 0; i < NI; ++i) {
+          const int hf = i / C::MT, mt = i % C::MT;
+          const u32x4 ao = to, aq = tq;
+          if (i + 1 < NI) {
+            const int row = 32 * qt + 16 * ((i + 1) / C::MT), mn = (i + 1) % C::MT;
+            to = tr_operand_swz<D>(Os, z, row, mn);
+            tq = tr_operand_swz<D>(Qs, z, row, mn);
+          }
+          dv[mt] = mfma32<true>(ao, pb[hf], dv[mt]);
+          dk[mt] = mfma32<true>(aq, db[hf], dk[mt]);
         }
       }
     }

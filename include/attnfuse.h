@@ -116,7 +116,12 @@ int attnfuse_rope_table_fill(float* table, int rows, int D, float rope_theta, vo
  * Precision and range (bf16): without RoPE the bf16 inputs feed Q K^T
  * exactly; with RoPE the rotated Q' and K' are rounded to fp16 (11-bit
  * significand) for the score product, so |R q| and |R k| must stay below the
- * fp16 maximum 65504.  P and V meet in a bf16 product; accumulation is fp32.
+ * fp16 maximum 65504, and each score may move by up to
+ * softmax_scale * sum_d |q'_d k'_d| * 2^-10: LSE_i then lies within the
+ * largest such amount over row i's visible keys of the exact value (about
+ * 1e-3 at softmax_scale = 1/sqrt(D) for unit-variance inputs, proportionally
+ * more at larger scales or norms).  P and V meet in a bf16 product;
+ * accumulation is fp32.
  */
 int attnfuse_fwd(const void* Q, const void* K, const void* V, void* O, float* LSE,
                  int B, int H, int H_kv, int S, int D, int dtype,

@@ -143,6 +143,31 @@ __device__ __forceinline__ void tile_commit(TileRegs<D, ROPE>& R, uint16_t* __re
   tile_commit_v<D, ROPE, V16>(R, Vs, tid);
 }
 
+// ---------------------------------------------------------------- dense bias rows
+// The 16 bias values a lane's score registers of one 32-key subtile need:
+// keys k0 + 8 a + 4 lg + e of the bias row `row` into register 4 a + e.  Each
+// group of four is consecutive in memory, so a subtile inside the sequence
+// takes four 16-byte loads; at the sequence end each key is guarded (0 past S).
+__device__ __forceinline__ void load_bias16(float (&bv)[16], const float* __restrict__ row, int k0, int lg, int S) {
+  if (k0 + 32 <= S) {   // wave-uniform
+#pragma unroll
+    for (int a = 0; a < 4; ++a) {
+      float4 x;
+      __builtin_memcpy(&x, row + k0 + 8 * a + 4 * lg, sizeof(x));   // 4-byte alignment is all a row guarantees
+      bv[4 * a] = x.x;
+      bv[4 * a + 1] = x.y;
+      bv[4 * a + 2] = x.z;
+      bv[4 * a + 3] = x.w;
+    }
+  } else {
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int n = k0 + 8 * (r >> 2) + 4 * lg + (r & 3);
+      bv[r] = (n < S) ? row[n] : 0.f;
+    }
+  }
+}
+
 // ---------------------------------------------------------------- block-sparse tile lists
 // Largest number of 64-wide blocks along the sequence a block-sparse launch
 // accepts (S <= 131072); the host rejects longer sequences.

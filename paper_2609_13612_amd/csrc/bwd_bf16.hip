@@ -507,6 +507,18 @@ __global__ __launch_bounds__(512) void bwd_dkdv_kernel(BwdParams p) {
       }
       // element r: query mq + 8 (r/4) + 4 lg + r%4, key n
       float pr[16], ds[16];
+      float bias[16] = {};   // the bias column of key n at the 16 rows
+      if constexpr (TBIAS) {
+        if (p.bias_sq == 0) {   // broadcast over queries (e.g. key padding): one value
+          const float b0 = bcol[0];
+#pragma unroll
+          for (int r = 0; r < 16; ++r) bias[r] = b0;
+        } else {
+#pragma unroll
+          for (int r = 0; r < 16; ++r)
+            bias[r] = bcol[(long long)min(mq + 8 * (r >> 2) + 4 * lg + (r & 3), S - 1) * p.bias_sq];
+        }
+      }
 #pragma unroll
       for (int a = 0; a < 4; ++a) {
         const int qlb = 32 * qt + 8 * a + 4 * lg;
@@ -518,8 +530,7 @@ __global__ __launch_bounds__(512) void bwd_dkdv_kernel(BwdParams p) {
         for (int e = 0; e < 4; ++e) {
           const int r = 4 * a + e;
           if constexpr (TBIAS || RELU) {
-            const int mr = mq + 8 * a + 4 * lg + e;
-            const float bv = TBIAS ? bcol[(long long)min(mr, S - 1) * p.bias_sq] : 0.f;
+            const float bv = bias[r];
             if constexpr (RELU) {   // P = max(s, 0), dS = dP where s > 0
               const float x = __builtin_fmaf(sc[r], p.scale, bv);
               pr[r] = fmaxf(x, 0.f);
@@ -782,11 +793,13 @@ __global__ __launch_bounds__(512) void bwd_dq_kernel(BwdParams p) {
         // element r: key nn = n0 + 32 kt + 8 (r/4) + 4 lg + r%4, query m
         float ds[16];
         bool pos[16];   // relu attention: s > 0
+        float bias[16] = {};
+        if constexpr (TBIAS) load_bias16(bias, brow, n0 + 32 * kt, lg, S);
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const int nn = n0 + 32 * kt + 8 * (r >> 2) + 4 * lg + (r & 3);
           if constexpr (TBIAS || RELU) {
-            const float bv = TBIAS ? ((nn < S) ? brow[nn] : 0.f) : 0.f;
+            const float bv = bias[r];
             if constexpr (RELU) {
               pos[r] = __builtin_fmaf(sc[r], p.scale, bv) > 0.f;
               ds[r] = 1.f;

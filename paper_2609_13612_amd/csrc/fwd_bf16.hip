@@ -236,17 +236,13 @@ __global__ __launch_bounds__(512) void fwd_bf16_kernel(FwdParams p) {
       // relu works in natural units, the softmax in log2 units
       const float cs = RELU ? p.scale : c2;
 #pragma unroll
-      for (int kt = 0; kt < 2; ++kt)
+      for (int kt = 0; kt < 2; ++kt) {
+        float bv[16] = {};
+        if constexpr (TBIAS) load_bias16(bv, brow, n0 + 32 * kt, lg, S);
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          float bv = 0.f;
-          if constexpr (TBIAS) {
-            const int n = n0 + 32 * kt + 8 * (r >> 2) + 4 * lg + (r & 3);
-            bv = (n < S) ? brow[n] : 0.f;
-            if constexpr (!RELU) bv *= kLog2e;
-          }
-          sc[kt][r] = __builtin_fmaf(sc[kt][r], cs, bv);
-        }
+        for (int r = 0; r < 16; ++r)
+          sc[kt][r] = __builtin_fmaf(sc[kt][r], cs, RELU ? bv[r] : bv[r] * kLog2e);
+      }
     }
     bool need_mask;
     if constexpr (MASK == MASK_NONE) need_mask = n0 + C::BN > S;

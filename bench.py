@@ -135,6 +135,8 @@ def parse():
     ap.add_argument("--no-decode", action="store_true", help="skip the decode (KV-cache) measurements")
     ap.add_argument("--no-sparse", action="store_true", help="skip the block-sparse (BigBird mask) measurements")
     ap.add_argument("--no-workloads", action="store_true", help="skip the other attention workloads")
+    ap.add_argument("--no-variants", action="store_true",
+                    help="skip the RoPE mask variants (paper geometry) and the bias / relu extensions")
     ap.add_argument("--seed", type=int, default=0)
     return ap.parse_args()
 
@@ -462,6 +464,104 @@ def main():
             del qw, kw_, vw, dow, ow_o, ow_l, ow_g, ow_ws
         torch.cuda.empty_cache()
 
+    # ---------------------------------------------------------------- RoPE mask variants and extensions
+    variants = None
+    if not args.no_variants:
+        from paper_2609_13612_amd.workloads import Workload
+        variants = {"rope_masks": {}, "extensions": {}}
+        # Fused vs rotate-then-attend for RoPE + Dense / Causal / SW (W = 256) on the GPT-2-small heads
+        # of the paper's variant comparison (B = 4, H = 12, D = 64), N = 512 .. 4096.
+        for mask, window in (("none", 0), ("causal", 0), ("sliding_window", 256)):
+            for S in (512, 1024, 2048, 4096):
+                vw = Workload(f"v_{mask}_{S}", 4, 12, 12, S, 64, rope="neox", theta=10000.0, mask=mask, window=window)
+                c = inputs.make_qkv(vw.B, vw.H, vw.Hkv, S, vw.D, seed=args.seed)
+                qv, kv_, vv = (c[n].to(dev) for n in ("q", "k", "v"))
+                del c
+                vkw = dict(theta=vw.theta, mask=mask, window=window or None)
+                vo = torch.empty_like(qv)
+                vl = torch.empty(vw.B, vw.H, S, device=dev, dtype=torch.float32)
+
+                def vfused():
+                    api.attnfuse_fwd(qv, kv_, vv, out=vo, lse=vl, rope="neox", **vkw)
+
+                nb = vw.rope_bytes()
+                npool = max(2, math.ceil(600e6 / nb))
+                vpool = [(qv.clone(), kv_.clone()) for _ in range(npool)]
+                vouts = [(torch.empty_like(qv), torch.empty_like(kv_)) for _ in range(npool)]
+                cnt = [0]
+
+                def vrot():
+                    i = cnt[0] % npool
+                    cnt[0] += 1
+                    api.attnfuse_rope(vpool[i][0], vpool[i][1], rope="neox", theta=vw.theta, out_q=vouts[i][0],
+                                      out_k=vouts[i][1])
+
+                qr_, kr_ = vouts[0]
+
+                def vplain():
+                    api.attnfuse_fwd(qr_, kr_, vv, out=vo, lse=vl, rope="none", **vkw)
+
+                res = {}
+                for label, fn, reps in (("fused", vfused, 50), ("rope", vrot, max(50, 2 * npool)), ("plain", vplain, 50)):
+                    for _ in range(10):
+                        fn()
+                    res[label] = statistics.median(time_calls(fn, reps))
+                sep = res["rope"] + res["plain"]
+                f_tf = vw.fwd_flops() / (res["fused"] * 1e-3) / 1e12
+                variants["rope_masks"][f"{mask}_n{S}"] = {
+                    "B": vw.B, "H": vw.H, "S": S, "D": vw.D, "mask": mask, "window": window,
+                    "fused_ms": round(res["fused"], 4), "fused_tflops": round(f_tf, 1),
+                    "rope_ms": round(res["rope"], 4), "fwd_norope_ms": round(res["plain"], 4),
+                    "fused_speedup": round(sep / res["fused"], 4)}
+                log(f"RoPE + {mask} N={S}: fused {res['fused']:.4f} ms, separate {sep:.4f} ms "
+                    f"(fused speedup {sep / res['fused']:.3f})")
+                del qv, kv_, vv, vo, vl, vpool, vouts
+        # Dense additive bias (a key-padding bias [B, 1, 1, S], broadcast over heads and queries) and relu
+        # attention, forward and backward, with RoPE and the causal mask at B = 4, H = 16, S = 4096, D = 128.
+        ew = Workload("ext_b4h16s4096d128", 4, 16, 16, 4096, 128, rope="neox", theta=10000.0, mask="causal")
+        c = inputs.make_qkv(ew.B, ew.H, ew.Hkv, ew.S, ew.D, seed=args.seed, with_do=True)
+        qe, ke, ve, doe = (c[n].to(dev) for n in ("q", "k", "v", "do"))
+        del c
+        gen = torch.Generator("cpu").manual_seed(args.seed + 7)
+        pad = (torch.rand(ew.B, 1, 1, ew.S, generator=gen) < 0.1).float() * -1e4   # about 10 % of keys padded
+        bias = pad.to(dev)
+        ekw = dict(rope="neox", theta=ew.theta, mask="causal")
+        eg = (torch.empty_like(qe), torch.empty_like(ke), torch.empty_like(ve))
+        ews = torch.empty(api.attnfuse_bwd_workspace_bytes(ew.B, ew.H, ew.Hkv, ew.S, ew.D, "neox"), device=dev,
+                          dtype=torch.uint8)
+        for label, norm, b_ in (("softmax_bias", "softmax", bias), ("relu", "relu", None)):
+            eo, el = api.attnfuse_fwd_bias_norm(qe, ke, ve, bias=b_, norm=norm, **ekw)
+
+            def efwd():
+                api.attnfuse_fwd_bias_norm(qe, ke, ve, bias=b_, norm=norm, out=eo, lse=el, **ekw)
+
+            def ebwd():
+                api.attnfuse_bwd_bias_norm(qe, ke, ve, eo, doe, el, bias=b_, norm=norm, dq=eg[0], dk=eg[1],
+                                           dv=eg[2], workspace=ews, **ekw)
+
+            for _ in range(5):
+                efwd()
+            f_ms = statistics.median(time_calls(efwd, 30))
+            for _ in range(3):
+                ebwd()
+            b_ms = statistics.median(time_calls(ebwd, 10))
+            f_tf = ew.fwd_flops() / (f_ms * 1e-3) / 1e12
+            b_tf = ew.bwd_flops() / (b_ms * 1e-3) / 1e12
+            variants["extensions"][label] = {
+                "B": ew.B, "H": ew.H, "S": ew.S, "D": ew.D, "rope": "neox", "mask": "causal",
+                "bias": "key padding [B,1,1,S]" if b_ is not None else None, "norm": norm,
+                "fwd_ms": round(f_ms, 4), "fwd_tflops": round(f_tf, 1), "fwd_frac_peak": round(f_tf / PEAK_BF16_TFLOPS, 4),
+                "bwd_ms": round(b_ms, 4), "bwd_tflops": round(b_tf, 1), "bwd_frac_peak": round(b_tf / PEAK_BF16_TFLOPS, 4)}
+            log(f"{label}: fwd {f_ms:.4f} ms ({f_tf:.0f} TF/s), bwd {b_ms:.4f} ms ({b_tf:.0f} TF/s)")
+            del eo, el
+        # the plain fused forward of the same shape, for reference
+        for _ in range(5):
+            api.attnfuse_fwd(qe, ke, ve, **ekw)
+        p_ms = statistics.median(time_calls(lambda: api.attnfuse_fwd(qe, ke, ve, **ekw), 30))
+        variants["extensions"]["plain_fwd_ms"] = round(p_ms, 4)
+        del qe, ke, ve, doe, eg, ews, bias, pad
+        torch.cuda.empty_cache()
+
     # ---------------------------------------------------------------- CPU oracle baseline
     cpu_baseline = None
     if not args.no_cpu_baseline:
@@ -534,6 +634,8 @@ def main():
         line["block_sparse"] = sparse
     if others is not None:
         line["workloads"] = others
+    if variants is not None:
+        line["variants"] = variants
     print(json.dumps(line), flush=True)
 
 

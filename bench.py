@@ -14,7 +14,8 @@ Alongside, on the same inputs and outside the timed steps:
   the rotation kernel's HBM bandwidth, measured over a buffer pool larger than
   twice the 256 MB Infinity Cache;
 * the fuse-vs-separate crossover over S = 1024..16384 (skip with --no-sweep),
-  each point the median of 50 calls after 10 warm-ups, and the rotation
+  each figure the GPU time per call from HIP-graph replays (median of 20
+  replays of 10 captured calls; the rotation over its whole pool), and the rotation
   calculus model fitted to it (crossover_model: fused extra time a*S^2,
   separate rotation b*S, model crossover b/a next to the measured one);
 * decode over a KV cache at the paper's three decode geometries (skip with
@@ -28,6 +29,10 @@ Alongside, on the same inputs and outside the timed steps:
   RoPE + causal shape, each forward and backward (median of 50 and 20 calls
   after 10 and 3 warm-ups) against the MFMA peak, and, with RoPE, the
   separate path (rotation + no-RoPE forward) next to the fused forward;
+* the paper's RoPE comparison rows (skip with --no-variants): fused vs
+  separate RoPE for no mask, causal and a 256-key sliding window at B=4,
+  H=12, D=64, S = 512..4096, timed like the sweep; and the dense-bias and
+  relu extensions' forward and backward at B=4, H=16, S=4096, D=128;
 * a plain device-to-device copy of 512 MiB: the achievable HBM bandwidth next
   to the rotation kernel's, and the calibration kernel for the HBM-traffic
   counters;
@@ -40,6 +45,7 @@ the kernel sources it was measured on; if the sources differ, it is null.
 Prints ONE JSON line.  Only --gpus 1 is supported.
 """
 import argparse
+import functools
 import json
 import math
 import os
@@ -223,6 +229,28 @@ def main():
         torch.cuda.synchronize()
         return [a.elapsed_time(b) for a, b in es]
 
+    def graph_call_ms(fns, reps=20):
+        """GPU time per call of a sequence of calls with no host work between them: the calls are
+        captured once into a HIP graph and the graph is replayed; median replay time / len(fns).
+        Below about 20 us per call the eager figures measure the binding's host overhead instead."""
+        g = torch.cuda.CUDAGraph()
+        torch.cuda.synchronize()
+        with torch.cuda.graph(g):
+            for fn in fns:
+                fn()
+        torch.cuda.synchronize()
+        for _ in range(3):
+            g.replay()
+        es = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+        for a, b in es:
+            a.record()
+            g.replay()
+            b.record()
+        torch.cuda.synchronize()
+        ms = statistics.median(a.elapsed_time(b) for a, b in es) / len(fns)
+        del g
+        return ms
+
     separate = None
     rope_bw = None
     if w.rope != "none":
@@ -271,12 +299,8 @@ def main():
             npool = max(2, math.ceil(600e6 / nb))
             pq = [(qs.clone(), ks.clone()) for _ in range(npool)]
             po = [(torch.empty_like(qs), torch.empty_like(ks)) for _ in range(npool)]
-            cnt = [0]
-
-            def rot_s():
-                i = cnt[0] % npool
-                cnt[0] += 1
-                api.attnfuse_rope(pq[i][0], pq[i][1], rope=w.rope, theta=w.theta, out_q=po[i][0], out_k=po[i][1])
+            rots = [functools.partial(api.attnfuse_rope, pq[i][0], pq[i][1], rope=w.rope, theta=w.theta,
+                                      out_q=po[i][0], out_k=po[i][1]) for i in range(npool)]
 
             def fused_s():
                 api.attnfuse_fwd(qs, ks, vs, out=os_, lse=ls, **kw)
@@ -284,13 +308,11 @@ def main():
             def none_s():
                 api.attnfuse_fwd(po[0][0], po[0][1], vs, out=os_, lse=ls, **dict(kw, rope="none"))
 
-            for fn in (rot_s, fused_s, none_s):
-                for _ in range(10):
-                    fn()
-            reps = 50
-            r_ms = statistics.median(time_calls(rot_s, max(reps, 2 * npool)))
-            f_ms = statistics.median(time_calls(fused_s, reps))
-            n_ms = statistics.median(time_calls(none_s, reps))
+            for fn in rots + [fused_s] * 10 + [none_s] * 10:
+                fn()
+            r_ms = graph_call_ms(rots)
+            f_ms = graph_call_ms([fused_s] * 10)
+            n_ms = graph_call_ms([none_s] * 10)
             sweep.append({"S": S, "fused_ms": round(f_ms, 4), "rope_ms": round(r_ms, 4), "norope_ms": round(n_ms, 4),
                           "fused_speedup": round((r_ms + n_ms) / f_ms, 4),
                           "fused_tflops": round(w.fwd_flops(S) / (f_ms * 1e-3) / 1e12, 1)})
@@ -488,24 +510,18 @@ def main():
                 npool = max(2, math.ceil(600e6 / nb))
                 vpool = [(qv.clone(), kv_.clone()) for _ in range(npool)]
                 vouts = [(torch.empty_like(qv), torch.empty_like(kv_)) for _ in range(npool)]
-                cnt = [0]
-
-                def vrot():
-                    i = cnt[0] % npool
-                    cnt[0] += 1
-                    api.attnfuse_rope(vpool[i][0], vpool[i][1], rope="neox", theta=vw.theta, out_q=vouts[i][0],
-                                      out_k=vouts[i][1])
-
+                vrots = [functools.partial(api.attnfuse_rope, vpool[i][0], vpool[i][1], rope="neox", theta=vw.theta,
+                                           out_q=vouts[i][0], out_k=vouts[i][1]) for i in range(npool)]
                 qr_, kr_ = vouts[0]
 
                 def vplain():
                     api.attnfuse_fwd(qr_, kr_, vv, out=vo, lse=vl, rope="none", **vkw)
 
                 res = {}
-                for label, fn, reps in (("fused", vfused, 50), ("rope", vrot, max(50, 2 * npool)), ("plain", vplain, 50)):
-                    for _ in range(10):
+                for label, fns in (("fused", [vfused] * 20), ("rope", vrots), ("plain", [vplain] * 20)):
+                    for fn in fns[:10]:
                         fn()
-                    res[label] = statistics.median(time_calls(fn, reps))
+                    res[label] = graph_call_ms(fns)
                 sep = res["rope"] + res["plain"]
                 f_tf = vw.fwd_flops() / (res["fused"] * 1e-3) / 1e12
                 variants["rope_masks"][f"{mask}_n{S}"] = {

@@ -19,7 +19,8 @@ Alongside, on the same inputs and outside the timed steps:
   calculus model fitted to it (crossover_model: fused extra time a*S^2,
   separate rotation b*S, model crossover b/a next to the measured one);
 * decode over a KV cache at the paper's three decode geometries (skip with
-  --no-decode): median latency and cache bandwidth against the HBM peak, the
+  --no-decode): GPU time per call from HIP-graph replays (and the eager
+  per-call median beside it) and cache bandwidth against the HBM peak, the
   caches rotated through a pool larger than twice the Infinity Cache;
 * block-sparse attention with a BigBird-style mask at N = 4096 (skip with
   --no-sparse): forward and backward medians, TFLOP/s over the visible pairs,
@@ -356,15 +357,20 @@ def main():
 
             for _ in range(10):
                 dec()
-            d_ms = statistics.median(time_calls(dec, max(50, 2 * npool)))
+            # GPU time per call (graph replays over the cache pool); the eager figure adds the
+            # binding's host overhead, which is comparable to a call's ~10-30 us of GPU work
+            d_eager = statistics.median(time_calls(dec, max(50, 2 * npool)))
+            d_ms = graph_call_ms([functools.partial(api.attnfuse_decode, qd, kv_pool[i][0], kv_pool[i][1], rope=dw.rope,
+                                                    theta=dw.theta, out=od, lse=ld, workspace=wsd)
+                                  for i in range(npool)])
             gbs = nb / (d_ms * 1e-3) / 1e9
             decode[name] = {"B": dw.B, "H": dw.H, "H_kv": dw.Hkv, "S_kv": dw.S_kv, "D": dw.D, "rope": dw.rope,
-                            "ms": round(d_ms, 4), "cache_bytes": nb,
+                            "ms": round(d_ms, 4), "ms_eager": round(d_eager, 4), "cache_bytes": nb,
                             "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS,
                                          "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4)},
                             "frac_of_copy": round(gbs / copy_gbs, 4), "cache_pool": npool,
                             "paper_h100_ms": PAPER_DECODE_MS.get(name)}
-            log(f"decode {name}: {d_ms:.4f} ms, {gbs:.0f} GB/s of cache")
+            log(f"decode {name}: {d_ms:.4f} ms, {gbs:.0f} GB/s of cache (eager calls {d_eager:.4f} ms)")
             del kv_pool, qd, od, ld, wsd
         torch.cuda.empty_cache()
 

@@ -143,6 +143,46 @@ __device__ __forceinline__ void tile_commit(TileRegs<D, ROPE>& R, uint16_t* __re
   tile_commit_v<D, ROPE, V16>(R, Vs, tid);
 }
 
+// ---------------------------------------------------------------- output rows
+// Store a wave's 32 rows of a bf16 output held as MFMA accumulators (lane
+// lq owns row lq; element 4 a + e of acc[mt] is column 32 mt + 8 a + 4 lg + e)
+// through the wave's own 32 rows of LDS at a pitch of D + 8 elements
+// (OUT_ROWS_ELEMS), so that every store instruction writes whole rows (64
+// lanes x 16 bytes) instead of each lane writing its own row in pieces.  The
+// padding keeps the row writes and the chunk reads within two bank passes
+// with every address an immediate offset.  Rows from `rows` on are not
+// stored.  The caller makes sure no other wave still reads the LDS region.
+template <int D>
+constexpr int OUT_ROWS_ELEMS = 32 * (D + 8);   // one wave's LDS rows (elements)
+
+template <int D>
+__device__ __forceinline__ void store_rows_bf16(const f32x16 (&acc)[D / 32], uint16_t* __restrict__ lds,
+                                                uint16_t* __restrict__ dst, int rows, int lane) {
+  constexpr int OP = D + 8;           // LDS row pitch (elements)
+  constexpr int CPR = D / 8;          // 16-byte chunks per row
+  constexpr int NCH = 32 * CPR / 64;  // chunks per lane
+  const int lq = lane & 31, lg = lane >> 5;
+#pragma unroll
+  for (int mt = 0; mt < D / 32; ++mt)
+#pragma unroll
+    for (int a = 0; a < 4; ++a) {
+      const u32x2 w = {pack_bf16(acc[mt][4 * a], acc[mt][4 * a + 1]), pack_bf16(acc[mt][4 * a + 2], acc[mt][4 * a + 3])};
+      *reinterpret_cast<u32x2*>(lds + lq * OP + 32 * mt + 8 * a + 4 * lg) = w;
+    }
+  // (a wave's LDS accesses complete in order: the reads below see these writes)
+  u32x4 ch[NCH];
+#pragma unroll
+  for (int i = 0; i < NCH; ++i) {
+    const int c = lane + 64 * i;
+    ch[i] = *reinterpret_cast<const u32x4*>(lds + (c / CPR) * OP + 8 * (c % CPR));
+  }
+#pragma unroll
+  for (int i = 0; i < NCH; ++i) {
+    const int c = lane + 64 * i, r = c / CPR;
+    if (r < rows) *reinterpret_cast<u32x4*>(dst + (size_t)r * D + 8 * (c % CPR)) = ch[i];
+  }
+}
+
 // ---------------------------------------------------------------- dense bias rows
 // The 16 bias values a lane's score registers of one 32-key subtile need:
 // keys k0 + 8 a + 4 lg + e of the bias row `row` into register 4 a + e.  Each

@@ -214,8 +214,10 @@ __device__ __forceinline__ void load_row_operand(u32x4 (&reg)[D / 16], const uin
 // lane owns row n: element r of tile mt is dim 32 mt + 8 (r/4) + 4 lg + r%4.
 template <int D, int ROPE>
 __device__ __forceinline__ void store_grad_rows(f32x16 (&acc)[D / 32], float scale, uint16_t* __restrict__ dst,
-                                                const float2* __restrict__ table, int n, int lg) {
+                                                const float2* __restrict__ table, int n0, int S,
+                                                uint16_t* __restrict__ lds, int lane) {
   constexpr int MT = D / 32;
+  const int lg = lane >> 5, n = min(n0 + (lane & 31), S - 1);   // this lane's row (rows past S: not stored)
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt) acc[mt] *= scale;
   if constexpr (ROPE == ROPE_NEOX) {
@@ -251,15 +253,7 @@ __device__ __forceinline__ void store_grad_rows(f32x16 (&acc)[D / 32], float sca
       }
     }
   }
-  uint16_t* row = dst + (size_t)n * D;
-#pragma unroll
-  for (int mt = 0; mt < MT; ++mt) {
-#pragma unroll
-    for (int a = 0; a < 4; ++a) {
-      u32x2 w = {pack_bf16(acc[mt][4 * a], acc[mt][4 * a + 1]), pack_bf16(acc[mt][4 * a + 2], acc[mt][4 * a + 3])};
-      *reinterpret_cast<u32x2*>(row + 32 * mt + 8 * a + 4 * lg) = w;
-    }
-  }
+  store_rows_bf16<D>(acc, lds, dst + (size_t)n0 * D, S - n0, lane);
 }
 
 // Transposed MFMA A operand from a row-major LDS tile: rows (keys or queries)
@@ -620,13 +614,18 @@ __global__ __launch_bounds__(512) void bwd_dkdv_kernel(BwdParams p) {
   if (qh == 0) put(dv);
   __syncthreads();
   if (qh == 1) add(dv);
+  __syncthreads();   // the exchange memory is free again: each wave's output rows go through it
 
-  if (n < S) {   // dS and dO carried the factor sigma (a power of two: exact)
+  {   // dS and dO carried the factor sigma (a power of two: exact)
+    static_assert(C::THREADS / 64 * OUT_ROWS_ELEMS<D> <= SMEM, "the output rows fit the staging memory");
     const float inv = 1.f / p.dscale[bg];
+    uint16_t* rows = smem + wave * OUT_ROWS_ELEMS<D>;
     if (qh == 0)
-      store_grad_rows<D, ROPE>(dk, p.scale * inv, static_cast<uint16_t*>(p.dk) + (size_t)bg * S * D, p.table, n, lg);
+      store_grad_rows<D, ROPE>(dk, p.scale * inv, static_cast<uint16_t*>(p.dk) + (size_t)bg * S * D, p.table, nw, S,
+                               rows, lane);
     else
-      store_grad_rows<D, ROPE_NONE>(dv, inv, static_cast<uint16_t*>(p.dv) + (size_t)bg * S * D, nullptr, n, lg);
+      store_grad_rows<D, ROPE_NONE>(dv, inv, static_cast<uint16_t*>(p.dv) + (size_t)bg * S * D, nullptr, nw, S, rows,
+                                    lane);
   }
 }
 
@@ -685,7 +684,9 @@ __global__ __launch_bounds__(512) void bwd_dq_kernel(BwdParams p) {
   constexpr bool TBIAS = EXT == EXT_BIAS || EXT == EXT_RELU_BIAS;
   constexpr bool RELU = EXT == EXT_RELU || EXT == EXT_RELU_BIAS;
   static_assert(TILE_LIST_SCRATCH_BYTES <= 2 * L::STAGE * (int)sizeof(uint16_t), "the tile-list scratch fits the stages");
-  __shared__ __attribute__((aligned(16))) uint16_t smem[2 * L::STAGE];
+  // the two key-tile stages, and at the end each wave's dQ rows on their way out
+  constexpr int SMEM = (2 * L::STAGE > C::NW * OUT_ROWS_ELEMS<D>) ? 2 * L::STAGE : C::NW * OUT_ROWS_ELEMS<D>;
+  __shared__ __attribute__((aligned(16))) uint16_t smem[SMEM];
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, lq = lane & 31, lg = lane >> 5;
   const int S = p.S;
@@ -864,7 +865,9 @@ __global__ __launch_bounds__(512) void bwd_dq_kernel(BwdParams p) {
       p.lse2[bh * S + m] = any ? lse2 + __log2f(ltot) : INFINITY;
     }
   }
-  if (m < S) store_grad_rows<D, ROPE>(dq, p.scale / sig, static_cast<uint16_t*>(p.dq) + bh * S * D, p.table, m, lg);
+  // the key loop ended on a barrier after every wave's last LDS read
+  store_grad_rows<D, ROPE>(dq, p.scale / sig, static_cast<uint16_t*>(p.dq) + bh * S * D, p.table, mw, S,
+                           smem + wave * OUT_ROWS_ELEMS<D>, lane);
 }
 
 // ---------------------------------------------------------------- launch

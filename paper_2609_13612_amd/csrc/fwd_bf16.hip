@@ -445,39 +445,18 @@ __global__ __launch_bounds__(512) void fwd_bf16_kernel(FwdParams p) {
     if (t < ntl) pv(pop, vst(t));
   }
 
-  // Epilogue: O = acc / l, LSE = (m + log2 l) ln 2.  O leaves through the
-  // wave's own rows of the staging memory (free once every wave is past the
-  // key loop), so that each store instruction writes whole rows (64 lanes x
-  // 16 bytes, four rows at D = 128) rather than 16-byte pieces of 32 rows.
+  // Epilogue: O = acc / l, LSE = (m + log2 l) ln 2.  O leaves as whole rows
+  // through the wave's rows of the staging memory, free once every wave is
+  // past the key loop (store_rows_bf16).
   const float l_tot = pair_sum(l_run);
   const float inv = RELU ? 1.f : (l_tot > 0.f) ? 1.f / l_tot : 0.f;
-  constexpr int OP = D + 8;   // row pitch of the staged O rows (elements)
-  static_assert(C::NW * 32 * OP <= (SPARSE ? 4 : 2) * C::STAGE, "the O rows fit the staging memory");
+  static_assert(C::NW * OUT_ROWS_ELEMS<D> <= (SPARSE ? 4 : 2) * C::STAGE, "the O rows fit the staging memory");
+#pragma unroll
+  for (int mt = 0; mt < C::MT; ++mt) acc[mt] *= inv;
   __syncthreads();
-  uint16_t* Ow = smem + wave * 32 * OP;
-#pragma unroll
-  for (int mt = 0; mt < C::MT; ++mt)
-#pragma unroll
-    for (int a = 0; a < 4; ++a) {
-      const u32x2 w = {pack_bf16(acc[mt][4 * a] * inv, acc[mt][4 * a + 1] * inv),
-                       pack_bf16(acc[mt][4 * a + 2] * inv, acc[mt][4 * a + 3] * inv)};
-      *reinterpret_cast<u32x2*>(Ow + lq * OP + 32 * mt + 8 * a + 4 * lg) = w;
-    }
-  if (kg == 0) {   // a wave's LDS accesses complete in order: the reads see its writes
-    uint16_t* O = static_cast<uint16_t*>(p.o) + (bh * S + mw) * D;
-    constexpr int CPR = D / 8;          // 16-byte chunks per row
-    constexpr int NCH = 32 * CPR / 64;  // chunks per lane
-    u32x4 ch[NCH];
-#pragma unroll
-    for (int i = 0; i < NCH; ++i) {
-      const int c = lane + 64 * i;
-      ch[i] = *reinterpret_cast<const u32x4*>(Ow + (c / CPR) * OP + 8 * (c % CPR));
-    }
-#pragma unroll
-    for (int i = 0; i < NCH; ++i) {
-      const int c = lane + 64 * i, r = c / CPR;
-      if (mw + r < S) *reinterpret_cast<u32x4*>(O + (size_t)r * D + 8 * (c % CPR)) = ch[i];
-    }
+  if (kg == 0) {
+    store_rows_bf16<D>(acc, smem + wave * OUT_ROWS_ELEMS<D>, static_cast<uint16_t*>(p.o) + (bh * S + mw) * D, S - mw,
+                       lane);
     if (!RELU && lg == 0 && m < S) p.lse[bh * S + m] = (l_tot > 0.f) ? (m_run + __log2f(l_tot)) * kLn2 : -INFINITY;
   }
 }

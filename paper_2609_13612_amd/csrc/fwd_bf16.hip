@@ -447,17 +447,36 @@ __global__ __launch_bounds__(512) void fwd_bf16_kernel(FwdParams p) {
 
   // Epilogue: O = acc / l, LSE = (m + log2 l) ln 2.  O leaves as whole rows
   // through the wave's rows of the staging memory, free once every wave is
-  // past the key loop (store_rows_bf16).
+  // past the key loop (store_rows_bf16).  Relu attention (unnormalised O, no
+  // LSE) keeps each lane's own row stores: its key loop, which already
+  // spills, ran 5 % slower with the staged store (the register allocation
+  // moved), and the form below is the one it was measured fastest with.
   const float l_tot = pair_sum(l_run);
-  const float inv = RELU ? 1.f : (l_tot > 0.f) ? 1.f / l_tot : 0.f;
-  static_assert(C::NW * OUT_ROWS_ELEMS<D> <= (SPARSE ? 4 : 2) * C::STAGE, "the O rows fit the staging memory");
+  if constexpr (RELU) {
+    if (m < S && kg == 0) {
+      const float inv = 1.f;
+      uint16_t* O = static_cast<uint16_t*>(p.o) + (bh * S + m) * D;
 #pragma unroll
-  for (int mt = 0; mt < C::MT; ++mt) acc[mt] *= inv;
-  __syncthreads();
-  if (kg == 0) {
-    store_rows_bf16<D>(acc, smem + wave * OUT_ROWS_ELEMS<D>, static_cast<uint16_t*>(p.o) + (bh * S + mw) * D, S - mw,
-                       lane);
-    if (!RELU && lg == 0 && m < S) p.lse[bh * S + m] = (l_tot > 0.f) ? (m_run + __log2f(l_tot)) * kLn2 : -INFINITY;
+      for (int mt = 0; mt < C::MT; ++mt) {
+#pragma unroll
+        for (int a = 0; a < 4; ++a) {
+          u32x2 w = {pack_bf16(acc[mt][4 * a] * inv, acc[mt][4 * a + 1] * inv),
+                     pack_bf16(acc[mt][4 * a + 2] * inv, acc[mt][4 * a + 3] * inv)};
+          *reinterpret_cast<u32x2*>(O + 32 * mt + 8 * a + 4 * lg) = w;
+        }
+      }
+    }
+  } else {
+    const float inv = (l_tot > 0.f) ? 1.f / l_tot : 0.f;
+    static_assert(C::NW * OUT_ROWS_ELEMS<D> <= (SPARSE ? 4 : 2) * C::STAGE, "the O rows fit the staging memory");
+#pragma unroll
+    for (int mt = 0; mt < C::MT; ++mt) acc[mt] *= inv;
+    __syncthreads();
+    if (kg == 0) {
+      store_rows_bf16<D>(acc, smem + wave * OUT_ROWS_ELEMS<D>, static_cast<uint16_t*>(p.o) + (bh * S + mw) * D, S - mw,
+                         lane);
+      if (lg == 0 && m < S) p.lse[bh * S + m] = (l_tot > 0.f) ? (m_run + __log2f(l_tot)) * kLn2 : -INFINITY;
+    }
   }
 }
 

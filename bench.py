@@ -230,15 +230,25 @@ def main():
         torch.cuda.synchronize()
         return [a.elapsed_time(b) for a, b in es]
 
+    graph_failures = []
+
     def graph_call_ms(fns, reps=20):
         """GPU time per call of a sequence of calls with no host work between them: the calls are
         captured once into a HIP graph and the graph is replayed; median replay time / len(fns).
-        Below about 20 us per call the eager figures measure the binding's host overhead instead."""
+        Below about 20 us per call the eager figures measure the binding's host overhead instead.
+        If the capture fails, the eager per-call median is returned and the failure is reported
+        in the JSON line (graph_timing_failures)."""
         g = torch.cuda.CUDAGraph()
         torch.cuda.synchronize()
-        with torch.cuda.graph(g):
-            for fn in fns:
-                fn()
+        try:
+            with torch.cuda.graph(g):
+                for fn in fns:
+                    fn()
+        except RuntimeError as e:
+            torch.cuda.synchronize()
+            graph_failures.append(str(e).splitlines()[0][:200])
+            log(f"graph capture failed ({graph_failures[-1]}); eager timing instead")
+            return statistics.median(time_calls(lambda: [fn() for fn in fns], reps)) / len(fns)
         torch.cuda.synchronize()
         for _ in range(3):
             g.replay()
@@ -658,6 +668,8 @@ def main():
         line["workloads"] = others
     if variants is not None:
         line["variants"] = variants
+    if graph_failures:
+        line["graph_timing_failures"] = graph_failures
     print(json.dumps(line), flush=True)
 
 

@@ -283,15 +283,15 @@ __device__ __forceinline__ u32x4 row_operand_swz(const uint16_t* tile, const Swz
 }
 
 // ---------------------------------------------------------------- dK / dV
-// Query-side tile of the dK/dV kernel: 64 query rows of Q' (fp16, rotated by
+// Query-side tile of the dK/dV kernel: BQ_ query rows of Q' (fp16, rotated by
 // the preprocessing kernel) or Q (bf16, converted to fp16 as it is staged)
 // and of dO (fp16), plus their LSE (log2 units) and delta.
-template <int D>
+template <int D, int BQ_ = 64>
 struct QTileCfg {
   static constexpr int NW = 8;                // two waves per SIMD
   static constexpr int THREADS = 64 * NW;
   static constexpr int KEYS = 32 * NW / 2;    // keys per workgroup: each 32 keys are shared by a wave pair
-  static constexpr int BQ = 64;               // query rows per tile: the pair splits them 32 + 32
+  static constexpr int BQ = BQ_;              // query rows per tile: the pair splits them in halves
   static constexpr int VP = D + 8;            // pitch of the resident K' and V rows (16-byte reads)
   static constexpr int V_ELEMS = KEYS * VP;
   static constexpr int KS = D / 16;
@@ -302,9 +302,9 @@ struct QTileCfg {
   static constexpr int IPT = (ITEMS + THREADS - 1) / THREADS;
 };
 
-template <int D>
+template <int D, int BQ = 64>
 struct QTileRegs {
-  using C = QTileCfg<D>;
+  using C = QTileCfg<D, BQ>;
   u32x4 q[C::IPT];
   u32x4 o[C::IPT];
   float lse2, del;
@@ -312,11 +312,11 @@ struct QTileRegs {
 
 // Rows past S are clamped to row S-1 so every load is unconditional; they get
 // LSE = +inf (so P = 0) and delta = 0, so they contribute nothing.
-template <int D>
-__device__ __forceinline__ void qtile_load(QTileRegs<D>& R, const uint16_t* __restrict__ Q,
+template <int D, int BQ>
+__device__ __forceinline__ void qtile_load(QTileRegs<D, BQ>& R, const uint16_t* __restrict__ Q,
                                            const uint16_t* __restrict__ dO, const float* __restrict__ lse2,
                                            const float* __restrict__ delta, int m0, int S, int tid) {
-  using C = QTileCfg<D>;
+  using C = QTileCfg<D, BQ>;
 #pragma unroll
   for (int i = 0; i < C::IPT; ++i) {
     const int it = tid + C::THREADS * i;
@@ -333,11 +333,11 @@ __device__ __forceinline__ void qtile_load(QTileRegs<D>& R, const uint16_t* __re
 }
 
 // TO_F16: Q arrives as bf16 (no RoPE) and is converted as it is staged.
-template <int D, bool TO_F16>
-__device__ __forceinline__ void qtile_commit(const QTileRegs<D>& R, uint16_t* __restrict__ Qs,
+template <int D, bool TO_F16, int BQ>
+__device__ __forceinline__ void qtile_commit(const QTileRegs<D, BQ>& R, uint16_t* __restrict__ Qs,
                                              uint16_t* __restrict__ Os, float* __restrict__ lse2s,
                                              float* __restrict__ dels, int tid) {
-  using C = QTileCfg<D>;
+  using C = QTileCfg<D, BQ>;
 #pragma unroll
   for (int i = 0; i < C::IPT; ++i) {
     const int it = tid + C::THREADS * i;
@@ -358,15 +358,19 @@ __device__ __forceinline__ void qtile_commit(const QTileRegs<D>& R, uint16_t* __
 }
 
 // One workgroup = 8 waves = 128 keys of one (batch, K/V head).  Waves w and
-// w + 4 share keys 32 (w % 4) .. +31 and split every 64-query tile, w taking
-// its first 32 rows and w + 4 the rest, so two waves per SIMD hide each
-// other's latencies; their partial dK/dV are summed through LDS at the end.
+// w + 4 share keys 32 (w % 4) .. +31 and split every query tile (64 rows;
+// 128 at D = 64 without a block mask), w taking its first half and w + 4 the
+// second, 32 rows at a time, so two waves per SIMD hide each other's
+// latencies; their partial dK/dV are summed through LDS at the end.
 // The block's K' rows (B operand of S = Q' K'^T) and V rows (fp16, B operand
 // of dP = dO V^T) stay resident in LDS, leaving the registers to the dK/dV
 // accumulators.
 template <int D, int ROPE, int MASK, bool ALIBI, bool SPARSE, int EXT = EXT_NONE>
 __global__ __launch_bounds__(512) void bwd_dkdv_kernel(BwdParams p) {
-  using C = QTileCfg<D>;
+  // at D = 64 a 128-row query tile halves the steps (barriers, staging) per
+  // key block; block masks work in 64-row blocks
+  using C = QTileCfg<D, (D == 64 && !SPARSE) ? 128 : 64>;
+  constexpr int NQ = C::BQ / 64;   // 32-row blocks of a tile per wave
   constexpr bool TBIAS = EXT == EXT_BIAS || EXT == EXT_RELU_BIAS;
   constexpr bool RELU = EXT == EXT_RELU || EXT == EXT_RELU_BIAS;
   constexpr bool ROT = ROPE != ROPE_NONE;    // Q' and K' come rotated (fp16) from the workspace
@@ -446,7 +450,7 @@ __global__ __launch_bounds__(512) void bwd_dkdv_kernel(BwdParams p) {
     dl = p.delta + bh * S;
   };
 
-  QTileRegs<D> R;
+  QTileRegs<D, C::BQ> R;
   if (steps > 0) {
     const uint16_t *Qh, *dOh;
     const float *l2, *dl;
@@ -456,7 +460,6 @@ __global__ __launch_bounds__(512) void bwd_dkdv_kernel(BwdParams p) {
   }
   __syncthreads();
 
-  const int qt = qh;                  // this wave's 32 rows of every query tile
   const SwzLane<D> zl(lane);
   for (int s = 0; s < steps; ++s) {
     const int st = s & 1;
@@ -473,114 +476,118 @@ __global__ __launch_bounds__(512) void bwd_dkdv_kernel(BwdParams p) {
       qtile_load<D>(R, Qh, dOh, l2, dl, tile_of(s + 1) * C::BQ, S, tid);
     }
     const int h = head_of(s);
-    const int mq = tile_of(s) * C::BQ + 32 * qt;   // first query row of this wave's half
     const float slope2 = ALIBI ? p.slopes[h] * kLog2e : 0.f;
     const float* __restrict__ bcol = nullptr;      // this lane's key column of the bias tensor
     if constexpr (TBIAS) bcol = p.bias + b * p.bias_sb + h * p.bias_sh + min(n, S - 1);
+#pragma unroll
+    for (int j = 0; j < NQ; ++j) {
+      const int qt = NQ * qh + j;                  // this wave's 32-row block of the tile
+      const int mq = tile_of(s) * C::BQ + 32 * qt;   // its first query row
 
-    bool visible = nw < S;
-    if constexpr (SPARSE) visible = visible && ((tl.rows[s % nq] >> jw) & 1);
-    if constexpr (MASK != MASK_NONE) visible = visible && (mq + 31 >= nw);
-    if constexpr (MASK == MASK_SLIDING_WINDOW) visible = visible && (mq <= nw + 31 + W - 1);
-    if (visible) {
-      bool need_mask = nw + 32 > S;
-      if constexpr (RELU) need_mask = need_mask || (mq + 32 > S);   // no LSE zeroes the rows past S
-      if constexpr (MASK != MASK_NONE) need_mask = need_mask || (mq < nw + 31);
-      if constexpr (MASK == MASK_SLIDING_WINDOW) need_mask = need_mask || (mq + 31 - W >= nw);
-      // S = Q' K'^T and dP = dO V^T for 32 queries (rows) x this wave's 32 keys
-      // (columns); the two MFMA chains are interleaved.
-      f32x16 sc = f32x16{}, dp = f32x16{};
-#pragma unroll
-      for (int k = 0; k < C::KS; ++k) {
-        const u32x4 aq = row_operand_swz<D>(Qs, z, 32 * qt, k);
-        const u32x4 ao = row_operand_swz<D>(Os, z, 32 * qt, k);
-        const u32x4 bk = *reinterpret_cast<const u32x4*>(Ks + (32 * kw + lq) * C::VP + 16 * k + 8 * lg);
-        const u32x4 bv = *reinterpret_cast<const u32x4*>(Vs + (32 * kw + lq) * C::VP + 16 * k + 8 * lg);
-        sc = mfma32<true>(aq, bk, sc);
-        dp = mfma32<true>(ao, bv, dp);
-      }
-      // element r: query mq + 8 (r/4) + 4 lg + r%4, key n
-      float pr[16], ds[16];
-      float bias[16] = {};   // the bias column of key n at the 16 rows
-      if constexpr (TBIAS) {
-        if (p.bias_sq == 0) {   // broadcast over queries (e.g. key padding): one value
-          const float b0 = bcol[0];
-#pragma unroll
-          for (int r = 0; r < 16; ++r) bias[r] = b0;
-        } else {
-#pragma unroll
-          for (int r = 0; r < 16; ++r)
-            bias[r] = bcol[(long long)min(mq + 8 * (r >> 2) + 4 * lg + (r & 3), S - 1) * p.bias_sq];
+      bool visible = nw < S;
+      if constexpr (SPARSE) visible = visible && ((tl.rows[s % nq] >> jw) & 1);
+      if constexpr (MASK != MASK_NONE) visible = visible && (mq + 31 >= nw);
+      if constexpr (MASK == MASK_SLIDING_WINDOW) visible = visible && (mq <= nw + 31 + W - 1);
+      if (visible) {
+        bool need_mask = nw + 32 > S;
+        if constexpr (RELU) need_mask = need_mask || (mq + 32 > S);   // no LSE zeroes the rows past S
+        if constexpr (MASK != MASK_NONE) need_mask = need_mask || (mq < nw + 31);
+        if constexpr (MASK == MASK_SLIDING_WINDOW) need_mask = need_mask || (mq + 31 - W >= nw);
+        // S = Q' K'^T and dP = dO V^T for 32 queries (rows) x this wave's 32 keys
+        // (columns); the two MFMA chains are interleaved.
+        f32x16 sc = f32x16{}, dp = f32x16{};
+  #pragma unroll
+        for (int k = 0; k < C::KS; ++k) {
+          const u32x4 aq = row_operand_swz<D>(Qs, z, 32 * qt, k);
+          const u32x4 ao = row_operand_swz<D>(Os, z, 32 * qt, k);
+          const u32x4 bk = *reinterpret_cast<const u32x4*>(Ks + (32 * kw + lq) * C::VP + 16 * k + 8 * lg);
+          const u32x4 bv = *reinterpret_cast<const u32x4*>(Vs + (32 * kw + lq) * C::VP + 16 * k + 8 * lg);
+          sc = mfma32<true>(aq, bk, sc);
+          dp = mfma32<true>(ao, bv, dp);
         }
-      }
-#pragma unroll
-      for (int a = 0; a < 4; ++a) {
-        const int qlb = 32 * qt + 8 * a + 4 * lg;
-        const float4 l4 = *reinterpret_cast<const float4*>(lse2s + qlb);
-        const float4 d4 = *reinterpret_cast<const float4*>(dels + qlb);
-        const float lv[4] = {l4.x, l4.y, l4.z, l4.w};
-        const float dv4[4] = {d4.x, d4.y, d4.z, d4.w};
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int r = 4 * a + e;
-          if constexpr (TBIAS || RELU) {
-            const float bv = bias[r];
-            if constexpr (RELU) {   // P = max(s, 0), dS = dP where s > 0
-              const float x = __builtin_fmaf(sc[r], p.scale, bv);
-              pr[r] = fmaxf(x, 0.f);
-              ds[r] = (x > 0.f) ? dp[r] : 0.f;
+        // element r: query mq + 8 (r/4) + 4 lg + r%4, key n
+        float pr[16], ds[16];
+        float bias[16] = {};   // the bias column of key n at the 16 rows
+        if constexpr (TBIAS) {
+          if (p.bias_sq == 0) {   // broadcast over queries (e.g. key padding): one value
+            const float b0 = bcol[0];
+  #pragma unroll
+            for (int r = 0; r < 16; ++r) bias[r] = b0;
+          } else {
+  #pragma unroll
+            for (int r = 0; r < 16; ++r)
+              bias[r] = bcol[(long long)min(mq + 8 * (r >> 2) + 4 * lg + (r & 3), S - 1) * p.bias_sq];
+          }
+        }
+  #pragma unroll
+        for (int a = 0; a < 4; ++a) {
+          const int qlb = 32 * qt + 8 * a + 4 * lg;
+          const float4 l4 = *reinterpret_cast<const float4*>(lse2s + qlb);
+          const float4 d4 = *reinterpret_cast<const float4*>(dels + qlb);
+          const float lv[4] = {l4.x, l4.y, l4.z, l4.w};
+          const float dv4[4] = {d4.x, d4.y, d4.z, d4.w};
+  #pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const int r = 4 * a + e;
+            if constexpr (TBIAS || RELU) {
+              const float bv = bias[r];
+              if constexpr (RELU) {   // P = max(s, 0), dS = dP where s > 0
+                const float x = __builtin_fmaf(sc[r], p.scale, bv);
+                pr[r] = fmaxf(x, 0.f);
+                ds[r] = (x > 0.f) ? dp[r] : 0.f;
+              } else {
+                pr[r] = fast_exp2(__builtin_fmaf(sc[r], c2, bv * kLog2e) - lv[e]);
+                ds[r] = dp[r] - dv4[e];
+              }
             } else {
-              pr[r] = fast_exp2(__builtin_fmaf(sc[r], c2, bv * kLog2e) - lv[e]);
+              const float x = ALIBI ? __builtin_fmaf(sc[r], c2, slope2 * (float)(n - (mq + 8 * a + 4 * lg + e))) : sc[r] * c2;
+              pr[r] = fast_exp2(x - lv[e]);
               ds[r] = dp[r] - dv4[e];
             }
-          } else {
-            const float x = ALIBI ? __builtin_fmaf(sc[r], c2, slope2 * (float)(n - (mq + 8 * a + 4 * lg + e))) : sc[r] * c2;
-            pr[r] = fast_exp2(x - lv[e]);
-            ds[r] = dp[r] - dv4[e];
           }
         }
-      }
-      if (need_mask) {   // wave-uniform: diagonal, window-edge and sequence-end tiles only
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int m = mq + 8 * (r >> 2) + 4 * lg + (r & 3);
-          bool ok = n < S;
-          if constexpr (RELU) ok = ok && (m < S);
-          if constexpr (MASK != MASK_NONE) ok = ok && (n <= m);
-          if constexpr (MASK == MASK_SLIDING_WINDOW) ok = ok && (n > m - W);
-          pr[r] = ok ? pr[r] : 0.f;
-          if constexpr (RELU) ds[r] = ok ? ds[r] : 0.f;
-        }
-      }
-      if constexpr (!RELU) {
-#pragma unroll
-        for (int r = 0; r < 16; ++r) ds[r] *= pr[r];
-      }
-      u32x4 pb[2], db[2];
-#pragma unroll
-      for (int hf = 0; hf < 2; ++hf)
-#pragma unroll
-        for (int w = 0; w < 4; ++w) {
-          pb[hf][w] = pack_f16(pr[8 * hf + 2 * w], pr[8 * hf + 2 * w + 1]);
-          db[hf][w] = pack_f16(ds[8 * hf + 2 * w], ds[8 * hf + 2 * w + 1]);
-        }
-      // dV^T += dO^T P and dK'^T += Q'^T dS (transposed operands from row-major
-      // tiles).  The next pair's operands are read before this pair's MFMAs, so
-      // each MFMA waits on a read issued one pair earlier rather than on its own.
-      {
-        constexpr int NI = 2 * C::MT;   // (hf, mt) pairs
-        u32x4 to = tr_operand_swz<D>(Os, z, 32 * qt, 0), tq = tr_operand_swz<D>(Qs, z, 32 * qt, 0);
-#pragma unroll
-        for (int i = 0; i < NI; ++i) {
-          const int hf = i / C::MT, mt = i % C::MT;
-          const u32x4 ao = to, aq = tq;
-          if (i + 1 < NI) {
-            const int row = 32 * qt + 16 * ((i + 1) / C::MT), mn = (i + 1) % C::MT;
-            to = tr_operand_swz<D>(Os, z, row, mn);
-            tq = tr_operand_swz<D>(Qs, z, row, mn);
+        if (need_mask) {   // wave-uniform: diagonal, window-edge and sequence-end tiles only
+  #pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int m = mq + 8 * (r >> 2) + 4 * lg + (r & 3);
+            bool ok = n < S;
+            if constexpr (RELU) ok = ok && (m < S);
+            if constexpr (MASK != MASK_NONE) ok = ok && (n <= m);
+            if constexpr (MASK == MASK_SLIDING_WINDOW) ok = ok && (n > m - W);
+            pr[r] = ok ? pr[r] : 0.f;
+            if constexpr (RELU) ds[r] = ok ? ds[r] : 0.f;
           }
-          dv[mt] = mfma32<true>(ao, pb[hf], dv[mt]);
-          dk[mt] = mfma32<true>(aq, db[hf], dk[mt]);
+        }
+        if constexpr (!RELU) {
+  #pragma unroll
+          for (int r = 0; r < 16; ++r) ds[r] *= pr[r];
+        }
+        u32x4 pb[2], db[2];
+  #pragma unroll
+        for (int hf = 0; hf < 2; ++hf)
+  #pragma unroll
+          for (int w = 0; w < 4; ++w) {
+            pb[hf][w] = pack_f16(pr[8 * hf + 2 * w], pr[8 * hf + 2 * w + 1]);
+            db[hf][w] = pack_f16(ds[8 * hf + 2 * w], ds[8 * hf + 2 * w + 1]);
+          }
+        // dV^T += dO^T P and dK'^T += Q'^T dS (transposed operands from row-major
+        // tiles).  The next pair's operands are read before this pair's MFMAs, so
+        // each MFMA waits on a read issued one pair earlier rather than on its own.
+        {
+          constexpr int NI = 2 * C::MT;   // (hf, mt) pairs
+          u32x4 to = tr_operand_swz<D>(Os, z, 32 * qt, 0), tq = tr_operand_swz<D>(Qs, z, 32 * qt, 0);
+  #pragma unroll
+          for (int i = 0; i < NI; ++i) {
+            const int hf = i / C::MT, mt = i % C::MT;
+            const u32x4 ao = to, aq = tq;
+            if (i + 1 < NI) {
+              const int row = 32 * qt + 16 * ((i + 1) / C::MT), mn = (i + 1) % C::MT;
+              to = tr_operand_swz<D>(Os, z, row, mn);
+              tq = tr_operand_swz<D>(Qs, z, row, mn);
+            }
+            dv[mt] = mfma32<true>(ao, pb[hf], dv[mt]);
+            dk[mt] = mfma32<true>(aq, db[hf], dk[mt]);
+          }
         }
       }
     }

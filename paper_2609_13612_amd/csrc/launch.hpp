@@ -89,6 +89,8 @@ struct RopeParams {
 int launch_fwd_bf16(int D, int rope, int mask, bool alibi, int ext, const FwdParams& p, hipStream_t st);
 int launch_fwd_fp32(int D, int rope, int mask, bool alibi, const FwdParams& p, hipStream_t st);
 int launch_bwd_bf16(int D, int rope, int mask, bool alibi, int ext, const BwdParams& p, hipStream_t st);
+// The dK/dV pass alone (the last launch of launch_bwd_bf16).
+int launch_bwd_dkdv_bf16(int D, int rope, int mask, bool alibi, int ext, const BwdParams& p, hipStream_t st);
 int launch_bwd_fp32(int D, int rope, int mask, bool alibi, const BwdParams& p, hipStream_t st);
 int launch_decode(int D, int rope, bool alibi, const DecodeParams& p, hipStream_t st);
 int launch_rope(bool fp32, int D, int rope, bool inverse, const RopeParams& p, hipStream_t st);

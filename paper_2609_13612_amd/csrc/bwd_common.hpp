@@ -107,7 +107,6 @@ __device__ __forceinline__ u32x4 row_operand_swz(const uint16_t* tile, const Swz
   return *reinterpret_cast<const u32x4*>(tile + row0 * D + (z.row_base ^ (16 * k)));
 }
 
-
 // ---------------------------------------------------------------- dispatch
 // Map the runtime variant (D, rope, mask, alibi, ext) to Pass::run<D, ROPE,
 // MASK, ALIBI, EXT>(p, st).  Extensions other than EXT_NONE are instantiated

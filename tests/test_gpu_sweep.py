@@ -79,7 +79,7 @@ def _decode_case(i):
                 alibi=bool(r.random() < 0.3), seed=4000 + i)
 
 
-@pytest.mark.parametrize("i", range(8))
+@pytest.mark.parametrize("i", range(68))
 def test_sweep_decode(i):
     need_gpu()
     c = _decode_case(i)
@@ -167,7 +167,7 @@ def _bias_tensor(shape, B, H, S, seed):
     return 1.5 * torch.randn(*dims, generator=g, dtype=torch.float32)
 
 
-@pytest.mark.parametrize("i", range(6))
+@pytest.mark.parametrize("i", range(46))
 def test_sweep_bias_norm(i):
     """Relu attention runs in its published 1/L form (folded into the scale and
     the bias) so its outputs stay O(1), as in the hand-picked relu tests."""

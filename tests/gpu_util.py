@@ -30,6 +30,7 @@ import numpy as np
 import pytest
 import torch
 
+import oracle
 from paper_2609_13612_amd import inputs
 
 BF16_MAX, BF16_MEAN, FP32_MAX, LSE_MAX = 2e-2, 2e-3, 1e-4, 1e-3
@@ -136,3 +137,60 @@ def assert_lse_close(gpu, ref, what, tol=LSE_MAX):
     err = np.abs(g[fin] - ref[fin])
     report(what, err, ref[fin], tol, tol)
     assert err.size == 0 or err.max() <= tol, f"{what}: LSE max-abs {err.max():.3e} > {tol}"
+
+
+def visible_pairs(S, mask, window):
+    """[S, S] boolean: query i sees key j under the mask (no mask, causal, or causal + window)."""
+    i = np.arange(S)[:, None]
+    j = np.arange(S)[None, :]
+    if mask == "none":
+        return np.ones((S, S), dtype=bool)
+    vis = j <= i
+    if mask == "sliding_window":
+        vis &= j > i - window
+    return vis
+
+
+def assert_rope_lse_close(lse, q, k, v, rope, theta, alibi_slopes, mask, window, scale):
+    """The LSE of a RoPE forward against its operand-precision model (q, k, v:
+    the fp64 inputs; alibi_slopes fp64 or None).
+
+    The kernels round the rotated Q' and K' to fp16 for the score MFMA; the
+    definition rotates exactly.  Rounding each operand moves it by at most
+    2^-11 of itself, so a score moves by at most
+        b_ij = scale * sum_d |q'_id k'_jd| * (2 * 2^-11 + 2^-16)
+    (the last term: fp32 accumulation over D products), and a row's LSE, whose
+    first-order change is the P-weighted mean of its scores' changes, by at most
+    the largest b_ij over the row's visible keys.  Checked: the LSE equals the
+    definition evaluated on the fp16-rounded rotated operands to the flat 1e-3
+    (the error is the operands' rounding and nothing else), and lies within
+    max_j b_ij (+ 2e-4 for the exp2 / log2 approximations and fp32 sums of the
+    online softmax) of the exact LSE.  Returns the two max-abs errors."""
+    B, H, S, D = q.shape
+    G = H // k.shape[1]
+    kw = dict(mask=mask, window=window, scale=scale)
+    _, L = oracle.attention_forward(q, k, v, rope=rope, theta=theta, alibi_slopes=alibi_slopes, **kw)
+    pos = np.arange(S, dtype=np.float64)
+    qr = oracle.rope_rotate(q, pos, theta, rope)
+    kr = oracle.rope_rotate(k, pos, theta, rope)
+    q16 = qr.astype(np.float16).astype(np.float64)
+    k16 = kr.astype(np.float16).astype(np.float64)
+    _, L16 = oracle.attention_forward(q16, k16, v, rope="none", alibi_slopes=alibi_slopes, **kw)
+    g = f64(lse) if isinstance(lse, torch.Tensor) else lse
+    assert np.array_equal(np.isneginf(g), np.isneginf(L)), "LSE: -inf pattern differs"
+    fin = np.isfinite(L)
+    err16 = np.abs(g[fin] - L16[fin])
+    report("LSE vs the fp16-operand definition", err16, L16[fin], LSE_MAX, LSE_MAX)
+    assert err16.size == 0 or err16.max() <= LSE_MAX, f"LSE vs the fp16-operand definition: {err16.max():.3e}"
+    sc = scale if scale is not None else D ** -0.5
+    vis = visible_pairs(S, mask, window)
+    err = np.where(fin, np.abs(g - np.where(fin, L, 0.0)), 0.0)
+    for b in range(B):
+        for h in range(H):
+            mag = np.abs(qr[b, h]) @ np.abs(kr[b, h // G]).T          # sum_d |q'_id k'_jd|
+            bnd = sc * mag * (2 * 2.0 ** -11 + 2.0 ** -16)
+            row_bound = np.where(vis, bnd, 0.0).max(axis=1) + 2e-4
+            over = err[b, h] > row_bound
+            assert not over.any(), (f"(b={b}, h={h}) LSE error {err[b, h][over].max():.3e} above its "
+                                    f"rounding bound {row_bound[over].min():.3e}")
+    return float(err.max()), float(err16.max()) if err16.size else 0.0

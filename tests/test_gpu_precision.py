@@ -22,12 +22,10 @@ scales up to 0.28 or rows with one or two visible keys exceeded 1e-3 (at most
 Without RoPE the bf16 inputs enter the MFMA exactly and the flat 1e-3 is
 checked everywhere else in the suite.
 """
-import numpy as np
 import pytest
 import torch
 
-import oracle
-from gpu_util import announce, device_inputs, f64, need_gpu
+from gpu_util import announce, assert_rope_lse_close, device_inputs, f64, need_gpu
 from paper_2609_13612_amd import api, inputs
 
 pytestmark = pytest.mark.gpu
@@ -43,17 +41,6 @@ CASES = [
 ]
 
 
-def _visible(S, mask, window):
-    i = np.arange(S)[:, None]
-    j = np.arange(S)[None, :]
-    if mask == "none":
-        return np.ones((S, S), dtype=bool)
-    vis = j <= i
-    if mask == "sliding_window":
-        vis &= j > i - window
-    return vis
-
-
 @pytest.mark.parametrize("case", CASES, ids=lambda c: f"{c[5]}-{c[7]}-S{c[3]}-D{c[4]}-scale{c[10]}")
 def test_rope_lse_within_operand_rounding_bound(case):
     need_gpu()
@@ -65,31 +52,7 @@ def test_rope_lse_within_operand_rounding_bound(case):
     _, lse = api.attnfuse_fwd(dev["q"], dev["k"], dev["v"], rope=rope, theta=theta,
                               alibi_slopes=None if slopes is None else slopes.cuda(), **kw)
     torch.cuda.synchronize()
-    q, k, v = f64(cpu["q"]), f64(cpu["k"]), f64(cpu["v"])
     os_ = None if slopes is None else f64(slopes)
-    _, L = oracle.attention_forward(q, k, v, rope=rope, theta=theta, alibi_slopes=os_, **kw)
-    pos = np.arange(S, dtype=np.float64)
-    qr = oracle.rope_rotate(q, pos, theta, rope)
-    kr = oracle.rope_rotate(k, pos, theta, rope)
-    q16 = qr.astype(np.float16).astype(np.float64)
-    k16 = kr.astype(np.float16).astype(np.float64)
-    _, L16 = oracle.attention_forward(q16, k16, v, rope="none", alibi_slopes=os_, **kw)
-    g = f64(lse)
-
-    err16 = np.abs(g - L16)
-    assert err16.max() <= 1e-3, f"LSE vs the fp16-operand definition: {err16.max():.3e}"
-
-    sc = scale if scale is not None else D ** -0.5
-    G = H // Hkv
-    vis = _visible(S, mask, window)
-    err = np.abs(g - L)
-    for b in range(B):
-        for h in range(H):
-            mag = np.abs(qr[b, h]) @ np.abs(kr[b, h // G]).T          # sum_d |q'_id k'_jd|
-            bnd = sc * mag * (2 * 2.0 ** -11 + 2.0 ** -16)
-            row_bound = np.where(vis, bnd, 0.0).max(axis=1) + 2e-4
-            over = err[b, h] > row_bound
-            assert not over.any(), (f"(b={b}, h={h}) LSE error {err[b, h][over].max():.3e} above its "
-                                    f"rounding bound {row_bound[over].min():.3e}")
-    print(f"LSE error vs exact {err.max():.3e} (flat 1e-3 {'met' if err.max() <= 1e-3 else 'exceeded'}), "
-          f"vs the fp16-operand definition {err16.max():.3e}")
+    err, err16 = assert_rope_lse_close(lse, f64(cpu["q"]), f64(cpu["k"]), f64(cpu["v"]), rope, theta, os_, **kw)
+    print(f"LSE error vs exact {err:.3e} (flat 1e-3 {'met' if err <= 1e-3 else 'exceeded'}), "
+          f"vs the fp16-operand definition {err16:.3e}")

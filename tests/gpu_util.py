@@ -139,21 +139,26 @@ def assert_lse_close(gpu, ref, what, tol=LSE_MAX):
     assert err.size == 0 or err.max() <= tol, f"{what}: LSE max-abs {err.max():.3e} > {tol}"
 
 
-def visible_pairs(S, mask, window):
-    """[S, S] boolean: query i sees key j under the mask (no mask, causal, or causal + window)."""
+def visible_pairs(S, mask, window, block_mask=None):
+    """[S, S] boolean: query i sees key j under the mask (no mask, causal, or causal + window)
+    and, if given, the block mask ((block size, active [nb, nb] bool) pair)."""
     i = np.arange(S)[:, None]
     j = np.arange(S)[None, :]
-    if mask == "none":
-        return np.ones((S, S), dtype=bool)
-    vis = j <= i
+    vis = np.ones((S, S), dtype=bool)
+    if mask != "none":
+        vis &= j <= i
     if mask == "sliding_window":
         vis &= j > i - window
+    if block_mask is not None:
+        bs, active = block_mask
+        vis &= active[i // bs, j // bs]
     return vis
 
 
-def assert_rope_lse_close(lse, q, k, v, rope, theta, alibi_slopes, mask, window, scale):
+def assert_rope_lse_close(lse, q, k, v, rope, theta, alibi_slopes, mask, window, scale, block_mask=None):
     """The LSE of a RoPE forward against its operand-precision model (q, k, v:
-    the fp64 inputs; alibi_slopes fp64 or None).
+    the fp64 inputs; alibi_slopes fp64 or None; block_mask the oracle's
+    (block size, active) pair or None).
 
     The kernels round the rotated Q' and K' to fp16 for the score MFMA; the
     definition rotates exactly.  Rounding each operand moves it by at most
@@ -168,7 +173,7 @@ def assert_rope_lse_close(lse, q, k, v, rope, theta, alibi_slopes, mask, window,
     online softmax) of the exact LSE.  Returns the two max-abs errors."""
     B, H, S, D = q.shape
     G = H // k.shape[1]
-    kw = dict(mask=mask, window=window, scale=scale)
+    kw = dict(mask=mask, window=window, scale=scale, block_mask=block_mask)
     _, L = oracle.attention_forward(q, k, v, rope=rope, theta=theta, alibi_slopes=alibi_slopes, **kw)
     pos = np.arange(S, dtype=np.float64)
     qr = oracle.rope_rotate(q, pos, theta, rope)
@@ -183,7 +188,7 @@ def assert_rope_lse_close(lse, q, k, v, rope, theta, alibi_slopes, mask, window,
     report("LSE vs the fp16-operand definition", err16, L16[fin], LSE_MAX, LSE_MAX)
     assert err16.size == 0 or err16.max() <= LSE_MAX, f"LSE vs the fp16-operand definition: {err16.max():.3e}"
     sc = scale if scale is not None else D ** -0.5
-    vis = visible_pairs(S, mask, window)
+    vis = visible_pairs(S, mask, window, block_mask)
     err = np.where(fin, np.abs(g - np.where(fin, L, 0.0)), 0.0)
     for b in range(B):
         for h in range(H):

@@ -155,6 +155,17 @@ def _sparse_case(i):
 
 @pytest.mark.parametrize("i", range(8))
 def test_sweep_blocksparse(i):
+    _blocksparse_case_run(i, rope_lse_model=False)
+
+
+@pytest.mark.parametrize("i", range(8, 68))
+def test_sweep_blocksparse_more(i):
+    """More seeds, with the RoPE LSE held to the operand-precision model as in
+    test_sweep_fwd_bwd_more."""
+    _blocksparse_case_run(i, rope_lse_model=True)
+
+
+def _blocksparse_case_run(i, rope_lse_model):
     need_gpu()
     c = _sparse_case(i)
     announce(f"block-sparse sweep {i}: {c}")
@@ -177,7 +188,11 @@ def test_sweep_blocksparse(i):
                                                         alibi_slopes=os_, block_mask=bm.as_oracle(), o=o_, **kw),
                    o_ref)
     assert_bf16_close(o, O, "O")
-    assert_lse_close(lse, L, "LSE")
+    if rope_lse_model and c["rope"] != "none":
+        assert_rope_lse_close(lse, f64(cpu["q"]), f64(cpu["k"]), f64(cpu["v"]), c["rope"], 1e4, os_, c["mask"],
+                              c["window"], None, block_mask=bm.as_oracle())
+    else:
+        assert_lse_close(lse, L, "LSE")
     for name, g, r in zip(("dQ", "dK", "dV"), grads, ref):
         assert_bf16_close(g, r, name)
 
